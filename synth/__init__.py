@@ -1,0 +1,203 @@
+"""Seeded synthetic workloads for the batched latent-rollout evaluator.
+
+This module only draws random numbers: the five workload shapes, the
+weights (N(0, 1/fan_in)) and the candidate batches (initial latents or
+program-feature vectors, ragged action sequences, hardware vectors). It holds
+none of the evaluator's arithmetic, so both the CPU oracle and the HIP path
+can take their inputs from here without sharing any computation.
+
+Workloads stand in for the paper's Ansor/TenSet candidate populations
+(Sec. 4.1 and the online integration of Sec. 3.6): the tuning logs, models and
+trained weights are not available, so shapes and distributions are synthetic.
+"""
+from __future__ import annotations
+
+import dataclasses
+from dataclasses import dataclass
+from typing import Dict, Optional
+
+import numpy as np
+
+__all__ = [
+    "Workload", "WORKLOADS", "workload", "make_weights", "make_inputs",
+    "scaled", "WEIGHT_ORDER",
+]
+
+
+@dataclass(frozen=True)
+class Workload:
+    """Shape and distribution of one synthetic candidate batch.
+
+    d: latent width; e: action-embedding width; n_kinds/n_params: action
+    types and integer parameters per step; H: transition hidden width;
+    C: cost-model hidden width; hw_dim/n_hw: hardware vector width and count;
+    S: subgraphs (contiguous candidate segments); feat_dim/enc_hidden: width
+    of the program-feature vector and encoder hidden layer (0 = the initial
+    latent is given directly); lengths: action-sequence length law.
+    """
+    name: str
+    B: int
+    d: int
+    e: int
+    n_kinds: int
+    n_params: int
+    H: int
+    C: int
+    hw_dim: int
+    n_hw: int
+    k: int
+    S: int = 1
+    feat_dim: int = 0
+    enc_hidden: int = 0
+    lengths: str = "uniform"       # "uniform" | "geometric"
+    len_lo: int = 1
+    len_hi: int = 8                # inclusive upper bound (uniform)
+    geo_mean: float = 24.0         # geometric law on {1,2,...}
+    T_max: int = 8                 # padded width of the action tensors
+    precisions: tuple = ("fp32",)
+
+    @property
+    def in_dim(self) -> int:
+        """Width of the transition input [z; e]."""
+        return self.d + self.e
+
+    @property
+    def cost_in(self) -> int:
+        """Width of the cost-model input [z_T; phi; h]."""
+        return self.d + self.e + self.hw_dim
+
+
+WORKLOADS: Dict[str, Workload] = {
+    # Tiny rollout, fp32.
+    "tiny": Workload(
+        name="tiny", B=256, d=64, e=32, n_kinds=12, n_params=4, H=128, C=128,
+        hw_dim=16, n_hw=1, k=16, lengths="uniform", len_lo=1, len_hi=8,
+        T_max=8, precisions=("fp32",)),
+    # One Ansor search round: 2048 candidates, top-64 measured.
+    "ansor_round": Workload(
+        name="ansor_round", B=2048, d=256, e=64, n_kinds=16, n_params=6,
+        H=512, C=512, hw_dim=32, n_hw=1, k=64, lengths="uniform", len_lo=1,
+        len_hi=32, T_max=32, precisions=("fp32", "bf16")),
+    # Long schedules with skewed (geometric, capped) lengths.
+    "long_schedule": Workload(
+        name="long_schedule", B=8192, d=256, e=64, n_kinds=16, n_params=6,
+        H=1024, C=512, hw_dim=32, n_hw=1, k=64, lengths="geometric",
+        geo_mean=24.0, T_max=64, precisions=("bf16",)),
+    # Large-latent throughput: the dense-contraction-bound shape.
+    "large_latent": Workload(
+        name="large_latent", B=65536, d=512, e=128, n_kinds=16, n_params=6,
+        H=2048, C=1024, hw_dim=32, n_hw=1, k=256, lengths="uniform",
+        len_lo=8, len_hi=48, T_max=48, precisions=("bf16",)),
+    # 32 subgraphs x 2048 candidates, encoder MLP for the initial states,
+    # every candidate scored under two hardware vectors.
+    "multi_subgraph": Workload(
+        name="multi_subgraph", B=65536, S=32, d=256, e=64, n_kinds=16,
+        n_params=6, H=512, C=512, hw_dim=32, n_hw=2, k=32, feat_dim=164,
+        enc_hidden=512, lengths="uniform", len_lo=1, len_hi=48, T_max=48,
+        precisions=("bf16",)),
+}
+
+
+def workload(name: str) -> Workload:
+    return WORKLOADS[name]
+
+
+def scaled(w: Workload, B: int, S: Optional[int] = None, **kw) -> Workload:
+    """Same model shapes, smaller batch (and optionally fewer segments)."""
+    S = w.S if S is None else S
+    if B % S:
+        raise ValueError("B must be a multiple of S")
+    return dataclasses.replace(w, B=B, S=S, **kw)
+
+
+# Fixed draw order of the weight tensors.  Each is N(0, 1/fan_in); a bias uses
+# the standard deviation of its layer's weight.
+WEIGHT_ORDER = (
+    "type_emb", "param_w", "param_b", "w1", "b1", "w2", "b2",
+    "wc1", "bc1", "wc2", "bc2", "we1", "be1", "we2", "be2",
+)
+
+
+def _weight_shapes(w: Workload):
+    """(shape, fan_in) per weight, PyTorch Linear layout [out][in]."""
+    s = {
+        "type_emb": ((w.n_kinds, w.e), w.n_kinds),     # one-hot linear
+        "param_w": ((w.e, w.n_params), w.n_params),
+        "param_b": ((w.e,), w.n_params),
+        "w1": ((w.H, w.in_dim), w.in_dim),
+        "b1": ((w.H,), w.in_dim),
+        "w2": ((w.d, w.H), w.H),
+        "b2": ((w.d,), w.H),
+        "wc1": ((w.C, w.cost_in), w.cost_in),
+        "bc1": ((w.C,), w.cost_in),
+        "wc2": ((w.C,), w.C),
+        "bc2": ((), w.C),
+    }
+    if w.feat_dim:
+        s.update({
+            "we1": ((w.enc_hidden, w.feat_dim), w.feat_dim),
+            "be1": ((w.enc_hidden,), w.feat_dim),
+            "we2": ((w.d, w.enc_hidden), w.enc_hidden),
+            "be2": ((w.d,), w.enc_hidden),
+        })
+    return s
+
+
+def make_weights(w: Workload, seed: int) -> Dict[str, np.ndarray]:
+    """All weights as float32 arrays, drawn in WEIGHT_ORDER from PCG64(seed)."""
+    rng = np.random.default_rng(seed)
+    shapes = _weight_shapes(w)
+    out = {}
+    for name in WEIGHT_ORDER:
+        if name not in shapes:
+            continue
+        shape, fan_in = shapes[name]
+        out[name] = (rng.standard_normal(shape) / np.sqrt(fan_in)).astype(np.float32)
+    return out
+
+
+def _lengths(w: Workload, rng: np.random.Generator) -> np.ndarray:
+    if w.lengths == "uniform":
+        L = rng.integers(w.len_lo, w.len_hi + 1, size=w.B)
+    elif w.lengths == "geometric":
+        L = np.minimum(rng.geometric(1.0 / w.geo_mean, size=w.B), w.T_max)
+    else:
+        raise ValueError(w.lengths)
+    return L.astype(np.int32)
+
+
+def make_inputs(w: Workload, seed: int, pad: str = "zero") -> Dict[str, np.ndarray]:
+    """One candidate batch.
+
+    Returns int32 `types [B][T_max]`, `params [B][T_max][P]`, `lens [B]`,
+    `seg_off [S+1]`, float32 `hw [n_hw][hw_dim]`, and either `z0 [S][d]`
+    (N(0,1)) or `feats [S][feat_dim]` (|N(0,1)|).  Parameters are
+    floor(2**U[0,10)), i.e. log-uniform integers in [1, 1023].  Entries at
+    t >= lens[i] are padding: zeros (pad="zero") or arbitrary, partly invalid
+    integers (pad="garbage") that a correct evaluator never reads.
+    """
+    rng = np.random.default_rng(seed)
+    lens = _lengths(w, rng)
+    types = rng.integers(0, w.n_kinds, size=(w.B, w.T_max)).astype(np.int32)
+    params = np.floor(2.0 ** rng.uniform(0.0, 10.0, size=(w.B, w.T_max, w.n_params))).astype(np.int32)
+    if w.feat_dim:
+        init = {"feats": np.abs(rng.standard_normal((w.S, w.feat_dim))).astype(np.float32)}
+    else:
+        init = {"z0": rng.standard_normal((w.S, w.d)).astype(np.float32)}
+    hw = rng.standard_normal((w.n_hw, w.hw_dim)).astype(np.float32)
+    t = np.arange(w.T_max)[None, :]
+    pad_mask = t >= lens[:, None]
+    if pad == "zero":
+        types[pad_mask] = 0
+        params[pad_mask] = 0
+    elif pad == "garbage":
+        g = np.random.default_rng(seed ^ 0x5EED)
+        types[pad_mask] = g.integers(-1000, 1000, size=int(pad_mask.sum()))
+        params[pad_mask] = g.integers(-(2 ** 31), 2 ** 31 - 1, size=(int(pad_mask.sum()), w.n_params))
+    else:
+        raise ValueError(pad)
+    seg = w.B // w.S
+    seg_off = (np.arange(w.S + 1) * seg).astype(np.int32)
+    out = {"types": types, "params": params, "lens": lens, "hw": hw, "seg_off": seg_off}
+    out.update(init)
+    return out
