@@ -182,8 +182,9 @@ def topk(scores: np.ndarray, seg_off, k: int):
         for s in range(S):
             lo, hi = int(seg_off[s]), int(seg_off[s + 1])
             y = scores[j, lo:hi]
-            key = np.where(np.isnan(y), np.inf, -y)
-            order = np.lexsort((np.arange(hi - lo), key))[:k]
+            nan = np.isnan(y)
+            # primary: NaN last; then descending score; then ascending index
+            order = np.lexsort((np.arange(hi - lo), np.where(nan, 0.0, -y), nan))[:k]
             idx[j, s] = lo + order
             val[j, s] = y[order]
     return idx, val

@@ -248,9 +248,10 @@ def test_topk_matches_brute_force_sort():
 
 
 def test_topk_duplicates_nan_and_full_segment():
-    y = np.array([[1.0, 3.0, 3.0, np.nan, -0.0, 0.0, 3.0]])
-    idx, val = O.topk(y, [0, 7], 7)
-    assert list(idx[0, 0]) == [1, 2, 6, 0, 4, 5, 3]
+    y = np.array([[1.0, 3.0, 3.0, np.nan, -0.0, 0.0, 3.0, -np.inf, np.inf]])
+    idx, val = O.topk(y, [0, 9], 9)
+    # +inf first, ties to the lower index, -0 == +0, -inf before NaN (last)
+    assert list(idx[0, 0]) == [8, 1, 2, 6, 0, 4, 5, 7, 3]
 
 
 # ----------------------------------------------------------------------------
