@@ -1,0 +1,196 @@
+/*
+ * wm.h - C ABI of the batched latent-rollout schedule evaluator (gfx950).
+ *
+ * The evaluator scores B candidate schedules of tensor-program subgraphs the
+ * way the paper's world-model evaluator does (Sec. 3.2, Eq. 2-3): encode the
+ * initial program state, roll the latent state forward once per scheduling
+ * action (Eq. 1, Sec. 3.4), score the terminal latent together with action
+ * and hardware features (Eq. 3, Sec. 3.5), and rank candidates within each
+ * workload (Sec. 3.5, Sec. 3.6).  The instantiation is a residual two-layer
+ * MLP transition, a type-embedding plus linear(log2 params) action embedding,
+ * mean action embedding as action features, and a two-layer MLP cost model:
+ *
+ *   e_t  = type_emb[type_t] + param_w . log2(params_t) + param_b
+ *   z_t  = z_{t-1} + W2 . GELU(W1 . [z_{t-1}; e_t] + b1) + b2,  t = 1..len_i
+ *   phi  = (1/len_i) sum_t e_t          (0 when len_i = 0)
+ *   y_j  = wc2 . GELU(Wc1 . [z_T; phi; h_j] + bc1) + bc2
+ *   GELU(x) = x (1 + erf(x / sqrt 2)) / 2
+ *
+ * Conventions for every call below:
+ *  - Pointers are device pointers unless marked HOST.  All tensors are dense,
+ *    row-major, C-contiguous, 4-byte elements (float32 or int32), and must be
+ *    4-byte aligned; float tensors read as vectors must be 16-byte aligned
+ *    (any torch/hipMalloc allocation is).
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Work
+ *    is enqueued asynchronously; a call returns after enqueueing.
+ *  - The caller owns every buffer it passes; the library owns only the
+ *    model's device copy of the weights.  Buffers, the model and the
+ *    workspace must stay alive until the enqueued work has completed.
+ *  - No call allocates device memory except wm_model_create.
+ *  - Argument problems the host can see are reported synchronously, before
+ *    anything is enqueued: a null required pointer, a negative size, a bad
+ *    segment table, k out of range, a workspace that is too small.  The
+ *    status is returned and wm_last_error() gives a message (thread-local).
+ *  - Problems in the data itself (a length outside [0, T_max], an action type
+ *    outside [0, n_kinds), a parameter < 1 at a step t < len_i) are detected
+ *    on the device and recorded in the workspace's error word; read it with
+ *    wm_device_status.  When it is set, outputs are unspecified (but no
+ *    out-of-bounds access happens).  Padding entries (t >= len_i) are never
+ *    read.
+ *  - Calls that share one workspace must not overlap in time.
+ */
+#ifndef WM_H
+#define WM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WM_MAX_SEGMENTS 512   /* subgraphs per call */
+#define WM_MAX_K 1024         /* top-k per (hardware vector, subgraph) */
+#define WM_MAX_T 4096         /* padded action-sequence width */
+
+typedef enum wm_status {
+  WM_OK = 0,
+  WM_ERR_INVALID_ARGUMENT = 1, /* host-visible argument error; nothing enqueued */
+  WM_ERR_UNSUPPORTED = 2,      /* dims/precision this build has no kernel for */
+  WM_ERR_OUT_OF_MEMORY = 3,    /* wm_model_create could not allocate */
+  WM_ERR_DEVICE = 4,           /* a HIP runtime call failed */
+  WM_ERR_INPUT_RANGE = 5       /* device-detected data error (wm_device_status) */
+} wm_status;
+
+typedef enum wm_precision {
+  WM_FP32 = 0, /* float32 operands, float32 matrix-core accumulation */
+  WM_BF16 = 1  /* bfloat16 (round-to-nearest-even) matrix operands, float32 accumulation */
+} wm_precision;
+
+typedef enum wm_norm {
+  WM_NORM_NONE = 0, /* residual MLP transition as above */
+  WM_NORM_L2 = 1    /* L2-normalise z after every step (Sec. 3.4); not built: WM_ERR_UNSUPPORTED */
+} wm_norm;
+
+/* Model shape.  d: latent width; embed_dim: action-embedding width e;
+ * n_kinds/n_params: action types and integer parameters per step;
+ * trans_hidden: transition hidden width H; cost_hidden: cost hidden width C;
+ * hw_dim: hardware-vector width (0 = no hardware features); feat_dim and
+ * enc_hidden: program-feature width F and encoder hidden width (feat_dim = 0:
+ * no encoder, the initial latents are given).  precision: wm_precision;
+ * norm: wm_norm.
+ * Supported by this build (else WM_ERR_UNSUPPORTED): (d, embed_dim) in
+ * {(64, 32), (256, 64)} for both precisions and (512, 128) for WM_BF16;
+ * trans_hidden and cost_hidden multiples of 64; hw_dim a multiple of 16 up
+ * to 32; n_kinds <= 32; 1 <= n_params <= 8; the double-buffered weight
+ * chunks plus embedding tables must fit the 160 KiB LDS. */
+typedef struct wm_dims {
+  int32_t d, embed_dim, n_kinds, n_params, trans_hidden, cost_hidden, hw_dim;
+  int32_t feat_dim, enc_hidden;
+  int32_t precision;
+  int32_t norm;
+} wm_dims;
+
+/* Weights, HOST float32, PyTorch Linear layout [out][in]:
+ *   type_emb [n_kinds][e], param_w [e][n_params], param_b [e],
+ *   w1 [H][d+e] (columns: z then e), b1 [H], w2 [d][H], b2 [d],
+ *   wc1 [C][d+e+hw_dim] (columns: z_T, phi, h), bc1 [C], wc2 [C], bc2,
+ *   we1 [enc_hidden][feat_dim], be1 [enc_hidden], we2 [d][enc_hidden], be2 [d]
+ *   (encoder pointers may be NULL when feat_dim = 0). */
+typedef struct wm_weights {
+  const float *type_emb, *param_w, *param_b;
+  const float *w1, *b1, *w2, *b2;
+  const float *wc1, *bc1, *wc2;
+  float bc2;
+  const float *we1, *be1, *we2, *be2;
+} wm_weights;
+
+typedef struct wm_model wm_model;
+
+/* Copy the weights to the current HIP device, rounding the matrices
+ * W1, W2, Wc1, We1, We2 to bfloat16 (nearest-even) in WM_BF16 mode and
+ * repacking them into the kernels' matrix-fragment order.  Synchronous.
+ * The model is immutable: concurrent calls with distinct workspaces are safe.
+ * Errors: INVALID_ARGUMENT (null pointer, non-positive dims), UNSUPPORTED,
+ * OUT_OF_MEMORY, DEVICE. */
+wm_status wm_model_create(const wm_dims* dims, const wm_weights* weights, wm_model** out);
+
+/* Free the model.  Only after all work using it has completed.  NULL is a no-op. */
+void wm_model_destroy(wm_model* model);
+
+/* Bytes of workspace wm_rollout / wm_evaluate need for a batch of B
+ * candidates in S subgraphs scored under n_hw hardware vectors (0 on a bad
+ * argument).  The caller allocates it (256-byte aligned) and must zero it
+ * once before first use; afterwards the library keeps the error word
+ * consistent (wm_device_status clears it). */
+size_t wm_workspace_bytes(const wm_model* model, int32_t B, int32_t T_max, int32_t S, int32_t n_hw);
+
+/* Initial latents from program features (the state encoder E of Sec. 3.3,
+ * Eq. 4, as a two-layer MLP): z0[s] = We2 . GELU(We1 . feats[s] + be1) + be2.
+ * feats [S][feat_dim] float32 -> z0 [S][d] float32.  Needs feat_dim > 0. */
+wm_status wm_encode_init(const wm_model* model, const float* feats, int32_t S, float* z0,
+                         void* stream);
+
+/* Batched multi-step latent rollout (Eq. 1-2, Sec. 3.4 and 3.6).
+ * Candidate i (0 <= i < B) belongs to subgraph s with
+ * seg_off[s] <= i < seg_off[s+1] and starts from z0[s].
+ *   z0      [S][d] float32
+ *   seg_off HOST int32 [S+1]: 0 = seg_off[0] <= ... <= seg_off[S] = B, 1 <= S <= WM_MAX_SEGMENTS
+ *   types   [B][T_max] int32, params [B][T_max][n_params] int32, lens [B] int32
+ *   zT      [B][d] float32 out: latent after lens[i] steps (z0 when lens[i] = 0)
+ *   phi     [B][e] float32 out (may be NULL): mean step embedding (0 when lens[i] = 0)
+ *   ws      workspace of at least wm_workspace_bytes(model, B, T_max, S, 1) bytes. */
+wm_status wm_rollout(const wm_model* model, const float* z0, const int32_t* seg_off, int32_t S,
+                     const int32_t* types, const int32_t* params, const int32_t* lens,
+                     int32_t B, int32_t T_max, float* zT, float* phi,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/* Cost model G (Eq. 3, Eq. 12): scores [n_hw][B] float32 out, from
+ * zT [B][d], phi [B][e] and hw [n_hw][hw_dim] (hw may be NULL when
+ * hw_dim = 0).  Higher scores rank first. */
+wm_status wm_score(const wm_model* model, const float* zT, const float* phi, int32_t B,
+                   const float* hw, int32_t n_hw, float* scores, void* stream);
+
+/* Within-workload ranking (Sec. 3.5): for every hardware vector j and
+ * subgraph s, the k best candidates of segment s ordered by descending score,
+ * ties to the lower candidate index, NaN last.
+ *   scores [n_hw][B] float32; seg_off HOST [S+1] as above;
+ *   1 <= k <= min(WM_MAX_K, smallest segment);
+ *   idx [n_hw][S][k] int32 out (global candidate indices);
+ *   val [n_hw][S][k] float32 out (may be NULL). */
+wm_status wm_topk(const float* scores, int32_t n_hw, int32_t B, const int32_t* seg_off,
+                  int32_t S, int32_t k, int32_t* idx, float* val, void* stream);
+
+/* The whole hot path in one call: [encode,] rollout, score, top-k
+ * (Eq. 2-3, Sec. 3.6).  init is z0 [S][d], or program features
+ * [S][feat_dim] when init_is_feats != 0 (needs an encoder).  scores
+ * [n_hw][B], zT [B][d] and val may be NULL (kept in the workspace /
+ * not written); idx is required.  ws needs
+ * wm_workspace_bytes(model, B, T_max, S, n_hw) bytes. */
+wm_status wm_evaluate(const wm_model* model, const float* init, int32_t init_is_feats,
+                      const int32_t* seg_off, int32_t S,
+                      const int32_t* types, const int32_t* params, const int32_t* lens,
+                      int32_t B, int32_t T_max, const float* hw, int32_t n_hw, int32_t k,
+                      float* scores, float* zT, int32_t* idx, float* val,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/* Synchronise `stream`, read and clear the workspace's device error word.
+ * Returns WM_OK, or WM_ERR_INPUT_RANGE with wm_last_error() naming the
+ * violation(s); WM_ERR_DEVICE if the stream reports a failure. */
+wm_status wm_device_status(void* ws, size_t ws_bytes, void* stream);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char* wm_last_error(void);
+
+/* Kernel timing with HIP events recorded on the launch stream around each
+ * launch of one kernel family (for benchmarks).  Ids: 0 rollout, 1 score,
+ * 2 top-k, 3 bucketing, 4 action features, 5 encoder.  Enabling resets the
+ * counters; reading synchronises on the recorded events.  At most 8192
+ * launches per kernel are recorded while enabled. */
+wm_status wm_timing_enable(int32_t on);
+wm_status wm_timing_read(int32_t kernel, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WM_H */

@@ -1,0 +1,16 @@
+"""MI355X-native batched latent-rollout evaluator (compiler world model).
+
+The hot path (rollout, scoring, top-k) runs in hand-written gfx950 HIP
+kernels behind the C ABI of include/wm.h; this package is the thin Python
+binding over it.
+"""
+from .binding import (  # noqa: F401
+    KERNELS, PRECISIONS, SYMBOLS, WMError, Model, device_status, encode_init, evaluate,
+    load_library, rollout, score, timing_enable, timing_read, topk,
+)
+
+
+def model_dims(w) -> dict:
+    """Model dims dict from an object with the workload fields (d, e, ...)."""
+    return {k: getattr(w, k) for k in ("d", "e", "n_kinds", "n_params", "H", "C", "hw_dim",
+                                       "feat_dim", "enc_hidden")}

@@ -1,0 +1,497 @@
+// C-ABI layer of the batched latent-rollout evaluator: model creation (weight
+// repacking into matrix-fragment order), host-side argument validation,
+// workspace carving, kernel orchestration, device error word, event timing.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "wm_internal.h"
+
+using namespace wm;
+
+struct wm_model {
+  DevModel dm;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+wm_status fail(wm_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+wm_status ok() {
+  g_last_error.clear();
+  return WM_OK;
+}
+
+#define WM_HIP_TRY(expr)                                                                 \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess) return fail(WM_ERR_DEVICE, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+// ---- bf16 (round to nearest even) ----------------------------------------
+uint16_t f32_to_bf16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
+  const uint32_t r = u + 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(r >> 16);
+}
+float bf16_value(float f) {
+  const uint32_t u = (uint32_t)f32_to_bf16(f) << 16;
+  float o;
+  std::memcpy(&o, &u, 4);
+  return o;
+}
+
+// Store one weight element of a packed fragment block.
+template <class Gm>
+void put(std::vector<uint8_t>& blk, size_t base, int F, int lane, int j, float v) {
+  const size_t off = base + (size_t)frag_offset<Gm>(F, lane, j);
+  if (Gm::ES == 2) {
+    const uint16_t b = f32_to_bf16(v);
+    std::memcpy(&blk[off], &b, 2);
+  } else {
+    std::memcpy(&blk[off], &v, 4);
+  }
+}
+
+void put_f32(std::vector<uint8_t>& blk, size_t off, float v) { std::memcpy(&blk[off], &v, 4); }
+
+// Transition chunks: for hidden chunk c, [W1 fragments][W2 fragments][b1 tail].
+template <class Gm>
+std::vector<uint8_t> pack_transition(const wm_dims& dm, const wm_weights& w) {
+  const int D = dm.d, E = dm.embed_dim, H = dm.trans_hidden, IN = D + E;
+  const int CB = TransChunk<Gm>::bytes(D, E), NK1 = TransChunk<Gm>::nk1(D, E);
+  const int NF2 = 32 / Gm::KF, NG = TransChunk<Gm>::ngroups(D, E);
+  std::vector<uint8_t> blk((size_t)(H / 32) * CB, 0);
+  for (int c = 0; c < H / 32; ++c) {
+    const size_t base = (size_t)c * CB;
+    for (int kf = 0; kf < NK1; ++kf)
+      for (int L = 0; L < 64; ++L)
+        for (int j = 0; j < Gm::SL; ++j) {
+          const int m = L & 31, h = L >> 5;
+          const int feat = x_feature<Gm>(D, kf, h, j);
+          put<Gm>(blk, base, kf, L, j, w.w1[(size_t)(32 * c + m) * IN + feat]);
+        }
+    for (int db = 0; db < D / 32; ++db)
+      for (int f = 0; f < NF2; ++f)
+        for (int L = 0; L < 64; ++L)
+          for (int j = 0; j < Gm::SL; ++j) {
+            const int m = L & 31, h = L >> 5;
+            const int hid = 32 * c + g_feature<Gm>(f, h, j);
+            put<Gm>(blk, base, NK1 + db * NF2 + f, L, j, w.w2[(size_t)(32 * db + m) * H + hid]);
+          }
+    for (int h = 0; h < 2; ++h)
+      for (int r = 0; r < 16; ++r)
+        put_f32(blk, base + (size_t)NG * 1024 + (size_t)(h * 16 + r) * 4, w.b1[32 * c + acc_row(h, r)]);
+  }
+  return blk;
+}
+
+// Cost chunks: for cost hidden chunk c, [Wc1 fragments][bc1 tail][wc2 tail].
+template <class Gm>
+std::vector<uint8_t> pack_cost(const wm_dims& dm, const wm_weights& w) {
+  const int D = dm.d, E = dm.embed_dim, HW = dm.hw_dim, C = dm.cost_hidden, IN = D + E + HW;
+  const int CB = CostChunk<Gm>::bytes(D, E, HW), NF = CostChunk<Gm>::nfrags(D, E, HW);
+  const int NG = CostChunk<Gm>::ngroups(D, E, HW);
+  std::vector<uint8_t> blk((size_t)(C / 32) * CB, 0);
+  for (int c = 0; c < C / 32; ++c) {
+    const size_t base = (size_t)c * CB;
+    for (int kf = 0; kf < NF; ++kf)
+      for (int L = 0; L < 64; ++L)
+        for (int j = 0; j < Gm::SL; ++j) {
+          const int m = L & 31, h = L >> 5;
+          put<Gm>(blk, base, kf, L, j, w.wc1[(size_t)(32 * c + m) * IN + nat_feature<Gm>(kf, h, j)]);
+        }
+    for (int h = 0; h < 2; ++h)
+      for (int r = 0; r < 16; ++r) {
+        const int row = 32 * c + acc_row(h, r);
+        put_f32(blk, base + (size_t)NG * 1024 + (size_t)(h * 16 + r) * 4, w.bc1[row]);
+        put_f32(blk, base + (size_t)NG * 1024 + 128 + (size_t)(h * 16 + r) * 4, w.wc2[row]);
+      }
+  }
+  return blk;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct WsLayout {
+  size_t err, perm, z0, zT, phi, scores, total;
+};
+
+WsLayout ws_layout(const DevModel& m, int B, int S, int n_hw) {
+  WsLayout L;
+  size_t o = 0;
+  L.err = o; o += 256;
+  L.perm = o; o = align256(o + (size_t)B * sizeof(int2));
+  L.z0 = o; o = align256(o + (size_t)S * m.dims.d * 4);
+  L.zT = o; o = align256(o + (size_t)B * m.dims.d * 4);
+  L.phi = o; o = align256(o + (size_t)B * m.dims.embed_dim * 4);
+  L.scores = o; o = align256(o + (size_t)n_hw * B * 4);
+  L.total = o;
+  return L;
+}
+
+// Host checks of a segment table; fills the kernel-argument copy.
+wm_status check_segments(const int32_t* seg_off, int32_t S, int32_t B, SegTable* tab,
+                         int32_t* min_seg) {
+  if (!seg_off) return fail(WM_ERR_INVALID_ARGUMENT, "seg_off is NULL");
+  if (S < 1 || S > WM_MAX_SEGMENTS)
+    return fail(WM_ERR_INVALID_ARGUMENT, "S must be in [1, " + std::to_string(WM_MAX_SEGMENTS) + "]");
+  if (seg_off[0] != 0 || seg_off[S] != B)
+    return fail(WM_ERR_INVALID_ARGUMENT, "seg_off must start at 0 and end at B");
+  int32_t mn = B;
+  for (int s = 0; s < S; ++s) {
+    if (seg_off[s + 1] < seg_off[s]) return fail(WM_ERR_INVALID_ARGUMENT, "seg_off is not non-decreasing");
+    mn = std::min(mn, seg_off[s + 1] - seg_off[s]);
+  }
+  tab->n = S;
+  for (int s = 0; s <= S; ++s) tab->off[s] = seg_off[s];
+  *min_seg = mn;
+  return WM_OK;
+}
+
+// ---- timing ----------------------------------------------------------------
+constexpr int kTimingCap = 8192;
+struct Timing {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> start[TK_COUNT], stop[TK_COUNT];
+  int count[TK_COUNT] = {};
+} g_timing;
+
+}  // namespace
+
+namespace wm {
+void timing_begin(int k, hipStream_t st) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  if (!g_timing.on || g_timing.count[k] >= kTimingCap) return;
+  const int i = g_timing.count[k];
+  if ((int)g_timing.start[k].size() <= i) {
+    hipEvent_t a, b;
+    if (hipEventCreate(&a) != hipSuccess) return;
+    if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+    g_timing.start[k].push_back(a);
+    g_timing.stop[k].push_back(b);
+  }
+  (void)hipEventRecord(g_timing.start[k][i], st);
+}
+void timing_end(int k, hipStream_t st) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  if (!g_timing.on || g_timing.count[k] >= kTimingCap) return;
+  const int i = g_timing.count[k];
+  if ((int)g_timing.stop[k].size() <= i) return;
+  (void)hipEventRecord(g_timing.stop[k][i], st);
+  g_timing.count[k] = i + 1;
+}
+}  // namespace wm
+
+#define WM_TIMED(K, ST, CALL)                                              \
+  do {                                                                     \
+    timing_begin(K, ST);                                                   \
+    hipError_t e_ = (CALL);                                                \
+    timing_end(K, ST);                                                     \
+    if (e_ != hipSuccess) return fail(WM_ERR_DEVICE, std::string("kernel launch: ") + hipGetErrorString(e_)); \
+  } while (0)
+
+extern "C" {
+
+const char* wm_last_error(void) { return g_last_error.c_str(); }
+
+wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** out) {
+  if (!dims || !w || !out) return fail(WM_ERR_INVALID_ARGUMENT, "null argument");
+  *out = nullptr;
+  const wm_dims& dm = *dims;
+  if (dm.d <= 0 || dm.embed_dim <= 0 || dm.n_kinds <= 0 || dm.n_params <= 0 ||
+      dm.trans_hidden <= 0 || dm.cost_hidden <= 0 || dm.hw_dim < 0 || dm.feat_dim < 0 ||
+      (dm.feat_dim > 0 && dm.enc_hidden <= 0))
+    return fail(WM_ERR_INVALID_ARGUMENT, "dims must be positive (hw_dim, feat_dim >= 0)");
+  if (dm.precision != WM_FP32 && dm.precision != WM_BF16)
+    return fail(WM_ERR_INVALID_ARGUMENT, "unknown precision");
+  if (dm.norm != WM_NORM_NONE && dm.norm != WM_NORM_L2)
+    return fail(WM_ERR_INVALID_ARGUMENT, "unknown norm");
+  if (dm.norm == WM_NORM_L2) return fail(WM_ERR_UNSUPPORTED, "WM_NORM_L2 is not built");
+  if (!w->type_emb || !w->param_w || !w->param_b || !w->w1 || !w->b1 || !w->w2 || !w->b2 ||
+      !w->wc1 || !w->bc1 || !w->wc2)
+    return fail(WM_ERR_INVALID_ARGUMENT, "null weight pointer");
+  if (dm.feat_dim > 0 && (!w->we1 || !w->be1 || !w->we2 || !w->be2))
+    return fail(WM_ERR_INVALID_ARGUMENT, "null encoder weight pointer");
+  if (!have_kernels(dm.precision, dm.d, dm.embed_dim))
+    return fail(WM_ERR_UNSUPPORTED, "no kernels for this (precision, d, embed_dim)");
+  if (dm.trans_hidden % 64 || dm.cost_hidden % 64 || dm.hw_dim % 16 || dm.hw_dim > 32 ||
+      dm.n_kinds > 32 || dm.n_params > 8)
+    return fail(WM_ERR_UNSUPPORTED,
+                "need trans_hidden, cost_hidden % 64 == 0, hw_dim % 16 == 0 and <= 32, n_kinds <= 32, n_params <= 8");
+
+  DevModel m{};
+  m.dims = dm;
+  m.prec = dm.precision;
+  const int D = dm.d, E = dm.embed_dim, K = dm.n_kinds, P = dm.n_params, HW = dm.hw_dim;
+  std::vector<uint8_t> trans, cost;
+  if (m.prec == WM_BF16) {
+    trans = pack_transition<GeomBF16>(dm, *w);
+    cost = pack_cost<GeomBF16>(dm, *w);
+    m.trans_chunk_bytes = TransChunk<GeomBF16>::bytes(D, E);
+    m.cost_chunk_bytes = CostChunk<GeomBF16>::bytes(D, E, HW);
+  } else {
+    if ((D + E + HW) % 8 != 0) return fail(WM_ERR_UNSUPPORTED, "fp32 needs d + embed_dim + hw_dim % 8 == 0");
+    trans = pack_transition<GeomF32>(dm, *w);
+    cost = pack_cost<GeomF32>(dm, *w);
+    m.trans_chunk_bytes = TransChunk<GeomF32>::bytes(D, E);
+    m.cost_chunk_bytes = CostChunk<GeomF32>::bytes(D, E, HW);
+  }
+  // rollout table: type_emb [K][E], param_w^T [P][E], param_b [E], b2 (accumulator order)
+  std::vector<float> tab;
+  tab.reserve((size_t)K * E + (size_t)P * E + E + D + 4);
+  for (int k = 0; k < K; ++k)
+    for (int f = 0; f < E; ++f) tab.push_back(w->type_emb[(size_t)k * E + f]);
+  for (int p = 0; p < P; ++p)
+    for (int f = 0; f < E; ++f) tab.push_back(w->param_w[(size_t)f * P + p]);
+  for (int f = 0; f < E; ++f) tab.push_back(w->param_b[f]);
+  for (int b = 0; b < D / 32; ++b)
+    for (int h = 0; h < 2; ++h)
+      for (int r = 0; r < 16; ++r) tab.push_back(w->b2[32 * b + acc_row(h, r)]);
+  while (tab.size() % 4) tab.push_back(0.0f);
+  m.roll_tab_bytes = (int)(tab.size() * 4);
+  if (rollout_lds_bytes(m) > 160 * 1024 || 2 * m.cost_chunk_bytes > 160 * 1024)
+    return fail(WM_ERR_UNSUPPORTED, "weight chunks do not fit the 160 KiB LDS");
+
+  // encoder (transposed; bf16-rounded values in bf16 mode)
+  std::vector<float> enc;
+  const int F = dm.feat_dim, Fh = dm.enc_hidden;
+  size_t enc_w1t = 0, enc_b1 = 0, enc_w2t = 0, enc_b2 = 0;
+  if (F > 0) {
+    auto r = [&](float v) { return m.prec == WM_BF16 ? bf16_value(v) : v; };
+    enc_w1t = enc.size();
+    for (int f = 0; f < F; ++f)
+      for (int o = 0; o < Fh; ++o) enc.push_back(r(w->we1[(size_t)o * F + f]));
+    enc_b1 = enc.size();
+    for (int o = 0; o < Fh; ++o) enc.push_back(w->be1[o]);
+    enc_w2t = enc.size();
+    for (int k = 0; k < Fh; ++k)
+      for (int o = 0; o < D; ++o) enc.push_back(r(w->we2[(size_t)o * Fh + k]));
+    enc_b2 = enc.size();
+    for (int o = 0; o < D; ++o) enc.push_back(w->be2[o]);
+  }
+
+  size_t off = 0;
+  const size_t o_trans = off; off = align256(off + trans.size());
+  const size_t o_cost = off; off = align256(off + cost.size());
+  const size_t o_tab = off; off = align256(off + tab.size() * 4);
+  const size_t o_enc = off; off = align256(off + enc.size() * 4);
+  void* dev = nullptr;
+  if (hipMalloc(&dev, off) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(WM_ERR_OUT_OF_MEMORY, "hipMalloc of the model failed");
+  }
+  uint8_t* base = static_cast<uint8_t*>(dev);
+  hipError_t e = hipMemcpy(base + o_trans, trans.data(), trans.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(base + o_cost, cost.data(), cost.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(base + o_tab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
+  if (e == hipSuccess && !enc.empty()) e = hipMemcpy(base + o_enc, enc.data(), enc.size() * 4, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(dev);
+    return fail(WM_ERR_DEVICE, std::string("hipMemcpy: ") + hipGetErrorString(e));
+  }
+  m.base = base;
+  m.trans = base + o_trans;
+  m.cost = base + o_cost;
+  m.roll_tab = reinterpret_cast<const float*>(base + o_tab);
+  m.emb_nat = m.roll_tab;
+  const float* encp = reinterpret_cast<const float*>(base + o_enc);
+  m.enc_w1t = encp + enc_w1t;
+  m.enc_b1 = encp + enc_b1;
+  m.enc_w2t = encp + enc_w2t;
+  m.enc_b2 = encp + enc_b2;
+  m.bc2 = w->bc2;
+  wm_model* out_m = new (std::nothrow) wm_model;
+  if (!out_m) {
+    (void)hipFree(dev);
+    return fail(WM_ERR_OUT_OF_MEMORY, "host allocation failed");
+  }
+  out_m->dm = m;
+  *out = out_m;
+  return ok();
+}
+
+void wm_model_destroy(wm_model* model) {
+  if (!model) return;
+  (void)hipFree(model->dm.base);
+  delete model;
+}
+
+size_t wm_workspace_bytes(const wm_model* model, int32_t B, int32_t T_max, int32_t S, int32_t n_hw) {
+  if (!model || B < 0 || T_max < 0 || S < 1 || n_hw < 1) return 0;
+  return ws_layout(model->dm, B, S, n_hw).total;
+}
+
+wm_status wm_encode_init(const wm_model* model, const float* feats, int32_t S, float* z0,
+                         void* stream) {
+  if (!model) return fail(WM_ERR_INVALID_ARGUMENT, "model is NULL");
+  if (model->dm.dims.feat_dim <= 0) return fail(WM_ERR_INVALID_ARGUMENT, "model has no encoder");
+  if (S < 0) return fail(WM_ERR_INVALID_ARGUMENT, "S < 0");
+  if (S == 0) return ok();
+  if (!feats || !z0) return fail(WM_ERR_INVALID_ARGUMENT, "feats/z0 is NULL");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  WM_TIMED(TK_ENCODE, st, launch_encode(model->dm, feats, S, z0, st));
+  return ok();
+}
+
+static wm_status check_rollout_args(const wm_model* model, const float* z0, const int32_t* types,
+                                    const int32_t* params, const int32_t* lens, int32_t B,
+                                    int32_t T_max, const float* zT) {
+  if (!model) return fail(WM_ERR_INVALID_ARGUMENT, "model is NULL");
+  if (B < 0) return fail(WM_ERR_INVALID_ARGUMENT, "B < 0");
+  if (T_max < 0 || T_max > WM_MAX_T)
+    return fail(WM_ERR_INVALID_ARGUMENT, "T_max must be in [0, " + std::to_string(WM_MAX_T) + "]");
+  if (B > 0 && (!z0 || !types || !params || !lens || !zT))
+    return fail(WM_ERR_INVALID_ARGUMENT, "null input/output pointer");
+  return WM_OK;
+}
+
+wm_status wm_rollout(const wm_model* model, const float* z0, const int32_t* seg_off, int32_t S,
+                     const int32_t* types, const int32_t* params, const int32_t* lens, int32_t B,
+                     int32_t T_max, float* zT, float* phi, void* ws, size_t ws_bytes,
+                     void* stream) {
+  wm_status s = check_rollout_args(model, z0, types, params, lens, B, T_max, zT);
+  if (s != WM_OK) return s;
+  SegTable seg;
+  int32_t min_seg = 0;
+  if ((s = check_segments(seg_off, S, B, &seg, &min_seg)) != WM_OK) return s;
+  if (!ws) return fail(WM_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  const WsLayout L = ws_layout(model->dm, B, S, 1);
+  if (ws_bytes < L.total) return fail(WM_ERR_INVALID_ARGUMENT, "workspace too small");
+  if (B == 0) return ok();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* w8 = static_cast<uint8_t*>(ws);
+  int32_t* err = reinterpret_cast<int32_t*>(w8 + L.err);
+  int2* perm = reinterpret_cast<int2*>(w8 + L.perm);
+  WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, err, st));
+  WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zT, err, st));
+  if (phi) WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
+  return ok();
+}
+
+wm_status wm_score(const wm_model* model, const float* zT, const float* phi, int32_t B,
+                   const float* hw, int32_t n_hw, float* scores, void* stream) {
+  if (!model) return fail(WM_ERR_INVALID_ARGUMENT, "model is NULL");
+  if (B < 0 || n_hw < 1) return fail(WM_ERR_INVALID_ARGUMENT, "need B >= 0 and n_hw >= 1");
+  if (B == 0) return ok();
+  if (!zT || !phi || !scores || (model->dm.dims.hw_dim > 0 && !hw))
+    return fail(WM_ERR_INVALID_ARGUMENT, "null input/output pointer");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  WM_TIMED(TK_SCORE, st, launch_score(model->dm, zT, phi, B, hw, n_hw, scores, st));
+  return ok();
+}
+
+static wm_status check_k(int32_t k, int32_t min_seg) {
+  if (k < 1 || k > WM_MAX_K) return fail(WM_ERR_INVALID_ARGUMENT, "k must be in [1, " + std::to_string(WM_MAX_K) + "]");
+  if (k > min_seg) return fail(WM_ERR_INVALID_ARGUMENT, "k exceeds the size of a segment");
+  return WM_OK;
+}
+
+wm_status wm_topk(const float* scores, int32_t n_hw, int32_t B, const int32_t* seg_off, int32_t S,
+                  int32_t k, int32_t* idx, float* val, void* stream) {
+  if (B < 0 || n_hw < 1) return fail(WM_ERR_INVALID_ARGUMENT, "need B >= 0 and n_hw >= 1");
+  SegTable seg;
+  int32_t min_seg = 0;
+  wm_status s = check_segments(seg_off, S, B, &seg, &min_seg);
+  if (s != WM_OK) return s;
+  if ((s = check_k(k, min_seg)) != WM_OK) return s;
+  if (!scores || !idx) return fail(WM_ERR_INVALID_ARGUMENT, "null scores/idx");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  WM_TIMED(TK_TOPK, st, launch_topk(scores, n_hw, B, seg, k, idx, val, st));
+  return ok();
+}
+
+wm_status wm_evaluate(const wm_model* model, const float* init, int32_t init_is_feats,
+                      const int32_t* seg_off, int32_t S, const int32_t* types,
+                      const int32_t* params, const int32_t* lens, int32_t B, int32_t T_max,
+                      const float* hw, int32_t n_hw, int32_t k, float* scores, float* zT,
+                      int32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream) {
+  if (!model) return fail(WM_ERR_INVALID_ARGUMENT, "model is NULL");
+  if (init_is_feats && model->dm.dims.feat_dim <= 0)
+    return fail(WM_ERR_INVALID_ARGUMENT, "init_is_feats needs a model with an encoder");
+  // zT is checked below once a workspace fallback is known
+  wm_status s = check_rollout_args(model, init, types, params, lens, B, T_max, reinterpret_cast<float*>(1));
+  if (s != WM_OK) return s;
+  if (n_hw < 1) return fail(WM_ERR_INVALID_ARGUMENT, "n_hw < 1");
+  SegTable seg;
+  int32_t min_seg = 0;
+  if ((s = check_segments(seg_off, S, B, &seg, &min_seg)) != WM_OK) return s;
+  if ((s = check_k(k, min_seg)) != WM_OK) return s;
+  if (!idx) return fail(WM_ERR_INVALID_ARGUMENT, "idx is NULL");
+  if (model->dm.dims.hw_dim > 0 && !hw) return fail(WM_ERR_INVALID_ARGUMENT, "hw is NULL");
+  if (!ws) return fail(WM_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  const WsLayout L = ws_layout(model->dm, B, S, n_hw);
+  if (ws_bytes < L.total) return fail(WM_ERR_INVALID_ARGUMENT, "workspace too small");
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* w8 = static_cast<uint8_t*>(ws);
+  int32_t* err = reinterpret_cast<int32_t*>(w8 + L.err);
+  int2* perm = reinterpret_cast<int2*>(w8 + L.perm);
+  float* z0 = const_cast<float*>(init);
+  if (init_is_feats) {
+    z0 = reinterpret_cast<float*>(w8 + L.z0);
+    WM_TIMED(TK_ENCODE, st, launch_encode(model->dm, init, S, z0, st));
+  }
+  float* zTo = zT ? zT : reinterpret_cast<float*>(w8 + L.zT);
+  float* phi = reinterpret_cast<float*>(w8 + L.phi);
+  float* sc = scores ? scores : reinterpret_cast<float*>(w8 + L.scores);
+  WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, err, st));
+  WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zTo, err, st));
+  WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
+  WM_TIMED(TK_SCORE, st, launch_score(model->dm, zTo, phi, B, hw, n_hw, sc, st));
+  WM_TIMED(TK_TOPK, st, launch_topk(sc, n_hw, B, seg, k, idx, val, st));
+  return ok();
+}
+
+wm_status wm_device_status(void* ws, size_t ws_bytes, void* stream) {
+  if (!ws || ws_bytes < 256) return fail(WM_ERR_INVALID_ARGUMENT, "workspace is NULL or too small");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  WM_HIP_TRY(hipStreamSynchronize(st));
+  int32_t word = 0;
+  WM_HIP_TRY(hipMemcpy(&word, ws, sizeof(word), hipMemcpyDeviceToHost));
+  if (word == 0) return ok();
+  WM_HIP_TRY(hipMemset(ws, 0, sizeof(word)));
+  std::string msg = "input out of range:";
+  if (word & ERRBIT_LEN) msg += " a length outside [0, T_max];";
+  if (word & ERRBIT_TYPE) msg += " an action type outside [0, n_kinds);";
+  if (word & ERRBIT_PARAM) msg += " an action parameter < 1;";
+  return fail(WM_ERR_INPUT_RANGE, msg);
+}
+
+wm_status wm_timing_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  g_timing.on = on != 0;
+  for (int k = 0; k < TK_COUNT; ++k) g_timing.count[k] = 0;
+  return ok();
+}
+
+wm_status wm_timing_read(int32_t kernel, double* total_ms, int64_t* launches) {
+  if (kernel < 0 || kernel >= TK_COUNT || !total_ms || !launches)
+    return fail(WM_ERR_INVALID_ARGUMENT, "bad timing query");
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  double tot = 0.0;
+  const int n = g_timing.count[kernel];
+  for (int i = 0; i < n; ++i) {
+    WM_HIP_TRY(hipEventSynchronize(g_timing.stop[kernel][i]));
+    float ms = 0.0f;
+    WM_HIP_TRY(hipEventElapsedTime(&ms, g_timing.start[kernel][i], g_timing.stop[kernel][i]));
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = n;
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,157 @@
+// Internal declarations shared by the C-ABI layer (wm_api.hip) and the
+// kernels (wm_kernels.hip).  Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/wm.h"
+
+namespace wm {
+
+// --------------------------------------------------------------------------
+// Matrix-fragment layout of the 32x32 matrix-core products (gfx950).
+//
+// Both products used here, v_mfma_f32_32x32x16_bf16 (8 bf16 per lane) and
+// v_mfma_f32_32x32x2_f32 (1 float per lane), share one accumulator layout:
+// lane L, accumulator register r in [0,16) holds row acc_row(L/32, r) and
+// column L%32 of the 32x32 result.  The A (resp. B) operand of lane L holds
+// row (resp. column) L%32, and operand slot j of lane half L/32 multiplies the
+// same k in A and in B, so any consistent assignment of contraction indices
+// to (half, slot) pairs is valid.  The kernels exploit that freedom so that
+// every intermediate stays in registers:
+//
+//  * The rollout computes the transposed products  G^T = W1 . X^T  and
+//    dZ^T = W2 . G^T, so weights are always the A operand and candidates are
+//    the 32 columns.  The latent z of a candidate is carried in accumulator
+//    layout (block b of 32 features, register r -> feature 32b+acc_row(h,r)),
+//    and is fed back as the B operand of the next step's first product
+//    without leaving its lane: operand fragment f of block b takes
+//    registers [f*SL, f*SL+SL).  The hidden activations G^T come out of the
+//    first product in the same layout and feed the second product the same
+//    way.  The weight matrices are packed with their contraction columns in
+//    that order (pack_* in wm_api.hip), so no data moves between lanes.
+//  * The embedding part of [z; e] and all cost-model inputs use the natural
+//    order: slot j of half h of fragment q is feature KF*q + SL*h + j.
+// --------------------------------------------------------------------------
+__host__ __device__ constexpr inline int acc_row(int half, int r) {
+  return 8 * (r >> 2) + 4 * half + (r & 3);
+}
+
+// Operand-fragment geometry of a precision.
+//   KF: contraction length of one product; SL: operand elements per lane;
+//   G:  fragments per 16-byte lane group (the unit of an LDS read);
+//   ES: bytes per stored weight element.
+template <int KF_, int SL_, int G_, int ES_>
+struct FragGeom {
+  static constexpr int KF = KF_, SL = SL_, G = G_, ES = ES_;
+};
+using GeomBF16 = FragGeom<16, 8, 1, 2>;
+using GeomF32 = FragGeom<2, 1, 4, 4>;
+
+// Feature index held by operand slot (half, j) of fragment kf of the
+// transition input X = [z; e] (width D + E).
+template <class Gm>
+__host__ __device__ constexpr inline int x_feature(int D, int kf, int half, int j) {
+  constexpr int per_block = 32 / Gm::KF;      // fragments per 32-feature block of z
+  if (kf < D / Gm::KF) {
+    const int b = kf / per_block, f = kf % per_block;
+    return 32 * b + acc_row(half, f * Gm::SL + j);
+  }
+  const int q = kf - D / Gm::KF;
+  return D + Gm::KF * q + Gm::SL * half + j;
+}
+
+// Hidden unit (within a 32-wide chunk) held by slot (half, j) of the
+// fragment f of GELU outputs that feeds the second product.
+template <class Gm>
+__host__ __device__ constexpr inline int g_feature(int f, int half, int j) {
+  return acc_row(half, f * Gm::SL + j);
+}
+
+// Natural order (embedding part, cost-model inputs).
+template <class Gm>
+__host__ __device__ constexpr inline int nat_feature(int kf, int half, int j) {
+  return Gm::KF * kf + Gm::SL * half + j;
+}
+
+// Byte offset of operand element (fragment F, lane L, slot j) inside a block
+// of packed fragments: fragments are grouped G at a time, each group is
+// 64 lanes x 16 bytes, lane-major.
+template <class Gm>
+__host__ __device__ constexpr inline int frag_offset(int F, int lane, int j) {
+  return (F / Gm::G) * 1024 + lane * 16 + ((F % Gm::G) * Gm::SL + j) * Gm::ES;
+}
+
+// Chunk geometry of the transition weights: one chunk = 32 hidden units,
+// [W1 fragments (NK1)][W2 fragments (D/32 blocks x 32/KF)][b1 tail: 32 floats
+// in accumulator order].
+template <class Gm>
+struct TransChunk {
+  static constexpr int nk1(int D, int E) { return (D + E) / Gm::KF; }
+  static constexpr int nfrags(int D, int E) { return nk1(D, E) + (D / 32) * (32 / Gm::KF); }
+  static constexpr int ngroups(int D, int E) { return nfrags(D, E) / Gm::G; }
+  static constexpr int bytes(int D, int E) { return ngroups(D, E) * 1024 + 128; }
+};
+
+// Chunk geometry of the cost-model first layer: one chunk = 32 hidden units,
+// [Wc1 fragments over (D+E+HW) inputs][tail: bc1 then wc2, 32 floats each, in
+// accumulator order].
+template <class Gm>
+struct CostChunk {
+  static constexpr int nfrags(int D, int E, int HW) { return (D + E + HW) / Gm::KF; }
+  static constexpr int ngroups(int D, int E, int HW) { return nfrags(D, E, HW) / Gm::G; }
+  static constexpr int bytes(int D, int E, int HW) { return ngroups(D, E, HW) * 1024 + 256; }
+};
+
+// Device error bits (workspace error word).
+enum : int { ERRBIT_LEN = 1, ERRBIT_TYPE = 2, ERRBIT_PARAM = 4 };
+
+struct SegTable {
+  int32_t n;                              // S
+  int32_t off[WM_MAX_SEGMENTS + 1];
+};
+
+// Device-resident model (one allocation, carved up).
+struct DevModel {
+  wm_dims dims;
+  int prec;                 // wm_precision
+  uint8_t* base;            // the allocation
+  const uint8_t* trans;     // H/32 transition chunks
+  const uint8_t* cost;      // C/32 cost chunks
+  const float* roll_tab;    // type_emb [K][E], param_w^T [P][E], param_b [E], b2 (acc order) [D]
+  const float* emb_nat;     // type_emb [K][E], param_w^T [P][E], param_b [E]
+  const float* enc_w1t;     // We1^T [F][Fh] (bf16-rounded values in bf16 mode)
+  const float* enc_b1;      // [Fh]
+  const float* enc_w2t;     // We2^T [Fh][D]
+  const float* enc_b2;      // [D]
+  float bc2;
+  int trans_chunk_bytes, cost_chunk_bytes, roll_tab_bytes;
+};
+
+// Launchers (wm_kernels.hip).  Return hipSuccess or the launch error.
+hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
+                         int2* perm, int32_t* err, hipStream_t st);
+hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
+                          const int32_t* types, const int32_t* params, const int32_t* lens,
+                          int32_t B, int32_t T_max, float* zT, int32_t* err, hipStream_t st);
+hipError_t launch_phi(const DevModel& m, const int32_t* types, const int32_t* params,
+                      const int32_t* lens, int32_t B, int32_t T_max, float* phi, hipStream_t st);
+hipError_t launch_score(const DevModel& m, const float* zT, const float* phi, int32_t B,
+                        const float* hw, int32_t n_hw, float* scores, hipStream_t st);
+hipError_t launch_topk(const float* scores, int32_t n_hw, int32_t B, const SegTable& seg,
+                       int32_t k, int32_t* idx, float* val, hipStream_t st);
+hipError_t launch_encode(const DevModel& m, const float* feats, int32_t S, float* z0,
+                         hipStream_t st);
+
+// Whether a (precision, d, e) combination has rollout/score kernels.
+bool have_kernels(int prec, int d, int e);
+// LDS bytes the rollout kernel needs for a model (0 if unsupported).
+int rollout_lds_bytes(const DevModel& m);
+
+// Kernel-family timing hooks (wm_api.hip).
+enum TimedKernel { TK_ROLLOUT = 0, TK_SCORE = 1, TK_TOPK = 2, TK_BUCKET = 3, TK_PHI = 4, TK_ENCODE = 5, TK_COUNT = 6 };
+void timing_begin(int kernel, hipStream_t st);
+void timing_end(int kernel, hipStream_t st);
+
+}  // namespace wm

@@ -1,0 +1,850 @@
+// Hand-written gfx950 kernels of the batched latent-rollout evaluator.
+//
+//  bucket_kernel   counting sort of candidates by action-sequence length
+//                  (longest first), length validation, subgraph lookup
+//  rollout_kernel  the multi-step transition z <- z + W2 GELU(W1 [z; e] + b1) + b2
+//                  (Eq. 1, Sec. 3.4), persistent over all steps of a tile of
+//                  32 candidates per wavefront, latent kept in registers,
+//                  weights streamed through LDS, matrix cores for both products
+//  phi_kernel      mean action embedding (action features, Sec. 3.5)
+//  score_kernel    cost model y = wc2 GELU(Wc1 [z_T; phi; h] + bc1) + bc2 (Eq. 3)
+//  encode_kernel   initial latents from program features (Sec. 3.3, Eq. 4)
+//  topk_kernel     per (hardware vector, subgraph) top-k by (-y, index)
+//                  (Sec. 3.5): radix select + bitonic sort in LDS
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "wm_internal.h"
+
+namespace wm {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// --------------------------------------------------------------------------
+// Precision traits: operand fragment type, conversion, matrix-core product.
+
+struct PBF16 : GeomBF16 {
+  using Frag = bf16x8;
+  static __device__ __forceinline__ f32x16 mfma(Frag a, Frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  // 8 floats -> 8 bf16 (round to nearest even)
+  static __device__ __forceinline__ Frag cvt(const float* v) {
+    Frag f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] = (__bf16)v[j];
+    return f;
+  }
+  // fragment `w` (0 <= w < G) of a 16-byte lane group
+  static __device__ __forceinline__ Frag pick(u32x4 g, int) { return __builtin_bit_cast(Frag, g); }
+};
+
+struct PF32 : GeomF32 {
+  using Frag = float;
+  static __device__ __forceinline__ f32x16 mfma(Frag a, Frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ Frag cvt(const float* v) { return v[0]; }
+  // Copy the element out first: a bit_cast applied directly to a vector
+  // element expression lowers to element 0 whatever the index.
+  static __device__ __forceinline__ Frag pick(u32x4 g, int w) {
+    const uint32_t u = g[w];
+    return __uint_as_float(u);
+  }
+};
+
+// GELU with the exact Gaussian CDF (device erff).
+__device__ __forceinline__ float gelu(float x) {
+  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+}
+
+__device__ __forceinline__ u32x4 lds_group(const uint8_t* base, int group, int lane) {
+  return *reinterpret_cast<const u32x4*>(base + group * 1024 + lane * 16);
+}
+
+// Copy `bytes` (multiple of 16) from global memory into LDS with the
+// direct global->LDS path: every lane moves 16 bytes, a wavefront fills 1 KiB
+// at LDS address base + lane*16.  Completion is tracked by vmcnt.
+__device__ __forceinline__ void stage_to_lds(const uint8_t* __restrict__ src, uint8_t* dst,
+                                             int bytes, int tid, int nthreads) {
+  const int units = bytes >> 4;
+  const int wave_base = tid & ~63;
+  for (int u0 = 0; u0 < units; u0 += nthreads) {
+    const int u = u0 + tid;
+    if (u < units) {
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(src + (size_t)u * 16),
+          (__attribute__((address_space(3))) void*)(dst + (size_t)(u0 + wave_base) * 16), 16, 0, 0);
+    }
+  }
+}
+
+__device__ __forceinline__ void wait_vm_then_barrier() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's global->LDS copies landed
+  __syncthreads();
+}
+
+__device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+// Subgraph of candidate i: the largest s with off[s] <= i.
+__device__ __forceinline__ int segment_of(const SegTable& seg, int i) {
+  int lo = 0, hi = seg.n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (seg.off[mid] <= i) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// ==========================================================================
+// Bucketing: one workgroup sorts all candidates by length, longest first.
+// perm[pos] = (candidate, subgraph).  Candidates are independent, so the order
+// within one length bucket does not affect any result.
+
+__global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict__ lens, int B,
+                                                       int T_max, const SegTable seg,
+                                                       int2* __restrict__ perm,
+                                                       int32_t* __restrict__ err) {
+  extern __shared__ int bsm[];
+  int* hist = bsm;
+  int* cur = bsm + (T_max + 1);
+  const int tid = threadIdx.x, nt = blockDim.x;
+  for (int i = tid; i <= T_max; i += nt) hist[i] = 0;
+  __syncthreads();
+  int bad = 0;
+  for (int i = tid; i < B; i += nt) {
+    int L = lens[i];
+    if (L < 0 || L > T_max) { bad = 1; L = clampi(L, 0, T_max); }
+    atomicAdd(&hist[L], 1);
+  }
+  if (bad) atomicOr(err, ERRBIT_LEN);
+  __syncthreads();
+  if (tid == 0) {
+    int acc = 0;
+    for (int L = T_max; L >= 0; --L) { cur[L] = acc; acc += hist[L]; }
+  }
+  __syncthreads();
+  for (int i = tid; i < B; i += nt) {
+    const int L = clampi(lens[i], 0, T_max);
+    const int pos = atomicAdd(&cur[L], 1);
+    perm[pos] = make_int2(i, segment_of(seg, i));
+  }
+}
+
+// ==========================================================================
+// Rollout.
+//
+// Workgroup = WAVES wavefronts; wavefront w owns the 32 candidates at sorted
+// positions [32*(WAVES*blockIdx.x + w), +32): lane L works on candidate
+// column L%32 together with lane L^32.  All wavefronts of a workgroup walk the
+// same sequence of 32-hidden-unit weight chunks, double-buffered in LDS, for
+// T_wg steps (T_wg = longest sequence of the workgroup; sorted order keeps
+// the tiles of a workgroup of similar length).  A candidate past its own
+// length keeps z unchanged: its GELU outputs and b2 are zeroed, so the second
+// product adds exact zeros.
+
+struct RollArgs {
+  const uint8_t* trans;     // packed transition chunks
+  const float* tab;         // rollout table (see DevModel::roll_tab)
+  const float* z0;          // [S][D]
+  const int2* perm;         // sorted (candidate, subgraph)
+  const int32_t* types;     // [B][T_max]
+  const int32_t* params;    // [B][T_max][P]
+  const int32_t* lens;      // [B]
+  float* zT;                // [B][D]
+  int32_t* err;
+  int B, T_max, P, K, H, chunk_bytes, tab_bytes;
+};
+
+// One 32-hidden-unit chunk of a transition step for one wavefront: reads
+// the chunk from `cur` while the workgroup's copy of the next chunk lands in
+// `nxt` (distinct LDS objects, so the compiler need not wait for that copy
+// before reading `cur`).
+template <class PR, int D, int E>
+struct RollStep {
+  using Frag = typename PR::Frag;
+  static constexpr int KF = PR::KF, SL = PR::SL, G = PR::G;
+  static constexpr int NZ = D / KF, NE = E / KF, NK1 = NZ + NE;
+  static constexpr int NF2 = 32 / KF, NB = D / 32;
+  static constexpr int CB = TransChunk<PR>::bytes(D, E);
+
+  static __device__ __forceinline__ void chunk(const uint8_t* cur, const Frag (&xz)[NZ],
+                                               const Frag (&xe)[NE], f32x16 (&zacc)[NB],
+                                               float actf, int lane, int h) {
+    // G^T chunk = W1[chunk] . X^T
+    f32x16 acc1 = {};
+#pragma unroll
+    for (int g = 0; g < NK1 / G; ++g) {
+      const u32x4 grp = lds_group(cur, g, lane);
+#pragma unroll
+      for (int w = 0; w < G; ++w) {
+        const int kf = g * G + w;
+        acc1 = PR::mfma(PR::pick(grp, w), kf < NZ ? xz[kf < NZ ? kf : 0] : xe[kf < NZ ? 0 : kf - NZ], acc1);
+      }
+    }
+    // bias + GELU; a finished candidate multiplies by 0 (exact zeros in dZ)
+    const float* b1t = reinterpret_cast<const float*>(cur + (CB - 128)) + 16 * h;
+    float bb[16];
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(b1t + 4 * r4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) bb[4 * r4 + i] = v[i];
+    }
+    Frag gf[NF2];
+#pragma unroll
+    for (int f = 0; f < NF2; ++f) {
+      float v[SL];
+#pragma unroll
+      for (int j = 0; j < SL; ++j) {
+        const int r = f * SL + j;
+        v[j] = gelu(acc1[r] + bb[r]) * actf;
+      }
+      gf[f] = PR::cvt(v);
+    }
+    // dZ^T += W2[:, chunk] . G^T
+#pragma unroll
+    for (int g = 0; g < (NB * NF2) / G; ++g) {
+      const u32x4 grp = lds_group(cur, NK1 / G + g, lane);
+#pragma unroll
+      for (int w = 0; w < G; ++w) {
+        const int F = g * G + w;
+        zacc[F / NF2] = PR::mfma(PR::pick(grp, w), gf[F % NF2], zacc[F / NF2]);
+      }
+    }
+  }
+};
+
+template <class PR, int D, int E, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a) {
+  using RS = RollStep<PR, D, E>;
+  using Frag = typename PR::Frag;
+  constexpr int KF = PR::KF, SL = PR::SL;
+  constexpr int NZ = RS::NZ, NE = RS::NE, NF2 = RS::NF2, NB = RS::NB, CB = RS::CB;
+  constexpr int NT = 64 * WAVES;
+  static_assert(RS::NK1 % PR::G == 0 && (NB * NF2) % PR::G == 0, "fragment groups");
+
+  __shared__ __attribute__((aligned(1024))) uint8_t bufA[CB];
+  __shared__ __attribute__((aligned(1024))) uint8_t bufB[CB];
+  extern __shared__ __attribute__((aligned(16))) float tab[];
+  const float* t_emb = tab;                       // [K][E]
+  const float* t_pw = tab + a.K * E;              // [P][E]
+  const float* t_pb = t_pw + a.P * E;             // [E]
+  const float* t_b2 = t_pb + E;                   // [NB][2][16] accumulator order
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, h = lane >> 5;
+  const int NC = a.H / 32;                        // even (checked on the host)
+
+  // Tables and the first weight chunk.
+  stage_to_lds(reinterpret_cast<const uint8_t*>(a.tab), reinterpret_cast<uint8_t*>(tab),
+               a.tab_bytes, tid, NT);
+  stage_to_lds(a.trans, bufA, CB, tid, NT);
+
+  const int pos = (blockIdx.x * WAVES + wave) * 32 + n;
+  const bool valid = pos < a.B;
+  const int2 pc = valid ? a.perm[pos] : make_int2(0, 0);
+  const int cand = pc.x;
+  const int len = valid ? clampi(a.lens[cand], 0, a.T_max) : 0;
+  // Longest sequence in the workgroup: its first sorted position.
+  const int T_wg = __builtin_amdgcn_readfirstlane(
+      clampi(a.lens[a.perm[blockIdx.x * WAVES * 32].x], 0, a.T_max));
+
+  // Latent in accumulator layout.
+  f32x16 zacc[NB];
+  {
+    const float* zs = a.z0 + (size_t)pc.y * D;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(zs + 32 * b + acc_row(h, 4 * r4));
+#pragma unroll
+        for (int i = 0; i < 4; ++i) zacc[b][4 * r4 + i] = v[i];
+      }
+  }
+
+  // Action of the current step (prefetched one step ahead).
+  const int32_t* ty_row = a.types + (size_t)cand * a.T_max;
+  const int32_t* pa_row = a.params + (size_t)cand * a.T_max * a.P;
+  int nx_type = 0;
+  int nx_par[8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p) nx_par[p] = 1;
+  if (0 < len) {
+    nx_type = ty_row[0];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) if (p < a.P) nx_par[p] = pa_row[p];
+  }
+  int errbits = 0;
+
+  wait_vm_then_barrier();
+
+  const int total_chunks = T_wg * NC;
+  int gch = 0;  // global chunk counter (step * NC + chunk); even at every step start
+  for (int t = 0; t < T_wg; ++t) {
+    const bool active = t < len;
+    const float actf = active ? 1.0f : 0.0f;
+    // ---- action embedding e_t for features KF*q + SL*h + j
+    float u[8];
+    int ty = 0;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) u[p] = 0.0f;
+    if (active) {
+      ty = nx_type;
+      if (ty < 0 || ty >= a.K) { errbits |= ERRBIT_TYPE; ty = 0; }
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        if (p < a.P) {
+          if (nx_par[p] < 1) errbits |= ERRBIT_PARAM;
+          u[p] = log2f((float)nx_par[p]);
+        }
+      }
+    }
+    if (t + 1 < len) {   // prefetch the next action
+      nx_type = ty_row[t + 1];
+#pragma unroll
+      for (int p = 0; p < 8; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(t + 1) * a.P + p];
+    }
+    Frag xe[NE];
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      const int f0 = KF * q + SL * h;
+      float ev[SL];
+#pragma unroll
+      for (int j = 0; j < SL; ++j) ev[j] = t_emb[ty * E + f0 + j];
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        if (p < a.P) {
+#pragma unroll
+          for (int j = 0; j < SL; ++j) ev[j] = fmaf(t_pw[p * E + f0 + j], u[p], ev[j]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + t_pb[f0 + j]) * actf;
+      xe[q] = PR::cvt(ev);
+    }
+    // ---- z operand fragments (state at the start of the step)
+    Frag xz[NZ];
+#pragma unroll
+    for (int kf = 0; kf < NZ; ++kf) {
+      float v[SL];
+#pragma unroll
+      for (int j = 0; j < SL; ++j) v[j] = zacc[kf / NF2][(kf % NF2) * SL + j];
+      xz[kf] = PR::cvt(v);
+    }
+
+    for (int c = 0; c < NC; c += 2, gch += 2) {
+      // chunk c from bufA while chunk c+1 lands in bufB
+      stage_to_lds(a.trans + (size_t)(c + 1) * CB, bufB, CB, tid, NT);
+      __builtin_amdgcn_sched_barrier(0);
+      RS::chunk(bufA, xz, xe, zacc, actf, lane, h);
+      wait_vm_then_barrier();
+      // chunk c+1 from bufB while the following chunk lands in bufA
+      if (gch + 2 < total_chunks) {
+        const int nc = (c + 2 == NC) ? 0 : c + 2;
+        stage_to_lds(a.trans + (size_t)nc * CB, bufA, CB, tid, NT);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      RS::chunk(bufB, xz, xe, zacc, actf, lane, h);
+      wait_vm_then_barrier();
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) zacc[b][r] += t_b2[(b * 2 + h) * 16 + r] * actf;
+  }
+  if (errbits) atomicOr(a.err, errbits);
+
+  if (valid) {
+    float* zo = a.zT + (size_t)cand * D;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        f32x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = zacc[b][4 * r4 + i];
+        *reinterpret_cast<f32x4*>(zo + 32 * b + acc_row(h, 4 * r4)) = v;
+      }
+  }
+}
+
+// ==========================================================================
+// Action features: phi_i = (1/len_i) sum_t e_t.  One thread per
+// (candidate, 4 features).
+
+__global__ __launch_bounds__(256) void phi_kernel(const float* __restrict__ emb,
+                                                   const int32_t* __restrict__ types,
+                                                   const int32_t* __restrict__ params,
+                                                   const int32_t* __restrict__ lens, int B,
+                                                   int T_max, int E, int P, int K,
+                                                   float* __restrict__ phi) {
+  const int per = E / 4;
+  const int gid = blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= B * per) return;
+  const int i = gid / per, f0 = (gid % per) * 4;
+  const float* t_emb = emb;
+  const float* t_pw = emb + K * E;
+  const float* t_pb = t_pw + P * E;
+  const int len = clampi(lens[i], 0, T_max);
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < len; ++t) {
+    const int ty = clampi(types[(size_t)i * T_max + t], 0, K - 1);
+    float s[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s[q] = t_emb[ty * E + f0 + q];
+    for (int p = 0; p < P; ++p) {
+      const float u = log2f((float)params[((size_t)i * T_max + t) * P + p]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s[q] = fmaf(t_pw[p * E + f0 + q], u, s[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[q] += s[q] + t_pb[f0 + q];
+  }
+  const float inv = len > 0 ? 1.0f / (float)len : 0.0f;
+  f32x4 o;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) o[q] = len > 0 ? acc[q] * inv : 0.0f;
+  *reinterpret_cast<f32x4*>(phi + (size_t)i * E + f0) = o;
+}
+
+// ==========================================================================
+// Cost model.  Wavefront = 32 candidates (original order), workgroup walks
+// the 32-wide chunks of the cost hidden layer with Wc1 fragments staged in
+// LDS.  The [z_T; phi] product is shared by all hardware vectors; each vector
+// adds its own small product.  Up to 4 hardware vectors per launch.
+
+constexpr int SCORE_MAX_HW = 32;        // hardware-vector width limit
+constexpr int SCORE_HW_PER_LAUNCH = 2;  // hardware vectors per score launch
+
+struct ScoreArgs {
+  const uint8_t* cost;
+  const float* zT;
+  const float* phi;
+  const float* hw;    // [n_hw][HW]
+  float* scores;      // [n_hw][B]
+  float bc2;
+  int B, C, HW, j0, nj, chunk_bytes;
+};
+
+template <class PR, int D, int E>
+struct ScoreStep {
+  using Frag = typename PR::Frag;
+  static constexpr int KF = PR::KF, SL = PR::SL, G = PR::G;
+  static constexpr int NX = (D + E) / KF;
+  static constexpr int MAXH = SCORE_MAX_HW / KF;
+
+  static __device__ __forceinline__ void chunk(const uint8_t* cur, int CB, int NH, int nj,
+                                               const Frag (&x)[NX],
+                                               const Frag (&hf)[SCORE_HW_PER_LAUNCH][MAXH],
+                                               float (&part)[SCORE_HW_PER_LAUNCH], int lane, int h) {
+    f32x16 acc = {};
+#pragma unroll
+    for (int g = 0; g < NX / G; ++g) {
+      const u32x4 grp = lds_group(cur, g, lane);
+#pragma unroll
+      for (int w = 0; w < G; ++w) acc = PR::mfma(PR::pick(grp, w), x[g * G + w], acc);
+    }
+    const float* tail = reinterpret_cast<const float*>(cur + (CB - 256));
+    const float* bc1t = tail + 16 * h;
+    const float* wc2t = tail + 32 + 16 * h;
+#pragma unroll
+    for (int jj = 0; jj < SCORE_HW_PER_LAUNCH; ++jj) {
+      if (jj < nj) {
+        f32x16 accj = acc;
+#pragma unroll
+        for (int q = 0; q < MAXH; ++q) {
+          if (q < NH) {
+            const int F = NX + q;
+            accj = PR::mfma(PR::pick(lds_group(cur, F / G, lane), F % G), hf[jj][q], accj);
+          }
+        }
+        float s = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s = fmaf(wc2t[r], gelu(accj[r] + bc1t[r]), s);
+        part[jj] += s;
+      }
+    }
+  }
+};
+
+template <class PR, int D, int E, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 1) void score_kernel(const ScoreArgs a) {
+  using SS = ScoreStep<PR, D, E>;
+  using Frag = typename PR::Frag;
+  constexpr int KF = PR::KF, SL = PR::SL;
+  constexpr int NX = SS::NX, MAXH = SS::MAXH;
+  constexpr int NT = 64 * WAVES;
+  constexpr int CBMAX = CostChunk<PR>::bytes(D, E, SCORE_MAX_HW);
+  __shared__ __attribute__((aligned(1024))) uint8_t bufA[CBMAX];
+  __shared__ __attribute__((aligned(1024))) uint8_t bufB[CBMAX];
+  const int CB = a.chunk_bytes;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, h = lane >> 5;
+  const int NH = a.HW / KF;
+  const int NC = a.C / 32;                        // even (checked on the host)
+
+  stage_to_lds(a.cost, bufA, CB, tid, NT);
+
+  const int cand = (blockIdx.x * WAVES + wave) * 32 + n;
+  const bool valid = cand < a.B;
+  const int ci = valid ? cand : 0;
+
+  Frag x[NX];
+#pragma unroll
+  for (int kf = 0; kf < NX; ++kf) {
+    float v[SL];
+#pragma unroll
+    for (int j = 0; j < SL; ++j) {
+      const int f = nat_feature<PR>(kf, h, j);
+      v[j] = f < D ? a.zT[(size_t)ci * D + f] : a.phi[(size_t)ci * E + (f - D)];
+    }
+    x[kf] = PR::cvt(v);
+  }
+  Frag hf[SCORE_HW_PER_LAUNCH][MAXH];
+#pragma unroll
+  for (int jj = 0; jj < SCORE_HW_PER_LAUNCH; ++jj)
+#pragma unroll
+    for (int q = 0; q < MAXH; ++q) {
+      float v[SL];
+#pragma unroll
+      for (int j = 0; j < SL; ++j)
+        v[j] = (jj < a.nj && q < NH) ? a.hw[(size_t)(a.j0 + jj) * a.HW + nat_feature<PR>(q, h, j)] : 0.0f;
+      hf[jj][q] = PR::cvt(v);
+    }
+  float part[SCORE_HW_PER_LAUNCH];
+#pragma unroll
+  for (int jj = 0; jj < SCORE_HW_PER_LAUNCH; ++jj) part[jj] = 0.0f;
+
+  wait_vm_then_barrier();
+  for (int c = 0; c < NC; c += 2) {
+    stage_to_lds(a.cost + (size_t)(c + 1) * CB, bufB, CB, tid, NT);
+    __builtin_amdgcn_sched_barrier(0);
+    SS::chunk(bufA, CB, NH, a.nj, x, hf, part, lane, h);
+    wait_vm_then_barrier();
+    if (c + 2 < NC) stage_to_lds(a.cost + (size_t)(c + 2) * CB, bufA, CB, tid, NT);
+    __builtin_amdgcn_sched_barrier(0);
+    SS::chunk(bufB, CB, NH, a.nj, x, hf, part, lane, h);
+    wait_vm_then_barrier();
+  }
+#pragma unroll
+  for (int jj = 0; jj < SCORE_HW_PER_LAUNCH; ++jj) {
+    if (jj < a.nj) {
+      const float y = part[jj] + __shfl_xor(part[jj], 32) + a.bc2;
+      if (valid && h == 0) a.scores[(size_t)(a.j0 + jj) * a.B + cand] = y;
+    }
+  }
+}
+
+// ==========================================================================
+// Encoder: one workgroup per subgraph.  In bf16 mode the input and the hidden
+// layer are rounded to bf16 (the weights already are).
+
+__global__ __launch_bounds__(256) void encode_kernel(const float* __restrict__ feats,
+                                                      const float* __restrict__ w1t,
+                                                      const float* __restrict__ b1,
+                                                      const float* __restrict__ w2t,
+                                                      const float* __restrict__ b2, int F,
+                                                      int Fh, int D, int bf16,
+                                                      float* __restrict__ z0) {
+  extern __shared__ float esm[];
+  float* xs = esm;        // [F]
+  float* hs = esm + F;    // [Fh]
+  const int s = blockIdx.x;
+  for (int f = threadIdx.x; f < F; f += blockDim.x) {
+    const float v = feats[(size_t)s * F + f];
+    xs[f] = bf16 ? (float)(__bf16)v : v;
+  }
+  __syncthreads();
+  for (int o = threadIdx.x; o < Fh; o += blockDim.x) {
+    float acc = 0.0f;
+    for (int f = 0; f < F; ++f) acc = fmaf(w1t[(size_t)f * Fh + o], xs[f], acc);
+    const float g = gelu(acc + b1[o]);
+    hs[o] = bf16 ? (float)(__bf16)g : g;
+  }
+  __syncthreads();
+  for (int o = threadIdx.x; o < D; o += blockDim.x) {
+    float acc = 0.0f;
+    for (int k = 0; k < Fh; ++k) acc = fmaf(w2t[(size_t)k * D + o], hs[k], acc);
+    z0[(size_t)s * D + o] = acc + b2[o];
+  }
+}
+
+// ==========================================================================
+// Top-k per (hardware vector j, subgraph s): one workgroup of 1024 threads.
+//
+// Scores map to order-preserving unsigned keys (NaN lowest, -0 == +0).  A
+// most-significant-digit radix select finds the k-th largest key K*; a second
+// radix select over the (complemented) local index finds how many candidates
+// tied at K* to keep, lowest index first.  The k selected candidates are then
+// bitonic-sorted in LDS by the 64-bit key (score key, ~index).
+
+__device__ __forceinline__ uint32_t score_key(float v) {
+  if (v != v) return 0u;                // NaN ranks last
+  if (v == 0.0f) v = 0.0f;              // -0 == +0
+  const uint32_t u = __float_as_uint(v);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+constexpr int TOPK_THREADS = 1024;
+constexpr int TOPK_WAVES = TOPK_THREADS / 64;
+
+// Largest-first radix select over keys key(i) of the elements with pred(i):
+// returns the `need`-th largest key (1-based) and, in *rank_in_eq, how many
+// elements equal to it must be taken.
+template <class KeyF, class PredF>
+__device__ uint32_t radix_select(int n, int need, KeyF key, PredF pred, uint32_t* hist_w,
+                                 int* shared_int, int* rank_in_eq) {
+  const int tid = threadIdx.x, wave = tid >> 6;
+  uint32_t prefix = 0, mask = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = tid; i < TOPK_WAVES * 256; i += TOPK_THREADS) hist_w[i] = 0;
+    __syncthreads();
+    for (int i = tid; i < n; i += TOPK_THREADS) {
+      if (pred(i)) {
+        const uint32_t kk = key(i);
+        if ((kk & mask) == prefix) atomicAdd(&hist_w[wave * 256 + ((kk >> shift) & 255)], 1u);
+      }
+    }
+    __syncthreads();
+    // combine the per-wave histograms into the first
+    for (int b = tid; b < 256; b += TOPK_THREADS) {
+      uint32_t s = 0;
+      for (int w = 0; w < TOPK_WAVES; ++w) s += hist_w[w * 256 + b];
+      hist_w[b] = s;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int rem = need, digit = 0;
+      for (int b = 255; b >= 0; --b) {
+        const int c = (int)hist_w[b];
+        if (c >= rem) { digit = b; break; }
+        rem -= c;
+      }
+      shared_int[0] = digit;
+      shared_int[1] = rem;
+    }
+    __syncthreads();
+    const int digit = shared_int[0];
+    need = shared_int[1];
+    prefix |= (uint32_t)digit << shift;
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  *rank_in_eq = need;
+  return prefix;
+}
+
+__global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const float* __restrict__ scores,
+                                                            int B, const SegTable seg, int k,
+                                                            int P2, int32_t* __restrict__ idx,
+                                                            float* __restrict__ val) {
+  __shared__ uint32_t hist_w[TOPK_WAVES * 256];
+  __shared__ unsigned long long sel[WM_MAX_K];
+  __shared__ int sh[4];
+  const int S = seg.n;
+  const int j = blockIdx.x / S, s = blockIdx.x % S;
+  const int lo = seg.off[s], hi = seg.off[s + 1], n = hi - lo;
+  const float* y = scores + (size_t)j * B + lo;
+  const int tid = threadIdx.x;
+
+  int need_eq = 0;
+  const uint32_t kstar = radix_select(
+      n, k, [&](int i) { return score_key(y[i]); }, [](int) { return true; }, hist_w, sh,
+      &need_eq);
+  // count of keys equal to K*
+  if (tid == 0) { sh[2] = 0; sh[3] = 0; }
+  __syncthreads();
+  int my_eq = 0;
+  for (int i = tid; i < n; i += TOPK_THREADS) my_eq += (score_key(y[i]) == kstar);
+  if (my_eq) atomicAdd(&sh[2], my_eq);
+  __syncthreads();
+  const int n_eq = sh[2];
+  // ties at K*: keep the need_eq lowest local indices (largest ~index)
+  uint32_t istar = 0;
+  if (need_eq < n_eq) {
+    int dummy = 0;
+    istar = radix_select(
+        n, need_eq, [](int i) { return ~(uint32_t)i; },
+        [&](int i) { return score_key(y[i]) == kstar; }, hist_w, sh, &dummy);
+  }
+  const uint32_t ilimit = (need_eq < n_eq) ? ~istar : 0xFFFFFFFFu;  // keep local index <= ilimit
+  if (tid == 0) sh[3] = 0;
+  for (int i = tid; i < P2; i += TOPK_THREADS) sel[i] = 0ull;
+  __syncthreads();
+  for (int i = tid; i < n; i += TOPK_THREADS) {
+    const uint32_t kk = score_key(y[i]);
+    if (kk > kstar || (kk == kstar && (uint32_t)i <= ilimit)) {
+      const int slot = atomicAdd(&sh[3], 1);
+      if (slot < k) sel[slot] = ((unsigned long long)kk << 32) | (unsigned long long)(~(uint32_t)i);
+    }
+  }
+  __syncthreads();
+  // bitonic sort, descending
+  for (int size = 2; size <= P2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < P2; i += TOPK_THREADS) {
+        const int partner = i ^ stride;
+        if (partner > i) {
+          const bool desc = (i & size) == 0;
+          const unsigned long long a0 = sel[i], a1 = sel[partner];
+          if (desc ? (a0 < a1) : (a0 > a1)) { sel[i] = a1; sel[partner] = a0; }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int r = tid; r < k; r += TOPK_THREADS) {
+    const int li = (int)(~(uint32_t)(sel[r] & 0xFFFFFFFFull));
+    const size_t o = ((size_t)j * S + s) * k + r;
+    idx[o] = lo + li;
+    if (val) val[o] = y[li];
+  }
+}
+
+// ==========================================================================
+// Launchers.
+
+namespace {
+
+
+template <class PR, int D, int E, int WAVES>
+hipError_t launch_rollout_t(const DevModel& m, const RollArgs& a, int blocks, hipStream_t st) {
+  const int lds = m.roll_tab_bytes;   // the two chunk buffers are static
+  auto kern = rollout_kernel<PR, D, E, WAVES>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * WAVES), lds, st, a);
+  return hipGetLastError();
+}
+
+template <class PR, int D, int E, int WAVES>
+hipError_t launch_score_t(const DevModel& m, const ScoreArgs& a, int blocks, hipStream_t st) {
+  const int lds = 0;                  // static chunk buffers
+  auto kern = score_kernel<PR, D, E, WAVES>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * WAVES), lds, st, a);
+  return hipGetLastError();
+}
+
+// Wavefronts per workgroup: as many as keep at least one workgroup per
+// compute unit (256), so small batches spread over more units.
+inline int pick_waves(int tiles) {
+  if (tiles >= 4 * 256) return 4;
+  if (tiles >= 2 * 256) return 2;
+  return 1;
+}
+
+// Instantiated (precision, d, e).  fp32 keeps z and its operand copy in
+// registers (d floats per lane pair), which caps it at d = 256.
+#define WM_CASE(P, PRT, D, E, CALL) \
+  if (prec == P && d == D && e == E) { using PR = PRT; CALL(PR, D, E); }
+
+#define WM_FOR_ALL_DE(CALL)                 \
+  WM_CASE(WM_FP32, PF32, 64, 32, CALL)      \
+  WM_CASE(WM_FP32, PF32, 256, 64, CALL)     \
+  WM_CASE(WM_BF16, PBF16, 64, 32, CALL)     \
+  WM_CASE(WM_BF16, PBF16, 256, 64, CALL)    \
+  WM_CASE(WM_BF16, PBF16, 512, 128, CALL)
+
+}  // namespace
+
+bool have_kernels(int prec, int d, int e) {
+#define WM_HAVE(PR, D, E) return true;
+  WM_FOR_ALL_DE(WM_HAVE)
+#undef WM_HAVE
+  return false;
+}
+
+int rollout_lds_bytes(const DevModel& m) { return 2 * m.trans_chunk_bytes + m.roll_tab_bytes; }
+
+hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
+                         int2* perm, int32_t* err, hipStream_t st) {
+  const int lds = 2 * (T_max + 1) * (int)sizeof(int);
+  hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(1024), lds, st, lens, B, T_max, seg, perm, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
+                          const int32_t* types, const int32_t* params, const int32_t* lens,
+                          int32_t B, int32_t T_max, float* zT, int32_t* err, hipStream_t st) {
+  RollArgs a;
+  a.trans = m.trans; a.tab = m.roll_tab; a.z0 = z0; a.perm = perm; a.types = types;
+  a.params = params; a.lens = lens; a.zT = zT; a.err = err; a.B = B; a.T_max = T_max;
+  a.P = m.dims.n_params; a.K = m.dims.n_kinds; a.H = m.dims.trans_hidden;
+  a.chunk_bytes = m.trans_chunk_bytes; a.tab_bytes = m.roll_tab_bytes;
+  const int tiles = (B + 31) / 32;
+  const int waves = pick_waves(tiles);
+  const int blocks = (tiles + waves - 1) / waves;
+  const int prec = m.prec, d = m.dims.d, e = m.dims.embed_dim;
+#define WM_ROLL(PR, D, E)                                                         \
+  {                                                                               \
+    if (waves == 4) return launch_rollout_t<PR, D, E, 4>(m, a, blocks, st);       \
+    if (waves == 2) return launch_rollout_t<PR, D, E, 2>(m, a, blocks, st);       \
+    return launch_rollout_t<PR, D, E, 1>(m, a, blocks, st);                       \
+  }
+  WM_FOR_ALL_DE(WM_ROLL)
+#undef WM_ROLL
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_phi(const DevModel& m, const int32_t* types, const int32_t* params,
+                      const int32_t* lens, int32_t B, int32_t T_max, float* phi, hipStream_t st) {
+  const int E = m.dims.embed_dim;
+  const long long threads = (long long)B * (E / 4);
+  const int blocks = (int)((threads + 255) / 256);
+  hipLaunchKernelGGL(phi_kernel, dim3(blocks), dim3(256), 0, st, m.emb_nat, types, params, lens,
+                     B, T_max, E, m.dims.n_params, m.dims.n_kinds, phi);
+  return hipGetLastError();
+}
+
+hipError_t launch_score(const DevModel& m, const float* zT, const float* phi, int32_t B,
+                        const float* hw, int32_t n_hw, float* scores, hipStream_t st) {
+  const int tiles = (B + 31) / 32;
+  const int waves = pick_waves(tiles);
+  const int blocks = (tiles + waves - 1) / waves;
+  const int prec = m.prec, d = m.dims.d, e = m.dims.embed_dim;
+  for (int j0 = 0; j0 < n_hw; j0 += SCORE_HW_PER_LAUNCH) {
+    ScoreArgs a;
+    a.cost = m.cost; a.zT = zT; a.phi = phi; a.hw = hw; a.scores = scores; a.bc2 = m.bc2;
+    a.B = B; a.C = m.dims.cost_hidden; a.HW = m.dims.hw_dim; a.j0 = j0;
+    a.nj = (n_hw - j0) < SCORE_HW_PER_LAUNCH ? (n_hw - j0) : SCORE_HW_PER_LAUNCH;
+    a.chunk_bytes = m.cost_chunk_bytes;
+    hipError_t err = hipErrorInvalidValue;
+#define WM_SCORE(PR, D, E)                                                       \
+  {                                                                              \
+    if (waves == 4) err = launch_score_t<PR, D, E, 4>(m, a, blocks, st);         \
+    else if (waves == 2) err = launch_score_t<PR, D, E, 2>(m, a, blocks, st);    \
+    else err = launch_score_t<PR, D, E, 1>(m, a, blocks, st);                    \
+  }
+    WM_FOR_ALL_DE(WM_SCORE)
+#undef WM_SCORE
+    if (err != hipSuccess) return err;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_topk(const float* scores, int32_t n_hw, int32_t B, const SegTable& seg,
+                       int32_t k, int32_t* idx, float* val, hipStream_t st) {
+  int P2 = 1;
+  while (P2 < k) P2 <<= 1;
+  hipLaunchKernelGGL(topk_kernel, dim3(n_hw * seg.n), dim3(TOPK_THREADS), 0, st, scores, B, seg,
+                     k, P2, idx, val);
+  return hipGetLastError();
+}
+
+hipError_t launch_encode(const DevModel& m, const float* feats, int32_t S, float* z0,
+                         hipStream_t st) {
+  const int F = m.dims.feat_dim, Fh = m.dims.enc_hidden, D = m.dims.d;
+  const int lds = (F + Fh) * (int)sizeof(float);
+  hipLaunchKernelGGL(encode_kernel, dim3(S), dim3(256), lds, st, feats, m.enc_w1t, m.enc_b1,
+                     m.enc_w2t, m.enc_b2, F, Fh, D, m.prec == WM_BF16 ? 1 : 0, z0);
+  return hipGetLastError();
+}
+
+}  // namespace wm

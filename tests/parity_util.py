@@ -1,0 +1,115 @@
+"""Helpers shared by the GPU parity tests: running the HIP path through the
+C ABI on seeded inputs and comparing with the oracle.
+
+Comparison rules (tolerances from the evaluator's accuracy target: 1e-4
+relative in fp32, 2e-2 relative in bf16):
+  * terminal latents: per candidate ||g - o||_2 / ||o||_2 <= tol;
+  * scores: |g - o| / max(|o|, rms of the segment's oracle scores) <= tol;
+  * top-k: with delta = tol * max(|s_k|, rms), the selected set must equal
+    the oracle's whenever the oracle gap s_k - s_{k+1} exceeds delta, rank r
+    must match wherever both neighbouring gaps exceed delta, and any index
+    outside the oracle set must score within delta of s_k.  Independently, the
+    returned order must be exactly the order of the GPU's own scores by
+    (-score, index).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
+
+
+def to_dev(I, dev):
+    import torch
+    return {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in I.items() if k != "seg_off"}
+
+
+def run_evaluate(model, w, I, k, dev="cuda", scores=True, zT=True):
+    """wm_evaluate on the inputs; returns numpy outputs and the device status."""
+    import torch
+    import paper_2606_09312_amd as wm
+    t = to_dev(I, dev)
+    init = t["feats"] if "feats" in t else t["z0"]
+    B = I["lens"].shape[0]
+    n_hw = I["hw"].shape[0]
+    sc = torch.empty((n_hw, B), dtype=torch.float32, device=dev) if scores else None
+    z = torch.empty((B, w.d), dtype=torch.float32, device=dev) if zT else None
+    out = wm.evaluate(model, init, I["seg_off"], t["types"], t["params"], t["lens"], t["hw"], k,
+                      init_is_feats="feats" in t, scores=sc, zT=z)
+    status = 0
+    try:
+        wm.device_status(out["ws"])
+    except wm.WMError as e:
+        status = e.status
+    res = {"idx": out["idx"].cpu().numpy(), "val": out["val"].cpu().numpy(), "status": status}
+    if scores:
+        res["scores"] = sc.cpu().numpy().astype(np.float64)
+    if zT:
+        res["zT"] = z.cpu().numpy().astype(np.float64)
+    return res
+
+
+def latent_rel(g, o):
+    num = np.linalg.norm(g - o, axis=1)
+    den = np.maximum(np.linalg.norm(o, axis=1), 1e-30)
+    return num / den
+
+
+def score_rel(g, o, seg_off):
+    g = np.atleast_2d(g)
+    o = np.atleast_2d(o)
+    out = np.zeros_like(o)
+    for s in range(len(seg_off) - 1):
+        lo, hi = seg_off[s], seg_off[s + 1]
+        if hi == lo:
+            continue
+        rms = np.sqrt(np.mean(o[:, lo:hi] ** 2, axis=1, keepdims=True))
+        out[:, lo:hi] = np.abs(g[:, lo:hi] - o[:, lo:hi]) / np.maximum(np.abs(o[:, lo:hi]), np.maximum(rms, 1e-30))
+    return out
+
+
+def check_topk_self_consistent(idx, val, scores, seg_off, k):
+    """Returned order == exact (-score, index) order of the GPU's own scores."""
+    scores = np.atleast_2d(scores)
+    for j in range(idx.shape[0]):
+        for s in range(len(seg_off) - 1):
+            lo, hi = seg_off[s], seg_off[s + 1]
+            y = scores[j, lo:hi].astype(np.float32).astype(np.float64)
+            nan = np.isnan(y)
+            want = lo + np.lexsort((np.arange(hi - lo), np.where(nan, 0.0, -y), nan))[:k]
+            np.testing.assert_array_equal(idx[j, s], want)
+            np.testing.assert_array_equal(val[j, s], scores[j, idx[j, s]].astype(np.float32))
+
+
+def check_topk_vs_oracle(idx, oracle_scores, seg_off, k, tol):
+    o = np.atleast_2d(oracle_scores)
+    for j in range(idx.shape[0]):
+        for s in range(len(seg_off) - 1):
+            lo, hi = seg_off[s], seg_off[s + 1]
+            y = o[j, lo:hi]
+            order = np.lexsort((np.arange(hi - lo), -y))
+            rms = np.sqrt(np.mean(y ** 2))
+            sk = y[order[k - 1]]
+            delta = tol * max(abs(sk), rms)
+            gpu = np.asarray(idx[j, s]) - lo
+            ref_set = set(order[:k].tolist())
+            if k < hi - lo and sk - y[order[k]] > delta:
+                assert set(gpu.tolist()) == ref_set, f"top-k set differs (hw {j}, seg {s})"
+            for i in gpu.tolist():
+                if i not in ref_set:
+                    assert abs(y[i] - sk) <= delta, f"index {i} outside the oracle top-k"
+            ys = y[order]
+            for r in range(k):
+                left = ys[r - 1] - ys[r] if r > 0 else np.inf
+                right = ys[r] - ys[r + 1] if r + 1 < hi - lo else np.inf
+                if left > delta and right > delta:
+                    assert gpu[r] == order[r], f"rank {r} differs (hw {j}, seg {s})"
+
+
+def sub_batch(I, pick, seg_of, z0_full):
+    """Candidates `pick` as a batch of their own, one subgraph each."""
+    n = len(pick)
+    return {
+        "types": I["types"][pick], "params": I["params"][pick], "lens": I["lens"][pick],
+        "hw": I["hw"], "z0": z0_full[seg_of[pick]], "seg_off": np.arange(n + 1, dtype=np.int32),
+    }

@@ -1,0 +1,291 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on
+identical seeded inputs, for every workload shape and precision, plus the
+degenerate cases of the method."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import wm_oracle as O
+
+from parity_util import (TOL, check_topk_self_consistent, check_topk_vs_oracle, latent_rel,
+                         run_evaluate, score_rel, sub_batch, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def wm():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_09312_amd as wm
+    wm.load_library()
+    return wm
+
+
+_models = {}
+
+
+def model_for(wm, name, prec, w=None, seed=1000):
+    key = (name, prec, seed, None if w is None else (w.d, w.e, w.H, w.C))
+    if key not in _models:
+        w = w or synth.workload(name)
+        W = synth.make_weights(w, seed)
+        _models[key] = (wm.Model(wm.model_dims(w), W, precision=prec), W)
+    return _models[key]
+
+
+# (workload, precision, B, S): several 32-candidate tiles and a ragged tail,
+# small enough for the float64 oracle to finish in seconds.
+CASES = [
+    ("tiny", "fp32", 300, 1),
+    ("tiny", "bf16", 300, 1),
+    ("ansor_round", "fp32", 300, 1),
+    ("ansor_round", "bf16", 300, 1),
+    ("long_schedule", "bf16", 270, 1),
+    ("large_latent", "bf16", 150, 1),
+    ("multi_subgraph", "bf16", 4 * 70, 4),
+]
+
+
+@pytest.mark.parametrize("name,prec,B,S", CASES)
+def test_parity_scaled(wm, name, prec, B, S):
+    base = synth.workload(name)
+    w = synth.scaled(base, B=B, S=S)
+    k = min(base.k, B // S)
+    print(f"[parity] {name} {prec} B={B} S={S} k={k}", flush=True)
+    model, W = model_for(wm, name, prec)
+    I = synth.make_inputs(w, 2000 + B, pad="garbage")
+    g = run_evaluate(model, w, I, k)
+    assert g["status"] == 0
+    ref = O.evaluate(W, I, k, prec)
+    tol = TOL[prec]
+    rel = latent_rel(g["zT"], ref["zT"])
+    assert rel.max() <= tol, f"z_T rel err {rel.max():.3e}"
+    srel = score_rel(g["scores"], ref["scores"], I["seg_off"])
+    assert srel.max() <= tol, f"score rel err {srel.max():.3e}"
+    check_topk_self_consistent(g["idx"], g["val"], g["scores"], I["seg_off"], k)
+    check_topk_vs_oracle(g["idx"], ref["scores"], I["seg_off"], k, tol)
+    print(f"  z_T max rel {rel.max():.2e}, score max rel {srel.max():.2e}", flush=True)
+
+
+# Full-size workloads in the benchmark's launch configuration; the oracle
+# recomputes a sample of candidates one by one.
+FULL = [("tiny", "fp32"), ("ansor_round", "fp32"), ("ansor_round", "bf16"),
+        ("long_schedule", "bf16"), ("large_latent", "bf16"), ("multi_subgraph", "bf16")]
+
+
+@pytest.mark.parametrize("name,prec", FULL)
+def test_parity_full_size_sampled(wm, name, prec):
+    w = synth.workload(name)
+    print(f"[full] {name} {prec} B={w.B}", flush=True)
+    model, W = model_for(wm, name, prec)
+    I = synth.make_inputs(w, 2000)
+    g = run_evaluate(model, w, I, w.k)
+    assert g["status"] == 0
+    check_topk_self_consistent(g["idx"], g["val"], g["scores"], I["seg_off"], w.k)
+    rng = np.random.default_rng(7)
+    # longest and shortest sequences plus random ones
+    order = np.argsort(I["lens"], kind="stable")
+    pick = np.unique(np.concatenate([order[:4], order[-4:], rng.choice(w.B, 16, replace=False)]))
+    Wd = O.prepare(W, prec)
+    z0 = O.encode(Wd, I["feats"], prec) if "feats" in I else I["z0"].astype(np.float64)
+    seg_of = O.segment_of(I["seg_off"], w.B)
+    sb = sub_batch(I, pick, seg_of, z0)
+    zT, phi = O.rollout(Wd, sb["z0"], sb["seg_off"], sb["types"], sb["params"], sb["lens"], prec)
+    y = O.score(Wd, zT, phi, I["hw"], prec)
+    tol = TOL[prec]
+    rel = latent_rel(g["zT"][pick], zT)
+    assert rel.max() <= tol, f"z_T rel err {rel.max():.3e}"
+    # scale for scores: rms of the GPU scores of each sampled candidate's segment
+    seg_rms = np.array([[np.sqrt(np.mean(g["scores"][j, I["seg_off"][s]:I["seg_off"][s + 1]] ** 2))
+                         for s in seg_of[pick]] for j in range(w.n_hw)])
+    srel = np.abs(g["scores"][:, pick] - y) / np.maximum(np.abs(y), seg_rms)
+    assert srel.max() <= tol, f"score rel err {srel.max():.3e}"
+    print(f"  sampled {len(pick)}: z_T max rel {rel.max():.2e}, score max rel {srel.max():.2e}",
+          flush=True)
+
+
+# --------------------------------------------------------------------------
+# Degenerate and edge cases
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_zero_length_returns_initial_state(wm, prec):
+    w = synth.scaled(synth.workload("ansor_round"), B=70)
+    model, W = model_for(wm, "ansor_round", prec)
+    I = synth.make_inputs(w, 5, pad="garbage")
+    I["lens"][:] = 0
+    g = run_evaluate(model, w, I, 8)
+    assert g["status"] == 0
+    np.testing.assert_array_equal(g["zT"], np.broadcast_to(I["z0"][0], g["zT"].shape))
+    ref = O.evaluate(W, I, 8, prec)
+    assert score_rel(g["scores"], ref["scores"], I["seg_off"]).max() <= TOL[prec]
+
+
+def test_all_full_length_and_single_candidate(wm):
+    w = synth.scaled(synth.workload("tiny"), B=65, len_lo=8, len_hi=8)
+    model, W = model_for(wm, "tiny", "fp32")
+    I = synth.make_inputs(w, 9)
+    assert (I["lens"] == w.T_max).all()
+    g = run_evaluate(model, w, I, 5)
+    ref = O.evaluate(W, I, 5, "fp32")
+    assert latent_rel(g["zT"], ref["zT"]).max() <= 1e-4
+    w1 = synth.scaled(w, B=1)
+    I1 = {k: (v[:1] if k in ("types", "params", "lens") else v) for k, v in I.items()}
+    I1["seg_off"] = np.array([0, 1], np.int32)
+    g1 = run_evaluate(model, w1, I1, 1)
+    assert g1["idx"][0, 0, 0] == 0
+    np.testing.assert_array_equal(g1["zT"][0], g["zT"][0])   # candidates are independent
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_duplicates_tie_to_lower_index_and_full_segment(wm, prec):
+    w = synth.scaled(synth.workload("tiny"), B=40)
+    model, W = model_for(wm, "tiny", prec)
+    I = synth.make_inputs(w, 11, pad="garbage")
+    for dst, src in ((7, 3), (30, 3), (12, 25)):
+        for key in ("types", "params", "lens"):
+            I[key][dst] = I[key][src]
+    g = run_evaluate(model, w, I, w.B)          # k = whole segment
+    s = g["scores"][0]
+    assert s[7] == s[3] and s[30] == s[3] and s[12] == s[25]
+    order = list(g["idx"][0, 0])
+    assert order.index(3) < order.index(7) < order.index(30)
+    assert order.index(12) < order.index(25) or s[12] != s[25]
+    assert sorted(order) == list(range(w.B))
+    check_topk_self_consistent(g["idx"], g["val"], g["scores"], I["seg_off"], w.B)
+
+
+def test_one_segment_per_candidate(wm):
+    base = synth.workload("tiny")
+    w = synth.scaled(base, B=48, S=48)
+    model, W = model_for(wm, "tiny", "fp32")
+    I = synth.make_inputs(w, 13)
+    g = run_evaluate(model, w, I, 1)
+    np.testing.assert_array_equal(g["idx"][0, :, 0], np.arange(48))
+    ref = O.evaluate(W, I, 1, "fp32")
+    assert latent_rel(g["zT"], ref["zT"]).max() <= 1e-4
+
+
+def test_multi_segment_multi_hw_ragged_segments(wm):
+    w = synth.scaled(synth.workload("multi_subgraph"), B=200, S=1)
+    model, W = model_for(wm, "multi_subgraph", "bf16")
+    I = synth.make_inputs(w, 17, pad="garbage")
+    I["seg_off"] = np.array([0, 37, 40, 111, 200], np.int32)
+    I["feats"] = np.abs(np.random.default_rng(3).standard_normal((4, w.feat_dim))).astype(np.float32)
+    k = 3
+    g = run_evaluate(model, w, I, k)
+    ref = O.evaluate(W, I, k, "bf16")
+    assert latent_rel(g["zT"], ref["zT"]).max() <= 2e-2
+    assert score_rel(g["scores"], ref["scores"], I["seg_off"]).max() <= 2e-2
+    check_topk_self_consistent(g["idx"], g["val"], g["scores"], I["seg_off"], k)
+    check_topk_vs_oracle(g["idx"], ref["scores"], I["seg_off"], k, 2e-2)
+
+
+@pytest.mark.parametrize("what", ["len_high", "len_negative", "type", "param"])
+def test_device_error_word(wm, what):
+    w = synth.scaled(synth.workload("tiny"), B=64)
+    model, W = model_for(wm, "tiny", "fp32")
+    I = synth.make_inputs(w, 19, pad="garbage")
+    I["lens"][5] = 3
+    if what == "len_high":
+        I["lens"][9] = w.T_max + 1
+    elif what == "len_negative":
+        I["lens"][9] = -2
+    elif what == "type":
+        I["types"][5, 2] = w.n_kinds
+    else:
+        I["params"][5, 1, 0] = 0
+    g = run_evaluate(model, w, I, 4)
+    assert g["status"] == 5
+    assert O.validate({"n_kinds": w.n_kinds}, B=w.B, T_max=w.T_max, seg_off=I["seg_off"],
+                      types=I["types"], params=I["params"], lens=I["lens"]) == O.ERR_INPUT_RANGE
+    # the word was cleared: a clean batch reports OK
+    I2 = synth.make_inputs(w, 19, pad="garbage")
+    assert run_evaluate(model, w, I2, 4)["status"] == 0
+
+
+def test_empty_batch_rollout(wm):
+    model, W = model_for(wm, "tiny", "fp32")
+    dev = "cuda"
+    z0 = torch.zeros((1, 64), device=dev)
+    empty_i = torch.zeros((0, 8), dtype=torch.int32, device=dev)
+    params = torch.zeros((0, 8, 4), dtype=torch.int32, device=dev)
+    lens = torch.zeros((0,), dtype=torch.int32, device=dev)
+    zT = torch.zeros((0, 64), device=dev)
+    ws = model.workspace(0, 8, 1, 1)
+    wm.rollout(model, z0, [0, 0], empty_i, params, lens, zT, None, ws)
+    wm.device_status(ws)
+
+
+def test_deterministic_and_permutation_invariant(wm):
+    w = synth.scaled(synth.workload("ansor_round"), B=500)
+    model, W = model_for(wm, "ansor_round", "bf16")
+    I = synth.make_inputs(w, 23, pad="garbage")
+    a = run_evaluate(model, w, I, 16)
+    b = run_evaluate(model, w, I, 16)
+    for key in ("zT", "scores", "idx", "val"):
+        np.testing.assert_array_equal(a[key], b[key])
+    p = np.random.default_rng(1).permutation(w.B)
+    Ip = dict(I, types=I["types"][p], params=I["params"][p], lens=I["lens"][p])
+    c = run_evaluate(model, w, Ip, 16)
+    np.testing.assert_array_equal(c["zT"], a["zT"][p])
+    np.testing.assert_array_equal(c["scores"], a["scores"][:, p])
+
+
+def test_separate_entry_points_match_fused(wm):
+    w = synth.scaled(synth.workload("multi_subgraph"), B=256, S=4)
+    model, W = model_for(wm, "multi_subgraph", "bf16")
+    I = synth.make_inputs(w, 29)
+    k = 8
+    fused = run_evaluate(model, w, I, k)
+    dev = "cuda"
+    t = to_dev(I, dev)
+    z0 = torch.empty((w.S, w.d), device=dev)
+    wm.encode_init(model, t["feats"], z0)
+    ref_z0 = O.encode(O.prepare(W, "bf16"), I["feats"], "bf16")
+    assert latent_rel(z0.cpu().numpy().astype(np.float64), ref_z0).max() <= 2e-2
+    zT = torch.empty((w.B, w.d), device=dev)
+    phi = torch.empty((w.B, w.e), device=dev)
+    ws = model.workspace(w.B, w.T_max, w.S, w.n_hw)
+    wm.rollout(model, z0, I["seg_off"], t["types"], t["params"], t["lens"], zT, phi, ws)
+    sc = torch.empty((w.n_hw, w.B), device=dev)
+    wm.score(model, zT, phi, t["hw"], sc)
+    idx = torch.empty((w.n_hw, w.S, k), dtype=torch.int32, device=dev)
+    val = torch.empty((w.n_hw, w.S, k), device=dev)
+    wm.topk(sc, I["seg_off"], k, idx, val)
+    wm.device_status(ws)
+    np.testing.assert_array_equal(zT.cpu().numpy(), fused["zT"].astype(np.float32))
+    np.testing.assert_array_equal(sc.cpu().numpy(), fused["scores"].astype(np.float32))
+    np.testing.assert_array_equal(idx.cpu().numpy(), fused["idx"])
+    ref = O.evaluate(W, I, k, "bf16")
+    assert np.abs(phi.cpu().numpy() - ref["phi"]).max() <= 1e-4 * max(1.0, np.abs(ref["phi"]).max())
+
+
+def test_topk_entry_point_edge_scores(wm):
+    dev = "cuda"
+    y = np.array([[1.0, 3.0, 3.0, np.nan, -0.0, 0.0, 3.0, -np.inf, np.inf, 2.0]], np.float32)
+    sc = torch.from_numpy(y).to(dev)
+    idx = torch.empty((1, 1, 10), dtype=torch.int32, device=dev)
+    val = torch.empty((1, 1, 10), device=dev)
+    wm.topk(sc, [0, 10], 10, idx, val)
+    torch.cuda.synchronize()
+    ref_idx, _ = O.topk(y.astype(np.float64), [0, 10], 10)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
+    # large segment with many exact ties: compare with the oracle's brute-force order
+    rng = np.random.default_rng(2)
+    y2 = np.round(rng.standard_normal((2, 70000)), 2).astype(np.float32)
+    sc2 = torch.from_numpy(y2).to(dev)
+    seg = [0, 1000, 1001, 70000]
+    idx2 = torch.empty((2, 3, 1), dtype=torch.int32, device=dev)
+    wm.topk(sc2, seg, 1, idx2)
+    ref2, _ = O.topk(y2.astype(np.float64), seg, 1)
+    np.testing.assert_array_equal(idx2.cpu().numpy(), ref2)
+    idx3 = torch.empty((2, 1, 700), dtype=torch.int32, device=dev)
+    val3 = torch.empty((2, 1, 700), device=dev)
+    wm.topk(sc2, [0, 70000], 700, idx3, val3)
+    ref3, rv3 = O.topk(y2.astype(np.float64), [0, 70000], 700)
+    np.testing.assert_array_equal(idx3.cpu().numpy(), ref3)
+    np.testing.assert_array_equal(val3.cpu().numpy(), rv3.astype(np.float32))
