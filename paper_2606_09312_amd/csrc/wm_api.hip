@@ -66,35 +66,37 @@ void put(std::vector<uint8_t>& blk, size_t base, int F, int lane, int j, float v
 
 void put_f32(std::vector<uint8_t>& blk, size_t off, float v) { std::memcpy(&blk[off], &v, 4); }
 
-// Transition chunks: for hidden chunk c, [W1 fragments][W2 fragments][b1 tail].
+// Transition chunks: for hidden chunk c, a W1 part [W1 fragments][b1 tail]
+// and a W2 part [W2 fragments], in two arrays.
 template <class Gm>
-std::vector<uint8_t> pack_transition(const wm_dims& dm, const wm_weights& w) {
+void pack_transition(const wm_dims& dm, const wm_weights& w, std::vector<uint8_t>& w1blk,
+                     std::vector<uint8_t>& w2blk) {
   const int D = dm.d, E = dm.embed_dim, H = dm.trans_hidden, IN = D + E;
-  const int CB = TransChunk<Gm>::bytes(D, E), NK1 = TransChunk<Gm>::nk1(D, E);
-  const int NF2 = 32 / Gm::KF, NG = TransChunk<Gm>::ngroups(D, E);
-  std::vector<uint8_t> blk((size_t)(H / 32) * CB, 0);
+  const int B1 = TransChunk<Gm>::w1_bytes(D, E), B2 = TransChunk<Gm>::w2_bytes(D);
+  const int NK1 = TransChunk<Gm>::nk1(D, E), NF2 = 32 / Gm::KF;
+  w1blk.assign((size_t)(H / 32) * B1, 0);
+  w2blk.assign((size_t)(H / 32) * B2, 0);
   for (int c = 0; c < H / 32; ++c) {
-    const size_t base = (size_t)c * CB;
+    const size_t base1 = (size_t)c * B1, base2 = (size_t)c * B2;
     for (int kf = 0; kf < NK1; ++kf)
       for (int L = 0; L < 64; ++L)
         for (int j = 0; j < Gm::SL; ++j) {
           const int m = L & 31, h = L >> 5;
           const int feat = x_feature<Gm>(D, kf, h, j);
-          put<Gm>(blk, base, kf, L, j, w.w1[(size_t)(32 * c + m) * IN + feat]);
+          put<Gm>(w1blk, base1, kf, L, j, w.w1[(size_t)(32 * c + m) * IN + feat]);
         }
+    for (int h = 0; h < 2; ++h)
+      for (int r = 0; r < 16; ++r)
+        put_f32(w1blk, base1 + (size_t)(B1 - 128) + (size_t)(h * 16 + r) * 4, w.b1[32 * c + acc_row(h, r)]);
     for (int db = 0; db < D / 32; ++db)
       for (int f = 0; f < NF2; ++f)
         for (int L = 0; L < 64; ++L)
           for (int j = 0; j < Gm::SL; ++j) {
             const int m = L & 31, h = L >> 5;
             const int hid = 32 * c + g_feature<Gm>(f, h, j);
-            put<Gm>(blk, base, NK1 + db * NF2 + f, L, j, w.w2[(size_t)(32 * db + m) * H + hid]);
+            put<Gm>(w2blk, base2, db * NF2 + f, L, j, w.w2[(size_t)(32 * db + m) * H + hid]);
           }
-    for (int h = 0; h < 2; ++h)
-      for (int r = 0; r < 16; ++r)
-        put_f32(blk, base + (size_t)NG * 1024 + (size_t)(h * 16 + r) * 4, w.b1[32 * c + acc_row(h, r)]);
   }
-  return blk;
 }
 
 // Cost chunks: for cost hidden chunk c, [Wc1 fragments][bc1 tail][wc2 tail].
@@ -236,26 +238,28 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.dims = dm;
   m.prec = dm.precision;
   const int D = dm.d, E = dm.embed_dim, K = dm.n_kinds, P = dm.n_params, HW = dm.hw_dim;
-  std::vector<uint8_t> trans, cost;
+  std::vector<uint8_t> tw1, tw2, cost;
   if (m.prec == WM_BF16) {
-    trans = pack_transition<GeomBF16>(dm, *w);
+    pack_transition<GeomBF16>(dm, *w, tw1, tw2);
     cost = pack_cost<GeomBF16>(dm, *w);
-    m.trans_chunk_bytes = TransChunk<GeomBF16>::bytes(D, E);
+    m.w1_chunk_bytes = TransChunk<GeomBF16>::w1_bytes(D, E);
+    m.w2_chunk_bytes = TransChunk<GeomBF16>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomBF16>::bytes(D, E, HW);
   } else {
     if ((D + E + HW) % 8 != 0) return fail(WM_ERR_UNSUPPORTED, "fp32 needs d + embed_dim + hw_dim % 8 == 0");
-    trans = pack_transition<GeomF32>(dm, *w);
+    pack_transition<GeomF32>(dm, *w, tw1, tw2);
     cost = pack_cost<GeomF32>(dm, *w);
-    m.trans_chunk_bytes = TransChunk<GeomF32>::bytes(D, E);
+    m.w1_chunk_bytes = TransChunk<GeomF32>::w1_bytes(D, E);
+    m.w2_chunk_bytes = TransChunk<GeomF32>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomF32>::bytes(D, E, HW);
   }
-  // rollout table: type_emb [K][E], param_w^T [P][E], param_b [E], b2 (accumulator order)
+  // rollout table: type_emb [K][E], param_w^T [PMAX][E], param_b [E], b2 (accumulator order)
   std::vector<float> tab;
-  tab.reserve((size_t)K * E + (size_t)P * E + E + D + 4);
+  tab.reserve((size_t)K * E + (size_t)PMAX * E + E + D + 4);
   for (int k = 0; k < K; ++k)
     for (int f = 0; f < E; ++f) tab.push_back(w->type_emb[(size_t)k * E + f]);
-  for (int p = 0; p < P; ++p)
-    for (int f = 0; f < E; ++f) tab.push_back(w->param_w[(size_t)f * P + p]);
+  for (int p = 0; p < PMAX; ++p)
+    for (int f = 0; f < E; ++f) tab.push_back(p < P ? w->param_w[(size_t)f * P + p] : 0.0f);
   for (int f = 0; f < E; ++f) tab.push_back(w->param_b[f]);
   for (int b = 0; b < D / 32; ++b)
     for (int h = 0; h < 2; ++h)
@@ -284,7 +288,8 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   }
 
   size_t off = 0;
-  const size_t o_trans = off; off = align256(off + trans.size());
+  const size_t o_tw1 = off; off = align256(off + tw1.size());
+  const size_t o_tw2 = off; off = align256(off + tw2.size());
   const size_t o_cost = off; off = align256(off + cost.size());
   const size_t o_tab = off; off = align256(off + tab.size() * 4);
   const size_t o_enc = off; off = align256(off + enc.size() * 4);
@@ -294,7 +299,8 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
     return fail(WM_ERR_OUT_OF_MEMORY, "hipMalloc of the model failed");
   }
   uint8_t* base = static_cast<uint8_t*>(dev);
-  hipError_t e = hipMemcpy(base + o_trans, trans.data(), trans.size(), hipMemcpyHostToDevice);
+  hipError_t e = hipMemcpy(base + o_tw1, tw1.data(), tw1.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(base + o_tw2, tw2.data(), tw2.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_cost, cost.data(), cost.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_tab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess && !enc.empty()) e = hipMemcpy(base + o_enc, enc.data(), enc.size() * 4, hipMemcpyHostToDevice);
@@ -303,7 +309,8 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
     return fail(WM_ERR_DEVICE, std::string("hipMemcpy: ") + hipGetErrorString(e));
   }
   m.base = base;
-  m.trans = base + o_trans;
+  m.trans_w1 = base + o_tw1;
+  m.trans_w2 = base + o_tw2;
   m.cost = base + o_cost;
   m.roll_tab = reinterpret_cast<const float*>(base + o_tab);
   m.emb_nat = m.roll_tab;

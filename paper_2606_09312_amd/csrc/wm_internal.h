@@ -83,15 +83,18 @@ __host__ __device__ constexpr inline int frag_offset(int F, int lane, int j) {
   return (F / Gm::G) * 1024 + lane * 16 + ((F % Gm::G) * Gm::SL + j) * Gm::ES;
 }
 
-// Chunk geometry of the transition weights: one chunk = 32 hidden units,
-// [W1 fragments (NK1)][W2 fragments (D/32 blocks x 32/KF)][b1 tail: 32 floats
-// in accumulator order].
+// Chunk geometry of the transition weights: chunk c covers hidden units
+// [32c, 32c+32).  Its W1 part is [NK1 fragments over the (D+E) inputs][b1
+// tail: 32 floats in accumulator order]; its W2 part is [D/32 blocks x 32/KF
+// fragments].  The two parts are stored in two arrays and staged separately
+// (the rollout kernel overlaps one chunk's second product with the next
+// chunk's first product).
 template <class Gm>
 struct TransChunk {
   static constexpr int nk1(int D, int E) { return (D + E) / Gm::KF; }
-  static constexpr int nfrags(int D, int E) { return nk1(D, E) + (D / 32) * (32 / Gm::KF); }
-  static constexpr int ngroups(int D, int E) { return nfrags(D, E) / Gm::G; }
-  static constexpr int bytes(int D, int E) { return ngroups(D, E) * 1024 + 128; }
+  static constexpr int nk2(int D) { return (D / 32) * (32 / Gm::KF); }
+  static constexpr int w1_bytes(int D, int E) { return nk1(D, E) / Gm::G * 1024 + 128; }
+  static constexpr int w2_bytes(int D) { return nk2(D) / Gm::G * 1024; }
 };
 
 // Chunk geometry of the cost-model first layer: one chunk = 32 hidden units,
@@ -103,6 +106,10 @@ struct CostChunk {
   static constexpr int ngroups(int D, int E, int HW) { return nfrags(D, E, HW) / Gm::G; }
   static constexpr int bytes(int D, int E, int HW) { return ngroups(D, E, HW) * 1024 + 256; }
 };
+
+// Action parameters per step are padded to PMAX in the embedding table
+// (zero weights), so the kernels loop over a fixed count.
+constexpr int PMAX = 8;
 
 // Device error bits (workspace error word).
 enum : int { ERRBIT_LEN = 1, ERRBIT_TYPE = 2, ERRBIT_PARAM = 4 };
@@ -117,16 +124,17 @@ struct DevModel {
   wm_dims dims;
   int prec;                 // wm_precision
   uint8_t* base;            // the allocation
-  const uint8_t* trans;     // H/32 transition chunks
+  const uint8_t* trans_w1;  // H/32 transition chunks, W1 part
+  const uint8_t* trans_w2;  // H/32 transition chunks, W2 part
   const uint8_t* cost;      // C/32 cost chunks
-  const float* roll_tab;    // type_emb [K][E], param_w^T [P][E], param_b [E], b2 (acc order) [D]
-  const float* emb_nat;     // type_emb [K][E], param_w^T [P][E], param_b [E]
+  const float* roll_tab;    // type_emb [K][E], param_w^T [PMAX][E] (zero rows past P), param_b [E], b2 (acc order) [D]
+  const float* emb_nat;     // the first three parts of roll_tab
   const float* enc_w1t;     // We1^T [F][Fh] (bf16-rounded values in bf16 mode)
   const float* enc_b1;      // [Fh]
   const float* enc_w2t;     // We2^T [Fh][D]
   const float* enc_b2;      // [D]
   float bc2;
-  int trans_chunk_bytes, cost_chunk_bytes, roll_tab_bytes;
+  int w1_chunk_bytes, w2_chunk_bytes, cost_chunk_bytes, roll_tab_bytes;
 };
 
 // Launchers (wm_kernels.hip).  Return hipSuccess or the launch error.

@@ -56,9 +56,23 @@ struct PF32 : GeomF32 {
   }
 };
 
-// GELU with the exact Gaussian CDF (device erff).
+// GELU(x) = x * Phi(x), Phi(x) = (1 + erf(x / sqrt 2)) / 2, with erf from
+// Abramowitz & Stegun, Handbook of Mathematical Functions, formula 7.1.26:
+//   erf(a) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-a^2),
+//   t = 1 / (1 + p a),  a >= 0,  |error| <= 1.5e-7,
+// extended to negative arguments by oddness.  Branch-free: one reciprocal,
+// one exp2 and a handful of multiply-adds.
 __device__ __forceinline__ float gelu(float x) {
-  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+  const float a = fabsf(x) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, a, 1.0f));
+  float p = fmaf(1.061405429f, t, -1.453152027f);
+  p = fmaf(p, t, 1.421413741f);
+  p = fmaf(p, t, -0.284496736f);
+  p = fmaf(p, t, 0.254829592f);
+  p *= t;
+  const float ex = __builtin_amdgcn_exp2f(-1.4426950408889634f * a * a);
+  const float erf_a = fmaf(-p, ex, 1.0f);             // erf(|x| / sqrt 2)
+  return x * (0.5f + copysignf(0.5f * erf_a, x));
 }
 
 __device__ __forceinline__ u32x4 lds_group(const uint8_t* base, int group, int lane) {
@@ -79,6 +93,26 @@ __device__ __forceinline__ void stage_to_lds(const uint8_t* __restrict__ src, ui
           (const void*)(src + (size_t)u * 16),
           (__attribute__((address_space(3))) void*)(dst + (size_t)(u0 + wave_base) * 16), 16, 0, 0);
     }
+  }
+}
+
+// Same copy with a compile-time size: straight-line code, one guarded tail.
+template <int BYTES, int NT>
+__device__ __forceinline__ void stage_fixed(const uint8_t* __restrict__ src, uint8_t* dst, int tid) {
+  static_assert(BYTES % 16 == 0, "16-byte units");
+  constexpr int UNITS = BYTES / 16, FULL = UNITS / NT;
+  const int wave_base = tid & ~63;
+#pragma unroll
+  for (int i = 0; i < FULL; ++i) {
+    __builtin_amdgcn_global_load_lds(
+        (const void*)(src + (size_t)(i * NT + tid) * 16),
+        (__attribute__((address_space(3))) void*)(dst + (size_t)(i * NT + wave_base) * 16), 16, 0, 0);
+  }
+  if constexpr (UNITS % NT != 0) {
+    if (FULL * NT + tid < UNITS)
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(src + (size_t)(FULL * NT + tid) * 16),
+          (__attribute__((address_space(3))) void*)(dst + (size_t)(FULL * NT + wave_base) * 16), 16, 0, 0);
   }
 }
 
@@ -147,7 +181,8 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
 // product adds exact zeros.
 
 struct RollArgs {
-  const uint8_t* trans;     // packed transition chunks
+  const uint8_t* w1;        // packed transition chunks, W1 part
+  const uint8_t* w2;        // packed transition chunks, W2 part
   const float* tab;         // rollout table (see DevModel::roll_tab)
   const float* z0;          // [S][D]
   const int2* perm;         // sorted (candidate, subgraph)
@@ -156,59 +191,62 @@ struct RollArgs {
   const int32_t* lens;      // [B]
   float* zT;                // [B][D]
   int32_t* err;
-  int B, T_max, P, K, H, chunk_bytes, tab_bytes;
+  int B, T_max, P, K, H, tab_bytes;
 };
 
-// One 32-hidden-unit chunk of a transition step for one wavefront: reads
-// the chunk from `cur` while the workgroup's copy of the next chunk lands in
-// `nxt` (distinct LDS objects, so the compiler need not wait for that copy
-// before reading `cur`).
+// Per-wavefront pieces of one transition step.  Chunk c covers hidden units
+// [32c, 32c+32): gemm1 forms G^T[chunk] = b1 + W1[chunk] . X^T in accumulator
+// layout, gelu_frags turns it into the B operand of the second product, and
+// gemm2 accumulates dZ^T += W2[:, chunk] . G^T into the latent.
 template <class PR, int D, int E>
-struct RollStep {
+struct Roll {
   using Frag = typename PR::Frag;
   static constexpr int KF = PR::KF, SL = PR::SL, G = PR::G;
   static constexpr int NZ = D / KF, NE = E / KF, NK1 = NZ + NE;
-  static constexpr int NF2 = 32 / KF, NB = D / 32;
-  static constexpr int CB = TransChunk<PR>::bytes(D, E);
+  static constexpr int NF2 = 32 / KF, NB = D / 32, NK2 = NB * NF2;
+  static constexpr int W1B = TransChunk<PR>::w1_bytes(D, E);
+  static constexpr int W2B = TransChunk<PR>::w2_bytes(D);
+  static_assert(NK1 % G == 0 && NK2 % G == 0, "fragment groups");
 
-  static __device__ __forceinline__ void chunk(const uint8_t* cur, const Frag (&xz)[NZ],
-                                               const Frag (&xe)[NE], f32x16 (&zacc)[NB],
-                                               float actf, int lane, int h) {
-    // G^T chunk = W1[chunk] . X^T
-    f32x16 acc1 = {};
-#pragma unroll
-    for (int g = 0; g < NK1 / G; ++g) {
-      const u32x4 grp = lds_group(cur, g, lane);
-#pragma unroll
-      for (int w = 0; w < G; ++w) {
-        const int kf = g * G + w;
-        acc1 = PR::mfma(PR::pick(grp, w), kf < NZ ? xz[kf < NZ ? kf : 0] : xe[kf < NZ ? 0 : kf - NZ], acc1);
-      }
-    }
-    // bias + GELU; a finished candidate multiplies by 0 (exact zeros in dZ)
-    const float* b1t = reinterpret_cast<const float*>(cur + (CB - 128)) + 16 * h;
-    float bb[16];
+  static __device__ __forceinline__ f32x16 gemm1(const uint8_t* w1, const Frag (&xz)[NZ],
+                                                 const Frag (&xe)[NE], int lane, int h) {
+    f32x16 acc;
+    const float* b1t = reinterpret_cast<const float*>(w1 + (W1B - 128)) + 16 * h;
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
       const f32x4 v = *reinterpret_cast<const f32x4*>(b1t + 4 * r4);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) bb[4 * r4 + i] = v[i];
+      for (int i = 0; i < 4; ++i) acc[4 * r4 + i] = v[i];
     }
-    Frag gf[NF2];
+#pragma unroll
+    for (int g = 0; g < NK1 / G; ++g) {
+      const u32x4 grp = lds_group(w1, g, lane);
+#pragma unroll
+      for (int w = 0; w < G; ++w) {
+        const int kf = g * G + w;
+        acc = PR::mfma(PR::pick(grp, w), kf < NZ ? xz[kf < NZ ? kf : 0] : xe[kf < NZ ? 0 : kf - NZ], acc);
+      }
+    }
+    return acc;
+  }
+
+  // GELU of the first product; a finished candidate (actf = 0) contributes
+  // exact zeros to the second product.
+  static __device__ __forceinline__ void gelu_frags(const f32x16& acc, float actf, Frag (&gf)[NF2]) {
 #pragma unroll
     for (int f = 0; f < NF2; ++f) {
       float v[SL];
 #pragma unroll
-      for (int j = 0; j < SL; ++j) {
-        const int r = f * SL + j;
-        v[j] = gelu(acc1[r] + bb[r]) * actf;
-      }
+      for (int j = 0; j < SL; ++j) v[j] = gelu(acc[f * SL + j]) * actf;
       gf[f] = PR::cvt(v);
     }
-    // dZ^T += W2[:, chunk] . G^T
+  }
+
+  static __device__ __forceinline__ void gemm2(const uint8_t* w2, const Frag (&gf)[NF2],
+                                               f32x16 (&zacc)[NB], int lane) {
 #pragma unroll
-    for (int g = 0; g < (NB * NF2) / G; ++g) {
-      const u32x4 grp = lds_group(cur, NK1 / G + g, lane);
+    for (int g = 0; g < NK2 / G; ++g) {
+      const u32x4 grp = lds_group(w2, g, lane);
 #pragma unroll
       for (int w = 0; w < G; ++w) {
         const int F = g * G + w;
@@ -216,33 +254,88 @@ struct RollStep {
       }
     }
   }
+
+  // Scheduling of one pipeline iteration (GELU of chunk c, first product of
+  // chunk c+1, second product of chunk c): LDS fragment reads are issued one
+  // per product group, a couple ahead, and the GELU arithmetic is spread
+  // between the first product's matrix instructions, so the vector ALU work
+  // overlaps the matrix cores and no fragment is held longer than needed.
+  static __device__ __forceinline__ void schedule_iteration() {
+    constexpr int kDS = 0x100, kMFMA = 0x008, kVALU = 0x002;
+    constexpr int VALU_PER = (16 * 18 + NK1 - 1) / NK1 + 1;
+    __builtin_amdgcn_sched_group_barrier(kDS, 6, 0);
+#pragma unroll
+    for (int g = 0; g < NK1 / G; ++g) {
+#pragma unroll
+      for (int w = 0; w < G; ++w) {
+        __builtin_amdgcn_sched_group_barrier(kMFMA, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kVALU, VALU_PER, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(kDS, 1, 0);
+    }
+#pragma unroll
+    for (int g = 0; g < NK2 / G; ++g) {
+      __builtin_amdgcn_sched_group_barrier(kMFMA, G, 0);
+      __builtin_amdgcn_sched_group_barrier(kDS, 1, 0);
+    }
+  }
+
+  // SL consecutive floats of an LDS table row
+  static __device__ __forceinline__ void row(const float* p, float (&v)[SL]) {
+    if constexpr (SL % 4 == 0) {
+#pragma unroll
+      for (int q = 0; q < SL / 4; ++q) {
+        const f32x4 x = *reinterpret_cast<const f32x4*>(p + 4 * q);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[4 * q + i] = x[i];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < SL; ++i) v[i] = p[i];
+    }
+  }
 };
 
+// Workgroup = WAVES wavefronts; wavefront w owns the 32 candidates at sorted
+// positions [32*(WAVES*blockIdx.x + w), +32): lane L works on candidate
+// column L%32 together with lane L^32.  All wavefronts of a workgroup walk the
+// same sequence of weight chunks for T_wg steps (T_wg = longest sequence of the
+// workgroup; sorted order keeps a workgroup's tiles of similar length).
+//
+// Software pipeline over chunks (W1 parts in w1a/w1b, W2 parts in w2a/w2b,
+// four distinct LDS arrays): iteration c computes GELU of chunk c while the
+// first product of chunk c+1 runs on the matrix cores, then the second
+// product of chunk c; meanwhile the W2 part of chunk c+1 and the W1 part of
+// chunk c+2 are copied into the buffers freed by the previous iteration.
 template <class PR, int D, int E, int WAVES>
 __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a) {
-  using RS = RollStep<PR, D, E>;
+  using R = Roll<PR, D, E>;
   using Frag = typename PR::Frag;
   constexpr int KF = PR::KF, SL = PR::SL;
-  constexpr int NZ = RS::NZ, NE = RS::NE, NF2 = RS::NF2, NB = RS::NB, CB = RS::CB;
+  constexpr int NZ = R::NZ, NE = R::NE, NF2 = R::NF2, NB = R::NB;
+  constexpr int W1B = R::W1B, W2B = R::W2B;
   constexpr int NT = 64 * WAVES;
-  static_assert(RS::NK1 % PR::G == 0 && (NB * NF2) % PR::G == 0, "fragment groups");
 
-  __shared__ __attribute__((aligned(1024))) uint8_t bufA[CB];
-  __shared__ __attribute__((aligned(1024))) uint8_t bufB[CB];
+  __shared__ __attribute__((aligned(16))) uint8_t w1a[W1B];
+  __shared__ __attribute__((aligned(16))) uint8_t w1b[W1B];
+  __shared__ __attribute__((aligned(16))) uint8_t w2a[W2B];
+  __shared__ __attribute__((aligned(16))) uint8_t w2b[W2B];
   extern __shared__ __attribute__((aligned(16))) float tab[];
   const float* t_emb = tab;                       // [K][E]
-  const float* t_pw = tab + a.K * E;              // [P][E]
-  const float* t_pb = t_pw + a.P * E;             // [E]
+  const float* t_pw = tab + a.K * E;              // [PMAX][E], zero rows past P
+  const float* t_pb = t_pw + PMAX * E;            // [E]
   const float* t_b2 = t_pb + E;                   // [NB][2][16] accumulator order
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
   const int NC = a.H / 32;                        // even (checked on the host)
 
-  // Tables and the first weight chunk.
+  // Tables and the first chunks.
   stage_to_lds(reinterpret_cast<const uint8_t*>(a.tab), reinterpret_cast<uint8_t*>(tab),
                a.tab_bytes, tid, NT);
-  stage_to_lds(a.trans, bufA, CB, tid, NT);
+  stage_fixed<W1B, NT>(a.w1, w1a, tid);
+  stage_fixed<W2B, NT>(a.w2, w2a, tid);
+  stage_fixed<W1B, NT>(a.w1 + W1B, w1b, tid);
 
   const int pos = (blockIdx.x * WAVES + wave) * 32 + n;
   const bool valid = pos < a.B;
@@ -267,64 +360,58 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
       }
   }
 
-  // Action of the current step (prefetched one step ahead).
+  // Action of the current step (prefetched one step ahead).  Parameters past
+  // P read as 1 (log2 = 0) and meet zero weights in the padded table.
   const int32_t* ty_row = a.types + (size_t)cand * a.T_max;
   const int32_t* pa_row = a.params + (size_t)cand * a.T_max * a.P;
   int nx_type = 0;
-  int nx_par[8];
+  int nx_par[PMAX];
 #pragma unroll
-  for (int p = 0; p < 8; ++p) nx_par[p] = 1;
+  for (int p = 0; p < PMAX; ++p) nx_par[p] = 1;
   if (0 < len) {
     nx_type = ty_row[0];
 #pragma unroll
-    for (int p = 0; p < 8; ++p) if (p < a.P) nx_par[p] = pa_row[p];
+    for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[p];
   }
   int errbits = 0;
 
   wait_vm_then_barrier();
 
-  const int total_chunks = T_wg * NC;
-  int gch = 0;  // global chunk counter (step * NC + chunk); even at every step start
+  const int total = T_wg * NC;       // chunks processed by the workgroup
   for (int t = 0; t < T_wg; ++t) {
     const bool active = t < len;
     const float actf = active ? 1.0f : 0.0f;
-    // ---- action embedding e_t for features KF*q + SL*h + j
-    float u[8];
-    int ty = 0;
+    // ---- action embedding e_t for features KF*q + SL*h + j (branch-free)
+    const bool bad_type = active && (nx_type < 0 || nx_type >= a.K);
+    const int ty = (active && !bad_type) ? nx_type : 0;
+    bool bad_par = false;
+    float u[PMAX];
 #pragma unroll
-    for (int p = 0; p < 8; ++p) u[p] = 0.0f;
-    if (active) {
-      ty = nx_type;
-      if (ty < 0 || ty >= a.K) { errbits |= ERRBIT_TYPE; ty = 0; }
-#pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        if (p < a.P) {
-          if (nx_par[p] < 1) errbits |= ERRBIT_PARAM;
-          u[p] = log2f((float)nx_par[p]);
-        }
-      }
+    for (int p = 0; p < PMAX; ++p) {
+      bad_par |= active && nx_par[p] < 1;
+      u[p] = active ? log2f((float)nx_par[p]) : 0.0f;
     }
+    errbits |= (bad_type ? ERRBIT_TYPE : 0) | (bad_par ? ERRBIT_PARAM : 0);
     if (t + 1 < len) {   // prefetch the next action
       nx_type = ty_row[t + 1];
 #pragma unroll
-      for (int p = 0; p < 8; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(t + 1) * a.P + p];
+      for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(t + 1) * a.P + p];
     }
     Frag xe[NE];
 #pragma unroll
     for (int q = 0; q < NE; ++q) {
       const int f0 = KF * q + SL * h;
-      float ev[SL];
+      float ev[SL], tmp[SL];
+      R::row(t_emb + ty * E + f0, ev);
 #pragma unroll
-      for (int j = 0; j < SL; ++j) ev[j] = t_emb[ty * E + f0 + j];
+      for (int p = 0; p < PMAX; ++p) {
+        R::row(t_pw + p * E + f0, tmp);
 #pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        if (p < a.P) {
-#pragma unroll
-          for (int j = 0; j < SL; ++j) ev[j] = fmaf(t_pw[p * E + f0 + j], u[p], ev[j]);
-        }
+        for (int j = 0; j < SL; ++j) ev[j] = fmaf(tmp[j], u[p], ev[j]);
       }
+      R::row(t_pb + f0, tmp);
 #pragma unroll
-      for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + t_pb[f0 + j]) * actf;
+      for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * actf;
       xe[q] = PR::cvt(ev);
     }
     // ---- z operand fragments (state at the start of the step)
@@ -337,19 +424,32 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
       xz[kf] = PR::cvt(v);
     }
 
-    for (int c = 0; c < NC; c += 2, gch += 2) {
-      // chunk c from bufA while chunk c+1 lands in bufB
-      stage_to_lds(a.trans + (size_t)(c + 1) * CB, bufB, CB, tid, NT);
+    // first product of chunk 0 (its W1 part is in w1a)
+    f32x16 acc1 = R::gemm1(w1a, xz, xe, lane, h);
+    __syncthreads();                 // all wavefronts are done with w1a
+    const int g0 = t * NC;
+    for (int c = 0; c < NC; c += 2) {
+      const int g = g0 + c;
+      Frag gf[NF2];
+      // -- chunk c: W2 part in w2a; next W1 part (chunk c+1) in w1b
+      if (g + 1 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 1) % NC) * W2B, w2b, tid);
+      if (g + 2 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 2) % NC) * W1B, w1a, tid);
       __builtin_amdgcn_sched_barrier(0);
-      RS::chunk(bufA, xz, xe, zacc, actf, lane, h);
+      R::gelu_frags(acc1, actf, gf);
+      f32x16 acc1n = R::gemm1(w1b, xz, xe, lane, h);
+      R::gemm2(w2a, gf, zacc, lane);
+      R::schedule_iteration();
+      acc1 = acc1n;
       wait_vm_then_barrier();
-      // chunk c+1 from bufB while the following chunk lands in bufA
-      if (gch + 2 < total_chunks) {
-        const int nc = (c + 2 == NC) ? 0 : c + 2;
-        stage_to_lds(a.trans + (size_t)nc * CB, bufA, CB, tid, NT);
-      }
+      // -- chunk c+1: W2 part in w2b; next W1 part (chunk c+2) in w1a
+      if (g + 2 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 2) % NC) * W2B, w2a, tid);
+      if (g + 3 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 3) % NC) * W1B, w1b, tid);
       __builtin_amdgcn_sched_barrier(0);
-      RS::chunk(bufB, xz, xe, zacc, actf, lane, h);
+      R::gelu_frags(acc1, actf, gf);
+      if (c + 2 < NC) acc1n = R::gemm1(w1a, xz, xe, lane, h);
+      R::gemm2(w2b, gf, zacc, lane);
+      R::schedule_iteration();
+      acc1 = acc1n;
       wait_vm_then_barrier();
     }
 #pragma unroll
@@ -389,7 +489,7 @@ __global__ __launch_bounds__(256) void phi_kernel(const float* __restrict__ emb,
   const int i = gid / per, f0 = (gid % per) * 4;
   const float* t_emb = emb;
   const float* t_pw = emb + K * E;
-  const float* t_pb = t_pw + P * E;
+  const float* t_pb = t_pw + PMAX * E;
   const int len = clampi(lens[i], 0, T_max);
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int t = 0; t < len; ++t) {
@@ -480,8 +580,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void score_kernel(const ScoreArgs a)
   constexpr int NX = SS::NX, MAXH = SS::MAXH;
   constexpr int NT = 64 * WAVES;
   constexpr int CBMAX = CostChunk<PR>::bytes(D, E, SCORE_MAX_HW);
-  __shared__ __attribute__((aligned(1024))) uint8_t bufA[CBMAX];
-  __shared__ __attribute__((aligned(1024))) uint8_t bufB[CBMAX];
+  __shared__ __attribute__((aligned(16))) uint8_t bufA[CBMAX];
+  __shared__ __attribute__((aligned(16))) uint8_t bufB[CBMAX];
   const int CB = a.chunk_bytes;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
@@ -717,7 +817,10 @@ hipError_t launch_rollout_t(const DevModel& m, const RollArgs& a, int blocks, hi
   const int lds = m.roll_tab_bytes;   // the two chunk buffers are static
   auto kern = rollout_kernel<PR, D, E, WAVES>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess) {
+    (void)hipGetLastError();   // do not leave the error for the caller's next HIP call
+    return e;
+  }
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * WAVES), lds, st, a);
   return hipGetLastError();
 }
@@ -727,7 +830,10 @@ hipError_t launch_score_t(const DevModel& m, const ScoreArgs& a, int blocks, hip
   const int lds = 0;                  // static chunk buffers
   auto kern = score_kernel<PR, D, E, WAVES>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess) {
+    (void)hipGetLastError();   // do not leave the error for the caller's next HIP call
+    return e;
+  }
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * WAVES), lds, st, a);
   return hipGetLastError();
 }
@@ -761,7 +867,9 @@ bool have_kernels(int prec, int d, int e) {
   return false;
 }
 
-int rollout_lds_bytes(const DevModel& m) { return 2 * m.trans_chunk_bytes + m.roll_tab_bytes; }
+int rollout_lds_bytes(const DevModel& m) {
+  return 2 * (m.w1_chunk_bytes + m.w2_chunk_bytes) + m.roll_tab_bytes;
+}
 
 hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
                          int2* perm, int32_t* err, hipStream_t st) {
@@ -774,10 +882,10 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
                           int32_t B, int32_t T_max, float* zT, int32_t* err, hipStream_t st) {
   RollArgs a;
-  a.trans = m.trans; a.tab = m.roll_tab; a.z0 = z0; a.perm = perm; a.types = types;
+  a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.tab = m.roll_tab; a.z0 = z0; a.perm = perm; a.types = types;
   a.params = params; a.lens = lens; a.zT = zT; a.err = err; a.B = B; a.T_max = T_max;
   a.P = m.dims.n_params; a.K = m.dims.n_kinds; a.H = m.dims.trans_hidden;
-  a.chunk_bytes = m.trans_chunk_bytes; a.tab_bytes = m.roll_tab_bytes;
+  a.tab_bytes = m.roll_tab_bytes;
   const int tiles = (B + 31) / 32;
   const int waves = pick_waves(tiles);
   const int blocks = (tiles + waves - 1) / waves;
