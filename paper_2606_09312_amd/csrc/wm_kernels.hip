@@ -40,6 +40,12 @@ struct PBF16 : GeomBF16 {
   }
   // fragment `w` (0 <= w < G) of a 16-byte lane group
   static __device__ __forceinline__ Frag pick(u32x4 g, int) { return __builtin_bit_cast(Frag, g); }
+  // all elements kept (mask = ~0) or zeroed (mask = 0)
+  static __device__ __forceinline__ Frag mask(Frag f, uint32_t m) {
+    u32x4 u = __builtin_bit_cast(u32x4, f);
+    u &= m;
+    return __builtin_bit_cast(Frag, u);
+  }
 };
 
 struct PF32 : GeomF32 {
@@ -54,25 +60,27 @@ struct PF32 : GeomF32 {
     const uint32_t u = g[w];
     return __uint_as_float(u);
   }
+  static __device__ __forceinline__ Frag mask(Frag f, uint32_t m) {
+    return __uint_as_float(__float_as_uint(f) & m);
+  }
 };
 
-// GELU(x) = x * Phi(x), Phi(x) = (1 + erf(x / sqrt 2)) / 2, with erf from
+// GELU(x) = x * Phi(x) = (x + |x| * erf(|x| / sqrt 2)) / 2, with erf from
 // Abramowitz & Stegun, Handbook of Mathematical Functions, formula 7.1.26:
 //   erf(a) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-a^2),
-//   t = 1 / (1 + p a),  a >= 0,  |error| <= 1.5e-7,
-// extended to negative arguments by oddness.  Branch-free: one reciprocal,
-// one exp2 and a handful of multiply-adds.
+//   t = 1 / (1 + p a), a >= 0, |error| <= 1.5e-7.
+// The 1/sqrt 2 scaling is folded into the constants: one reciprocal, one
+// exp2, ten multiply-adds, no branches; -> 0 and -> x in the tails, 0 at 0.
 __device__ __forceinline__ float gelu(float x) {
-  const float a = fabsf(x) * 0.70710678118654752f;
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, a, 1.0f));
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.70710678118654752f, ax, 1.0f));
   float p = fmaf(1.061405429f, t, -1.453152027f);
   p = fmaf(p, t, 1.421413741f);
   p = fmaf(p, t, -0.284496736f);
   p = fmaf(p, t, 0.254829592f);
-  p *= t;
-  const float ex = __builtin_amdgcn_exp2f(-1.4426950408889634f * a * a);
-  const float erf_a = fmaf(-p, ex, 1.0f);             // erf(|x| / sqrt 2)
-  return x * (0.5f + copysignf(0.5f * erf_a, x));
+  const float ex = __builtin_amdgcn_exp2f((x * x) * (-0.5f * 1.4426950408889634f));
+  const float erf_a = fmaf(-(p * t), ex, 1.0f);
+  return 0.5f * fmaf(ax, erf_a, x);
 }
 
 __device__ __forceinline__ u32x4 lds_group(const uint8_t* base, int group, int lane) {
@@ -230,15 +238,15 @@ struct Roll {
     return acc;
   }
 
-  // GELU of the first product; a finished candidate (actf = 0) contributes
+  // GELU of the first product; a finished candidate (mask = 0) contributes
   // exact zeros to the second product.
-  static __device__ __forceinline__ void gelu_frags(const f32x16& acc, float actf, Frag (&gf)[NF2]) {
+  static __device__ __forceinline__ void gelu_frags(const f32x16& acc, uint32_t mask, Frag (&gf)[NF2]) {
 #pragma unroll
     for (int f = 0; f < NF2; ++f) {
       float v[SL];
 #pragma unroll
-      for (int j = 0; j < SL; ++j) v[j] = gelu(acc[f * SL + j]) * actf;
-      gf[f] = PR::cvt(v);
+      for (int j = 0; j < SL; ++j) v[j] = gelu(acc[f * SL + j]);
+      gf[f] = PR::mask(PR::cvt(v), mask);
     }
   }
 
@@ -381,6 +389,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
   for (int t = 0; t < T_wg; ++t) {
     const bool active = t < len;
     const float actf = active ? 1.0f : 0.0f;
+    const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
     // ---- action embedding e_t for features KF*q + SL*h + j (branch-free)
     const bool bad_type = active && (nx_type < 0 || nx_type >= a.K);
     const int ty = (active && !bad_type) ? nx_type : 0;
@@ -435,7 +444,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
       if (g + 1 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 1) % NC) * W2B, w2b, tid);
       if (g + 2 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 2) % NC) * W1B, w1a, tid);
       __builtin_amdgcn_sched_barrier(0);
-      R::gelu_frags(acc1, actf, gf);
+      R::gelu_frags(acc1, amask, gf);
       f32x16 acc1n = R::gemm1(w1b, xz, xe, lane, h);
       R::gemm2(w2a, gf, zacc, lane);
       R::schedule_iteration();
@@ -445,7 +454,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
       if (g + 2 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 2) % NC) * W2B, w2a, tid);
       if (g + 3 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 3) % NC) * W1B, w1b, tid);
       __builtin_amdgcn_sched_barrier(0);
-      R::gelu_frags(acc1, actf, gf);
+      R::gelu_frags(acc1, amask, gf);
       if (c + 2 < NC) acc1n = R::gemm1(w1a, xz, xe, lane, h);
       R::gemm2(w2b, gf, zacc, lane);
       R::schedule_iteration();
