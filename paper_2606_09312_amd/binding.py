@@ -65,6 +65,9 @@ def load_library(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with paper_2606_09312_amd.build.build()")
+    # Load torch first so the library binds to the HIP runtime torch uses
+    # (one runtime per process; device buffers and streams come from torch).
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     lib.wm_model_create.argtypes = [ctypes.POINTER(Dims), ctypes.POINTER(Weights), ctypes.POINTER(vp)]

@@ -46,6 +46,18 @@ struct PBF16 : GeomBF16 {
     u &= m;
     return __builtin_bit_cast(Frag, u);
   }
+  // two GELU outputs -> one packed register (bf16 pair), masked
+  using Packed = uint32_t;
+  static __device__ __forceinline__ Packed pack2(float a, float b, uint32_t m) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 v = {(__bf16)a, (__bf16)b};
+    return __builtin_bit_cast(uint32_t, v) & m;
+  }
+  // operand fragment f (8 values = 4 packed pairs) of the second product
+  static __device__ __forceinline__ Frag gfrag(const Packed (&gp)[8], int f) {
+    const u32x4 u = {gp[4 * f], gp[4 * f + 1], gp[4 * f + 2], gp[4 * f + 3]};
+    return __builtin_bit_cast(Frag, u);
+  }
 };
 
 struct PF32 : GeomF32 {
@@ -62,6 +74,15 @@ struct PF32 : GeomF32 {
   }
   static __device__ __forceinline__ Frag mask(Frag f, uint32_t m) {
     return __uint_as_float(__float_as_uint(f) & m);
+  }
+  // fp32 keeps both values of a pair unpacked
+  struct Packed { float a, b; };
+  static __device__ __forceinline__ Packed pack2(float a, float b, uint32_t m) {
+    return {__uint_as_float(__float_as_uint(a) & m), __uint_as_float(__float_as_uint(b) & m)};
+  }
+  // operand fragment f (one value) of the second product
+  static __device__ __forceinline__ Frag gfrag(const Packed (&gp)[8], int f) {
+    return (f & 1) ? gp[f >> 1].b : gp[f >> 1].a;
   }
 };
 
@@ -203,9 +224,9 @@ struct RollArgs {
 };
 
 // Per-wavefront pieces of one transition step.  Chunk c covers hidden units
-// [32c, 32c+32): gemm1 forms G^T[chunk] = b1 + W1[chunk] . X^T in accumulator
-// layout, gelu_frags turns it into the B operand of the second product, and
-// gemm2 accumulates dZ^T += W2[:, chunk] . G^T into the latent.
+// [32c, 32c+32): the first product forms G^T[chunk] = b1 + W1[chunk] . X^T in
+// accumulator layout, its GELU becomes the B operand of the second product,
+// which accumulates dZ^T += W2[:, chunk] . G^T into the latent.
 template <class PR, int D, int E>
 struct Roll {
   using Frag = typename PR::Frag;
@@ -216,75 +237,72 @@ struct Roll {
   static constexpr int W2B = TransChunk<PR>::w2_bytes(D);
   static_assert(NK1 % G == 0 && NK2 % G == 0, "fragment groups");
 
-  static __device__ __forceinline__ f32x16 gemm1(const uint8_t* w1, const Frag (&xz)[NZ],
-                                                 const Frag (&xe)[NE], int lane, int h) {
-    f32x16 acc;
-    const float* b1t = reinterpret_cast<const float*>(w1 + (W1B - 128)) + 16 * h;
+  // One pipeline iteration as a single stream of "items" (one 16-byte-per-
+  // lane fragment group read from LDS each): first the N1 groups of the first
+  // product of the next chunk (from w1n), then the N2 groups of the second
+  // product of the current chunk (from w2c).  Reads run P items ahead in a
+  // register ring; the GELU of the current chunk's first product is computed
+  // a few values per item while the next chunk's first product runs, and is
+  // complete before the second product starts.  A scheduling fence after every
+  // item keeps this order (left alone, the scheduler serialises read, wait and
+  // matrix instruction at this register pressure).
+  //   DO_G1: compute acc1n = b1 + W1[next chunk] . X^T
+  //   DO_G2: GELU(acc1) -> second product into zacc
+  template <bool DO_G1, bool DO_G2>
+  static __device__ __forceinline__ void iteration(const uint8_t* w1n, const uint8_t* w2c,
+                                                   const Frag (&xz)[NZ], const Frag (&xe)[NE],
+                                                   const f32x16& acc1, uint32_t mask,
+                                                   f32x16& acc1n, f32x16 (&zacc)[NB],
+                                                   int lane, int h) {
+    constexpr int N1 = DO_G1 ? NK1 / G : 0;
+    constexpr int N2 = DO_G2 ? NK2 / G : 0;
+    constexpr int NI = N1 + N2;
+    constexpr int P = 4;                                   // LDS reads in flight
+    constexpr int PAIRS = 8;                               // GELU value pairs (16 values)
+    if constexpr (DO_G1) {
+      const float* b1t = reinterpret_cast<const float*>(w1n + (W1B - 128)) + 16 * h;
 #pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(b1t + 4 * r4);
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(b1t + 4 * r4);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc[4 * r4 + i] = v[i];
-    }
-#pragma unroll
-    for (int g = 0; g < NK1 / G; ++g) {
-      const u32x4 grp = lds_group(w1, g, lane);
-#pragma unroll
-      for (int w = 0; w < G; ++w) {
-        const int kf = g * G + w;
-        acc = PR::mfma(PR::pick(grp, w), kf < NZ ? xz[kf < NZ ? kf : 0] : xe[kf < NZ ? 0 : kf - NZ], acc);
+        for (int i = 0; i < 4; ++i) acc1n[4 * r4 + i] = v[i];
       }
     }
-    return acc;
-  }
-
-  // GELU of the first product; a finished candidate (mask = 0) contributes
-  // exact zeros to the second product.
-  static __device__ __forceinline__ void gelu_frags(const f32x16& acc, uint32_t mask, Frag (&gf)[NF2]) {
+    // GELU outputs, packed two at a time as they are produced
+    typename PR::Packed gp[PAIRS];
+    if constexpr (DO_G2 && N1 == 0) {      // nothing to hide the GELU under
 #pragma unroll
-    for (int f = 0; f < NF2; ++f) {
-      float v[SL];
-#pragma unroll
-      for (int j = 0; j < SL; ++j) v[j] = gelu(acc[f * SL + j]);
-      gf[f] = PR::mask(PR::cvt(v), mask);
+      for (int q = 0; q < PAIRS; ++q) gp[q] = PR::pack2(gelu(acc1[2 * q]), gelu(acc1[2 * q + 1]), mask);
     }
-  }
-
-  static __device__ __forceinline__ void gemm2(const uint8_t* w2, const Frag (&gf)[NF2],
-                                               f32x16 (&zacc)[NB], int lane) {
+    u32x4 ring[P];
 #pragma unroll
-    for (int g = 0; g < NK2 / G; ++g) {
-      const u32x4 grp = lds_group(w2, g, lane);
+    for (int i = 0; i < P && i < NI; ++i)
+      ring[i] = lds_group(i < N1 ? w1n : w2c, i < N1 ? i : i - N1, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int w = 0; w < G; ++w) {
-        const int F = g * G + w;
-        zacc[F / NF2] = PR::mfma(PR::pick(grp, w), gf[F % NF2], zacc[F / NF2]);
+    for (int i = 0; i < NI; ++i) {
+      const u32x4 grp = ring[i % P];
+      if (i + P < NI) ring[i % P] = lds_group(i + P < N1 ? w1n : w2c, i + P < N1 ? i + P : i + P - N1, lane);
+      if (i < N1) {
+#pragma unroll
+        for (int w = 0; w < G; ++w) {
+          const int kf = i * G + w;
+          acc1n = PR::mfma(PR::pick(grp, w), kf < NZ ? xz[kf < NZ ? kf : 0] : xe[kf < NZ ? 0 : kf - NZ], acc1n);
+        }
+        if constexpr (DO_G2) {
+          // value pairs spread evenly over the N1 items of the first product
+#pragma unroll
+          for (int q = 0; q < PAIRS; ++q)
+            if ((q * N1) / PAIRS == i) gp[q] = PR::pack2(gelu(acc1[2 * q]), gelu(acc1[2 * q + 1]), mask);
+        }
+      } else {
+#pragma unroll
+        for (int w = 0; w < G; ++w) {
+          const int F = (i - N1) * G + w;
+          zacc[F / NF2] = PR::mfma(PR::pick(grp, w), PR::gfrag(gp, F % NF2), zacc[F / NF2]);
+        }
       }
-    }
-  }
-
-  // Scheduling of one pipeline iteration (GELU of chunk c, first product of
-  // chunk c+1, second product of chunk c): LDS fragment reads are issued one
-  // per product group, a couple ahead, and the GELU arithmetic is spread
-  // between the first product's matrix instructions, so the vector ALU work
-  // overlaps the matrix cores and no fragment is held longer than needed.
-  static __device__ __forceinline__ void schedule_iteration() {
-    constexpr int kDS = 0x100, kMFMA = 0x008, kVALU = 0x002;
-    constexpr int VALU_PER = (16 * 18 + NK1 - 1) / NK1 + 1;
-    __builtin_amdgcn_sched_group_barrier(kDS, 6, 0);
-#pragma unroll
-    for (int g = 0; g < NK1 / G; ++g) {
-#pragma unroll
-      for (int w = 0; w < G; ++w) {
-        __builtin_amdgcn_sched_group_barrier(kMFMA, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(kVALU, VALU_PER, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(kDS, 1, 0);
-    }
-#pragma unroll
-    for (int g = 0; g < NK2 / G; ++g) {
-      __builtin_amdgcn_sched_group_barrier(kMFMA, G, 0);
-      __builtin_amdgcn_sched_group_barrier(kDS, 1, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
@@ -320,6 +338,10 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
   using R = Roll<PR, D, E>;
   using Frag = typename PR::Frag;
   constexpr int KF = PR::KF, SL = PR::SL;
+  // Overlap each chunk's GELU with the next chunk's first product (two
+  // accumulators).  At d = 512 the latent fills the accumulator registers and
+  // the second accumulator does not fit, so the chunks run one at a time.
+  constexpr bool PIPE = D <= 256;
   constexpr int NZ = R::NZ, NE = R::NE, NF2 = R::NF2, NB = R::NB;
   constexpr int W1B = R::W1B, W2B = R::W2B;
   constexpr int NT = 64 * WAVES;
@@ -343,7 +365,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
                a.tab_bytes, tid, NT);
   stage_fixed<W1B, NT>(a.w1, w1a, tid);
   stage_fixed<W2B, NT>(a.w2, w2a, tid);
-  stage_fixed<W1B, NT>(a.w1 + W1B, w1b, tid);
+  if constexpr (PIPE) stage_fixed<W1B, NT>(a.w1 + W1B, w1b, tid);
 
   const int pos = (blockIdx.x * WAVES + wave) * 32 + n;
   const bool valid = pos < a.B;
@@ -433,33 +455,54 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
       xz[kf] = PR::cvt(v);
     }
 
-    // first product of chunk 0 (its W1 part is in w1a)
-    f32x16 acc1 = R::gemm1(w1a, xz, xe, lane, h);
-    __syncthreads();                 // all wavefronts are done with w1a
     const int g0 = t * NC;
-    for (int c = 0; c < NC; c += 2) {
-      const int g = g0 + c;
-      Frag gf[NF2];
-      // -- chunk c: W2 part in w2a; next W1 part (chunk c+1) in w1b
-      if (g + 1 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 1) % NC) * W2B, w2b, tid);
-      if (g + 2 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 2) % NC) * W1B, w1a, tid);
-      __builtin_amdgcn_sched_barrier(0);
-      R::gelu_frags(acc1, amask, gf);
-      f32x16 acc1n = R::gemm1(w1b, xz, xe, lane, h);
-      R::gemm2(w2a, gf, zacc, lane);
-      R::schedule_iteration();
-      acc1 = acc1n;
-      wait_vm_then_barrier();
-      // -- chunk c+1: W2 part in w2b; next W1 part (chunk c+2) in w1a
-      if (g + 2 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 2) % NC) * W2B, w2a, tid);
-      if (g + 3 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 3) % NC) * W1B, w1b, tid);
-      __builtin_amdgcn_sched_barrier(0);
-      R::gelu_frags(acc1, amask, gf);
-      if (c + 2 < NC) acc1n = R::gemm1(w1a, xz, xe, lane, h);
-      R::gemm2(w2b, gf, zacc, lane);
-      R::schedule_iteration();
-      acc1 = acc1n;
-      wait_vm_then_barrier();
+    if constexpr (PIPE) {
+      // first product of chunk 0 (its W1 part is in w1a); accumulators accA
+      // and accB alternate between "GELU input" and "next first product"
+      f32x16 accA, accB;
+      R::template iteration<true, false>(w1a, w2a, xz, xe, accB, amask, accA, zacc, lane, h);
+      __syncthreads();                 // all wavefronts are done with w1a
+      for (int c = 0; c < NC; c += 2) {
+        const int g = g0 + c;
+        // -- chunk c: W2 part in w2a; next W1 part (chunk c+1) in w1b
+        if (g + 1 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 1) % NC) * W2B, w2b, tid);
+        if (g + 2 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 2) % NC) * W1B, w1a, tid);
+        __builtin_amdgcn_sched_barrier(0);
+        R::template iteration<true, true>(w1b, w2a, xz, xe, accA, amask, accB, zacc, lane, h);
+        wait_vm_then_barrier();
+        // -- chunk c+1: W2 part in w2b; next W1 part (chunk c+2) in w1a.  At
+        // c + 2 == NC this first product is discarded (w1a then holds the
+        // next step's chunk 0 or stale data; the step prologue recomputes it
+        // with the new X): one branch-free body keeps register use down.
+        if (g + 2 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 2) % NC) * W2B, w2a, tid);
+        if (g + 3 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 3) % NC) * W1B, w1b, tid);
+        __builtin_amdgcn_sched_barrier(0);
+        R::template iteration<true, true>(w1a, w2b, xz, xe, accB, amask, accA, zacc, lane, h);
+        wait_vm_then_barrier();
+      }
+    } else {
+      // one accumulator: first product, GELU, second product per chunk; chunk
+      // c+1 (both parts) lands in the other buffer pair meanwhile
+      f32x16 acc;
+      for (int c = 0; c < NC; c += 2) {
+        const int g = g0 + c;
+        if (g + 1 < total) {
+          stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 1) % NC) * W1B, w1b, tid);
+          stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 1) % NC) * W2B, w2b, tid);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        R::template iteration<true, false>(w1a, w2a, xz, xe, acc, amask, acc, zacc, lane, h);
+        R::template iteration<false, true>(w1a, w2a, xz, xe, acc, amask, acc, zacc, lane, h);
+        wait_vm_then_barrier();
+        if (g + 2 < total) {
+          stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 2) % NC) * W1B, w1a, tid);
+          stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 2) % NC) * W2B, w2a, tid);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        R::template iteration<true, false>(w1b, w2b, xz, xe, acc, amask, acc, zacc, lane, h);
+        R::template iteration<false, true>(w1b, w2b, xz, xe, acc, amask, acc, zacc, lane, h);
+        wait_vm_then_barrier();
+      }
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b)
