@@ -223,6 +223,22 @@ struct RollArgs {
   int B, T_max, P, K, H, tab_bytes;
 };
 
+// Copies of the next weight chunk (its W1 and/or W2 part) into LDS, issued
+// a few at a time between the matrix-fragment groups of an iteration so the
+// L2 -> LDS traffic runs continuously underneath the computation.
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+struct CopyPlan {
+  const uint8_t* s1;
+  lds_u8* d1;
+  bool e1;            // copy the W1 part
+  const uint8_t* s2;
+  lds_u8* d2;
+  bool e2;            // copy the W2 part
+};
+
+__device__ __forceinline__ lds_u8* to_lds(uint8_t* p) { return (lds_u8*)p; }
+
 // Per-wavefront pieces of one transition step.  Chunk c covers hidden units
 // [32c, 32c+32): the first product forms G^T[chunk] = b1 + W1[chunk] . X^T in
 // accumulator layout, its GELU becomes the B operand of the second product,
@@ -248,15 +264,40 @@ struct Roll {
   // matrix instruction at this register pressure).
   //   DO_G1: compute acc1n = b1 + W1[next chunk] . X^T
   //   DO_G2: GELU(acc1) -> second product into zacc
-  template <bool DO_G1, bool DO_G2>
+  // Copy unit u (16 bytes per lane) of a CopyPlan: units [0, U1) are the W1
+  // part, [U1, U1 + U2) the W2 part.
+  template <int NT>
+  static constexpr int U1 = (W1B / 16 + NT - 1) / NT;
+  template <int NT>
+  static constexpr int U2 = (W2B / 16 + NT - 1) / NT;
+  template <int NT>
+  static __device__ __forceinline__ void copy_unit(const CopyPlan& cp, int u, int tid) {
+    const int wave_base = tid & ~63;
+    if (u < U1<NT>) {
+      const int k = u * NT;
+      if (cp.e1 && k + tid < W1B / 16)
+        __builtin_amdgcn_global_load_lds(
+            (const void*)(cp.s1 + (size_t)(k + tid) * 16),
+            (__attribute__((address_space(3))) void*)(cp.d1 + (k + wave_base) * 16), 16, 0, 0);
+    } else {
+      const int k = (u - U1<NT>) * NT;
+      if (cp.e2 && k + tid < W2B / 16)
+        __builtin_amdgcn_global_load_lds(
+            (const void*)(cp.s2 + (size_t)(k + tid) * 16),
+            (__attribute__((address_space(3))) void*)(cp.d2 + (k + wave_base) * 16), 16, 0, 0);
+    }
+  }
+
+  template <bool DO_G1, bool DO_G2, int NT, bool COPY>
   static __device__ __forceinline__ void iteration(const uint8_t* w1n, const uint8_t* w2c,
                                                    const Frag (&xz)[NZ], const Frag (&xe)[NE],
                                                    const f32x16& acc1, uint32_t mask,
                                                    f32x16& acc1n, f32x16 (&zacc)[NB],
-                                                   int lane, int h) {
+                                                   int lane, int h, const CopyPlan& cp, int tid) {
     constexpr int N1 = DO_G1 ? NK1 / G : 0;
     constexpr int N2 = DO_G2 ? NK2 / G : 0;
     constexpr int NI = N1 + N2;
+    constexpr int NU = COPY ? U1<NT> + U2<NT> : 0;     // copy units, spread over the items
     constexpr int P = 4;                                   // LDS reads in flight
     constexpr int PAIRS = 8;                               // GELU value pairs (16 values)
     if constexpr (DO_G1) {
@@ -283,6 +324,11 @@ struct Roll {
     for (int i = 0; i < NI; ++i) {
       const u32x4 grp = ring[i % P];
       if (i + P < NI) ring[i % P] = lds_group(i + P < N1 ? w1n : w2c, i + P < N1 ? i + P : i + P - N1, lane);
+      if constexpr (NU > 0) {
+#pragma unroll
+        for (int u = 0; u < NU; ++u)
+          if ((u * NI) / NU == i) copy_unit<NT>(cp, u, tid);
+      }
       if (i < N1) {
 #pragma unroll
         for (int w = 0; w < G; ++w) {
@@ -456,51 +502,57 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
     }
 
     const int g0 = t * NC;
+    const CopyPlan none = {nullptr, nullptr, false, nullptr, nullptr, false};
     if constexpr (PIPE) {
       // first product of chunk 0 (its W1 part is in w1a); accumulators accA
       // and accB alternate between "GELU input" and "next first product"
       f32x16 accA, accB;
-      R::template iteration<true, false>(w1a, w2a, xz, xe, accB, amask, accA, zacc, lane, h);
+      R::template iteration<true, false, NT, false>(w1a, w2a, xz, xe, accB, amask, accA, zacc,
+                                                    lane, h, none, tid);
       __syncthreads();                 // all wavefronts are done with w1a
       for (int c = 0; c < NC; c += 2) {
         const int g = g0 + c;
-        // -- chunk c: W2 part in w2a; next W1 part (chunk c+1) in w1b
+        // -- chunk c: W2 part in w2a, next W1 part (chunk c+1) in w1b; the W2
+        // part of chunk c+1 is copied into w2b and the W1 part of chunk c+2
+        // into w1a (issued together up front: spreading them measured slower
+        // for this schedule)
         if (g + 1 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 1) % NC) * W2B, w2b, tid);
         if (g + 2 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 2) % NC) * W1B, w1a, tid);
         __builtin_amdgcn_sched_barrier(0);
-        R::template iteration<true, true>(w1b, w2a, xz, xe, accA, amask, accB, zacc, lane, h);
+        R::template iteration<true, true, NT, false>(w1b, w2a, xz, xe, accA, amask, accB, zacc,
+                                                     lane, h, none, tid);
         wait_vm_then_barrier();
-        // -- chunk c+1: W2 part in w2b; next W1 part (chunk c+2) in w1a.  At
+        // -- chunk c+1: W2 part in w2b, next W1 part (chunk c+2) in w1a.  At
         // c + 2 == NC this first product is discarded (w1a then holds the
         // next step's chunk 0 or stale data; the step prologue recomputes it
         // with the new X): one branch-free body keeps register use down.
         if (g + 2 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 2) % NC) * W2B, w2a, tid);
         if (g + 3 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 3) % NC) * W1B, w1b, tid);
         __builtin_amdgcn_sched_barrier(0);
-        R::template iteration<true, true>(w1a, w2b, xz, xe, accB, amask, accA, zacc, lane, h);
+        R::template iteration<true, true, NT, false>(w1a, w2b, xz, xe, accB, amask, accA, zacc,
+                                                     lane, h, none, tid);
         wait_vm_then_barrier();
       }
     } else {
       // one accumulator: first product, GELU, second product per chunk; chunk
-      // c+1 (both parts) lands in the other buffer pair meanwhile
+      // c+1 (both parts) is copied into the other buffer pair meanwhile, the
+      // copy instructions spread over the first product
       f32x16 acc;
       for (int c = 0; c < NC; c += 2) {
         const int g = g0 + c;
-        if (g + 1 < total) {
-          stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 1) % NC) * W1B, w1b, tid);
-          stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 1) % NC) * W2B, w2b, tid);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        R::template iteration<true, false>(w1a, w2a, xz, xe, acc, amask, acc, zacc, lane, h);
-        R::template iteration<false, true>(w1a, w2a, xz, xe, acc, amask, acc, zacc, lane, h);
+        const CopyPlan cp0 = {a.w1 + (size_t)((c + 1) % NC) * W1B, to_lds(w1b), g + 1 < total,
+                              a.w2 + (size_t)((c + 1) % NC) * W2B, to_lds(w2b), g + 1 < total};
+        R::template iteration<true, false, NT, true>(w1a, w2a, xz, xe, acc, amask, acc, zacc,
+                                                     lane, h, cp0, tid);
+        R::template iteration<false, true, NT, false>(w1a, w2a, xz, xe, acc, amask, acc, zacc,
+                                                      lane, h, none, tid);
         wait_vm_then_barrier();
-        if (g + 2 < total) {
-          stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 2) % NC) * W1B, w1a, tid);
-          stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 2) % NC) * W2B, w2a, tid);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        R::template iteration<true, false>(w1b, w2b, xz, xe, acc, amask, acc, zacc, lane, h);
-        R::template iteration<false, true>(w1b, w2b, xz, xe, acc, amask, acc, zacc, lane, h);
+        const CopyPlan cp1 = {a.w1 + (size_t)((c + 2) % NC) * W1B, to_lds(w1a), g + 2 < total,
+                              a.w2 + (size_t)((c + 2) % NC) * W2B, to_lds(w2a), g + 2 < total};
+        R::template iteration<true, false, NT, true>(w1b, w2b, xz, xe, acc, amask, acc, zacc,
+                                                     lane, h, cp1, tid);
+        R::template iteration<false, true, NT, false>(w1b, w2b, xz, xe, acc, amask, acc, zacc,
+                                                      lane, h, none, tid);
         wait_vm_then_barrier();
       }
     }
