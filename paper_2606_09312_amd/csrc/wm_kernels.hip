@@ -578,6 +578,255 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
 }
 
 // ==========================================================================
+// Small-batch rollout: when there are too few 32-candidate tiles to occupy
+// the chip, one workgroup of SPLIT wavefronts works on one tile and splits the
+// hidden units of every step among its wavefronts: wavefront w takes the
+// chunks w, w + SPLIT, ...  Each wavefront streams its chunks' A fragments
+// straight from L2 into a register ring (the wavefronts read different
+// chunks, so staging in LDS would save nothing), accumulates a partial update
+// dZ_w over the whole latent, and once per step the partial updates are
+// summed through LDS: wavefront w owns latent blocks [w*NB/SPLIT, ...) in
+// fp32, adds the sum and b2 to them, and publishes their bf16 (or fp32)
+// operand fragments, which every wavefront reads back as X for the next step.
+template <class PR, int D, int E>
+struct SplitGeom {
+  static constexpr int N1 = Roll<PR, D, E>::NK1 / PR::G;
+  static constexpr int N2 = Roll<PR, D, E>::NK2 / PR::G;
+  static constexpr int NI = N1 + N2;            // fragment groups per chunk
+  // enough loads in flight to cover an L2 hit (~600 cycles): a bf16 group
+  // feeds one 32-cycle product, an fp32 group four 64-cycle products
+  static constexpr int ring_depth() {
+    const int cap = PR::G == 1 ? 12 : 4;
+    for (int r = cap; r > 1; --r)
+      if (NI % r == 0) return r;
+    return 1;
+  }
+  static constexpr int RD = ring_depth();       // loads in flight (divides NI)
+};
+
+template <class PR, int D, int E, int SPLIT>
+__global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const RollArgs a) {
+  using R = Roll<PR, D, E>;
+  using SG = SplitGeom<PR, D, E>;
+  using Frag = typename PR::Frag;
+  constexpr int KF = PR::KF, SL = PR::SL, G = PR::G;
+  constexpr int NZ = R::NZ, NE = R::NE, NF2 = R::NF2, NB = R::NB;
+  constexpr int W1B = R::W1B, W2B = R::W2B;
+  constexpr int NT = 64 * SPLIT;
+  constexpr int NBQ = NB / SPLIT;               // latent blocks owned by a wavefront
+  constexpr int N1 = SG::N1, NI = SG::NI, RD = SG::RD;
+  constexpr int REGION = NB * 4 * 1024;         // one wavefront's partial update
+  static_assert(NB % SPLIT == 0, "latent blocks split evenly");
+
+  extern __shared__ __attribute__((aligned(16))) float tab[];
+  const float* t_emb = tab;
+  const float* t_pw = tab + a.K * E;
+  const float* t_pb = t_pw + PMAX * E;
+  const float* t_b2 = t_pb + E;
+  uint8_t* red = reinterpret_cast<uint8_t*>(tab) + a.tab_bytes;   // SPLIT regions
+  uint8_t* xbuf = red;                          // X fragments (reuses region space)
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int n = lane & 31, h = lane >> 5;
+  const int NC = a.H / 32;                      // >= SPLIT (checked on the host)
+
+  stage_to_lds(reinterpret_cast<const uint8_t*>(a.tab), reinterpret_cast<uint8_t*>(tab),
+               a.tab_bytes, tid, NT);
+
+  const int pos = blockIdx.x * 32 + n;
+  const bool valid = pos < a.B;
+  const int2 pc = valid ? a.perm[pos] : make_int2(0, 0);
+  const int cand = pc.x;
+  const int len = valid ? clampi(a.lens[cand], 0, a.T_max) : 0;
+  const int T_wg = __builtin_amdgcn_readfirstlane(
+      clampi(a.lens[a.perm[blockIdx.x * 32].x], 0, a.T_max));
+
+  // owned latent blocks (fp32) and the full X operand
+  const float* zs = a.z0 + (size_t)pc.y * D;
+  f32x16 zq[NBQ];
+#pragma unroll
+  for (int bq = 0; bq < NBQ; ++bq)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(zs + 32 * (w * NBQ + bq) + acc_row(h, 4 * r4));
+#pragma unroll
+      for (int i = 0; i < 4; ++i) zq[bq][4 * r4 + i] = v[i];
+    }
+  Frag xz[NZ];
+#pragma unroll
+  for (int kf = 0; kf < NZ; ++kf) {
+    float v[SL];
+#pragma unroll
+    for (int j = 0; j < SL; ++j) v[j] = zs[x_feature<PR>(D, kf, h, j)];
+    xz[kf] = PR::cvt(v);
+  }
+
+  const int32_t* ty_row = a.types + (size_t)cand * a.T_max;
+  const int32_t* pa_row = a.params + (size_t)cand * a.T_max * a.P;
+  int nx_type = 0;
+  int nx_par[PMAX];
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p) nx_par[p] = 1;
+  if (0 < len) {
+    nx_type = ty_row[0];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[p];
+  }
+  int errbits = 0;
+
+  // A-fragment group i of chunk c (W1 part first, then W2 part)
+  auto group_ptr = [&](int c, int i) -> const u32x4* {
+    const uint8_t* base = i < N1 ? a.w1 + (size_t)c * W1B + (size_t)i * 1024
+                                 : a.w2 + (size_t)c * W2B + (size_t)(i - N1) * 1024;
+    return reinterpret_cast<const u32x4*>(base + lane * 16);
+  };
+  // register ring: slot i % RD holds group i of the current chunk; the last RD
+  // groups of a chunk prefetch the first RD groups of the next one
+  u32x4 ring[RD];
+#pragma unroll
+  for (int i = 0; i < RD; ++i) ring[i] = *group_ptr(w, i);
+
+  wait_vm_then_barrier();
+
+  for (int t = 0; t < T_wg; ++t) {
+    const bool active = t < len;
+    const float actf = active ? 1.0f : 0.0f;
+    const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
+    const bool bad_type = active && (nx_type < 0 || nx_type >= a.K);
+    const int ty = (active && !bad_type) ? nx_type : 0;
+    bool bad_par = false;
+    float u[PMAX];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) {
+      bad_par |= active && nx_par[p] < 1;
+      u[p] = active ? log2f((float)nx_par[p]) : 0.0f;
+    }
+    errbits |= (bad_type ? ERRBIT_TYPE : 0) | (bad_par ? ERRBIT_PARAM : 0);
+    if (t + 1 < len) {
+      nx_type = ty_row[t + 1];
+#pragma unroll
+      for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(t + 1) * a.P + p];
+    }
+    Frag xe[NE];
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      const int f0 = KF * q + SL * h;
+      float ev[SL], tmp[SL];
+      R::row(t_emb + ty * E + f0, ev);
+#pragma unroll
+      for (int p = 0; p < PMAX; ++p) {
+        R::row(t_pw + p * E + f0, tmp);
+#pragma unroll
+        for (int j = 0; j < SL; ++j) ev[j] = fmaf(tmp[j], u[p], ev[j]);
+      }
+      R::row(t_pb + f0, tmp);
+#pragma unroll
+      for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * actf;
+      xe[q] = PR::cvt(ev);
+    }
+
+    f32x16 dz[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) dz[b] = f32x16{};
+    for (int c = w; c < NC; c += SPLIT) {
+      const int cn = (c + SPLIT < NC) ? c + SPLIT : w;     // next chunk of this wavefront
+      const float* b1g = reinterpret_cast<const float*>(a.w1 + (size_t)c * W1B + (W1B - 128)) + 16 * h;
+      f32x4 b1v[4];
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) b1v[r4] = *reinterpret_cast<const f32x4*>(b1g + 4 * r4);
+      f32x16 acc = {};
+      typename PR::Packed gp[8];
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const u32x4 grp = ring[i % RD];
+        ring[i % RD] = (i + RD < NI) ? *group_ptr(c, i + RD) : *group_ptr(cn, i + RD - NI);
+        if (i < N1) {
+#pragma unroll
+          for (int ww = 0; ww < G; ++ww) {
+            const int kf = i * G + ww;
+            acc = PR::mfma(PR::pick(grp, ww), kf < NZ ? xz[kf < NZ ? kf : 0] : xe[kf < NZ ? 0 : kf - NZ], acc);
+          }
+          if (i == N1 - 1) {
+            // bias, GELU, mask -> operand of the second product
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4)
+#pragma unroll
+              for (int j = 0; j < 4; ++j) acc[4 * r4 + j] += b1v[r4][j];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) gp[q] = PR::pack2(gelu(acc[2 * q]), gelu(acc[2 * q + 1]), amask);
+          }
+        } else {
+#pragma unroll
+          for (int ww = 0; ww < G; ++ww) {
+            const int F = (i - N1) * G + ww;
+            dz[F / NF2] = PR::mfma(PR::pick(grp, ww), PR::gfrag(gp, F % NF2), dz[F / NF2]);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+
+    // ---- reduce the partial updates through LDS
+    uint8_t* mine = red + (size_t)w * REGION;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        f32x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = dz[b][4 * r4 + i];
+        *reinterpret_cast<f32x4*>(mine + (b * 4 + r4) * 1024 + lane * 16) = v;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int bq = 0; bq < NBQ; ++bq) {
+      const int b = w * NBQ + bq;
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        f32x4 sum = *reinterpret_cast<const f32x4*>(red + (b * 4 + r4) * 1024 + lane * 16);
+#pragma unroll
+        for (int ww = 1; ww < SPLIT; ++ww)
+          sum += *reinterpret_cast<const f32x4*>(red + (size_t)ww * REGION + (b * 4 + r4) * 1024 + lane * 16);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          zq[bq][4 * r4 + i] += sum[i] + t_b2[(b * 2 + h) * 16 + 4 * r4 + i] * actf;
+      }
+    }
+    __syncthreads();                            // region space becomes the X buffer
+    // ---- publish the X fragments of the owned blocks, read back all of X
+#pragma unroll
+    for (int bq = 0; bq < NBQ; ++bq)
+#pragma unroll
+      for (int f = 0; f < NF2; ++f) {
+        const int kf = (w * NBQ + bq) * NF2 + f;
+        float v[SL];
+#pragma unroll
+        for (int j = 0; j < SL; ++j) v[j] = zq[bq][f * SL + j];
+        const Frag x = PR::cvt(v);
+        *reinterpret_cast<Frag*>(xbuf + frag_offset<PR>(kf, lane, 0)) = x;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int kf = 0; kf < NZ; ++kf) xz[kf] = *reinterpret_cast<const Frag*>(xbuf + frag_offset<PR>(kf, lane, 0));
+    __syncthreads();                            // X read before the next step's partial updates
+  }
+  if (errbits) atomicOr(a.err, errbits);
+  if (valid) {
+    float* zo = a.zT + (size_t)cand * D;
+#pragma unroll
+    for (int bq = 0; bq < NBQ; ++bq)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        f32x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = zq[bq][4 * r4 + i];
+        *reinterpret_cast<f32x4*>(zo + 32 * (w * NBQ + bq) + acc_row(h, 4 * r4)) = v;
+      }
+  }
+}
+
+// ==========================================================================
 // Action features: phi_i = (1/len_i) sum_t e_t.  One thread per
 // (candidate, 4 features).
 
@@ -944,6 +1193,8 @@ hipError_t launch_score_t(const DevModel& m, const ScoreArgs& a, int blocks, hip
 
 // Wavefronts per workgroup: as many as keep at least one workgroup per
 // compute unit (256), so small batches spread over more units.
+constexpr int SPLIT_MAX_TILES = 256;   // = compute units
+
 inline int pick_waves(int tiles) {
   if (tiles >= 4 * 256) return 4;
   if (tiles >= 2 * 256) return 2;
@@ -982,6 +1233,19 @@ hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const Se
   return hipGetLastError();
 }
 
+template <class PR, int D, int E, int SPLIT>
+hipError_t launch_rollout_split_t(const DevModel& m, const RollArgs& a, int tiles, hipStream_t st) {
+  const int lds = m.roll_tab_bytes + SPLIT * (D / 32) * 4 * 1024;
+  auto kern = rollout_split_kernel<PR, D, E, SPLIT>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
+  }
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * SPLIT), lds, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
                           int32_t B, int32_t T_max, float* zT, int32_t* err, hipStream_t st) {
@@ -994,11 +1258,20 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
   const int waves = pick_waves(tiles);
   const int blocks = (tiles + waves - 1) / waves;
   const int prec = m.prec, d = m.dims.d, e = m.dims.embed_dim;
-#define WM_ROLL(PR, D, E)                                                         \
-  {                                                                               \
-    if (waves == 4) return launch_rollout_t<PR, D, E, 4>(m, a, blocks, st);       \
-    if (waves == 2) return launch_rollout_t<PR, D, E, 2>(m, a, blocks, st);       \
-    return launch_rollout_t<PR, D, E, 1>(m, a, blocks, st);                       \
+  // At most one tile per compute unit: split each tile's hidden units over
+  // the compute unit's SIMDs instead (d <= 256: the partial updates fit LDS).
+  const bool split = tiles <= SPLIT_MAX_TILES && d <= 256;
+#define WM_ROLL(PR, D, E)                                                                \
+  {                                                                                      \
+    /* fp32 at d = 256 does not fit the split kernel's registers */                    \
+    if constexpr (D <= 256 && (PR::G == 1 || D <= 64)) {                                 \
+      constexpr int SPLIT = (D / 32) >= 4 ? 4 : (D / 32);                                \
+      if (split && m.dims.trans_hidden / 32 >= SPLIT)                                    \
+        return launch_rollout_split_t<PR, D, E, SPLIT>(m, a, tiles, st);                 \
+    }                                                                                    \
+    if (waves == 4) return launch_rollout_t<PR, D, E, 4>(m, a, blocks, st);              \
+    if (waves == 2) return launch_rollout_t<PR, D, E, 2>(m, a, blocks, st);              \
+    return launch_rollout_t<PR, D, E, 1>(m, a, blocks, st);                              \
   }
   WM_FOR_ALL_DE(WM_ROLL)
 #undef WM_ROLL
