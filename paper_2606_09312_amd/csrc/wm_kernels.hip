@@ -847,16 +847,16 @@ __global__ __launch_bounds__(256) void phi_kernel(const float* __restrict__ emb,
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int t = 0; t < len; ++t) {
     const int ty = clampi(types[(size_t)i * T_max + t], 0, K - 1);
-    float s[4];
+    float sv[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) s[q] = t_emb[ty * E + f0 + q];
+    for (int q = 0; q < 4; ++q) sv[q] = t_emb[ty * E + f0 + q];
     for (int p = 0; p < P; ++p) {
       const float u = log2f((float)params[((size_t)i * T_max + t) * P + p]);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) s[q] = fmaf(t_pw[p * E + f0 + q], u, s[q]);
+      for (int q = 0; q < 4; ++q) sv[q] = fmaf(t_pw[p * E + f0 + q], u, sv[q]);
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[q] += s[q] + t_pb[f0 + q];
+    for (int q = 0; q < 4; ++q) acc[q] += sv[q] + t_pb[f0 + q];
   }
   const float inv = len > 0 ? 1.0f / (float)len : 0.0f;
   f32x4 o;
@@ -993,6 +993,105 @@ __global__ __launch_bounds__(64 * WAVES, 1) void score_kernel(const ScoreArgs a)
   }
 }
 
+// Cost model for small batches: a workgroup of SPLIT wavefronts per 32
+// candidates, wavefront w taking cost-hidden chunks w, w + SPLIT, ... with
+// fragments read straight from L2; the partial scores are summed through LDS
+// in a fixed order (deterministic).
+template <class PR, int D, int E, int SPLIT>
+__global__ __launch_bounds__(64 * SPLIT, 1) void score_split_kernel(const ScoreArgs a) {
+  using Frag = typename PR::Frag;
+  constexpr int KF = PR::KF, SL = PR::SL, G = PR::G;
+  constexpr int NX = (D + E) / KF;
+  constexpr int MAXH = SCORE_MAX_HW / KF;
+  constexpr int HPL = SCORE_HW_PER_LAUNCH;
+  __shared__ float red[SPLIT][HPL][64];
+  const int CB = a.chunk_bytes;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int n = lane & 31, h = lane >> 5;
+  const int NH = a.HW / KF;
+  const int NC = a.C / 32;
+  const int cand = blockIdx.x * 32 + n;
+  const bool valid = cand < a.B;
+  const int ci = valid ? cand : 0;
+
+  Frag x[NX];
+#pragma unroll
+  for (int kf = 0; kf < NX; ++kf) {
+    float v[SL];
+#pragma unroll
+    for (int j = 0; j < SL; ++j) {
+      const int f = nat_feature<PR>(kf, h, j);
+      v[j] = f < D ? a.zT[(size_t)ci * D + f] : a.phi[(size_t)ci * E + (f - D)];
+    }
+    x[kf] = PR::cvt(v);
+  }
+  Frag hf[HPL][MAXH];
+#pragma unroll
+  for (int jj = 0; jj < HPL; ++jj)
+#pragma unroll
+    for (int q = 0; q < MAXH; ++q) {
+      float v[SL];
+#pragma unroll
+      for (int j = 0; j < SL; ++j)
+        v[j] = (jj < a.nj && q < NH) ? a.hw[(size_t)(a.j0 + jj) * a.HW + nat_feature<PR>(q, h, j)] : 0.0f;
+      hf[jj][q] = PR::cvt(v);
+    }
+  float part[HPL];
+#pragma unroll
+  for (int jj = 0; jj < HPL; ++jj) part[jj] = 0.0f;
+
+  for (int c = w; c < NC; c += SPLIT) {
+    const uint8_t* cb = a.cost + (size_t)c * CB;
+    f32x16 acc = {};
+#pragma unroll
+    for (int g = 0; g < NX / G; ++g) {
+      const u32x4 grp = *reinterpret_cast<const u32x4*>(cb + g * 1024 + lane * 16);
+#pragma unroll
+      for (int ww = 0; ww < G; ++ww) acc = PR::mfma(PR::pick(grp, ww), x[g * G + ww], acc);
+    }
+    const float* tail = reinterpret_cast<const float*>(cb + (CB - 256));
+    float bc1t[16], wc2t[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      bc1t[r] = tail[16 * h + r];
+      wc2t[r] = tail[32 + 16 * h + r];
+    }
+#pragma unroll
+    for (int jj = 0; jj < HPL; ++jj) {
+      if (jj < a.nj) {
+        f32x16 accj = acc;
+#pragma unroll
+        for (int q = 0; q < MAXH; ++q) {
+          if (q < NH) {
+            const int F = NX + q;
+            const u32x4 grp = *reinterpret_cast<const u32x4*>(cb + (F / G) * 1024 + lane * 16);
+            accj = PR::mfma(PR::pick(grp, F % G), hf[jj][q], accj);
+          }
+        }
+        float sum = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sum = fmaf(wc2t[r], gelu(accj[r] + bc1t[r]), sum);
+        part[jj] += sum;
+      }
+    }
+  }
+#pragma unroll
+  for (int jj = 0; jj < HPL; ++jj) red[w][jj][lane] = part[jj];
+  __syncthreads();
+  if (w == 0) {
+#pragma unroll
+    for (int jj = 0; jj < HPL; ++jj) {
+      if (jj < a.nj) {
+        float y = red[0][jj][lane];
+#pragma unroll
+        for (int ww = 1; ww < SPLIT; ++ww) y += red[ww][jj][lane];
+        y += __shfl_xor(y, 32) + a.bc2;
+        if (valid && h == 0) a.scores[(size_t)(a.j0 + jj) * a.B + cand] = y;
+      }
+    }
+  }
+}
+
 // ==========================================================================
 // Encoder: one workgroup per subgraph.  In bf16 mode the input and the hidden
 // layer are rounded to bf16 (the weights already are).
@@ -1071,15 +1170,34 @@ __device__ uint32_t radix_select(int n, int need, KeyF key, PredF pred, uint32_t
       hist_w[b] = s;
     }
     __syncthreads();
-    if (tid == 0) {
-      int rem = need, digit = 0;
-      for (int b = 255; b >= 0; --b) {
-        const int c = (int)hist_w[b];
-        if (c >= rem) { digit = b; break; }
-        rem -= c;
+    if (tid < 64) {
+      // lane l holds bins 255-4l .. 252-4l; an inclusive scan over lanes
+      // (highest bins first) finds the bin where the count reaches `need`
+      const int l = tid;
+      int c4[4], sum = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        c4[q] = (int)hist_w[255 - 4 * l - q];
+        sum += c4[q];
       }
-      shared_int[0] = digit;
-      shared_int[1] = rem;
+      int incl = sum;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int v = __shfl_up(incl, off);
+        if (l >= off) incl += v;
+      }
+      const unsigned long long hit = __ballot(incl >= need);
+      const int first = __ffsll((long long)hit) - 1;
+      if (l == first) {
+        int rem = need - (incl - sum), digit = 255 - 4 * l;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (c4[q] >= rem) { digit = 255 - 4 * l - q; break; }
+          rem -= c4[q];
+        }
+        shared_int[0] = digit;
+        shared_int[1] = rem;
+      }
     }
     __syncthreads();
     const int digit = shared_int[0];
@@ -1152,7 +1270,8 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const float* __restr
     }
   }
   for (int r = tid; r < k; r += TOPK_THREADS) {
-    const int li = (int)(~(uint32_t)(sel[r] & 0xFFFFFFFFull));
+    // (exactly k keys are selected; the clamp only guards the read)
+    const int li = clampi((int)(~(uint32_t)(sel[r] & 0xFFFFFFFFull)), 0, n - 1);
     const size_t o = ((size_t)j * S + s) * k + r;
     idx[o] = lo + li;
     if (val) val[o] = y[li];
@@ -1303,7 +1422,10 @@ hipError_t launch_score(const DevModel& m, const float* zT, const float* phi, in
     hipError_t err = hipErrorInvalidValue;
 #define WM_SCORE(PR, D, E)                                                       \
   {                                                                              \
-    if (waves == 4) err = launch_score_t<PR, D, E, 4>(m, a, blocks, st);         \
+    if (tiles <= SPLIT_MAX_TILES && a.C / 32 >= 4) {                             \
+      hipLaunchKernelGGL((score_split_kernel<PR, D, E, 4>), dim3(tiles), dim3(256), 0, st, a); \
+      err = hipGetLastError();                                                   \
+    } else if (waves == 4) err = launch_score_t<PR, D, E, 4>(m, a, blocks, st);  \
     else if (waves == 2) err = launch_score_t<PR, D, E, 2>(m, a, blocks, st);    \
     else err = launch_score_t<PR, D, E, 1>(m, a, blocks, st);                    \
   }
