@@ -11,6 +11,9 @@ Sec. 3.4), recurrent rollout over the action sequence (Sec. 3.4, Sec. 3.6),
 action features phi = mean of the step embeddings, score
 y = wc2 GELU(Wc1 [z_T; phi; h] + bc1) + bc2 (Eq. 3, Eq. 12), within-workload
 ranking by descending score with the lower index first on ties (Sec. 3.5).
+The paper-form transition (norm="l2", Sec. 3.4 with TransH hyperplanes)
+removes from z its component along the unit vector of Wh e before the
+update and rescales the updated state to unit length.
 """
 from __future__ import annotations
 
@@ -53,9 +56,16 @@ def _vec(W, name):
     return [float(x) for x in W[name]]
 
 
-def candidate(W, z0_row, types_row, params_rows, length, hw_rows, bf16):
+def _scale_to_unit(vec):
+    """vec / |vec| (Euclidean); a zero vector is returned unchanged."""
+    n = math.sqrt(math.fsum(x * x for x in vec))
+    return [x / n for x in vec] if n > 0 else list(vec)
+
+
+def candidate(W, z0_row, types_row, params_rows, length, hw_rows, bf16, norm="none"):
     """Roll out and score one candidate.  Returns (zT, phi, [y_j for each hw])."""
     W1, W2, Wc1 = _mat(W, "w1", bf16), _mat(W, "w2", bf16), _mat(W, "wc1", bf16)
+    Wh = _mat(W, "wh", bf16) if norm == "l2" else None
     b1, b2, bc1, wc2 = _vec(W, "b1"), _vec(W, "b2"), _vec(W, "bc1"), _vec(W, "wc2")
     bc2 = float(W["bc2"])
     temb = [[float(x) for x in row] for row in W["type_emb"]]
@@ -73,6 +83,12 @@ def candidate(W, z0_row, types_row, params_rows, length, hw_rows, bf16):
             for p in range(len(u)):
                 s += pw[f][p] * u[p]
             e.append(s + pb[f])
+        if norm == "l2":
+            # unit normal of the action's hyperplane, then drop z's part along it
+            er = [_rnd(v, bf16) for v in e]
+            nrm = _scale_to_unit([sum(Wh[r][c] * er[c] for c in range(E)) for r in range(d)])
+            along = sum(nrm[r] * z[r] for r in range(d))
+            z = [z[r] - along * nrm[r] for r in range(d)]
         x = [_rnd(v, bf16) for v in z + e]
         g = []
         for r in range(len(W1)):
@@ -86,7 +102,7 @@ def candidate(W, z0_row, types_row, params_rows, length, hw_rows, bf16):
             for c in range(len(g)):
                 s += W2[r][c] * g[c]
             znew.append(z[r] + (s + b2[r]))
-        z = znew
+        z = _scale_to_unit(znew) if norm == "l2" else znew
         for f in range(E):
             acc[f] += e[f]
     phi = [a / length for a in acc] if length > 0 else [0.0] * E
@@ -122,7 +138,7 @@ def encode_row(W, feat_row, bf16):
     return out
 
 
-def evaluate(W, inputs, k, precision):
+def evaluate(W, inputs, k, precision, norm="none"):
     """Whole path, candidate by candidate; top-k by a full Python sort."""
     bf16 = precision == "bf16"
     seg_off = [int(v) for v in inputs["seg_off"]]
@@ -137,7 +153,7 @@ def evaluate(W, inputs, k, precision):
         for i in range(seg_off[s], seg_off[s + 1]):
             L = int(inputs["lens"][i])
             zi, pi, yi = candidate(W, z0[s], inputs["types"][i], inputs["params"][i], L,
-                                   inputs["hw"], bf16)
+                                   inputs["hw"], bf16, norm)
             zT.append(zi)
             phi.append(pi)
             ys.append(yi)

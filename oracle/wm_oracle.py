@@ -22,9 +22,23 @@ model, type-embedding plus linear(log2 params) action embedding):
   y    = wc2 . GELU(Wc1 . [z_T; phi; h] + bc1) + bc2
   GELU(x) = x * (1 + erf(x / sqrt 2)) / 2
 
+Paper-form transition (norm="l2"; Sec. 3.4: the state is first moved into
+an action-conditioned hyperplane in the manner of TransH [Wang et al., AAAI
+2014], then updated by the residual network, then normalised; the losses
+of Sec. 3.4 live in that normalised space):
+
+  v    = Wh . e_t                  normal of the action's hyperplane
+  z'   = z - (w . z) w,  w = v / ||v||_2   (z' = z when v = 0)
+  u    = z' + W2 . GELU(W1 . [z'; e_t] + b1) + b2
+  z_t  = u / ||u||_2                       (z_t = u when u = 0)
+
+z_0 itself is used as given (only transition outputs are normalised), and
+an empty sequence still returns z_0.
+
 bf16 mode rounds, to the nearest bfloat16 with ties to even (function R),
-exactly the matrix-product operands: the matrices W1, W2, Wc1, We1, We2 once,
-and the vectors [z; e], GELU(.) of the transition, [z_T; phi; h], the encoder
+exactly the matrix-product operands: the matrices W1, W2, Wc1, We1, We2 (and
+Wh) once, and the vectors [z; e] (z' in the paper form), e as the operand of
+Wh, GELU(.) of the transition, [z_T; phi; h], the encoder
 input and the encoder hidden layer.  Everything else (biases, the embedding,
 the residual sum, phi, the cost hidden layer and the final wc2 dot) stays
 unrounded.  The oracle evaluates all of this in float64.
@@ -46,7 +60,8 @@ ERR_INVALID_ARGUMENT = 1
 ERR_UNSUPPORTED = 2
 ERR_INPUT_RANGE = 5
 
-MATRICES = ("w1", "w2", "wc1", "we1", "we2")
+MATRICES = ("w1", "w2", "wc1", "we1", "we2", "wh")
+NORMS = ("none", "l2")
 
 
 def bf16_round(x) -> np.ndarray:
@@ -98,11 +113,32 @@ def embed(W, types_t: np.ndarray, params_t: np.ndarray) -> np.ndarray:
     return W["type_emb"][types_t] + u @ W["param_w"].T + W["param_b"]
 
 
-def transition(W, z: np.ndarray, e: np.ndarray, precision: str) -> np.ndarray:
-    """One application of F (Eq. 1 / Eq. 8): residual two-layer MLP on [z; e]."""
+def _unit_rows(v: np.ndarray) -> np.ndarray:
+    """Each row divided by its Euclidean norm; all-zero rows stay zero."""
+    n = np.sqrt(np.sum(v * v, axis=1, keepdims=True))
+    return np.divide(v, n, out=np.zeros_like(v), where=n > 0)
+
+
+def hyperplane_project(W, z: np.ndarray, e: np.ndarray, precision: str) -> np.ndarray:
+    """z - (w . z) w with w the unit normal Wh . e of the action (Sec. 3.4, TransH)."""
+    w = _unit_rows(_R(e, precision) @ W["wh"].T)
+    return z - np.sum(w * z, axis=1, keepdims=True) * w
+
+
+def transition(W, z: np.ndarray, e: np.ndarray, precision: str, norm: str = "none") -> np.ndarray:
+    """One application of F (Eq. 1 / Eq. 8): residual two-layer MLP on [z; e].
+
+    norm="l2" is the paper's form (Sec. 3.4): project z onto the action's
+    hyperplane first, and normalise the result to unit length.
+    """
+    if norm not in NORMS:
+        raise ValueError(norm)
+    if norm == "l2":
+        z = hyperplane_project(W, z, e, precision)
     x = _R(np.concatenate([z, e], axis=1), precision)
     g = _R(gelu(x @ W["w1"].T + W["b1"]), precision)
-    return z + (g @ W["w2"].T + W["b2"])
+    u = z + (g @ W["w2"].T + W["b2"])
+    return _unit_rows(u) if norm == "l2" else u
 
 
 def encode(W, feats: np.ndarray, precision: str) -> np.ndarray:
@@ -121,7 +157,7 @@ def segment_of(seg_off: np.ndarray, B: int) -> np.ndarray:
 
 
 def rollout(W, z0: np.ndarray, seg_off, types, params, lens, precision: str,
-            trajectory: bool = False):
+            trajectory: bool = False, norm: str = "none"):
     """Multi-step latent rollout over ragged action sequences (Sec. 3.4, 3.6).
 
     Each candidate i starts from z0 of its subgraph and applies F once per
@@ -139,7 +175,7 @@ def rollout(W, z0: np.ndarray, seg_off, types, params, lens, precision: str,
     for t in range(T):
         act = np.nonzero(lens > t)[0]
         e = embed(W, types[act, t], params[act, t, :])
-        z[act] = transition(W, z[act], e, precision)
+        z[act] = transition(W, z[act], e, precision, norm)
         acc[act] += e
         if trajectory:
             traj.append(z.copy())
@@ -227,7 +263,8 @@ def validate(dims: Dict[str, int], *, B, T_max, seg_off, k=None, n_hw=None,
 
 
 def evaluate(weights: Dict[str, np.ndarray], inputs: Dict[str, np.ndarray], k: int,
-             precision: str, dims: Optional[Dict[str, int]] = None) -> Dict[str, np.ndarray]:
+             precision: str, dims: Optional[Dict[str, int]] = None,
+             norm: str = "none") -> Dict[str, np.ndarray]:
     """The whole hot path: [encode], rollout, score, top-k (Eq. 2-3, Sec. 3.6)."""
     W = prepare(weights, precision)
     if "feats" in inputs:
@@ -235,7 +272,7 @@ def evaluate(weights: Dict[str, np.ndarray], inputs: Dict[str, np.ndarray], k: i
     else:
         z0 = np.asarray(inputs["z0"], dtype=np.float64)
     zT, phi = rollout(W, z0, inputs["seg_off"], inputs["types"], inputs["params"],
-                      inputs["lens"], precision)
+                      inputs["lens"], precision, norm=norm)
     y = score(W, zT, phi, inputs["hw"], precision)
     idx, val = topk(y, inputs["seg_off"], k)
     return {"z0": z0, "zT": zT, "phi": phi, "scores": y, "idx": idx, "val": val}

@@ -114,7 +114,7 @@ def scaled(w: Workload, B: int, S: Optional[int] = None, **kw) -> Workload:
 # the standard deviation of its layer's weight.
 WEIGHT_ORDER = (
     "type_emb", "param_w", "param_b", "w1", "b1", "w2", "b2",
-    "wc1", "bc1", "wc2", "bc2", "we1", "be1", "we2", "be2",
+    "wc1", "bc1", "wc2", "bc2", "we1", "be1", "we2", "be2", "wh",
 )
 
 
@@ -132,6 +132,9 @@ def _weight_shapes(w: Workload):
         "bc1": ((w.C,), w.cost_in),
         "wc2": ((w.C,), w.C),
         "bc2": ((), w.C),
+        # hyperplane-normal map of the paper-form transition (drawn last, so
+        # the tensors above do not depend on whether it is used)
+        "wh": ((w.d, w.e), w.e),
     }
     if w.feat_dim:
         s.update({
