@@ -16,6 +16,17 @@
  *   y_j  = wc2 . GELU(Wc1 . [z_T; phi; h_j] + bc1) + bc2
  *   GELU(x) = x (1 + erf(x / sqrt 2)) / 2
  *
+ * With norm = WM_NORM_L2 the transition takes the paper's own form (Sec. 3.4:
+ * a TransH-style move into an action-conditioned hyperplane, the residual
+ * update, then normalisation):
+ *
+ *   v    = Wh . e_t,   w = v / |v|_2           (w = 0 when v = 0)
+ *   z'   = z_{t-1} - (w . z_{t-1}) w
+ *   u    = z' + W2 . GELU(W1 . [z'; e_t] + b1) + b2
+ *   z_t  = u / |u|_2                           (z_t = u when u = 0)
+ *
+ * z_0 is used as given (an empty sequence returns it unscaled).
+ *
  * Conventions for every call below:
  *  - Pointers are device pointers unless marked HOST.  All tensors are dense,
  *    row-major, C-contiguous, 4-byte elements (float32 or int32), and must be
@@ -69,7 +80,7 @@ typedef enum wm_precision {
 
 typedef enum wm_norm {
   WM_NORM_NONE = 0, /* residual MLP transition as above */
-  WM_NORM_L2 = 1    /* L2-normalise z after every step (Sec. 3.4); not built: WM_ERR_UNSUPPORTED */
+  WM_NORM_L2 = 1    /* hyperplane projection before, unit length after every step (Sec. 3.4) */
 } wm_norm;
 
 /* Model shape.  d: latent width; embed_dim: action-embedding width e;
@@ -96,19 +107,21 @@ typedef struct wm_dims {
  *   w1 [H][d+e] (columns: z then e), b1 [H], w2 [d][H], b2 [d],
  *   wc1 [C][d+e+hw_dim] (columns: z_T, phi, h), bc1 [C], wc2 [C], bc2,
  *   we1 [enc_hidden][feat_dim], be1 [enc_hidden], we2 [d][enc_hidden], be2 [d]
- *   (encoder pointers may be NULL when feat_dim = 0). */
+ *   (encoder pointers may be NULL when feat_dim = 0),
+ *   wh [d][e]: hyperplane-normal map of WM_NORM_L2 (may be NULL otherwise). */
 typedef struct wm_weights {
   const float *type_emb, *param_w, *param_b;
   const float *w1, *b1, *w2, *b2;
   const float *wc1, *bc1, *wc2;
   float bc2;
   const float *we1, *be1, *we2, *be2;
+  const float *wh;
 } wm_weights;
 
 typedef struct wm_model wm_model;
 
 /* Copy the weights to the current HIP device, rounding the matrices
- * W1, W2, Wc1, We1, We2 to bfloat16 (nearest-even) in WM_BF16 mode and
+ * W1, W2, Wc1, We1, We2 (and Wh) to bfloat16 (nearest-even) in WM_BF16 mode and
  * repacking them into the kernels' matrix-fragment order.  Synchronous.
  * The model is immutable: concurrent calls with distinct workspaces are safe.
  * Errors: INVALID_ARGUMENT (null pointer, non-positive dims), UNSUPPORTED,

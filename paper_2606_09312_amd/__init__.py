@@ -5,7 +5,7 @@ kernels behind the C ABI of include/wm.h; this package is the thin Python
 binding over it.
 """
 from .binding import (  # noqa: F401
-    KERNELS, PRECISIONS, SYMBOLS, WMError, Model, device_status, encode_init, evaluate,
+    KERNELS, NORMS, PRECISIONS, SYMBOLS, WMError, Model, device_status, encode_init, evaluate,
     load_library, rollout, score, timing_enable, timing_read, topk,
 )
 

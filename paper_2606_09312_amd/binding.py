@@ -20,6 +20,7 @@ WM_ERR_OUT_OF_MEMORY, WM_ERR_DEVICE, WM_ERR_INPUT_RANGE = 3, 4, 5
 WM_FP32, WM_BF16 = 0, 1
 WM_NORM_NONE, WM_NORM_L2 = 0, 1
 PRECISIONS = {"fp32": WM_FP32, "bf16": WM_BF16}
+NORMS = {"none": WM_NORM_NONE, "l2": WM_NORM_L2}
 KERNELS = {"rollout": 0, "score": 1, "topk": 2, "bucket": 3, "phi": 4, "encode": 5}
 
 # Exported symbols (kept in step with include/wm.h).
@@ -52,6 +53,7 @@ class Weights(ctypes.Structure):
         ("w1", _FP), ("b1", _FP), ("w2", _FP), ("b2", _FP),
         ("wc1", _FP), ("bc1", _FP), ("wc2", _FP), ("bc2", ctypes.c_float),
         ("we1", _FP), ("be1", _FP), ("we2", _FP), ("be2", _FP),
+        ("wh", _FP),
     ]
 
 
@@ -127,15 +129,19 @@ def _stream(stream):
 class Model:
     """Device copy of the evaluator's weights (wm_model_create)."""
 
-    def __init__(self, dims: Dict[str, int], weights: Dict[str, np.ndarray], precision: str = "bf16"):
+    def __init__(self, dims: Dict[str, int], weights: Dict[str, np.ndarray], precision: str = "bf16",
+                 norm: str = "none"):
+        """norm="l2" selects the paper-form transition (hyperplane projection
+        and unit length; needs weights["wh"])."""
         lib = load_library()
         self.dims = dict(dims)
         self.precision = precision
+        self.norm = norm
         d = Dims(d=dims["d"], embed_dim=dims["e"], n_kinds=dims["n_kinds"],
                  n_params=dims["n_params"], trans_hidden=dims["H"], cost_hidden=dims["C"],
                  hw_dim=dims["hw_dim"], feat_dim=dims.get("feat_dim", 0),
                  enc_hidden=dims.get("enc_hidden", 0), precision=PRECISIONS[precision],
-                 norm=dims.get("norm", WM_NORM_NONE))
+                 norm=NORMS[norm])
         self._keep = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in weights.items()}
         w = Weights()
         for name, _ in Weights._fields_:

@@ -124,6 +124,22 @@ std::vector<uint8_t> pack_cost(const wm_dims& dm, const wm_weights& w) {
   return blk;
 }
 
+// Hyperplane-normal map: block b, fragment q over the embedding (natural
+// order) -> rows 32b + L%32 of Wh.
+template <class Gm>
+std::vector<uint8_t> pack_hyper(const wm_dims& dm, const wm_weights& w) {
+  const int D = dm.d, E = dm.embed_dim, NE = E / Gm::KF;
+  std::vector<uint8_t> blk((size_t)HyperGeom<Gm>::bytes(D, E), 0);
+  for (int b = 0; b < D / 32; ++b)
+    for (int q = 0; q < NE; ++q)
+      for (int L = 0; L < 64; ++L)
+        for (int j = 0; j < Gm::SL; ++j) {
+          const int m = L & 31, h = L >> 5;
+          put<Gm>(blk, 0, b * NE + q, L, j, w.wh[(size_t)(32 * b + m) * E + nat_feature<Gm>(q, h, j)]);
+        }
+  return blk;
+}
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct WsLayout {
@@ -221,7 +237,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
     return fail(WM_ERR_INVALID_ARGUMENT, "unknown precision");
   if (dm.norm != WM_NORM_NONE && dm.norm != WM_NORM_L2)
     return fail(WM_ERR_INVALID_ARGUMENT, "unknown norm");
-  if (dm.norm == WM_NORM_L2) return fail(WM_ERR_UNSUPPORTED, "WM_NORM_L2 is not built");
+  if (dm.norm == WM_NORM_L2 && !w->wh) return fail(WM_ERR_INVALID_ARGUMENT, "WM_NORM_L2 needs wh");
   if (!w->type_emb || !w->param_w || !w->param_b || !w->w1 || !w->b1 || !w->w2 || !w->b2 ||
       !w->wc1 || !w->bc1 || !w->wc2)
     return fail(WM_ERR_INVALID_ARGUMENT, "null weight pointer");
@@ -238,10 +254,12 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.dims = dm;
   m.prec = dm.precision;
   const int D = dm.d, E = dm.embed_dim, K = dm.n_kinds, P = dm.n_params, HW = dm.hw_dim;
-  std::vector<uint8_t> tw1, tw2, cost;
+  std::vector<uint8_t> tw1, tw2, cost, twh;
+  const bool l2 = dm.norm == WM_NORM_L2;
   if (m.prec == WM_BF16) {
     pack_transition<GeomBF16>(dm, *w, tw1, tw2);
     cost = pack_cost<GeomBF16>(dm, *w);
+    if (l2) twh = pack_hyper<GeomBF16>(dm, *w);
     m.w1_chunk_bytes = TransChunk<GeomBF16>::w1_bytes(D, E);
     m.w2_chunk_bytes = TransChunk<GeomBF16>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomBF16>::bytes(D, E, HW);
@@ -249,6 +267,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
     if ((D + E + HW) % 8 != 0) return fail(WM_ERR_UNSUPPORTED, "fp32 needs d + embed_dim + hw_dim % 8 == 0");
     pack_transition<GeomF32>(dm, *w, tw1, tw2);
     cost = pack_cost<GeomF32>(dm, *w);
+    if (l2) twh = pack_hyper<GeomF32>(dm, *w);
     m.w1_chunk_bytes = TransChunk<GeomF32>::w1_bytes(D, E);
     m.w2_chunk_bytes = TransChunk<GeomF32>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomF32>::bytes(D, E, HW);
@@ -266,6 +285,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
       for (int r = 0; r < 16; ++r) tab.push_back(w->b2[32 * b + acc_row(h, r)]);
   while (tab.size() % 4) tab.push_back(0.0f);
   m.roll_tab_bytes = (int)(tab.size() * 4);
+  m.wh_bytes = (int)twh.size();
   if (rollout_lds_bytes(m) > 160 * 1024 || 2 * m.cost_chunk_bytes > 160 * 1024)
     return fail(WM_ERR_UNSUPPORTED, "weight chunks do not fit the 160 KiB LDS");
 
@@ -291,6 +311,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   const size_t o_tw1 = off; off = align256(off + tw1.size());
   const size_t o_tw2 = off; off = align256(off + tw2.size());
   const size_t o_cost = off; off = align256(off + cost.size());
+  const size_t o_wh = off; off = align256(off + twh.size());
   const size_t o_tab = off; off = align256(off + tab.size() * 4);
   const size_t o_enc = off; off = align256(off + enc.size() * 4);
   void* dev = nullptr;
@@ -302,6 +323,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   hipError_t e = hipMemcpy(base + o_tw1, tw1.data(), tw1.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_tw2, tw2.data(), tw2.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_cost, cost.data(), cost.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess && !twh.empty()) e = hipMemcpy(base + o_wh, twh.data(), twh.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_tab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess && !enc.empty()) e = hipMemcpy(base + o_enc, enc.data(), enc.size() * 4, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
@@ -312,6 +334,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.trans_w1 = base + o_tw1;
   m.trans_w2 = base + o_tw2;
   m.cost = base + o_cost;
+  m.trans_wh = twh.empty() ? nullptr : base + o_wh;
   m.roll_tab = reinterpret_cast<const float*>(base + o_tab);
   m.emb_nat = m.roll_tab;
   const float* encp = reinterpret_cast<const float*>(base + o_enc);

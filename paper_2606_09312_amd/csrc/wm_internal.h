@@ -107,6 +107,23 @@ struct CostChunk {
   static constexpr int bytes(int D, int E, int HW) { return ngroups(D, E, HW) * 1024 + 256; }
 };
 
+// Hyperplane-normal map Wh [d][e] of the paper-form transition, packed as
+// A-operand fragments of the product V^T = Wh . E^T: block b (rows
+// [32b, 32b+32) of Wh, i.e. features of the latent in accumulator layout)
+// holds E/KF fragments over the embedding in natural order, so the B operand
+// is the step's embedding fragment set and V lands in the latent's layout.
+template <class Gm>
+struct HyperGeom {
+  static constexpr int groups_per_block(int E) { return E / Gm::KF / Gm::G; }
+  static constexpr int bytes(int D, int E) { return (D / 32) * groups_per_block(E) * 1024; }
+};
+// The rollout kernel keeps Wh in LDS when the double-buffered chunks leave
+// room for it (and for the embedding table), otherwise streams it from L2.
+constexpr int WH_LDS_LIMIT = 112 * 1024;
+constexpr bool wh_in_lds(int w1_chunk_bytes, int w2_chunk_bytes, int wh_bytes) {
+  return 2 * (w1_chunk_bytes + w2_chunk_bytes) + wh_bytes <= WH_LDS_LIMIT;
+}
+
 // Action parameters per step are padded to PMAX in the embedding table
 // (zero weights), so the kernels loop over a fixed count.
 constexpr int PMAX = 8;
@@ -127,6 +144,7 @@ struct DevModel {
   const uint8_t* trans_w1;  // H/32 transition chunks, W1 part
   const uint8_t* trans_w2;  // H/32 transition chunks, W2 part
   const uint8_t* cost;      // C/32 cost chunks
+  const uint8_t* trans_wh;  // Wh fragments (WM_NORM_L2 only)
   const float* roll_tab;    // type_emb [K][E], param_w^T [PMAX][E] (zero rows past P), param_b [E], b2 (acc order) [D]
   const float* emb_nat;     // the first three parts of roll_tab
   const float* enc_w1t;     // We1^T [F][Fh] (bf16-rounded values in bf16 mode)
@@ -135,6 +153,7 @@ struct DevModel {
   const float* enc_b2;      // [D]
   float bc2;
   int w1_chunk_bytes, w2_chunk_bytes, cost_chunk_bytes, roll_tab_bytes;
+  int wh_bytes;             // 0 unless WM_NORM_L2
 };
 
 // Launchers (wm_kernels.hip).  Return hipSuccess or the launch error.

@@ -212,6 +212,7 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
 struct RollArgs {
   const uint8_t* w1;        // packed transition chunks, W1 part
   const uint8_t* w2;        // packed transition chunks, W2 part
+  const uint8_t* wh;        // packed hyperplane-normal map (paper-form transition)
   const float* tab;         // rollout table (see DevModel::roll_tab)
   const float* z0;          // [S][D]
   const int2* perm;         // sorted (candidate, subgraph)
@@ -379,7 +380,123 @@ struct Roll {
 // first product of chunk c+1 runs on the matrix cores, then the second
 // product of chunk c; meanwhile the W2 part of chunk c+1 and the W1 part of
 // chunk c+2 are copied into the buffers freed by the previous iteration.
-template <class PR, int D, int E, int WAVES>
+// Paper-form transition (Sec. 3.4, TransH-style hyperplanes): before the
+// residual update the latent loses its component along the unit normal of
+// the action's hyperplane, v = Wh . e_t, and after it the latent is scaled to
+// unit length.  Both are applied at the start of a step, on the previous
+// step's output u:  z' = (u - alpha v) s  with  s = 1/|u|  (when the previous
+// step was a real step of this candidate) and  alpha = (v.u)/(v.v)  (when
+// this step is one), which equals normalising first and projecting onto the
+// hyperplane of unit normal v/|v| afterwards.  V^T = Wh . E^T runs on the
+// matrix cores with the step's embedding fragments as B operand, so v lands
+// in the latent's accumulator layout; the dot products are per-lane partial
+// sums completed across the lane pair (L, L^32) that holds one candidate.
+template <class PR, int D, int E>
+struct Hyper {
+  using Frag = typename PR::Frag;
+  static constexpr int NE = E / PR::KF, NB = D / 32, G = PR::G;
+  static constexpr int GPB = HyperGeom<PR>::groups_per_block(E);   // fragment groups per block
+  static constexpr int NG = NB * GPB;
+  static constexpr int BYTES = HyperGeom<PR>::bytes(D, E);
+  // keep V in registers between the two passes where the latent leaves room
+  static constexpr bool HOLD = D <= 64 || (G == 1 && D <= 256);
+
+  static __device__ __forceinline__ u32x4 group(const uint8_t* src, int g, int lane) {
+    return *reinterpret_cast<const u32x4*>(src + g * 1024 + lane * 16);
+  }
+  // Per-lane base address for reads from global memory, made opaque to the
+  // optimiser: otherwise the loop-invariant address of every fragment group
+  // is hoisted out of the step loop and kept live (64 bits each), which
+  // spills.  LDS addresses need no such care (16-bit immediate offsets).
+  static __device__ __forceinline__ const uint8_t* lane_base(const uint8_t* src, int lane) {
+    const uint8_t* p = src + lane * 16;
+    asm volatile("" : "+v"(p));
+    return p;
+  }
+  static __device__ __forceinline__ float pair_sum(float x) { return x + __shfl_xor(x, 32); }
+
+  // One pass over V block by block (RD fragment-group reads in flight).
+  //   PASS 0: partial dots v.z, v.v, z.z (and V kept when HOLD)
+  //   PASS 1: z <- (z - al v) s
+  template <int PASS, int RD, bool GLOBAL>
+  static __device__ __forceinline__ void pass(const uint8_t* src, const Frag (&xe)[NE],
+                                              f32x16 (&z)[NB], f32x16 (&vh)[HOLD ? NB : 1],
+                                              float& vz, float& vv, float& zz, float al, float s,
+                                              int lane) {
+    // global source: lane offset folded into an opaque base (lane argument 0)
+    const uint8_t* base = GLOBAL ? lane_base(src, lane) : src;
+    const int ln = GLOBAL ? 0 : lane;
+    u32x4 ring[RD];
+#pragma unroll
+    for (int i = 0; i < RD && i < NG; ++i) ring[i] = group(base, i, ln);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      f32x16 vb = {};
+#pragma unroll
+      for (int k = 0; k < GPB; ++k) {
+        const int g = b * GPB + k;
+        const u32x4 grp = ring[g % RD];
+        if (g + RD < NG) ring[g % RD] = group(base, g + RD, ln);
+#pragma unroll
+        for (int w = 0; w < G; ++w) vb = PR::mfma(PR::pick(grp, w), xe[k * G + w], vb);
+        // keep the reads RD groups ahead, not hoisted all to the top
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (PASS == 0) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          vz = fmaf(vb[r], z[b][r], vz);
+          vv = fmaf(vb[r], vb[r], vv);
+          zz = fmaf(z[b][r], z[b][r], zz);
+        }
+        if constexpr (HOLD) vh[b] = vb;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) z[b][r] = (z[b][r] - al * vb[r]) * s;
+      }
+    }
+  }
+
+  template <int RD, bool GLOBAL>
+  static __device__ __forceinline__ void step_in(f32x16 (&z)[NB], const Frag (&xe)[NE],
+                                                 const uint8_t* src, bool project, bool renorm,
+                                                 int lane) {
+    float vz = 0.0f, vv = 0.0f, zz = 0.0f;
+    f32x16 vh[HOLD ? NB : 1];
+    pass<0, RD, GLOBAL>(src, xe, z, vh, vz, vv, zz, 0.0f, 1.0f, lane);
+    vz = pair_sum(vz);
+    vv = pair_sum(vv);
+    zz = pair_sum(zz);
+    const float s = (renorm && zz > 0.0f) ? rsqrtf(zz) : 1.0f;
+    const float al = (project && vv > 0.0f) ? vz / vv : 0.0f;
+    if constexpr (HOLD) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) z[b][r] = (z[b][r] - al * vh[b][r]) * s;
+    } else {
+      pass<1, RD, GLOBAL>(src, xe, z, vh, vz, vv, zz, al, s, lane);
+    }
+  }
+
+  // z <- z / |z| (when `renorm` and z != 0)
+  static __device__ __forceinline__ void unit(f32x16 (&z)[NB], bool renorm) {
+    float zz = 0.0f;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) zz = fmaf(z[b][r], z[b][r], zz);
+    zz = pair_sum(zz);
+    const float s = (renorm && zz > 0.0f) ? rsqrtf(zz) : 1.0f;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) z[b][r] *= s;
+  }
+};
+
+template <class PR, int D, int E, int WAVES, bool NORM>
 __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a) {
   using R = Roll<PR, D, E>;
   using Frag = typename PR::Frag;
@@ -396,6 +513,10 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
   __shared__ __attribute__((aligned(16))) uint8_t w1b[W1B];
   __shared__ __attribute__((aligned(16))) uint8_t w2a[W2B];
   __shared__ __attribute__((aligned(16))) uint8_t w2b[W2B];
+  using HY = Hyper<PR, D, E>;
+  // the hyperplane-normal map stays in LDS when it fits beside the chunks
+  constexpr bool WH_LDS = NORM && wh_in_lds(W1B, W2B, HY::BYTES);
+  __shared__ __attribute__((aligned(16))) uint8_t whs[WH_LDS ? HY::BYTES : 16];
   extern __shared__ __attribute__((aligned(16))) float tab[];
   const float* t_emb = tab;                       // [K][E]
   const float* t_pw = tab + a.K * E;              // [PMAX][E], zero rows past P
@@ -412,6 +533,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
   stage_fixed<W1B, NT>(a.w1, w1a, tid);
   stage_fixed<W2B, NT>(a.w2, w2a, tid);
   if constexpr (PIPE) stage_fixed<W1B, NT>(a.w1 + W1B, w1b, tid);
+  if constexpr (WH_LDS) stage_fixed<HY::BYTES, NT>(a.wh, whs, tid);
 
   const int pos = (blockIdx.x * WAVES + wave) * 32 + n;
   const bool valid = pos < a.B;
@@ -491,6 +613,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
       for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * actf;
       xe[q] = PR::cvt(ev);
     }
+    if constexpr (NORM) {
+      // unit length for the previous step's output, hyperplane projection for this step
+      if constexpr (WH_LDS) HY::template step_in<4, false>(zacc, xe, whs, active, t > 0 && t <= len, lane);
+      else HY::template step_in<8, true>(zacc, xe, a.wh, active, t > 0 && t <= len, lane);
+    }
     // ---- z operand fragments (state at the start of the step)
     Frag xz[NZ];
 #pragma unroll
@@ -561,6 +688,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
 #pragma unroll
       for (int r = 0; r < 16; ++r) zacc[b][r] += t_b2[(b * 2 + h) * 16 + r] * actf;
   }
+  // outputs of a workgroup's longest sequences still need their unit length
+  if constexpr (NORM) HY::unit(zacc, T_wg > 0 && T_wg <= len);
   if (errbits) atomicOr(a.err, errbits);
 
   if (valid) {
@@ -604,7 +733,14 @@ struct SplitGeom {
   static constexpr int RD = ring_depth();       // loads in flight (divides NI)
 };
 
-template <class PR, int D, int E, int SPLIT>
+//
+// Paper-form transition: wavefront w also forms v = Wh . e for its own latent
+// blocks (Wh fragments of those blocks stay in registers), and at the end of
+// step t it folds the unit length of u_t and the projection of step t+1 into
+// its blocks: the three dot products u.u, v.u, v.v are summed over the
+// wavefronts through a small LDS area, in the same barrier interval as the
+// partial-update reduction.
+template <class PR, int D, int E, int SPLIT, bool NORM>
 __global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const RollArgs a) {
   using R = Roll<PR, D, E>;
   using SG = SplitGeom<PR, D, E>;
@@ -625,6 +761,9 @@ __global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const Roll
   const float* t_b2 = t_pb + E;
   uint8_t* red = reinterpret_cast<uint8_t*>(tab) + a.tab_bytes;   // SPLIT regions
   uint8_t* xbuf = red;                          // X fragments (reuses region space)
+  float* dots = reinterpret_cast<float*>(red + (size_t)SPLIT * REGION);   // [SPLIT][3][32]
+  using HY = Hyper<PR, D, E>;
+  constexpr int GPB = HY::GPB;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
@@ -674,6 +813,113 @@ __global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const Roll
   }
   int errbits = 0;
 
+  // Embedding fragments of step s (zero past the candidate's length); reads
+  // the prefetched action of step s and prefetches step s + 1.
+  auto embed_step = [&](int s, Frag (&xe)[NE]) {
+    const bool act = s < len;
+    const float af = act ? 1.0f : 0.0f;
+    const bool bad_type = act && (nx_type < 0 || nx_type >= a.K);
+    const int ty = (act && !bad_type) ? nx_type : 0;
+    bool bad_par = false;
+    float u[PMAX];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) {
+      bad_par |= act && nx_par[p] < 1;
+      u[p] = act ? log2f((float)nx_par[p]) : 0.0f;
+    }
+    errbits |= (bad_type ? ERRBIT_TYPE : 0) | (bad_par ? ERRBIT_PARAM : 0);
+    if (s + 1 < len) {
+      nx_type = ty_row[s + 1];
+#pragma unroll
+      for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(s + 1) * a.P + p];
+    }
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      const int f0 = KF * q + SL * h;
+      float ev[SL], tmp[SL];
+      R::row(t_emb + ty * E + f0, ev);
+#pragma unroll
+      for (int p = 0; p < PMAX; ++p) {
+        R::row(t_pw + p * E + f0, tmp);
+#pragma unroll
+        for (int j = 0; j < SL; ++j) ev[j] = fmaf(tmp[j], u[p], ev[j]);
+      }
+      R::row(t_pb + f0, tmp);
+#pragma unroll
+      for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * af;
+      xe[q] = PR::cvt(ev);
+    }
+  };
+
+  // Paper form: Wh fragments of the owned blocks (constant over the launch).
+  u32x4 whq[NORM ? NBQ * GPB : 1];
+  if constexpr (NORM) {
+#pragma unroll
+    for (int i = 0; i < NBQ * GPB; ++i) whq[i] = HY::group(a.wh, w * NBQ * GPB + i, lane);
+  }
+  // Paper form, end of a step: zq <- (zq - alpha v) s over the owned blocks,
+  // s = 1/|u| when the finished step was one of this candidate's, alpha =
+  // (v.u)/(v.v) for the projection of step tn when that is one of its steps.
+  auto boundary = [&](const Frag (&xe)[NE], bool renorm, bool project) {
+    f32x16 vq[NBQ];
+    float vz = 0.0f, vv = 0.0f, zz = 0.0f;
+#pragma unroll
+    for (int bq = 0; bq < NBQ; ++bq) {
+      f32x16 vb = {};
+#pragma unroll
+      for (int k = 0; k < GPB; ++k)
+#pragma unroll
+        for (int ww = 0; ww < G; ++ww) vb = PR::mfma(PR::pick(whq[bq * GPB + k], ww), xe[k * G + ww], vb);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        vz = fmaf(vb[r], zq[bq][r], vz);
+        vv = fmaf(vb[r], vb[r], vv);
+        zz = fmaf(zq[bq][r], zq[bq][r], zz);
+      }
+      vq[bq] = vb;
+    }
+    vz = HY::pair_sum(vz);
+    vv = HY::pair_sum(vv);
+    zz = HY::pair_sum(zz);
+    if (h == 0) {
+      dots[(w * 3 + 0) * 32 + n] = vz;
+      dots[(w * 3 + 1) * 32 + n] = vv;
+      dots[(w * 3 + 2) * 32 + n] = zz;
+    }
+    __syncthreads();
+    vz = 0.0f; vv = 0.0f; zz = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < SPLIT; ++ww) {
+      vz += dots[(ww * 3 + 0) * 32 + n];
+      vv += dots[(ww * 3 + 1) * 32 + n];
+      zz += dots[(ww * 3 + 2) * 32 + n];
+    }
+    const float sc = (renorm && zz > 0.0f) ? rsqrtf(zz) : 1.0f;
+    const float al = (project && vv > 0.0f) ? vz / vv : 0.0f;
+#pragma unroll
+    for (int bq = 0; bq < NBQ; ++bq)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) zq[bq][r] = (zq[bq][r] - al * vq[bq][r]) * sc;
+  };
+  // publish the X fragments of the owned blocks, read back all of X
+  auto exchange_x = [&]() {
+#pragma unroll
+    for (int bq = 0; bq < NBQ; ++bq)
+#pragma unroll
+      for (int f = 0; f < NF2; ++f) {
+        const int kf = (w * NBQ + bq) * NF2 + f;
+        float v[SL];
+#pragma unroll
+        for (int j = 0; j < SL; ++j) v[j] = zq[bq][f * SL + j];
+        const Frag x = PR::cvt(v);
+        *reinterpret_cast<Frag*>(xbuf + frag_offset<PR>(kf, lane, 0)) = x;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int kf = 0; kf < NZ; ++kf) xz[kf] = *reinterpret_cast<const Frag*>(xbuf + frag_offset<PR>(kf, lane, 0));
+    __syncthreads();                            // X read before the next step's partial updates
+  };
+
   // A-fragment group i of chunk c (W1 part first, then W2 part)
   auto group_ptr = [&](int c, int i) -> const u32x4* {
     const uint8_t* base = i < N1 ? a.w1 + (size_t)c * W1B + (size_t)i * 1024
@@ -688,42 +934,19 @@ __global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const Roll
 
   wait_vm_then_barrier();
 
+  Frag xe[NE];
+  if constexpr (NORM) {
+    // step 0: embedding, projection of z0 (no unit length: z0 is used as given)
+    embed_step(0, xe);
+    boundary(xe, false, 0 < len);
+    exchange_x();
+  }
+
   for (int t = 0; t < T_wg; ++t) {
     const bool active = t < len;
     const float actf = active ? 1.0f : 0.0f;
     const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
-    const bool bad_type = active && (nx_type < 0 || nx_type >= a.K);
-    const int ty = (active && !bad_type) ? nx_type : 0;
-    bool bad_par = false;
-    float u[PMAX];
-#pragma unroll
-    for (int p = 0; p < PMAX; ++p) {
-      bad_par |= active && nx_par[p] < 1;
-      u[p] = active ? log2f((float)nx_par[p]) : 0.0f;
-    }
-    errbits |= (bad_type ? ERRBIT_TYPE : 0) | (bad_par ? ERRBIT_PARAM : 0);
-    if (t + 1 < len) {
-      nx_type = ty_row[t + 1];
-#pragma unroll
-      for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(t + 1) * a.P + p];
-    }
-    Frag xe[NE];
-#pragma unroll
-    for (int q = 0; q < NE; ++q) {
-      const int f0 = KF * q + SL * h;
-      float ev[SL], tmp[SL];
-      R::row(t_emb + ty * E + f0, ev);
-#pragma unroll
-      for (int p = 0; p < PMAX; ++p) {
-        R::row(t_pw + p * E + f0, tmp);
-#pragma unroll
-        for (int j = 0; j < SL; ++j) ev[j] = fmaf(tmp[j], u[p], ev[j]);
-      }
-      R::row(t_pb + f0, tmp);
-#pragma unroll
-      for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * actf;
-      xe[q] = PR::cvt(ev);
-    }
+    if constexpr (!NORM) embed_step(t, xe);
 
     f32x16 dz[NB];
 #pragma unroll
@@ -793,23 +1016,14 @@ __global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const Roll
           zq[bq][4 * r4 + i] += sum[i] + t_b2[(b * 2 + h) * 16 + 4 * r4 + i] * actf;
       }
     }
-    __syncthreads();                            // region space becomes the X buffer
-    // ---- publish the X fragments of the owned blocks, read back all of X
-#pragma unroll
-    for (int bq = 0; bq < NBQ; ++bq)
-#pragma unroll
-      for (int f = 0; f < NF2; ++f) {
-        const int kf = (w * NBQ + bq) * NF2 + f;
-        float v[SL];
-#pragma unroll
-        for (int j = 0; j < SL; ++j) v[j] = zq[bq][f * SL + j];
-        const Frag x = PR::cvt(v);
-        *reinterpret_cast<Frag*>(xbuf + frag_offset<PR>(kf, lane, 0)) = x;
-      }
-    __syncthreads();
-#pragma unroll
-    for (int kf = 0; kf < NZ; ++kf) xz[kf] = *reinterpret_cast<const Frag*>(xbuf + frag_offset<PR>(kf, lane, 0));
-    __syncthreads();                            // X read before the next step's partial updates
+    if constexpr (NORM) {
+      // the barrier inside also turns the region space into the X buffer
+      embed_step(t + 1, xe);
+      boundary(xe, active, t + 1 < len);
+    } else {
+      __syncthreads();                          // region space becomes the X buffer
+    }
+    exchange_x();
   }
   if (errbits) atomicOr(a.err, errbits);
   if (valid) {
@@ -1284,10 +1498,10 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const float* __restr
 namespace {
 
 
-template <class PR, int D, int E, int WAVES>
+template <class PR, int D, int E, int WAVES, bool NORM>
 hipError_t launch_rollout_t(const DevModel& m, const RollArgs& a, int blocks, hipStream_t st) {
-  const int lds = m.roll_tab_bytes;   // the two chunk buffers are static
-  auto kern = rollout_kernel<PR, D, E, WAVES>;
+  const int lds = m.roll_tab_bytes;   // the chunk buffers are static
+  auto kern = rollout_kernel<PR, D, E, WAVES, NORM>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();   // do not leave the error for the caller's next HIP call
@@ -1342,7 +1556,9 @@ bool have_kernels(int prec, int d, int e) {
 }
 
 int rollout_lds_bytes(const DevModel& m) {
-  return 2 * (m.w1_chunk_bytes + m.w2_chunk_bytes) + m.roll_tab_bytes;
+  int b = 2 * (m.w1_chunk_bytes + m.w2_chunk_bytes) + m.roll_tab_bytes;
+  if (m.wh_bytes && wh_in_lds(m.w1_chunk_bytes, m.w2_chunk_bytes, m.wh_bytes)) b += m.wh_bytes;
+  return b;
 }
 
 hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
@@ -1352,10 +1568,11 @@ hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const Se
   return hipGetLastError();
 }
 
-template <class PR, int D, int E, int SPLIT>
+template <class PR, int D, int E, int SPLIT, bool NORM>
 hipError_t launch_rollout_split_t(const DevModel& m, const RollArgs& a, int tiles, hipStream_t st) {
-  const int lds = m.roll_tab_bytes + SPLIT * (D / 32) * 4 * 1024;
-  auto kern = rollout_split_kernel<PR, D, E, SPLIT>;
+  // table, SPLIT partial-update regions, and (paper form) the dot-product area
+  const int lds = m.roll_tab_bytes + SPLIT * (D / 32) * 4 * 1024 + (NORM ? SPLIT * 3 * 32 * 4 : 0);
+  auto kern = rollout_split_kernel<PR, D, E, SPLIT, NORM>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -1365,11 +1582,28 @@ hipError_t launch_rollout_split_t(const DevModel& m, const RollArgs& a, int tile
   return hipGetLastError();
 }
 
+// One (precision, d, e, transition form): split kernel for at most one tile
+// per compute unit, else the persistent kernel with 1, 2 or 4 wavefronts per
+// workgroup.
+template <class PR, int D, int E, bool NORM>
+hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, int blocks,
+                             int waves, bool split, hipStream_t st) {
+  // fp32 at d = 256 does not fit the split kernel's registers
+  if constexpr (D <= 256 && (PR::G == 1 || D <= 64)) {
+    constexpr int SPLIT = (D / 32) >= 4 ? 4 : (D / 32);
+    if (split && m.dims.trans_hidden / 32 >= SPLIT)
+      return launch_rollout_split_t<PR, D, E, SPLIT, NORM>(m, a, tiles, st);
+  }
+  if (waves == 4) return launch_rollout_t<PR, D, E, 4, NORM>(m, a, blocks, st);
+  if (waves == 2) return launch_rollout_t<PR, D, E, 2, NORM>(m, a, blocks, st);
+  return launch_rollout_t<PR, D, E, 1, NORM>(m, a, blocks, st);
+}
+
 hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
                           int32_t B, int32_t T_max, float* zT, int32_t* err, hipStream_t st) {
   RollArgs a;
-  a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.tab = m.roll_tab; a.z0 = z0; a.perm = perm; a.types = types;
+  a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.wh = m.trans_wh; a.tab = m.roll_tab; a.z0 = z0; a.perm = perm; a.types = types;
   a.params = params; a.lens = lens; a.zT = zT; a.err = err; a.B = B; a.T_max = T_max;
   a.P = m.dims.n_params; a.K = m.dims.n_kinds; a.H = m.dims.trans_hidden;
   a.tab_bytes = m.roll_tab_bytes;
@@ -1380,18 +1614,10 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
   // At most one tile per compute unit: split each tile's hidden units over
   // the compute unit's SIMDs instead (d <= 256: the partial updates fit LDS).
   const bool split = tiles <= SPLIT_MAX_TILES && d <= 256;
+  const bool norm = m.dims.norm == WM_NORM_L2;
 #define WM_ROLL(PR, D, E)                                                                \
-  {                                                                                      \
-    /* fp32 at d = 256 does not fit the split kernel's registers */                    \
-    if constexpr (D <= 256 && (PR::G == 1 || D <= 64)) {                                 \
-      constexpr int SPLIT = (D / 32) >= 4 ? 4 : (D / 32);                                \
-      if (split && m.dims.trans_hidden / 32 >= SPLIT)                                    \
-        return launch_rollout_split_t<PR, D, E, SPLIT>(m, a, tiles, st);                 \
-    }                                                                                    \
-    if (waves == 4) return launch_rollout_t<PR, D, E, 4>(m, a, blocks, st);              \
-    if (waves == 2) return launch_rollout_t<PR, D, E, 2>(m, a, blocks, st);              \
-    return launch_rollout_t<PR, D, E, 1>(m, a, blocks, st);                              \
-  }
+  return norm ? launch_rollout_de<PR, D, E, true>(m, a, tiles, blocks, waves, split, st)  \
+              : launch_rollout_de<PR, D, E, false>(m, a, tiles, blocks, waves, split, st);
   WM_FOR_ALL_DE(WM_ROLL)
 #undef WM_ROLL
   return hipErrorInvalidValue;

@@ -57,7 +57,7 @@ def test_model_create_rejects_before_device_work():
     lib = wm.load_library()
     h = ctypes.c_void_p()
     assert lib.wm_model_create(None, None, ctypes.byref(h)) == B.WM_ERR_INVALID_ARGUMENT
-    # unsupported latent width and the unbuilt normalised transition
+    # unsupported latent width, bad transition form, hidden width
     w = {k: np.zeros(4, np.float32) for k in ("type_emb", "param_w", "param_b", "w1", "b1", "w2",
                                                  "b2", "wc1", "bc1", "wc2")}
     wts = B.Weights()
@@ -69,8 +69,11 @@ def test_model_create_rejects_before_device_work():
                hw_dim=16, feat_dim=0, enc_hidden=0, precision=B.WM_FP32, norm=B.WM_NORM_NONE)
     assert lib.wm_model_create(ctypes.byref(d), ctypes.byref(wts), ctypes.byref(h)) == B.WM_ERR_UNSUPPORTED
     d.d = 64
+    # the paper-form transition needs its hyperplane-normal map; unknown forms are rejected
     d.norm = B.WM_NORM_L2
-    assert lib.wm_model_create(ctypes.byref(d), ctypes.byref(wts), ctypes.byref(h)) == B.WM_ERR_UNSUPPORTED
+    assert lib.wm_model_create(ctypes.byref(d), ctypes.byref(wts), ctypes.byref(h)) == B.WM_ERR_INVALID_ARGUMENT
+    d.norm = 7
+    assert lib.wm_model_create(ctypes.byref(d), ctypes.byref(wts), ctypes.byref(h)) == B.WM_ERR_INVALID_ARGUMENT
     d.norm = B.WM_NORM_NONE
     d.trans_hidden = 96   # not a multiple of 64
     assert lib.wm_model_create(ctypes.byref(d), ctypes.byref(wts), ctypes.byref(h)) == B.WM_ERR_UNSUPPORTED
