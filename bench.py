@@ -27,9 +27,10 @@ PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense matrix-core peaks
 PEAK_HBM_GBS = 8000.0
 
 
-def step_flops(w) -> int:
-    """Matrix-product FLOPs of one transition step of one candidate."""
-    return 2 * w.H * (w.d + w.e) + 2 * w.H * w.d
+def step_flops(w, norm: str = "none") -> int:
+    """Matrix-product FLOPs of one transition step of one candidate (the
+    paper form adds the hyperplane normal Wh . e)."""
+    return 2 * w.H * (w.d + w.e) + 2 * w.H * w.d + (2 * w.d * w.e if norm == "l2" else 0)
 
 
 def score_flops(w) -> int:
@@ -38,15 +39,16 @@ def score_flops(w) -> int:
     return 2 * w.C * (w.d + w.e) + w.n_hw * (2 * w.C * w.hw_dim + 2 * w.C)
 
 
-def rollout_bytes(w, lens) -> int:
+def rollout_bytes(w, lens, norm: str = "none") -> int:
     """Algorithmic HBM bytes of one rollout launch: valid action entries,
     lengths, initial latents, transition weights once, terminal latents."""
     steps = int(lens.sum())
-    wbytes = (2 if PREC == "bf16" else 4) * (w.H * (w.d + w.e) + w.d * w.H)
+    wbytes = (2 if PREC == "bf16" else 4) * (w.H * (w.d + w.e) + w.d * w.H
+                                             + (w.d * w.e if norm == "l2" else 0))
     return steps * 4 * (1 + w.n_params) + 4 * w.B + 4 * w.S * w.d + wbytes + 4 * w.B * w.d
 
 
-def cpu_baseline(w, W, I, prec, budget_s: float):
+def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none"):
     """Oracle throughput on a bounded random sample of the batch (candidates
     are independent, so throughput scales with the sample)."""
     from oracle import wm_oracle as O
@@ -66,7 +68,8 @@ def cpu_baseline(w, W, I, prec, budget_s: float):
         sub = {"types": I["types"][pick], "params": I["params"][pick], "lens": I["lens"][pick],
                "z0": z0[seg_of[pick]], "seg_off": np.arange(n + 1)}
         t0 = time.perf_counter()
-        zT, phi = O.rollout(Wd, sub["z0"], sub["seg_off"], sub["types"], sub["params"], sub["lens"], prec)
+        zT, phi = O.rollout(Wd, sub["z0"], sub["seg_off"], sub["types"], sub["params"], sub["lens"],
+                            prec, norm=norm)
         y = O.score(Wd, zT, phi, I["hw"], prec)
         O.topk(y, [0, n], min(w.k, n))
         total_t += time.perf_counter() - t0
@@ -88,6 +91,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="ansor_round", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--precision", default=None, choices=["fp32", "bf16"])
+    ap.add_argument("--norm", default="none", choices=["none", "l2"],
+                    help="transition form: residual MLP (none) or the paper's projected, "
+                         "unit-length form (l2)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -107,7 +113,7 @@ def main():
     dev = torch.device("cuda:0")
     W = synth.make_weights(w, 1000)
     I = synth.make_inputs(w, 2000)
-    model = wm.Model(wm.model_dims(w), W, precision=prec)
+    model = wm.Model(wm.model_dims(w), W, precision=prec, norm=args.norm)
     t = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in I.items() if k != "seg_off"}
     init = t["feats"] if "feats" in t else t["z0"]
     scores = torch.empty((w.n_hw, w.B), dtype=torch.float32, device=dev)
@@ -152,7 +158,7 @@ def main():
         torch.cuda.synchronize()
 
     lens = I["lens"].astype(np.int64)
-    flops_roll = int(lens.sum()) * step_flops(w)
+    flops_roll = int(lens.sum()) * step_flops(w, args.norm)
     roll_s = kern["rollout"]["avg_ms"] / 1e3
     achieved = flops_roll / roll_s / 1e12
     peak = PEAK_TFLOPS[prec]
@@ -175,16 +181,18 @@ def main():
         "config": {"workload": f"{w.name}: B={w.B} candidates, S={w.S} subgraphs, d={w.d}, "
                                f"e={w.e}, H={w.H}, C={w.C}, T_max={w.T_max}, k={w.k}, "
                                f"n_hw={w.n_hw}", "precision": prec,
+                   "transition": "residual MLP" if args.norm == "none" else
+                                 "hyperplane projection + residual MLP + unit length",
                    "global_batch": w.B, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "rollout", "achieved": achieved, "peak": peak,
                      "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
                      "flop_per_launch": flops_roll,
-                     "algorithmic_bytes_per_launch": rollout_bytes(w, lens)},
+                     "algorithmic_bytes_per_launch": rollout_bytes(w, lens, args.norm)},
         "kernels_avg_ms": {k: v["avg_ms"] for k, v in kern.items()},
         "whole_path_tflops": total_flops * args.steps / elapsed / 1e12,
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(w, W, I, prec, args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(w, W, I, prec, args.cpu_budget, args.norm)
     print(json.dumps(out), flush=True)
 
 
