@@ -143,14 +143,15 @@ std::vector<uint8_t> pack_hyper(const wm_dims& dm, const wm_weights& w) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t err, perm, z0, zT, phi, scores, total;
+  size_t err, perm, hist, z0, zT, phi, scores, total;
 };
 
-WsLayout ws_layout(const DevModel& m, int B, int S, int n_hw) {
+WsLayout ws_layout(const DevModel& m, int B, int T_max, int S, int n_hw) {
   WsLayout L;
   size_t o = 0;
   L.err = o; o += 256;
   L.perm = o; o = align256(o + (size_t)B * sizeof(int2));
+  L.hist = o; o = align256(o + (size_t)bucket_groups(B) * (size_t)(T_max + 1) * 4);
   L.z0 = o; o = align256(o + (size_t)S * m.dims.d * 4);
   L.zT = o; o = align256(o + (size_t)B * m.dims.d * 4);
   L.phi = o; o = align256(o + (size_t)B * m.dims.embed_dim * 4);
@@ -360,8 +361,8 @@ void wm_model_destroy(wm_model* model) {
 }
 
 size_t wm_workspace_bytes(const wm_model* model, int32_t B, int32_t T_max, int32_t S, int32_t n_hw) {
-  if (!model || B < 0 || T_max < 0 || S < 1 || n_hw < 1) return 0;
-  return ws_layout(model->dm, B, S, n_hw).total;
+  if (!model || B < 0 || T_max < 0 || T_max > WM_MAX_T || S < 1 || n_hw < 1) return 0;
+  return ws_layout(model->dm, B, T_max, S, n_hw).total;
 }
 
 wm_status wm_encode_init(const wm_model* model, const float* feats, int32_t S, float* z0,
@@ -398,14 +399,14 @@ wm_status wm_rollout(const wm_model* model, const float* z0, const int32_t* seg_
   int32_t min_seg = 0;
   if ((s = check_segments(seg_off, S, B, &seg, &min_seg)) != WM_OK) return s;
   if (!ws) return fail(WM_ERR_INVALID_ARGUMENT, "workspace is NULL");
-  const WsLayout L = ws_layout(model->dm, B, S, 1);
+  const WsLayout L = ws_layout(model->dm, B, T_max, S, 1);
   if (ws_bytes < L.total) return fail(WM_ERR_INVALID_ARGUMENT, "workspace too small");
   if (B == 0) return ok();
   hipStream_t st = static_cast<hipStream_t>(stream);
   uint8_t* w8 = static_cast<uint8_t*>(ws);
   int32_t* err = reinterpret_cast<int32_t*>(w8 + L.err);
   int2* perm = reinterpret_cast<int2*>(w8 + L.perm);
-  WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, err, st));
+  WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, reinterpret_cast<int32_t*>(w8 + L.hist), err, st));
   WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zT, err, st));
   if (phi) WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
   return ok();
@@ -462,7 +463,7 @@ wm_status wm_evaluate(const wm_model* model, const float* init, int32_t init_is_
   if (!idx) return fail(WM_ERR_INVALID_ARGUMENT, "idx is NULL");
   if (model->dm.dims.hw_dim > 0 && !hw) return fail(WM_ERR_INVALID_ARGUMENT, "hw is NULL");
   if (!ws) return fail(WM_ERR_INVALID_ARGUMENT, "workspace is NULL");
-  const WsLayout L = ws_layout(model->dm, B, S, n_hw);
+  const WsLayout L = ws_layout(model->dm, B, T_max, S, n_hw);
   if (ws_bytes < L.total) return fail(WM_ERR_INVALID_ARGUMENT, "workspace too small");
 
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -477,7 +478,7 @@ wm_status wm_evaluate(const wm_model* model, const float* init, int32_t init_is_
   float* zTo = zT ? zT : reinterpret_cast<float*>(w8 + L.zT);
   float* phi = reinterpret_cast<float*>(w8 + L.phi);
   float* sc = scores ? scores : reinterpret_cast<float*>(w8 + L.scores);
-  WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, err, st));
+  WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, reinterpret_cast<int32_t*>(w8 + L.hist), err, st));
   WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zTo, err, st));
   WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
   WM_TIMED(TK_SCORE, st, launch_score(model->dm, zTo, phi, B, hw, n_hw, sc, st));

@@ -128,6 +128,21 @@ constexpr bool wh_in_lds(int w1_chunk_bytes, int w2_chunk_bytes, int wh_bytes) {
 // (zero weights), so the kernels loop over a fixed count.
 constexpr int PMAX = 8;
 
+// Bucketing: one workgroup sorts batches of up to BUCKET_SINGLE_MAX
+// candidates; larger batches use three passes over chunks of candidates
+// (per-chunk length histograms in the workspace, one scan, a scatter).
+constexpr int BUCKET_SINGLE_MAX = 8192;
+constexpr int BUCKET_CHUNK = 4096;
+// Chunks of a multi-workgroup bucketing (0: the single-workgroup kernel);
+// at most 256 chunks, so the scan stays small for any batch.
+inline int bucket_chunk(int B) {
+  const int c = (B + 255) / 256;
+  return c > BUCKET_CHUNK ? c : BUCKET_CHUNK;
+}
+inline int bucket_groups(int B) {
+  return B <= BUCKET_SINGLE_MAX ? 0 : (B + bucket_chunk(B) - 1) / bucket_chunk(B);
+}
+
 // Device error bits (workspace error word).
 enum : int { ERRBIT_LEN = 1, ERRBIT_TYPE = 2, ERRBIT_PARAM = 4 };
 
@@ -157,8 +172,9 @@ struct DevModel {
 };
 
 // Launchers (wm_kernels.hip).  Return hipSuccess or the launch error.
+// hist: bucket_groups(B) * (T_max + 1) ints of workspace (unused when 0)
 hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
-                         int2* perm, int32_t* err, hipStream_t st);
+                         int2* perm, int32_t* hist, int32_t* err, hipStream_t st);
 hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
                           int32_t B, int32_t T_max, float* zT, int32_t* err, hipStream_t st);

@@ -197,6 +197,104 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
   }
 }
 
+// Large batches: the same counting sort over chunks of candidates, one
+// workgroup per chunk.  Pass 1 writes each chunk's length histogram to
+// hist[chunk][L]; pass 2 (one workgroup) turns the histograms into each
+// chunk's first output position per length (longest lengths first, chunks
+// in order within a length); pass 3 scatters every chunk from those cursors.
+
+__global__ __launch_bounds__(1024) void bucket_count_kernel(const int32_t* __restrict__ lens, int B,
+                                                             int T_max, int chunk,
+                                                             int32_t* __restrict__ hist,
+                                                             int32_t* __restrict__ err) {
+  extern __shared__ int bsm[];
+  const int nb = T_max + 1, tid = threadIdx.x, nt = blockDim.x;
+  for (int L = tid; L < nb; L += nt) bsm[L] = 0;
+  __syncthreads();
+  const int lo = blockIdx.x * chunk, hi = min(lo + chunk, B);
+  int bad = 0;
+  for (int i = lo + tid; i < hi; i += nt) {
+    int L = lens[i];
+    if (L < 0 || L > T_max) { bad = 1; L = clampi(L, 0, T_max); }
+    atomicAdd(&bsm[L], 1);
+  }
+  if (bad) atomicOr(err, ERRBIT_LEN);
+  __syncthreads();
+  for (int L = tid; L < nb; L += nt) hist[(size_t)blockIdx.x * nb + L] = bsm[L];
+}
+
+// Exclusive scan of one value per thread over the workgroup (1024 threads).
+__device__ __forceinline__ int block_exclusive_scan(int v, int* wsum) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[w] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int k = 0; k < nw; ++k) { const int t = wsum[k]; wsum[k] = acc; acc += t; }
+  }
+  __syncthreads();
+  return wsum[w] + x - v;
+}
+
+__global__ __launch_bounds__(1024) void bucket_scan_kernel(int T_max, int groups,
+                                                            int32_t* __restrict__ hist) {
+  extern __shared__ int bsm[];
+  int* base = bsm;                       // [nb]: first position of each length
+  int* wsum = bsm + (T_max + 1);         // [16]
+  const int nb = T_max + 1, tid = threadIdx.x, nt = blockDim.x;
+  // thread tid owns positions [tid*per, tid*per + per) of the length order
+  // T_max, T_max - 1, ..., 0 (longest first)
+  const int per = (nb + nt - 1) / nt;
+  int own = 0;
+  for (int j = tid * per; j < min(nb, tid * per + per); ++j) {
+    const int L = T_max - j;
+    int tot = 0;
+    for (int g = 0; g < groups; ++g) tot += hist[(size_t)g * nb + L];
+    base[L] = tot;
+    own += tot;
+  }
+  int run = block_exclusive_scan(own, wsum);
+  for (int j = tid * per; j < min(nb, tid * per + per); ++j) {
+    const int L = T_max - j;
+    const int tot = base[L];
+    base[L] = run;
+    run += tot;
+  }
+  __syncthreads();
+  // per-chunk cursors: chunks in order within each length
+  for (int L = tid; L < nb; L += nt) {
+    int c = base[L];
+    for (int g = 0; g < groups; ++g) {
+      const int v = hist[(size_t)g * nb + L];
+      hist[(size_t)g * nb + L] = c;
+      c += v;
+    }
+  }
+}
+
+__global__ __launch_bounds__(1024) void bucket_scatter_kernel(const int32_t* __restrict__ lens,
+                                                               int B, int T_max, int chunk,
+                                                               const SegTable seg,
+                                                               const int32_t* __restrict__ hist,
+                                                               int2* __restrict__ perm) {
+  extern __shared__ int bsm[];
+  const int nb = T_max + 1, tid = threadIdx.x, nt = blockDim.x;
+  for (int L = tid; L < nb; L += nt) bsm[L] = hist[(size_t)blockIdx.x * nb + L];
+  __syncthreads();
+  const int lo = blockIdx.x * chunk, hi = min(lo + chunk, B);
+  for (int i = lo + tid; i < hi; i += nt) {
+    const int L = clampi(lens[i], 0, T_max);
+    const int pos = atomicAdd(&bsm[L], 1);
+    perm[pos] = make_int2(i, segment_of(seg, i));
+  }
+}
+
 // ==========================================================================
 // Rollout.
 //
@@ -1041,8 +1139,19 @@ __global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const Roll
 }
 
 // ==========================================================================
-// Action features: phi_i = (1/len_i) sum_t e_t.  One thread per
-// (candidate, 4 features).
+// Action features: phi_i = (1/len_i) sum_t e_t.  The sum is regrouped by
+// what varies per step:  sum_t e_t = sum_k n_k type_emb[k] + param_w .
+// sum_t log2(params_t) + len_i param_b, with n_k the number of steps of
+// kind k.  One wavefront per candidate: lanes take the steps (64 at a time),
+// kind counts come from one ballot per kind, the log2-parameter sums from a
+// wavefront reduction; then every lane forms features f = lane, lane+64, ...
+// Kinds are clamped into range here (the rollout kernel reports them).
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
+  return x;
+}
 
 __global__ __launch_bounds__(256) void phi_kernel(const float* __restrict__ emb,
                                                    const int32_t* __restrict__ types,
@@ -1050,33 +1159,44 @@ __global__ __launch_bounds__(256) void phi_kernel(const float* __restrict__ emb,
                                                    const int32_t* __restrict__ lens, int B,
                                                    int T_max, int E, int P, int K,
                                                    float* __restrict__ phi) {
-  const int per = E / 4;
-  const int gid = blockIdx.x * blockDim.x + threadIdx.x;
-  if (gid >= B * per) return;
-  const int i = gid / per, f0 = (gid % per) * 4;
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (i >= B) return;                                  // whole wavefront leaves together
   const float* t_emb = emb;
-  const float* t_pw = emb + K * E;
+  const float* t_pw = emb + K * E;                     // [PMAX][E], zero rows past P
   const float* t_pb = t_pw + PMAX * E;
   const int len = clampi(lens[i], 0, T_max);
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int t = 0; t < len; ++t) {
-    const int ty = clampi(types[(size_t)i * T_max + t], 0, K - 1);
-    float sv[4];
+  int cnt[32];                                         // n_k (wave-uniform), K <= 32
 #pragma unroll
-    for (int q = 0; q < 4; ++q) sv[q] = t_emb[ty * E + f0 + q];
-    for (int p = 0; p < P; ++p) {
-      const float u = log2f((float)params[((size_t)i * T_max + t) * P + p]);
+  for (int k = 0; k < 32; ++k) cnt[k] = 0;
+  float us[PMAX];                                      // per-lane sums of log2(params)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) sv[q] = fmaf(t_pw[p * E + f0 + q], u, sv[q]);
-    }
+  for (int p = 0; p < PMAX; ++p) us[p] = 0.0f;
+  const int32_t* ty_row = types + (size_t)i * T_max;
+  const int32_t* pa_row = params + (size_t)i * T_max * P;
+  for (int t0 = 0; t0 < len; t0 += 64) {
+    const int t = t0 + lane;
+    const bool v = t < len;
+    const int ty = v ? clampi(ty_row[t], 0, K - 1) : -1;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[q] += sv[q] + t_pb[f0 + q];
+    for (int p = 0; p < PMAX; ++p)
+      if (p < P && v) us[p] += log2f((float)pa_row[(size_t)t * P + p]);
+#pragma unroll
+    for (int k = 0; k < 32; ++k)
+      if (k < K) cnt[k] += __popcll(__ballot(ty == k));
   }
-  const float inv = len > 0 ? 1.0f / (float)len : 0.0f;
-  f32x4 o;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) o[q] = len > 0 ? acc[q] * inv : 0.0f;
-  *reinterpret_cast<f32x4*>(phi + (size_t)i * E + f0) = o;
+  for (int p = 0; p < PMAX; ++p) us[p] = p < P ? wave_sum(us[p]) : 0.0f;
+  const float inv = len > 0 ? 1.0f / (float)len : 0.0f;
+  for (int f = lane; f < E; f += 64) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 32; ++k)
+      if (k < K) acc = fmaf((float)cnt[k], t_emb[k * E + f], acc);
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) acc = fmaf(us[p], t_pw[p * E + f], acc);
+    phi[(size_t)i * E + f] = len > 0 ? fmaf(acc, inv, t_pb[f]) : 0.0f;
+  }
 }
 
 // ==========================================================================
@@ -1562,9 +1682,21 @@ int rollout_lds_bytes(const DevModel& m) {
 }
 
 hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
-                         int2* perm, int32_t* err, hipStream_t st) {
-  const int lds = 2 * (T_max + 1) * (int)sizeof(int);
-  hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(1024), lds, st, lens, B, T_max, seg, perm, err);
+                         int2* perm, int32_t* hist, int32_t* err, hipStream_t st) {
+  const int groups = bucket_groups(B);
+  if (groups == 0) {
+    const int lds = 2 * (T_max + 1) * (int)sizeof(int);
+    hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(1024), lds, st, lens, B, T_max, seg, perm, err);
+    return hipGetLastError();
+  }
+  const int chunk = bucket_chunk(B);
+  const int lds = (T_max + 1) * (int)sizeof(int);
+  hipLaunchKernelGGL(bucket_count_kernel, dim3(groups), dim3(1024), lds, st, lens, B, T_max, chunk,
+                     hist, err);
+  hipLaunchKernelGGL(bucket_scan_kernel, dim3(1), dim3(1024), lds + 16 * (int)sizeof(int), st, T_max,
+                     groups, hist);
+  hipLaunchKernelGGL(bucket_scatter_kernel, dim3(groups), dim3(1024), lds, st, lens, B, T_max, chunk,
+                     seg, hist, perm);
   return hipGetLastError();
 }
 
@@ -1626,8 +1758,8 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
 hipError_t launch_phi(const DevModel& m, const int32_t* types, const int32_t* params,
                       const int32_t* lens, int32_t B, int32_t T_max, float* phi, hipStream_t st) {
   const int E = m.dims.embed_dim;
-  const long long threads = (long long)B * (E / 4);
-  const int blocks = (int)((threads + 255) / 256);
+  if (B == 0) return hipSuccess;
+  const int blocks = (B + 3) / 4;                 // four candidates (wavefronts) per workgroup
   hipLaunchKernelGGL(phi_kernel, dim3(blocks), dim3(256), 0, st, m.emb_nat, types, params, lens,
                      B, T_max, E, m.dims.n_params, m.dims.n_kinds, phi);
   return hipGetLastError();

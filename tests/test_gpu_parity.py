@@ -289,3 +289,29 @@ def test_topk_entry_point_edge_scores(wm):
     ref3, rv3 = O.topk(y2.astype(np.float64), [0, 70000], 700)
     np.testing.assert_array_equal(idx3.cpu().numpy(), ref3)
     np.testing.assert_array_equal(val3.cpu().numpy(), rv3.astype(np.float32))
+
+
+@pytest.mark.parametrize("lens_kind", ["mixed", "all_max", "mostly_empty", "bad_length"])
+def test_large_batch_bucketing(wm, lens_kind):
+    """Batches above one workgroup's bucketing limit go through the chunked
+    counting sort (ragged last chunk here); every candidate is checked."""
+    w = synth.scaled(synth.workload("tiny"), B=12345)
+    model, W = model_for(wm, "tiny", "fp32")
+    I = synth.make_inputs(w, 53, pad="garbage")
+    rng = np.random.default_rng(5)
+    if lens_kind == "all_max":
+        I = synth.make_inputs(synth.scaled(w, B=w.B, len_lo=w.T_max, len_hi=w.T_max), 53)
+    elif lens_kind == "mostly_empty":
+        I["lens"][rng.random(w.B) < 0.9] = 0
+    elif lens_kind == "bad_length":
+        I["lens"][11111] = w.T_max + 5
+    print(f"[bucketing] B={w.B} {lens_kind}", flush=True)
+    g = run_evaluate(model, w, I, w.k)
+    if lens_kind == "bad_length":
+        assert g["status"] == 5
+        return
+    assert g["status"] == 0
+    ref = O.evaluate(W, I, w.k, "fp32")
+    rel = latent_rel(g["zT"], ref["zT"])
+    assert rel.max() <= 1e-4, f"z_T rel err {rel.max():.3e}"
+    check_topk_vs_oracle(g["idx"], ref["scores"], I["seg_off"], w.k, 1e-4)
