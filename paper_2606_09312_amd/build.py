@@ -13,6 +13,9 @@ FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     # keep float code off the packed-fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # let the fully unrolled item streams of the rollout kernels unroll (their
+    # register rings and operand arrays need compile-time indices)
+    "-mllvm", "-pragma-unroll-threshold=1000000",
 ]
 
 

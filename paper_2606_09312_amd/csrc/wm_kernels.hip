@@ -1139,6 +1139,353 @@ __global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const Roll
 }
 
 // ==========================================================================
+// Small-batch rollout, row-owned form (d = 256): one workgroup of W
+// wavefronts per tile, two per SIMD in bf16.  Wavefront w computes the first
+// product and GELU of the hidden chunks w, w + W, ... and writes the GELU
+// outputs as operand fragments to LDS; after one barrier it forms the update
+// of its own NB/W latent blocks over all NC chunks, reading every chunk's GELU
+// fragments from LDS and the matching W2 rows from L2.  Nothing is reduced
+// across wavefronts, there are two barriers per step, and the W2 rows a
+// wavefront reads are only its own blocks', so each wavefront streams 1/W of
+// the step's weights.  A step is one fully unrolled stream of 16-byte-per-lane
+// weight groups (first-product groups of the wavefront's chunks, then its W2
+// groups of every chunk) read RD ahead into a register ring that wraps into
+// the next step (the weights are the same every step).
+template <class PR, int D, int E, int NC, int W>
+struct RowsGeom {
+  using R = Roll<PR, D, E>;
+  static constexpr int G = PR::G;
+  static constexpr int NB = R::NB, NBW = NB / W;          // latent blocks per wavefront
+  static constexpr int NCW = NC / W;                      // first-product chunks per wavefront
+  static constexpr int N1 = R::NK1 / G;                   // W1 groups per chunk
+  static constexpr int G2 = R::NF2 / G;                   // W2 groups per (chunk, block)
+  static constexpr int N2 = NBW * G2;                     // W2 groups per chunk
+  static constexpr int NA = NCW * N1, NI = NA + NC * N2;  // items per step
+  static constexpr int GB = R::NF2 / G;                   // GELU fragment groups per chunk
+  // groups in flight: the ring wraps into the next step, so item j must sit
+  // in slot j % RD in every step, which needs RD to divide NI
+  static constexpr int ring_depth() {
+    const int cap = G == 1 ? 12 : 8;
+    for (int r = cap; r > 1; --r)
+      if (NI % r == 0) return r;
+    return 1;
+  }
+  static constexpr int RD = ring_depth();
+  static_assert(NB % W == 0 && NC % W == 0, "even split");
+  // LDS: [table][GELU fragments: NC * GB KiB][X fragments: NZ / G KiB][dots]
+  static constexpr int GELU_BYTES = NC * GB * 1024;
+  static constexpr int X_BYTES = (R::NZ / G) * 1024;
+};
+
+template <class PR, int D, int E, int NC, int W, bool NORM>
+__global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs a) {
+  using R = Roll<PR, D, E>;
+  using RG = RowsGeom<PR, D, E, NC, W>;
+  using Frag = typename PR::Frag;
+  using HY = Hyper<PR, D, E>;
+  constexpr int KF = PR::KF, SL = PR::SL, G = PR::G;
+  constexpr int NZ = R::NZ, NE = R::NE, NF2 = R::NF2, NB = R::NB;
+  constexpr int W1B = R::W1B, W2B = R::W2B;
+  constexpr int NBW = RG::NBW, NCW = RG::NCW, N1 = RG::N1, G2 = RG::G2, N2 = RG::N2;
+  constexpr int NA = RG::NA, NI = RG::NI, RD = RG::RD, GB = RG::GB;
+  constexpr int NT = 64 * W;
+  constexpr int GPB = HY::GPB;
+
+  extern __shared__ __attribute__((aligned(16))) float tab[];
+  const float* t_emb = tab;
+  const float* t_pw = tab + a.K * E;
+  const float* t_pb = t_pw + PMAX * E;
+  const float* t_b2 = t_pb + E;
+  uint8_t* gbuf = reinterpret_cast<uint8_t*>(tab) + a.tab_bytes;   // GELU fragments
+  uint8_t* xbuf = gbuf + RG::GELU_BYTES;                            // X fragments
+  float* dots = reinterpret_cast<float*>(xbuf + RG::X_BYTES);       // [W][3][32]
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int n = lane & 31, h = lane >> 5;
+
+  stage_to_lds(reinterpret_cast<const uint8_t*>(a.tab), reinterpret_cast<uint8_t*>(tab),
+               a.tab_bytes, tid, NT);
+
+  const int pos = blockIdx.x * 32 + n;
+  const bool valid = pos < a.B;
+  const int2 pc = valid ? a.perm[pos] : make_int2(0, 0);
+  const int cand = pc.x;
+  const int len = valid ? clampi(a.lens[cand], 0, a.T_max) : 0;
+  const int T_wg = __builtin_amdgcn_readfirstlane(
+      clampi(a.lens[a.perm[blockIdx.x * 32].x], 0, a.T_max));
+
+  // owned latent blocks (fp32) and the full X operand
+  const float* zs = a.z0 + (size_t)pc.y * D;
+  f32x16 zq[NBW];
+#pragma unroll
+  for (int bq = 0; bq < NBW; ++bq)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(zs + 32 * (w * NBW + bq) + acc_row(h, 4 * r4));
+#pragma unroll
+      for (int i = 0; i < 4; ++i) zq[bq][4 * r4 + i] = v[i];
+    }
+  Frag xz[NZ];
+#pragma unroll
+  for (int kf = 0; kf < NZ; ++kf) {
+    float v[SL];
+#pragma unroll
+    for (int j = 0; j < SL; ++j) v[j] = zs[x_feature<PR>(D, kf, h, j)];
+    xz[kf] = PR::cvt(v);
+  }
+
+  const int32_t* ty_row = a.types + (size_t)cand * a.T_max;
+  const int32_t* pa_row = a.params + (size_t)cand * a.T_max * a.P;
+  int nx_type = 0;
+  int nx_par[PMAX];
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p) nx_par[p] = 1;
+  if (0 < len) {
+    nx_type = ty_row[0];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[p];
+  }
+  int errbits = 0;
+
+  auto embed_step = [&](int s, Frag (&xe)[NE]) {
+    const bool act = s < len;
+    const float af = act ? 1.0f : 0.0f;
+    const bool bad_type = act && (nx_type < 0 || nx_type >= a.K);
+    const int ty = (act && !bad_type) ? nx_type : 0;
+    bool bad_par = false;
+    float u[PMAX];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) {
+      bad_par |= act && nx_par[p] < 1;
+      u[p] = act ? log2f((float)nx_par[p]) : 0.0f;
+    }
+    errbits |= (bad_type ? ERRBIT_TYPE : 0) | (bad_par ? ERRBIT_PARAM : 0);
+    if (s + 1 < len) {
+      nx_type = ty_row[s + 1];
+#pragma unroll
+      for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(s + 1) * a.P + p];
+    }
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      const int f0 = KF * q + SL * h;
+      float ev[SL], tmp[SL];
+      R::row(t_emb + ty * E + f0, ev);
+#pragma unroll
+      for (int p = 0; p < PMAX; ++p) {
+        R::row(t_pw + p * E + f0, tmp);
+#pragma unroll
+        for (int j = 0; j < SL; ++j) ev[j] = fmaf(tmp[j], u[p], ev[j]);
+      }
+      R::row(t_pb + f0, tmp);
+#pragma unroll
+      for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * af;
+      xe[q] = PR::cvt(ev);
+    }
+  };
+
+  // Paper form (see the split kernel): owned Wh fragments, dots through LDS.
+  u32x4 whq[NORM ? NBW * GPB : 1];
+  if constexpr (NORM) {
+#pragma unroll
+    for (int i = 0; i < NBW * GPB; ++i) whq[i] = HY::group(a.wh, w * NBW * GPB + i, lane);
+  }
+  auto boundary = [&](const Frag (&xe)[NE], bool renorm, bool project) {
+    f32x16 vq[NBW];
+    float vz = 0.0f, vv = 0.0f, zz = 0.0f;
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq) {
+      f32x16 vb = {};
+#pragma unroll
+      for (int k = 0; k < GPB; ++k)
+#pragma unroll
+        for (int ww = 0; ww < G; ++ww) vb = PR::mfma(PR::pick(whq[bq * GPB + k], ww), xe[k * G + ww], vb);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        vz = fmaf(vb[r], zq[bq][r], vz);
+        vv = fmaf(vb[r], vb[r], vv);
+        zz = fmaf(zq[bq][r], zq[bq][r], zz);
+      }
+      vq[bq] = vb;
+    }
+    vz = HY::pair_sum(vz);
+    vv = HY::pair_sum(vv);
+    zz = HY::pair_sum(zz);
+    if (h == 0) {
+      dots[(w * 3 + 0) * 32 + n] = vz;
+      dots[(w * 3 + 1) * 32 + n] = vv;
+      dots[(w * 3 + 2) * 32 + n] = zz;
+    }
+    __syncthreads();
+    vz = 0.0f; vv = 0.0f; zz = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < W; ++ww) {
+      vz += dots[(ww * 3 + 0) * 32 + n];
+      vv += dots[(ww * 3 + 1) * 32 + n];
+      zz += dots[(ww * 3 + 2) * 32 + n];
+    }
+    const float sc = (renorm && zz > 0.0f) ? rsqrtf(zz) : 1.0f;
+    const float al = (project && vv > 0.0f) ? vz / vv : 0.0f;
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) zq[bq][r] = (zq[bq][r] - al * vq[bq][r]) * sc;
+  };
+  // publish the owned blocks' X fragments, read back all of X (own buffer:
+  // the next overwrite comes after the next step's first barrier)
+  auto exchange_x = [&]() {
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq)
+#pragma unroll
+      for (int f = 0; f < NF2; ++f) {
+        const int kf = (w * NBW + bq) * NF2 + f;
+        float v[SL];
+#pragma unroll
+        for (int j = 0; j < SL; ++j) v[j] = zq[bq][f * SL + j];
+        const Frag x = PR::cvt(v);
+        *reinterpret_cast<Frag*>(xbuf + frag_offset<PR>(kf, lane, 0)) = x;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int kf = 0; kf < NZ; ++kf) xz[kf] = *reinterpret_cast<const Frag*>(xbuf + frag_offset<PR>(kf, lane, 0));
+  };
+
+  // Weight group of stream item i (i < NI), relative to the wavefront's two
+  // base addresses; compile-time after unrolling.
+  auto item_off = [](int i) -> size_t {
+    if (i < NA) return (size_t)((i / N1) * W) * W1B + (size_t)(i % N1) * 1024;
+    const int j = i - NA;
+    return (size_t)(j / N2) * W2B + (size_t)(j % N2) * 1024;
+  };
+  const uint8_t* baseA = a.w1 + (size_t)w * W1B + lane * 16;
+  const uint8_t* baseB = a.w2 + (size_t)(w * N2) * 1024 + lane * 16;
+  auto item_ptr = [&](const uint8_t* pA, const uint8_t* pB, int i) -> const u32x4* {
+    return reinterpret_cast<const u32x4*>((i < NA ? pA : pB) + item_off(i));
+  };
+
+  u32x4 ring[RD];
+#pragma unroll
+  for (int i = 0; i < RD; ++i) ring[i] = *item_ptr(baseA, baseB, i);
+
+  wait_vm_then_barrier();
+
+  Frag xe[NE];
+  if constexpr (NORM) {
+    embed_step(0, xe);
+    boundary(xe, false, 0 < len);
+    exchange_x();
+  }
+
+  for (int t = 0; t < T_wg; ++t) {
+    const bool active = t < len;
+    const float actf = active ? 1.0f : 0.0f;
+    const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
+    if constexpr (!NORM) embed_step(t, xe);
+    // opaque per-step bases: the item addresses are rebuilt from them rather
+    // than hoisted out of the step loop (one 64-bit address per item)
+    const uint8_t* pA = baseA;
+    const uint8_t* pB = baseB;
+    asm volatile("" : "+v"(pA), "+v"(pB));
+
+    f32x16 acc = {};
+    f32x4 b1v[4];
+    f32x16 dz[NBW];
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq) dz[bq] = f32x16{};
+    typename PR::Packed gp[8];
+    u32x4 gcur[GB], gnext[GB];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const u32x4 grp = ring[i % RD];
+      ring[i % RD] = *item_ptr(pA, pB, (i + RD) % NI);   // wraps into the next step
+      if (i < NA) {
+        // ---- first product of chunk w + cw*W, group g
+        const int cw = i / N1, g = i % N1;
+        if (g == 0) {
+          acc = f32x16{};
+          const float* b1g = reinterpret_cast<const float*>(a.w1 + (size_t)(w + cw * W) * W1B + (W1B - 128)) + 16 * h;
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) b1v[r4] = *reinterpret_cast<const f32x4*>(b1g + 4 * r4);
+        }
+#pragma unroll
+        for (int ww = 0; ww < G; ++ww) {
+          const int kf = g * G + ww;
+          acc = PR::mfma(PR::pick(grp, ww), kf < NZ ? xz[kf < NZ ? kf : 0] : xe[kf < NZ ? 0 : kf - NZ], acc);
+        }
+        if (g == N1 - 1) {
+          // bias, GELU, mask -> operand fragments of chunk c in LDS
+          const int c = w + cw * W;
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[4 * r4 + j] += b1v[r4][j];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) gp[q] = PR::pack2(gelu(acc[2 * q]), gelu(acc[2 * q + 1]), amask);
+#pragma unroll
+          for (int f = 0; f < NF2; ++f)
+            *reinterpret_cast<Frag*>(gbuf + frag_offset<PR>(c * NF2 + f, lane, 0)) = PR::gfrag(gp, f);
+        }
+        if (i == NA - 1) {
+          __syncthreads();             // every chunk's GELU fragments are in LDS
+#pragma unroll
+          for (int gg = 0; gg < GB; ++gg) gcur[gg] = lds_group(gbuf, gg, lane);
+#pragma unroll
+          for (int gg = 0; gg < GB; ++gg) gnext[gg] = lds_group(gbuf, (NC > 1 ? GB : 0) + gg, lane);
+        }
+      } else {
+        // ---- update of the owned blocks from chunk c, group k
+        const int j = i - NA, c = j / N2, k = j % N2;
+        const int bq = k / G2, gg2 = k % G2;
+#pragma unroll
+        for (int ww = 0; ww < G; ++ww) {
+          const int f = gg2 * G + ww;             // GELU fragment of chunk c
+          const u32x4 gf = gcur[(f * SL * PR::ES) / 16];
+          Frag b;
+          if constexpr (G == 1) b = PR::pick(gf, 0);
+          else b = PR::pick(gf, f % G);
+          dz[bq] = PR::mfma(PR::pick(grp, ww), b, dz[bq]);
+        }
+        if (k == N2 - 1) {
+          // rotate the GELU fragments: chunk c+1 current, chunk c+2 prefetched
+#pragma unroll
+          for (int gg = 0; gg < GB; ++gg) gcur[gg] = gnext[gg];
+          if (c + 2 < NC) {
+#pragma unroll
+            for (int gg = 0; gg < GB; ++gg) gnext[gg] = lds_group(gbuf, (c + 2) * GB + gg, lane);
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // ---- owned blocks: z += dZ + b2
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq) {
+      const int b = w * NBW + bq;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) zq[bq][r] += dz[bq][r] + t_b2[(b * 2 + h) * 16 + r] * actf;
+    }
+    if constexpr (NORM) {
+      embed_step(t + 1, xe);
+      boundary(xe, active, t + 1 < len);
+    }
+    exchange_x();
+  }
+  if (errbits) atomicOr(a.err, errbits);
+  if (valid) {
+    float* zo = a.zT + (size_t)cand * D;
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        f32x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = zq[bq][4 * r4 + i];
+        *reinterpret_cast<f32x4*>(zo + 32 * (w * NBW + bq) + acc_row(h, 4 * r4)) = v;
+      }
+  }
+}
+
+// ==========================================================================
 // Action features: phi_i = (1/len_i) sum_t e_t.  The sum is regrouped by
 // what varies per step:  sum_t e_t = sum_k n_k type_emb[k] + param_w .
 // sum_t log2(params_t) + len_i param_b, with n_k the number of steps of
@@ -1714,12 +2061,38 @@ hipError_t launch_rollout_split_t(const DevModel& m, const RollArgs& a, int tile
   return hipGetLastError();
 }
 
+template <class PR, int D, int E, int NC, int W, bool NORM>
+hipError_t launch_rollout_rows_t(const DevModel& m, const RollArgs& a, int tiles, hipStream_t st) {
+  using RG = RowsGeom<PR, D, E, NC, W>;
+  const int lds = m.roll_tab_bytes + RG::GELU_BYTES + RG::X_BYTES + (NORM ? W * 3 * 32 * 4 : 0);
+  auto kern = rollout_rows_kernel<PR, D, E, NC, W, NORM>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
+  }
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * W), lds, st, a);
+  return hipGetLastError();
+}
+
 // One (precision, d, e, transition form): split kernel for at most one tile
 // per compute unit, else the persistent kernel with 1, 2 or 4 wavefronts per
 // workgroup.
 template <class PR, int D, int E, bool NORM>
 hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, int blocks,
                              int waves, bool split, hipStream_t st) {
+  // d = 256: row-owned form for the hidden widths it is instantiated for
+  if constexpr (D == 256) {
+    if (split) {
+      const int NC = m.dims.trans_hidden / 32;
+      if constexpr (PR::G == 1) {
+        if (NC == 16) return launch_rollout_rows_t<PR, D, E, 16, 8, NORM>(m, a, tiles, st);
+        if (NC == 32) return launch_rollout_rows_t<PR, D, E, 32, 8, NORM>(m, a, tiles, st);
+      } else {
+        if (NC == 16) return launch_rollout_rows_t<PR, D, E, 16, 4, NORM>(m, a, tiles, st);
+      }
+    }
+  }
   // fp32 at d = 256 does not fit the split kernel's registers
   if constexpr (D <= 256 && (PR::G == 1 || D <= 64)) {
     constexpr int SPLIT = (D / 32) >= 4 ? 4 : (D / 32);
