@@ -22,6 +22,12 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// Global-memory (address space 1) views.  A pointer that passes through an
+// asm statement keeps its address space only if its type says so; a generic
+// pointer would turn the loads into flat loads, which also count against the
+// LDS counter, so every LDS wait would drain them.
+typedef __attribute__((address_space(1))) const uint8_t gu8;
+typedef __attribute__((address_space(1))) const u32x4 gu32x4;
 
 // --------------------------------------------------------------------------
 // Precision traits: operand fragment type, conversion, matrix-core product.
@@ -507,9 +513,12 @@ struct Hyper {
   // is hoisted out of the step loop and kept live (64 bits each), which
   // spills.  LDS addresses need no such care (16-bit immediate offsets).
   static __device__ __forceinline__ const uint8_t* lane_base(const uint8_t* src, int lane) {
-    const uint8_t* p = src + lane * 16;
+    gu8* p = ((gu8*)(src)) + lane * 16;
     asm volatile("" : "+v"(p));
-    return p;
+    return (const uint8_t*)p;
+  }
+  static __device__ __forceinline__ u32x4 gload(const uint8_t* p) {
+    return *reinterpret_cast<gu32x4*>(((gu8*)(p)));
   }
   static __device__ __forceinline__ float pair_sum(float x) { return x + __shfl_xor(x, 32); }
 
@@ -524,9 +533,13 @@ struct Hyper {
     // global source: lane offset folded into an opaque base (lane argument 0)
     const uint8_t* base = GLOBAL ? lane_base(src, lane) : src;
     const int ln = GLOBAL ? 0 : lane;
+    auto ld = [&](int g) -> u32x4 {
+      if constexpr (GLOBAL) return gload(base + g * 1024);
+      else return group(base, g, ln);
+    };
     u32x4 ring[RD];
 #pragma unroll
-    for (int i = 0; i < RD && i < NG; ++i) ring[i] = group(base, i, ln);
+    for (int i = 0; i < RD && i < NG; ++i) ring[i] = ld(i);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -535,7 +548,7 @@ struct Hyper {
       for (int k = 0; k < GPB; ++k) {
         const int g = b * GPB + k;
         const u32x4 grp = ring[g % RD];
-        if (g + RD < NG) ring[g % RD] = group(base, g + RD, ln);
+        if (g + RD < NG) ring[g % RD] = ld(g + RD);
 #pragma unroll
         for (int w = 0; w < G; ++w) vb = PR::mfma(PR::pick(grp, w), xe[k * G + w], vb);
         // keep the reads RD groups ahead, not hoisted all to the top
@@ -1356,10 +1369,10 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     const int j = i - NA;
     return (size_t)(j / N2) * W2B + (size_t)(j % N2) * 1024;
   };
-  const uint8_t* baseA = a.w1 + (size_t)w * W1B + lane * 16;
-  const uint8_t* baseB = a.w2 + (size_t)(w * N2) * 1024 + lane * 16;
-  auto item_ptr = [&](const uint8_t* pA, const uint8_t* pB, int i) -> const u32x4* {
-    return reinterpret_cast<const u32x4*>((i < NA ? pA : pB) + item_off(i));
+  gu8* baseA = ((gu8*)(a.w1)) + (size_t)w * W1B + lane * 16;
+  gu8* baseB = ((gu8*)(a.w2)) + (size_t)(w * N2) * 1024 + lane * 16;
+  auto item_ptr = [&](gu8* pA, gu8* pB, int i) -> gu32x4* {
+    return reinterpret_cast<gu32x4*>((i < NA ? pA : pB) + item_off(i));
   };
 
   u32x4 ring[RD];
@@ -1382,8 +1395,8 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     if constexpr (!NORM) embed_step(t, xe);
     // opaque per-step bases: the item addresses are rebuilt from them rather
     // than hoisted out of the step loop (one 64-bit address per item)
-    const uint8_t* pA = baseA;
-    const uint8_t* pB = baseB;
+    gu8* pA = baseA;
+    gu8* pB = baseB;
     asm volatile("" : "+v"(pA), "+v"(pB));
 
     f32x16 acc = {};
