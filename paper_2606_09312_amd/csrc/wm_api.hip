@@ -273,11 +273,11 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
     m.w2_chunk_bytes = TransChunk<GeomF32>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomF32>::bytes(D, E, HW);
   }
-  // rollout table: type_emb [K][E], param_w^T [PMAX][E], param_b [E], b2 (accumulator order)
+  // rollout table: type_emb [K][E + 4], param_w^T [PMAX][E], param_b [E], b2 (accumulator order)
   std::vector<float> tab;
-  tab.reserve((size_t)K * E + (size_t)PMAX * E + E + D + 4);
+  tab.reserve((size_t)K * temb_stride(E) + (size_t)PMAX * E + E + D + 4);
   for (int k = 0; k < K; ++k)
-    for (int f = 0; f < E; ++f) tab.push_back(w->type_emb[(size_t)k * E + f]);
+    for (int f = 0; f < temb_stride(E); ++f) tab.push_back(f < E ? w->type_emb[(size_t)k * E + f] : 0.0f);
   for (int p = 0; p < PMAX; ++p)
     for (int f = 0; f < E; ++f) tab.push_back(p < P ? w->param_w[(size_t)f * P + p] : 0.0f);
   for (int f = 0; f < E; ++f) tab.push_back(w->param_b[f]);

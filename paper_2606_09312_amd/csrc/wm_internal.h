@@ -128,6 +128,11 @@ constexpr bool wh_in_lds(int w1_chunk_bytes, int w2_chunk_bytes, int wh_bytes) {
 // (zero weights), so the kernels loop over a fixed count.
 constexpr int PMAX = 8;
 
+// Row stride (floats) of the type-embedding rows in the rollout table: four
+// floats of padding put rows of different action types in different LDS
+// banks (lanes of a wavefront read rows of different types at once).
+__host__ __device__ constexpr inline int temb_stride(int E) { return E + 4; }
+
 // Bucketing: one workgroup sorts batches of up to BUCKET_SINGLE_MAX
 // candidates; larger batches use three passes over chunks of candidates
 // (per-chunk length histograms in the workspace, one scan, a scatter).
@@ -160,7 +165,7 @@ struct DevModel {
   const uint8_t* trans_w2;  // H/32 transition chunks, W2 part
   const uint8_t* cost;      // C/32 cost chunks
   const uint8_t* trans_wh;  // Wh fragments (WM_NORM_L2 only)
-  const float* roll_tab;    // type_emb [K][E], param_w^T [PMAX][E] (zero rows past P), param_b [E], b2 (acc order) [D]
+  const float* roll_tab;    // type_emb [K][E + 4] (padded rows), param_w^T [PMAX][E] (zero rows past P), param_b [E], b2 (acc order) [D]
   const float* emb_nat;     // the first three parts of roll_tab
   const float* enc_w1t;     // We1^T [F][Fh] (bf16-rounded values in bf16 mode)
   const float* enc_b1;      // [Fh]

@@ -629,8 +629,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
   constexpr bool WH_LDS = NORM && wh_in_lds(W1B, W2B, HY::BYTES);
   __shared__ __attribute__((aligned(16))) uint8_t whs[WH_LDS ? HY::BYTES : 16];
   extern __shared__ __attribute__((aligned(16))) float tab[];
-  const float* t_emb = tab;                       // [K][E]
-  const float* t_pw = tab + a.K * E;              // [PMAX][E], zero rows past P
+  const float* t_emb = tab;                       // [K][E + 4]
+  const float* t_pw = tab + a.K * temb_stride(E);              // [PMAX][E], zero rows past P
   const float* t_pb = t_pw + PMAX * E;            // [E]
   const float* t_b2 = t_pb + E;                   // [NB][2][16] accumulator order
 
@@ -712,7 +712,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
     for (int q = 0; q < NE; ++q) {
       const int f0 = KF * q + SL * h;
       float ev[SL], tmp[SL];
-      R::row(t_emb + ty * E + f0, ev);
+      R::row(t_emb + ty * temb_stride(E) + f0, ev);
 #pragma unroll
       for (int p = 0; p < PMAX; ++p) {
         R::row(t_pw + p * E + f0, tmp);
@@ -867,7 +867,7 @@ __global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const Roll
 
   extern __shared__ __attribute__((aligned(16))) float tab[];
   const float* t_emb = tab;
-  const float* t_pw = tab + a.K * E;
+  const float* t_pw = tab + a.K * temb_stride(E);
   const float* t_pb = t_pw + PMAX * E;
   const float* t_b2 = t_pb + E;
   uint8_t* red = reinterpret_cast<uint8_t*>(tab) + a.tab_bytes;   // SPLIT regions
@@ -948,7 +948,7 @@ __global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const Roll
     for (int q = 0; q < NE; ++q) {
       const int f0 = KF * q + SL * h;
       float ev[SL], tmp[SL];
-      R::row(t_emb + ty * E + f0, ev);
+      R::row(t_emb + ty * temb_stride(E) + f0, ev);
 #pragma unroll
       for (int p = 0; p < PMAX; ++p) {
         R::row(t_pw + p * E + f0, tmp);
@@ -1185,9 +1185,12 @@ struct RowsGeom {
   }
   static constexpr int RD = ring_depth();
   static_assert(NB % W == 0 && NC % W == 0, "even split");
-  // LDS: [table][GELU fragments: NC * GB KiB][X fragments: NZ / G KiB][dots]
+  // LDS: [table][GELU fragments: NC * GB KiB][X fragments: NZ / G KiB]
+  //      [embedding fragments: NE / G KiB][dots]
   static constexpr int GELU_BYTES = NC * GB * 1024;
   static constexpr int X_BYTES = (R::NZ / G) * 1024;
+  static constexpr int NEG = R::NE / G;                   // embedding fragment groups
+  static constexpr int XE_BYTES = NEG * 1024;
 };
 
 template <class PR, int D, int E, int NC, int W, bool NORM>
@@ -1206,12 +1209,13 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 
   extern __shared__ __attribute__((aligned(16))) float tab[];
   const float* t_emb = tab;
-  const float* t_pw = tab + a.K * E;
+  const float* t_pw = tab + a.K * temb_stride(E);
   const float* t_pb = t_pw + PMAX * E;
   const float* t_b2 = t_pb + E;
   uint8_t* gbuf = reinterpret_cast<uint8_t*>(tab) + a.tab_bytes;   // GELU fragments
   uint8_t* xbuf = gbuf + RG::GELU_BYTES;                            // X fragments
-  float* dots = reinterpret_cast<float*>(xbuf + RG::X_BYTES);       // [W][3][32]
+  uint8_t* xebuf = xbuf + RG::X_BYTES;                              // embedding fragments
+  float* dots = reinterpret_cast<float*>(xebuf + RG::XE_BYTES);     // [W][3][32]
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
@@ -1259,14 +1263,16 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[p];
   }
   int errbits = 0;
+  Frag xe[NE];
 
-  auto embed_step = [&](int s, Frag (&xe)[NE]) {
+  // Action of step s: kind, log2 parameters, activity; error bits; prefetch
+  // of step s + 1 (every wavefront: they all hold the tile's candidates).
+  auto decode = [&](int s, int& ty, float (&u)[PMAX], float& af) {
     const bool act = s < len;
-    const float af = act ? 1.0f : 0.0f;
+    af = act ? 1.0f : 0.0f;
     const bool bad_type = act && (nx_type < 0 || nx_type >= a.K);
-    const int ty = (act && !bad_type) ? nx_type : 0;
+    ty = (act && !bad_type) ? nx_type : 0;
     bool bad_par = false;
-    float u[PMAX];
 #pragma unroll
     for (int p = 0; p < PMAX; ++p) {
       bad_par |= act && nx_par[p] < 1;
@@ -1278,21 +1284,45 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 #pragma unroll
       for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(s + 1) * a.P + p];
     }
+  };
+  // embedding fragment q (features KF*q + SL*h + j)
+  auto embed_frag = [&](int ty, const float (&u)[PMAX], float af, int q) -> Frag {
+    const int f0 = KF * q + SL * h;
+    float ev[SL], tmp[SL];
+    R::row(t_emb + ty * temb_stride(E) + f0, ev);
 #pragma unroll
-    for (int q = 0; q < NE; ++q) {
-      const int f0 = KF * q + SL * h;
-      float ev[SL], tmp[SL];
-      R::row(t_emb + ty * E + f0, ev);
+    for (int p = 0; p < PMAX; ++p) {
+      R::row(t_pw + p * E + f0, tmp);
 #pragma unroll
-      for (int p = 0; p < PMAX; ++p) {
-        R::row(t_pw + p * E + f0, tmp);
+      for (int j = 0; j < SL; ++j) ev[j] = fmaf(tmp[j], u[p], ev[j]);
+    }
+    R::row(t_pb + f0, tmp);
 #pragma unroll
-        for (int j = 0; j < SL; ++j) ev[j] = fmaf(tmp[j], u[p], ev[j]);
+    for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * af;
+    return PR::cvt(ev);
+  };
+  // all fragments in this wavefront (paper form: the normal map needs them
+  // before the step's exchange)
+  auto embed_step = [&](int s, Frag (&xe)[NE]) {
+    int ty;
+    float u[PMAX], af;
+    decode(s, ty, u, af);
+#pragma unroll
+    for (int q = 0; q < NE; ++q) xe[q] = embed_frag(ty, u, af, q);
+  };
+  // this wavefront's share of the fragment groups, into LDS (read back with X)
+  auto embed_share = [&](int s) {
+    int ty;
+    float u[PMAX], af;
+    decode(s, ty, u, af);
+#pragma unroll
+    for (int gq = 0; gq < RG::NEG; ++gq) {
+      if (gq % W != w) continue;
+#pragma unroll
+      for (int k = 0; k < G; ++k) {
+        const int q = gq * G + k;
+        *reinterpret_cast<Frag*>(xebuf + frag_offset<PR>(q, lane, 0)) = embed_frag(ty, u, af, q);
       }
-      R::row(t_pb + f0, tmp);
-#pragma unroll
-      for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * af;
-      xe[q] = PR::cvt(ev);
     }
   };
 
@@ -1360,6 +1390,10 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     __syncthreads();
 #pragma unroll
     for (int kf = 0; kf < NZ; ++kf) xz[kf] = *reinterpret_cast<const Frag*>(xbuf + frag_offset<PR>(kf, lane, 0));
+    if constexpr (!NORM) {
+#pragma unroll
+      for (int q = 0; q < NE; ++q) xe[q] = *reinterpret_cast<const Frag*>(xebuf + frag_offset<PR>(q, lane, 0));
+    }
   };
 
   // Weight group of stream item i (i < NI), relative to the wavefront's two
@@ -1381,18 +1415,18 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 
   wait_vm_then_barrier();
 
-  Frag xe[NE];
   if constexpr (NORM) {
     embed_step(0, xe);
     boundary(xe, false, 0 < len);
-    exchange_x();
+  } else {
+    embed_share(0);
   }
+  exchange_x();
 
   for (int t = 0; t < T_wg; ++t) {
     const bool active = t < len;
     const float actf = active ? 1.0f : 0.0f;
     const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
-    if constexpr (!NORM) embed_step(t, xe);
     // opaque per-step bases: the item addresses are rebuilt from them rather
     // than hoisted out of the step loop (one 64-bit address per item)
     gu8* pA = baseA;
@@ -1480,6 +1514,8 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     if constexpr (NORM) {
       embed_step(t + 1, xe);
       boundary(xe, active, t + 1 < len);
+    } else {
+      embed_share(t + 1);
     }
     exchange_x();
   }
@@ -1523,7 +1559,7 @@ __global__ __launch_bounds__(256) void phi_kernel(const float* __restrict__ emb,
   const int i = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (i >= B) return;                                  // whole wavefront leaves together
   const float* t_emb = emb;
-  const float* t_pw = emb + K * E;                     // [PMAX][E], zero rows past P
+  const float* t_pw = emb + K * temb_stride(E);        // [PMAX][E], zero rows past P
   const float* t_pb = t_pw + PMAX * E;
   const int len = clampi(lens[i], 0, T_max);
   int cnt[32];                                         // n_k (wave-uniform), K <= 32
@@ -1552,7 +1588,7 @@ __global__ __launch_bounds__(256) void phi_kernel(const float* __restrict__ emb,
     float acc = 0.0f;
 #pragma unroll
     for (int k = 0; k < 32; ++k)
-      if (k < K) acc = fmaf((float)cnt[k], t_emb[k * E + f], acc);
+      if (k < K) acc = fmaf((float)cnt[k], t_emb[k * temb_stride(E) + f], acc);
 #pragma unroll
     for (int p = 0; p < PMAX; ++p) acc = fmaf(us[p], t_pw[p * E + f], acc);
     phi[(size_t)i * E + f] = len > 0 ? fmaf(acc, inv, t_pb[f]) : 0.0f;
@@ -2077,7 +2113,8 @@ hipError_t launch_rollout_split_t(const DevModel& m, const RollArgs& a, int tile
 template <class PR, int D, int E, int NC, int W, bool NORM>
 hipError_t launch_rollout_rows_t(const DevModel& m, const RollArgs& a, int tiles, hipStream_t st) {
   using RG = RowsGeom<PR, D, E, NC, W>;
-  const int lds = m.roll_tab_bytes + RG::GELU_BYTES + RG::X_BYTES + (NORM ? W * 3 * 32 * 4 : 0);
+  const int lds = m.roll_tab_bytes + RG::GELU_BYTES + RG::X_BYTES + RG::XE_BYTES +
+                  (NORM ? W * 3 * 32 * 4 : 0);
   auto kern = rollout_rows_kernel<PR, D, E, NC, W, NORM>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
