@@ -27,6 +27,46 @@ PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense matrix-core peaks
 PEAK_HBM_GBS = 8000.0
 
 
+KERNEL_SOURCES = ("paper_2606_09312_amd/csrc/wm_kernels.hip", "paper_2606_09312_amd/csrc/wm_internal.h",
+                  "paper_2606_09312_amd/csrc/wm_api.hip", "paper_2606_09312_amd/build.py")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_rollout.md")
+
+
+def kernel_source_hash() -> str:
+    """sha256 over the kernel sources and build flags (traffic figures are
+    valid only for the code they were measured on)."""
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, precision: str, norm: str):
+    """Calibrated HBM bytes per rollout launch from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE passes scaled by a copy of known size),
+    or None when the summary is missing, does not cover this configuration or
+    was taken on different kernel sources."""
+    if norm != "none" or not os.path.exists(TRAFFIC_FILE):
+        return None
+    text = open(TRAFFIC_FILE).read()
+    want = None
+    for line in text.splitlines():
+        if line.startswith("kernel_source_sha256:"):
+            want = line.split(":", 1)[1].strip()
+    if want != kernel_source_hash():
+        return None
+    for line in text.splitlines():
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) == 6 and cells[0] == workload and cells[1] == precision:
+            try:
+                return float(cells[5])
+            except ValueError:
+                return None
+    return None
+
+
 def step_flops(w, norm: str = "none") -> int:
     """Matrix-product FLOPs of one transition step of one candidate (the
     paper form adds the hyperplane normal Wh . e)."""
@@ -185,7 +225,8 @@ def main():
                                  "hyperplane projection + residual MLP + unit length",
                    "global_batch": w.B, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "rollout", "achieved": achieved, "peak": peak,
-                     "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                     "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": measured_traffic(w.name, prec, args.norm),
                      "flop_per_launch": flops_roll,
                      "algorithmic_bytes_per_launch": rollout_bytes(w, lens, args.norm)},
         "kernels_avg_ms": {k: v["avg_ms"] for k, v in kern.items()},
