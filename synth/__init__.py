@@ -20,7 +20,7 @@ import numpy as np
 
 __all__ = [
     "Workload", "WORKLOADS", "workload", "make_weights", "make_inputs",
-    "scaled", "WEIGHT_ORDER",
+    "scaled", "WEIGHT_ORDER", "make_forest",
 ]
 
 
@@ -55,6 +55,8 @@ class Workload:
     geo_mean: float = 24.0         # geometric law on {1,2,...}
     T_max: int = 8                 # padded width of the action tensors
     precisions: tuple = ("fp32",)
+    n_trees: int = 256             # tree-ensemble ranker: trees and depth
+    tree_depth: int = 8
 
     @property
     def in_dim(self) -> int:
@@ -204,3 +206,40 @@ def make_inputs(w: Workload, seed: int, pad: str = "zero") -> Dict[str, np.ndarr
     out = {"types": types, "params": params, "lens": lens, "hw": hw, "seg_off": seg_off}
     out.update(init)
     return out
+
+
+def make_forest(w: Workload, seed: int, n_trees: Optional[int] = None, depth: Optional[int] = None,
+                z_scale: float = 1.0) -> Dict[str, np.ndarray]:
+    """A random tree ensemble over x = [z_T ; phi_s ; h] (a stand-in for a
+    trained ranker).  Complete trees of the given depth, breadth-first:
+    `feat` [NT][2^D - 1] int32 feature indices drawn uniformly, `thr`
+    [NT][2^D - 1] float32 thresholds drawn from a range that suits the
+    feature's block (z: N(0, z_scale); kind counts: U(0, 2 T_max / K);
+    length: U(1, T_max); log2-parameter statistics: U(0, 10); hardware:
+    N(0, 1)), `leaf` [NT][2^D] float32 ~ N(0, 0.1), `base` 0.5.
+    """
+    rng = np.random.default_rng(seed)
+    NT = w.n_trees if n_trees is None else n_trees
+    D = w.tree_depth if depth is None else depth
+    K, P = w.n_kinds, w.n_params
+    n_phi = K + 1 + 2 * P
+    F = w.d + n_phi + w.hw_dim
+    n_int = 2 ** D - 1
+    feat = rng.integers(0, F, size=(NT, n_int)).astype(np.int32)
+    r = rng.random((NT, n_int))
+    g = rng.standard_normal((NT, n_int))
+    thr = np.empty((NT, n_int))
+    j = feat - w.d                                   # index within phi_s (when >= 0)
+    is_z = feat < w.d
+    is_cnt = (j >= 0) & (j < K)
+    is_len = j == K
+    is_par = (j > K) & (j < n_phi)
+    is_hw = feat >= w.d + n_phi
+    thr[is_z] = z_scale * g[is_z]
+    thr[is_cnt] = r[is_cnt] * 2.0 * w.T_max / K
+    thr[is_len] = 1.0 + r[is_len] * (w.T_max - 1)
+    thr[is_par] = 10.0 * r[is_par]
+    thr[is_hw] = g[is_hw]
+    leaf = 0.1 * rng.standard_normal((NT, n_int + 1))
+    return {"feat": feat, "thr": thr.astype(np.float32), "leaf": leaf.astype(np.float32),
+            "base": np.float32(0.5)}
