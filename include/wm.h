@@ -187,6 +187,62 @@ wm_status wm_evaluate(const wm_model* model, const float* init, int32_t init_is_
                       float* scores, float* zT, int32_t* idx, float* val,
                       void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Tree-ensemble ranker (the paper's G, Sec. 3.5) --------------------
+ * The paper ranks candidates with a gradient-boosted tree ensemble over the
+ * predicted terminal state, a structured action-feature vector and the
+ * hardware vector:
+ *
+ *   phi_s = [ n_0 .. n_{K-1}, T, mean_t log2(params_t), max_t log2(params_t) ]
+ *           (n_k = steps of kind k; per parameter slot mean and max; all
+ *           zero when T = 0; width K + 1 + 2P)
+ *   x     = [ z_T ; phi_s ; h ]
+ *   y     = base + sum over trees of the leaf reached by x
+ *
+ * A tree of depth D is complete and breadth-first: internal node i
+ * (0 <= i < 2^D - 1) has a feature index f_i and a float32 threshold c_i, and
+ * x goes to child 2i+1 when x[f_i] < c_i (float32 comparison), else to
+ * child 2i+2 (a NaN goes right); leaf l is node 2^D - 1 + l. */
+typedef struct wm_forest wm_forest;
+
+/* Copy a forest to the current device.  HOST arrays: feat [n_trees][2^depth
+ * - 1] int32 in [0, n_features), thr [n_trees][2^depth - 1], leaf
+ * [n_trees][2^depth].  1 <= depth <= 12, 1 <= n_features <= 4096.
+ * Synchronous.  Errors: INVALID_ARGUMENT (null array, bad sizes, a feature
+ * index out of range), OUT_OF_MEMORY, DEVICE. */
+wm_status wm_forest_create(int32_t n_trees, int32_t depth, int32_t n_features,
+                           const int32_t* feat, const float* thr, const float* leaf,
+                           float base, wm_forest** out);
+
+/* Free the forest (after all work using it has completed).  NULL: no-op. */
+void wm_forest_destroy(wm_forest* forest);
+
+/* Structured action features phi_s [B][n_kinds + 1 + 2 n_params] float32
+ * out, from types [B][T_max], params [B][T_max][n_params], lens [B] (device).
+ * Kinds outside [0, n_kinds) are not counted; a parameter < 1 gives a
+ * non-finite log2 (these are reported by the rollout in wm_evaluate_trees).
+ * 1 <= n_kinds <= 32, 1 <= n_params <= 8. */
+wm_status wm_phi_struct(const int32_t* types, const int32_t* params, const int32_t* lens,
+                        int32_t B, int32_t T_max, int32_t n_kinds, int32_t n_params,
+                        float* phi_s, void* stream);
+
+/* Tree-ensemble scores [n_hw][B] of x = [zT [B][d] ; phi_s [B][phi_dim] ;
+ * hw [n_hw][hw_dim]] (device); d + phi_dim + hw_dim must equal the forest's
+ * n_features.  Leaf values are summed in float32 in a fixed order. */
+wm_status wm_score_trees(const wm_forest* forest, const float* zT, int32_t d,
+                         const float* phi_s, int32_t phi_dim, int32_t B, const float* hw,
+                         int32_t n_hw, int32_t hw_dim, float* scores, void* stream);
+
+/* wm_evaluate with the tree-ensemble ranker: [encode,] rollout (the model's
+ * transition), structured action features, tree scores, top-k.  The forest's
+ * n_features must be d + n_kinds + 1 + 2 n_params + hw_dim of the model.
+ * Same arguments, outputs and workspace as wm_evaluate. */
+wm_status wm_evaluate_trees(const wm_model* model, const wm_forest* forest, const float* init,
+                            int32_t init_is_feats, const int32_t* seg_off, int32_t S,
+                            const int32_t* types, const int32_t* params, const int32_t* lens,
+                            int32_t B, int32_t T_max, const float* hw, int32_t n_hw, int32_t k,
+                            float* scores, float* zT, int32_t* idx, float* val,
+                            void* ws, size_t ws_bytes, void* stream);
+
 /* Synchronise `stream`, read and clear the workspace's device error word.
  * Returns WM_OK, or WM_ERR_INPUT_RANGE with wm_last_error() naming the
  * violation(s); WM_ERR_DEVICE if the stream reports a failure. */
@@ -197,7 +253,8 @@ const char* wm_last_error(void);
 
 /* Kernel timing with HIP events recorded on the launch stream around each
  * launch of one kernel family (for benchmarks).  Ids: 0 rollout, 1 score,
- * 2 top-k, 3 bucketing, 4 action features, 5 encoder.  Enabling resets the
+ * 2 top-k, 3 bucketing, 4 action features, 5 encoder, 6 structured action
+ * features, 7 tree-ensemble scores.  Enabling resets the
  * counters; reading synchronises on the recorded events.  At most 8192
  * launches per kernel are recorded while enabled. */
 wm_status wm_timing_enable(int32_t on);

@@ -103,9 +103,10 @@ def score_trees(zT, phi_s, hw, feat, thr, leaf, base: float) -> np.ndarray:
                      for j in range(hw.shape[0])])
 
 
-def decision_margin(x, feat, thr) -> np.ndarray:
-    """Smallest |float32(x[f]) - float32(c)| over the nodes each row visits,
-    relative to max(1, |c|): how close the row comes to flipping a decision."""
+def decision_margin(x, feat, thr, n_check=None) -> np.ndarray:
+    """Smallest |float32(x[f]) - float32(c)| over the nodes each row visits
+    (only nodes testing a feature f < n_check when given): how far the row
+    stays from flipping a decision."""
     x32 = np.asarray(x, dtype=np.float64).astype(np.float32)
     feat = np.asarray(feat)
     thr32 = np.asarray(thr, dtype=np.float32)
@@ -120,6 +121,9 @@ def decision_margin(x, feat, thr) -> np.ndarray:
             f = feat[t, node]
             c = thr32[t, node].astype(np.float64)
             v = x32[rows, f].astype(np.float64)
-            m = np.minimum(m, np.abs(v - c) / np.maximum(1.0, np.abs(c)))
+            gap = np.abs(v - c)
+            if n_check is not None:
+                gap = np.where(f < n_check, gap, np.inf)
+            m = np.minimum(m, gap)
             node = 2 * node + np.where(v < c, 1, 2)
     return m

@@ -5,8 +5,9 @@ kernels behind the C ABI of include/wm.h; this package is the thin Python
 binding over it.
 """
 from .binding import (  # noqa: F401
-    KERNELS, NORMS, PRECISIONS, SYMBOLS, WMError, Model, device_status, encode_init, evaluate,
-    load_library, rollout, score, timing_enable, timing_read, topk,
+    KERNELS, NORMS, PRECISIONS, SYMBOLS, WMError, Forest, Model, device_status, encode_init,
+    evaluate, load_library, phi_struct, rollout, score, score_trees, timing_enable, timing_read,
+    topk,
 )
 
 

@@ -21,13 +21,15 @@ WM_FP32, WM_BF16 = 0, 1
 WM_NORM_NONE, WM_NORM_L2 = 0, 1
 PRECISIONS = {"fp32": WM_FP32, "bf16": WM_BF16}
 NORMS = {"none": WM_NORM_NONE, "l2": WM_NORM_L2}
-KERNELS = {"rollout": 0, "score": 1, "topk": 2, "bucket": 3, "phi": 4, "encode": 5}
+KERNELS = {"rollout": 0, "score": 1, "topk": 2, "bucket": 3, "phi": 4, "encode": 5,
+           "phi_struct": 6, "trees": 7}
 
 # Exported symbols (kept in step with include/wm.h).
 SYMBOLS = (
     "wm_model_create", "wm_model_destroy", "wm_workspace_bytes", "wm_encode_init",
     "wm_rollout", "wm_score", "wm_topk", "wm_evaluate", "wm_device_status",
-    "wm_last_error", "wm_timing_enable", "wm_timing_read",
+    "wm_last_error", "wm_timing_enable", "wm_timing_read", "wm_forest_create",
+    "wm_forest_destroy", "wm_phi_struct", "wm_score_trees", "wm_evaluate_trees",
 )
 
 
@@ -97,6 +99,17 @@ def load_library(path: str = LIB_PATH):
     lib.wm_timing_enable.restype = i32
     lib.wm_timing_read.argtypes = [i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
     lib.wm_timing_read.restype = i32
+    lib.wm_forest_create.argtypes = [i32, i32, i32, vp, vp, vp, ctypes.c_float, ctypes.POINTER(vp)]
+    lib.wm_forest_create.restype = i32
+    lib.wm_forest_destroy.argtypes = [vp]
+    lib.wm_forest_destroy.restype = None
+    lib.wm_phi_struct.argtypes = [vp, vp, vp, i32, i32, i32, i32, vp, vp]
+    lib.wm_phi_struct.restype = i32
+    lib.wm_score_trees.argtypes = [vp, vp, i32, vp, i32, i32, vp, i32, i32, vp, vp]
+    lib.wm_score_trees.restype = i32
+    lib.wm_evaluate_trees.argtypes = [vp, vp, vp, i32, vp, i32, vp, vp, vp, i32, i32, vp, i32, i32,
+                                      vp, vp, vp, vp, vp, sz, vp]
+    lib.wm_evaluate_trees.restype = i32
     _lib = lib
     return lib
 
@@ -197,9 +210,52 @@ def topk(scores, seg_off, k, idx, val=None, stream=None):
                                   len(seg) - 1, k, _ptr(idx), _ptr(val), _stream(stream)))
 
 
+class Forest:
+    """Device copy of a tree-ensemble ranker (wm_forest_create)."""
+
+    def __init__(self, feat, thr, leaf, base: float, n_features: int):
+        lib = load_library()
+        feat = np.ascontiguousarray(feat, dtype=np.int32)
+        self._keep = (feat, np.ascontiguousarray(thr, dtype=np.float32),
+                      np.ascontiguousarray(leaf, dtype=np.float32))
+        n_trees, n_int = feat.shape
+        depth = int(round(np.log2(n_int + 1)))
+        self.n_trees, self.depth, self.n_features = n_trees, depth, n_features
+        h = ctypes.c_void_p()
+        _check(lib.wm_forest_create(n_trees, depth, n_features,
+                                    *[a.ctypes.data_as(ctypes.c_void_p) for a in self._keep],
+                                    float(base), ctypes.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None):
+            load_library().wm_forest_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def phi_struct(types, params, lens, n_kinds: int, phi_s, stream=None):
+    B, T_max = types.shape[0], types.shape[1]
+    _check(load_library().wm_phi_struct(_ptr(types), _ptr(params), _ptr(lens), B, T_max, n_kinds,
+                                        params.shape[2], _ptr(phi_s), _stream(stream)))
+
+
+def score_trees(forest: Forest, zT, phi_s, hw, scores, stream=None):
+    _check(load_library().wm_score_trees(forest.handle, _ptr(zT), zT.shape[1], _ptr(phi_s),
+                                         phi_s.shape[1], zT.shape[0], _ptr(hw), hw.shape[0],
+                                         hw.shape[1], _ptr(scores), _stream(stream)))
+
+
 def evaluate(model: Model, init, seg_off, types, params, lens, hw, k, *, init_is_feats=False,
-             scores=None, zT=None, idx=None, val=None, ws=None, stream=None):
-    """Fused [encode,] rollout, score and top-k (wm_evaluate) on device tensors.
+             scores=None, zT=None, idx=None, val=None, ws=None, stream=None, forest=None):
+    """Fused [encode,] rollout, score and top-k (wm_evaluate) on device tensors;
+    with a Forest, the tree-ensemble ranker on structured action features
+    (wm_evaluate_trees).
 
     Returns a dict with idx [n_hw][S][k], val, and scores / zT when given.
     """
@@ -215,10 +271,13 @@ def evaluate(model: Model, init, seg_off, types, params, lens, hw, k, *, init_is
         val = torch.empty((n_hw, S, k), dtype=torch.float32, device=dev)
     if ws is None:
         ws = model.workspace(B, T_max, S, n_hw, device=dev)
-    _check(load_library().wm_evaluate(
-        model.handle, _ptr(init), 1 if init_is_feats else 0, segp, S, _ptr(types), _ptr(params),
-        _ptr(lens), B, T_max, _ptr(hw), n_hw, k, _ptr(scores), _ptr(zT), _ptr(idx), _ptr(val),
-        _ptr(ws), ws.numel(), _stream(stream)))
+    args = (_ptr(init), 1 if init_is_feats else 0, segp, S, _ptr(types), _ptr(params),
+            _ptr(lens), B, T_max, _ptr(hw), n_hw, k, _ptr(scores), _ptr(zT), _ptr(idx), _ptr(val),
+            _ptr(ws), ws.numel(), _stream(stream))
+    if forest is None:
+        _check(load_library().wm_evaluate(model.handle, *args))
+    else:
+        _check(load_library().wm_evaluate_trees(model.handle, forest.handle, *args))
     return {"idx": idx, "val": val, "scores": scores, "zT": zT, "ws": ws}
 
 

@@ -17,6 +17,10 @@ struct wm_model {
   DevModel dm;
 };
 
+struct wm_forest {
+  DevForest df;
+};
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -143,7 +147,7 @@ std::vector<uint8_t> pack_hyper(const wm_dims& dm, const wm_weights& w) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t err, perm, hist, z0, zT, phi, scores, total;
+  size_t err, perm, hist, z0, zT, phi, phi_s, scores, total;
 };
 
 WsLayout ws_layout(const DevModel& m, int B, int T_max, int S, int n_hw) {
@@ -155,6 +159,7 @@ WsLayout ws_layout(const DevModel& m, int B, int T_max, int S, int n_hw) {
   L.z0 = o; o = align256(o + (size_t)S * m.dims.d * 4);
   L.zT = o; o = align256(o + (size_t)B * m.dims.d * 4);
   L.phi = o; o = align256(o + (size_t)B * m.dims.embed_dim * 4);
+  L.phi_s = o; o = align256(o + (size_t)B * phi_struct_dim(m.dims.n_kinds, m.dims.n_params) * 4);
   L.scores = o; o = align256(o + (size_t)n_hw * B * 4);
   L.total = o;
   return L;
@@ -482,6 +487,131 @@ wm_status wm_evaluate(const wm_model* model, const float* init, int32_t init_is_
   WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zTo, err, st));
   WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
   WM_TIMED(TK_SCORE, st, launch_score(model->dm, zTo, phi, B, hw, n_hw, sc, st));
+  WM_TIMED(TK_TOPK, st, launch_topk(sc, n_hw, B, seg, k, idx, val, st));
+  return ok();
+}
+
+wm_status wm_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, const int32_t* feat,
+                           const float* thr, const float* leaf, float base, wm_forest** out) {
+  if (!out) return fail(WM_ERR_INVALID_ARGUMENT, "out is NULL");
+  *out = nullptr;
+  if (!feat || !thr || !leaf) return fail(WM_ERR_INVALID_ARGUMENT, "null forest array");
+  if (n_trees < 1 || depth < 1 || depth > FOREST_MAX_DEPTH || n_features < 1 || n_features > TREE_MAX_FEATURES)
+    return fail(WM_ERR_INVALID_ARGUMENT, "need n_trees >= 1, 1 <= depth <= " + std::to_string(FOREST_MAX_DEPTH) +
+                                          ", 1 <= n_features <= " + std::to_string(TREE_MAX_FEATURES));
+  const size_t n_int = ((size_t)1 << depth) - 1;
+  std::vector<int2> nodes((size_t)n_trees * n_int);
+  for (size_t q = 0; q < nodes.size(); ++q) {
+    if (feat[q] < 0 || feat[q] >= n_features)
+      return fail(WM_ERR_INVALID_ARGUMENT, "feature index out of range at node " + std::to_string(q));
+    int32_t bits;
+    std::memcpy(&bits, &thr[q], 4);
+    nodes[q] = make_int2(feat[q], bits);
+  }
+  const size_t nb = nodes.size() * sizeof(int2), lb = (size_t)n_trees * (n_int + 1) * 4;
+  void* dev = nullptr;
+  if (hipMalloc(&dev, align256(nb) + lb) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(WM_ERR_OUT_OF_MEMORY, "hipMalloc of the forest failed");
+  }
+  uint8_t* base8 = static_cast<uint8_t*>(dev);
+  hipError_t e = hipMemcpy(base8, nodes.data(), nb, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(base8 + align256(nb), leaf, lb, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(dev);
+    return fail(WM_ERR_DEVICE, std::string("hipMemcpy: ") + hipGetErrorString(e));
+  }
+  wm_forest* f = new (std::nothrow) wm_forest;
+  if (!f) {
+    (void)hipFree(dev);
+    return fail(WM_ERR_OUT_OF_MEMORY, "host allocation failed");
+  }
+  f->df.n_trees = n_trees;
+  f->df.depth = depth;
+  f->df.n_features = n_features;
+  f->df.base = base;
+  f->df.alloc = base8;
+  f->df.nodes = reinterpret_cast<const int2*>(base8);
+  f->df.leaves = reinterpret_cast<const float*>(base8 + align256(nb));
+  *out = f;
+  return ok();
+}
+
+void wm_forest_destroy(wm_forest* forest) {
+  if (!forest) return;
+  (void)hipFree(forest->df.alloc);
+  delete forest;
+}
+
+wm_status wm_phi_struct(const int32_t* types, const int32_t* params, const int32_t* lens, int32_t B,
+                        int32_t T_max, int32_t n_kinds, int32_t n_params, float* phi_s, void* stream) {
+  if (B < 0 || T_max < 0 || T_max > WM_MAX_T) return fail(WM_ERR_INVALID_ARGUMENT, "need B >= 0, 0 <= T_max <= WM_MAX_T");
+  if (n_kinds < 1 || n_kinds > 32 || n_params < 1 || n_params > PMAX)
+    return fail(WM_ERR_UNSUPPORTED, "need 1 <= n_kinds <= 32 and 1 <= n_params <= 8");
+  if (B == 0) return ok();
+  if (!types || !params || !lens || !phi_s) return fail(WM_ERR_INVALID_ARGUMENT, "null pointer");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  WM_TIMED(TK_PHI_STRUCT, st, launch_phi_struct(types, params, lens, B, T_max, n_kinds, n_params, phi_s, st));
+  return ok();
+}
+
+wm_status wm_score_trees(const wm_forest* forest, const float* zT, int32_t d, const float* phi_s,
+                         int32_t phi_dim, int32_t B, const float* hw, int32_t n_hw, int32_t hw_dim,
+                         float* scores, void* stream) {
+  if (!forest) return fail(WM_ERR_INVALID_ARGUMENT, "forest is NULL");
+  if (B < 0 || n_hw < 1 || d < 0 || phi_dim < 0 || hw_dim < 0)
+    return fail(WM_ERR_INVALID_ARGUMENT, "need B >= 0, n_hw >= 1, non-negative widths");
+  if (d + phi_dim + hw_dim != forest->df.n_features)
+    return fail(WM_ERR_INVALID_ARGUMENT, "d + phi_dim + hw_dim must equal the forest's n_features");
+  if (B == 0) return ok();
+  if (!zT || (phi_dim > 0 && !phi_s) || (hw_dim > 0 && !hw) || !scores)
+    return fail(WM_ERR_INVALID_ARGUMENT, "null input/output pointer");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  WM_TIMED(TK_TREES, st, launch_score_trees(forest->df, zT, d, phi_s, phi_dim, B, hw, n_hw, hw_dim, scores, st));
+  return ok();
+}
+
+wm_status wm_evaluate_trees(const wm_model* model, const wm_forest* forest, const float* init,
+                            int32_t init_is_feats, const int32_t* seg_off, int32_t S,
+                            const int32_t* types, const int32_t* params, const int32_t* lens,
+                            int32_t B, int32_t T_max, const float* hw, int32_t n_hw, int32_t k,
+                            float* scores, float* zT, int32_t* idx, float* val, void* ws,
+                            size_t ws_bytes, void* stream) {
+  if (!model || !forest) return fail(WM_ERR_INVALID_ARGUMENT, "model/forest is NULL");
+  if (init_is_feats && model->dm.dims.feat_dim <= 0) return fail(WM_ERR_INVALID_ARGUMENT, "model has no encoder");
+  wm_status s = check_rollout_args(model, init, types, params, lens, B, T_max, reinterpret_cast<float*>(1));
+  if (s != WM_OK) return s;
+  if (n_hw < 1) return fail(WM_ERR_INVALID_ARGUMENT, "n_hw < 1");
+  const wm_dims& dm = model->dm.dims;
+  const int phi_dim = phi_struct_dim(dm.n_kinds, dm.n_params);
+  if (dm.d + phi_dim + dm.hw_dim != forest->df.n_features)
+    return fail(WM_ERR_INVALID_ARGUMENT, "the forest's n_features must be d + (n_kinds + 1 + 2 n_params) + hw_dim");
+  SegTable seg;
+  int32_t min_seg = 0;
+  if ((s = check_segments(seg_off, S, B, &seg, &min_seg)) != WM_OK) return s;
+  if ((s = check_k(k, min_seg)) != WM_OK) return s;
+  if (!idx) return fail(WM_ERR_INVALID_ARGUMENT, "idx is NULL");
+  if (dm.hw_dim > 0 && !hw) return fail(WM_ERR_INVALID_ARGUMENT, "hw is NULL");
+  if (!ws) return fail(WM_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  const WsLayout L = ws_layout(model->dm, B, T_max, S, n_hw);
+  if (ws_bytes < L.total) return fail(WM_ERR_INVALID_ARGUMENT, "workspace too small");
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* w8 = static_cast<uint8_t*>(ws);
+  int32_t* err = reinterpret_cast<int32_t*>(w8 + L.err);
+  int2* perm = reinterpret_cast<int2*>(w8 + L.perm);
+  float* z0 = const_cast<float*>(init);
+  if (init_is_feats) {
+    z0 = reinterpret_cast<float*>(w8 + L.z0);
+    WM_TIMED(TK_ENCODE, st, launch_encode(model->dm, init, S, z0, st));
+  }
+  float* zTo = zT ? zT : reinterpret_cast<float*>(w8 + L.zT);
+  float* phs = reinterpret_cast<float*>(w8 + L.phi_s);
+  float* sc = scores ? scores : reinterpret_cast<float*>(w8 + L.scores);
+  WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, reinterpret_cast<int32_t*>(w8 + L.hist), err, st));
+  WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zTo, err, st));
+  WM_TIMED(TK_PHI_STRUCT, st, launch_phi_struct(types, params, lens, B, T_max, dm.n_kinds, dm.n_params, phs, st));
+  WM_TIMED(TK_TREES, st, launch_score_trees(forest->df, zTo, dm.d, phs, phi_dim, B, hw, n_hw, dm.hw_dim, sc, st));
   WM_TIMED(TK_TOPK, st, launch_topk(sc, n_hw, B, seg, k, idx, val, st));
   return ok();
 }

@@ -176,6 +176,23 @@ struct DevModel {
   int wh_bytes;             // 0 unless WM_NORM_L2
 };
 
+// Tree-ensemble ranker: complete breadth-first trees of depth `depth`;
+// node (feature, float bits of threshold) pairs [n_trees][2^depth - 1],
+// leaves [n_trees][2^depth].  Feature indices are checked at creation.
+struct DevForest {
+  int32_t n_trees, depth, n_features;
+  float base;
+  uint8_t* alloc;
+  const int2* nodes;
+  const float* leaves;
+};
+constexpr int FOREST_MAX_DEPTH = 12;
+constexpr int TREE_MAX_FEATURES = 4096;
+
+// Width of the structured action-feature vector: kind counts, length,
+// per-slot mean and max of log2(param).
+__host__ __device__ constexpr inline int phi_struct_dim(int K, int P) { return K + 1 + 2 * P; }
+
 // Launchers (wm_kernels.hip).  Return hipSuccess or the launch error.
 // hist: bucket_groups(B) * (T_max + 1) ints of workspace (unused when 0)
 hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
@@ -192,13 +209,21 @@ hipError_t launch_topk(const float* scores, int32_t n_hw, int32_t B, const SegTa
 hipError_t launch_encode(const DevModel& m, const float* feats, int32_t S, float* z0,
                          hipStream_t st);
 
+hipError_t launch_phi_struct(const int32_t* types, const int32_t* params, const int32_t* lens,
+                             int32_t B, int32_t T_max, int32_t K, int32_t P, float* phi_s,
+                             hipStream_t st);
+hipError_t launch_score_trees(const DevForest& f, const float* zT, int32_t d, const float* phi_s,
+                              int32_t phi_dim, int32_t B, const float* hw, int32_t n_hw,
+                              int32_t hw_dim, float* scores, hipStream_t st);
+
 // Whether a (precision, d, e) combination has rollout/score kernels.
 bool have_kernels(int prec, int d, int e);
 // LDS bytes the rollout kernel needs for a model (0 if unsupported).
 int rollout_lds_bytes(const DevModel& m);
 
 // Kernel-family timing hooks (wm_api.hip).
-enum TimedKernel { TK_ROLLOUT = 0, TK_SCORE = 1, TK_TOPK = 2, TK_BUCKET = 3, TK_PHI = 4, TK_ENCODE = 5, TK_COUNT = 6 };
+enum TimedKernel { TK_ROLLOUT = 0, TK_SCORE = 1, TK_TOPK = 2, TK_BUCKET = 3, TK_PHI = 4, TK_ENCODE = 5,
+                   TK_PHI_STRUCT = 6, TK_TREES = 7, TK_COUNT = 8 };
 void timing_begin(int kernel, hipStream_t st);
 void timing_end(int kernel, hipStream_t st);
 

@@ -1596,6 +1596,114 @@ __global__ __launch_bounds__(256) void phi_kernel(const float* __restrict__ emb,
 }
 
 // ==========================================================================
+// Structured action features (the ranker's phi, Sec. 3.5): per candidate the
+// number of steps of each kind, the length, and per parameter slot the mean
+// and the maximum of log2(param) over the steps (all zero when the sequence
+// is empty).  One wavefront per candidate, lanes over steps; kinds outside
+// [0, K) are not counted.
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m));
+  return x;
+}
+
+__global__ __launch_bounds__(256) void phi_struct_kernel(const int32_t* __restrict__ types,
+                                                          const int32_t* __restrict__ params,
+                                                          const int32_t* __restrict__ lens, int B,
+                                                          int T_max, int K, int P,
+                                                          float* __restrict__ phi_s) {
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (i >= B) return;                                  // whole wavefront leaves together
+  const int len = clampi(lens[i], 0, T_max);
+  const int32_t* ty_row = types + (size_t)i * T_max;
+  const int32_t* pa_row = params + (size_t)i * T_max * P;
+  int cnt[32];
+#pragma unroll
+  for (int k = 0; k < 32; ++k) cnt[k] = 0;
+  float us[PMAX], um[PMAX];
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p) { us[p] = 0.0f; um[p] = -INFINITY; }
+  for (int t0 = 0; t0 < len; t0 += 64) {
+    const int t = t0 + lane;
+    const bool v = t < len;
+    const int ty = v ? ty_row[t] : -1;
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p)
+      if (p < P && v) {
+        const float u = log2f((float)pa_row[(size_t)t * P + p]);
+        us[p] += u;
+        um[p] = fmaxf(um[p], u);
+      }
+#pragma unroll
+    for (int k = 0; k < 32; ++k)
+      if (k < K) cnt[k] += __popcll(__ballot(ty == k));
+  }
+  float* o = phi_s + (size_t)i * phi_struct_dim(K, P);
+  const float inv = len > 0 ? 1.0f / (float)len : 0.0f;
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p) {
+    if (p >= P) break;
+    const float s = wave_sum(us[p]);
+    const float m = wave_max(um[p]);
+    if (lane == 0) {
+      o[K + 1 + p] = len > 0 ? s * inv : 0.0f;
+      o[K + 1 + P + p] = len > 0 ? m : 0.0f;
+    }
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int k = 0; k < 32; ++k)
+      if (k < K) o[k] = (float)cnt[k];
+    o[K] = (float)len;
+  }
+}
+
+// ==========================================================================
+// Tree-ensemble ranker (the paper's G, Sec. 3.5): y = base + sum over trees
+// of the leaf reached by x = [z_T ; phi_s ; h].  One workgroup per
+// (candidate, hardware vector): x is staged in LDS, each thread walks trees
+// tid, tid + 256, ... (node i -> child 2i+1 when x[f] < c, else 2i+2, so a
+// NaN goes right), and the leaf values are summed in a fixed order.
+
+constexpr int TREE_THREADS = 256;
+
+__global__ __launch_bounds__(TREE_THREADS) void score_trees_kernel(
+    const int2* __restrict__ nodes, const float* __restrict__ leaves, int NT, int depth, float base,
+    const float* __restrict__ zT, int d, const float* __restrict__ phi_s, int phi_dim,
+    const float* __restrict__ hw, int hw_dim, int B, float* __restrict__ scores) {
+  extern __shared__ float tsm[];
+  float* x = tsm;                                      // [d + phi_dim + hw_dim]
+  float* red = tsm + d + phi_dim + hw_dim;             // [TREE_THREADS / 64]
+  const int i = blockIdx.x, j = blockIdx.y, tid = threadIdx.x;
+  for (int f = tid; f < d; f += TREE_THREADS) x[f] = zT[(size_t)i * d + f];
+  for (int f = tid; f < phi_dim; f += TREE_THREADS) x[d + f] = phi_s[(size_t)i * phi_dim + f];
+  for (int f = tid; f < hw_dim; f += TREE_THREADS) x[d + phi_dim + f] = hw[(size_t)j * hw_dim + f];
+  __syncthreads();
+  const int n_int = (1 << depth) - 1;
+  float acc = 0.0f;
+  for (int t = tid; t < NT; t += TREE_THREADS) {
+    const int2* tn = nodes + (size_t)t * n_int;
+    int node = 0;
+    for (int l = 0; l < depth; ++l) {
+      const int2 nd = tn[node];
+      node = 2 * node + (x[nd.x] < __int_as_float(nd.y) ? 1 : 2);
+    }
+    acc += leaves[(size_t)t * (n_int + 1) + (node - n_int)];
+  }
+  acc = wave_sum(acc);
+  if ((tid & 63) == 0) red[tid >> 6] = acc;
+  __syncthreads();
+  if (tid == 0) {
+    float y = base;
+#pragma unroll
+    for (int w = 0; w < TREE_THREADS / 64; ++w) y += red[w];
+    scores[(size_t)j * B + i] = y;
+  }
+}
+
+// ==========================================================================
 // Cost model.  Wavefront = 32 candidates (original order), workgroup walks
 // the 32-wide chunks of the cost hidden layer with Wc1 fragments staged in
 // LDS.  The [z_T; phi] product is shared by all hardware vectors; each vector
@@ -2185,6 +2293,27 @@ hipError_t launch_phi(const DevModel& m, const int32_t* types, const int32_t* pa
   const int blocks = (B + 3) / 4;                 // four candidates (wavefronts) per workgroup
   hipLaunchKernelGGL(phi_kernel, dim3(blocks), dim3(256), 0, st, m.emb_nat, types, params, lens,
                      B, T_max, E, m.dims.n_params, m.dims.n_kinds, phi);
+  return hipGetLastError();
+}
+
+hipError_t launch_phi_struct(const int32_t* types, const int32_t* params, const int32_t* lens,
+                             int32_t B, int32_t T_max, int32_t K, int32_t P, float* phi_s,
+                             hipStream_t st) {
+  if (B == 0) return hipSuccess;
+  if (K > 32 || P > PMAX) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(phi_struct_kernel, dim3((B + 3) / 4), dim3(256), 0, st, types, params, lens, B,
+                     T_max, K, P, phi_s);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_trees(const DevForest& f, const float* zT, int32_t d, const float* phi_s,
+                              int32_t phi_dim, int32_t B, const float* hw, int32_t n_hw,
+                              int32_t hw_dim, float* scores, hipStream_t st) {
+  if (B == 0) return hipSuccess;
+  const int lds = (d + phi_dim + hw_dim + TREE_THREADS / 64) * (int)sizeof(float);
+  hipLaunchKernelGGL(score_trees_kernel, dim3(B, n_hw), dim3(TREE_THREADS), lds, st, f.nodes,
+                     f.leaves, f.n_trees, f.depth, f.base, zT, d, phi_s, phi_dim, hw, hw_dim, B,
+                     scores);
   return hipGetLastError();
 }
 

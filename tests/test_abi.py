@@ -94,3 +94,23 @@ def test_binding_raises_when_library_missing(tmp_path):
             B.load_library(str(tmp_path / "nope.so"))
     finally:
         B._lib = saved
+
+
+def test_forest_create_validates_before_device_work():
+    lib = wm.load_library()
+    h = ctypes.c_void_p()
+    feat = np.array([0, 1, 5], np.int32)
+    thr = np.zeros(3, np.float32)
+    leaf = np.zeros(4, np.float32)
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    # feature index 5 >= n_features 5
+    assert lib.wm_forest_create(1, 2, 5, p(feat), p(thr), p(leaf), 0.0, ctypes.byref(h)) == B.WM_ERR_INVALID_ARGUMENT
+    assert "out of range" in lib.wm_last_error().decode()
+    neg = np.array([0, -1, 2], np.int32)
+    assert lib.wm_forest_create(1, 2, 6, p(neg), p(thr), p(leaf), 0.0, ctypes.byref(h)) == B.WM_ERR_INVALID_ARGUMENT
+    for depth in (0, 13):
+        assert lib.wm_forest_create(1, depth, 6, p(feat), p(thr), p(leaf), 0.0, ctypes.byref(h)) == B.WM_ERR_INVALID_ARGUMENT
+    assert lib.wm_forest_create(1, 2, 6, None, p(thr), p(leaf), 0.0, ctypes.byref(h)) == B.WM_ERR_INVALID_ARGUMENT
+    assert lib.wm_score_trees(None, None, 0, None, 0, 0, None, 1, 0, None, None) == B.WM_ERR_INVALID_ARGUMENT
+    assert lib.wm_phi_struct(None, None, None, 4, 8, 33, 2, None, None) == B.WM_ERR_UNSUPPORTED
+    assert lib.wm_phi_struct(None, None, None, -1, 8, 4, 2, None, None) == B.WM_ERR_INVALID_ARGUMENT

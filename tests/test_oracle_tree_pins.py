@@ -70,6 +70,7 @@ def test_stump_by_hand_ties_and_nan():
     np.testing.assert_array_equal(got, [-0.5, 3.5, 3.5, 3.5])     # tie and NaN go right
     m = T.decision_margin(x, feat, thr)
     assert m[1] == 0.0 and m[0] == pytest.approx(0.25)
+    assert np.all(T.decision_margin(x, feat, thr, n_check=2) == np.inf)   # feature 2 not checked
 
 
 def test_depth_two_paths_by_hand():
