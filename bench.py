@@ -88,7 +88,7 @@ def rollout_bytes(w, lens, norm: str = "none") -> int:
     return steps * 4 * (1 + w.n_params) + 4 * w.B + 4 * w.S * w.d + wbytes + 4 * w.B * w.d
 
 
-def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none"):
+def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none", forest=None):
     """Oracle throughput on a bounded random sample of the batch (candidates
     are independent, so throughput scales with the sample)."""
     from oracle import wm_oracle as O
@@ -110,7 +110,13 @@ def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none"):
         t0 = time.perf_counter()
         zT, phi = O.rollout(Wd, sub["z0"], sub["seg_off"], sub["types"], sub["params"], sub["lens"],
                             prec, norm=norm)
-        y = O.score(Wd, zT, phi, I["hw"], prec)
+        if forest is None:
+            y = O.score(Wd, zT, phi, I["hw"], prec)
+        else:
+            from oracle import trees as TR
+            phs = TR.structured_phi(sub["types"], sub["params"], sub["lens"], w.n_kinds)
+            y = TR.score_trees(zT, phs, I["hw"], forest["feat"], forest["thr"], forest["leaf"],
+                               float(forest["base"]))
         O.topk(y, [0, n], min(w.k, n))
         total_t += time.perf_counter() - t0
         total_c += n
@@ -120,7 +126,8 @@ def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none"):
     return {"value": total_c / total_t, "unit": "candidates/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"{total_c} randomly drawn candidates of the {w.B}-candidate batch "
-                      f"(float64 NumPy oracle, rollout+score+top-k, {total_t:.1f} s)"}
+                      f"(float64 NumPy oracle, rollout+{'score' if forest is None else 'trees'}"
+                      f"+top-k, {total_t:.1f} s)"}
 
 
 def main():
@@ -134,6 +141,9 @@ def main():
     ap.add_argument("--norm", default="none", choices=["none", "l2"],
                     help="transition form: residual MLP (none) or the paper's projected, "
                          "unit-length form (l2)")
+    ap.add_argument("--ranker", default="mlp", choices=["mlp", "trees"],
+                    help="cost model: the MLP on the mean action embedding, or the paper's "
+                         "tree ensemble on structured action features")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -160,10 +170,17 @@ def main():
     idx = torch.empty((w.n_hw, w.S, w.k), dtype=torch.int32, device=dev)
     val = torch.empty((w.n_hw, w.S, w.k), dtype=torch.float32, device=dev)
     ws = model.workspace(w.B, w.T_max, w.S, w.n_hw)
+    forest_arrays = forest = None
+    if args.ranker == "trees":
+        forest_arrays = synth.make_forest(w, 3000, z_scale=0.05 if args.norm == "l2" else 1.0)
+        n_feat = w.d + (w.n_kinds + 1 + 2 * w.n_params) + w.hw_dim
+        forest = wm.Forest(forest_arrays["feat"], forest_arrays["thr"], forest_arrays["leaf"],
+                           float(forest_arrays["base"]), n_feat)
 
     def step():
         wm.evaluate(model, init, I["seg_off"], t["types"], t["params"], t["lens"], t["hw"], w.k,
-                    init_is_feats="feats" in t, scores=scores, idx=idx, val=val, ws=ws)
+                    init_is_feats="feats" in t, scores=scores, idx=idx, val=val, ws=ws,
+                    forest=forest)
 
     for _ in range(args.warmup):
         step()
@@ -183,7 +200,7 @@ def main():
         step()
     torch.cuda.synchronize()
     kern = {}
-    for name in ("bucket", "rollout", "phi", "score", "topk", "encode"):
+    for name in ("bucket", "rollout", "phi", "score", "topk", "encode", "phi_struct", "trees"):
         ms, n = wm.timing_read(name)
         if n:
             kern[name] = {"avg_ms": ms / n, "launches": n}
@@ -204,7 +221,7 @@ def main():
     peak = PEAK_TFLOPS[prec]
     ms_per_step = elapsed / args.steps * 1e3
     value = w.B * args.steps / elapsed
-    total_flops = flops_roll + w.B * score_flops(w)
+    total_flops = flops_roll + (w.B * score_flops(w) if forest is None else 0)
     out = {
         "metric": "candidate schedules evaluated/sec (rollout+score+top-k)",
         "value": value,
@@ -223,6 +240,9 @@ def main():
                                f"n_hw={w.n_hw}", "precision": prec,
                    "transition": "residual MLP" if args.norm == "none" else
                                  "hyperplane projection + residual MLP + unit length",
+                   "ranker": "MLP on mean action embedding" if forest is None else
+                             f"{w.n_trees} trees of depth {w.tree_depth} on structured action "
+                             f"features",
                    "global_batch": w.B, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "rollout", "achieved": achieved, "peak": peak,
                      "unit": "TFLOP/s", "frac": achieved / peak,
@@ -233,7 +253,7 @@ def main():
         "whole_path_tflops": total_flops * args.steps / elapsed / 1e12,
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(w, W, I, prec, args.cpu_budget, args.norm)
+        out["cpu_baseline"] = cpu_baseline(w, W, I, prec, args.cpu_budget, args.norm, forest_arrays)
     print(json.dumps(out), flush=True)
 
 

@@ -1663,43 +1663,66 @@ __global__ __launch_bounds__(256) void phi_struct_kernel(const int32_t* __restri
 // ==========================================================================
 // Tree-ensemble ranker (the paper's G, Sec. 3.5): y = base + sum over trees
 // of the leaf reached by x = [z_T ; phi_s ; h].  One workgroup per
-// (candidate, hardware vector): x is staged in LDS, each thread walks trees
-// tid, tid + 256, ... (node i -> child 2i+1 when x[f] < c, else 2i+2, so a
-// NaN goes right), and the leaf values are summed in a fixed order.
+// TREE_CPB candidates and one hardware vector: the candidates' x are staged
+// in LDS, each thread walks trees tid, tid + 256, ... for all TREE_CPB
+// candidates in lockstep (independent chains of dependent node loads; node
+// i -> child 2i+1 when x[f] < c, else 2i+2, so a NaN goes right), and every
+// candidate's leaf values are summed in a fixed order.
 
 constexpr int TREE_THREADS = 256;
+constexpr int TREE_CPB = 8;
 
 __global__ __launch_bounds__(TREE_THREADS) void score_trees_kernel(
     const int2* __restrict__ nodes, const float* __restrict__ leaves, int NT, int depth, float base,
     const float* __restrict__ zT, int d, const float* __restrict__ phi_s, int phi_dim,
     const float* __restrict__ hw, int hw_dim, int B, float* __restrict__ scores) {
   extern __shared__ float tsm[];
-  float* x = tsm;                                      // [d + phi_dim + hw_dim]
-  float* red = tsm + d + phi_dim + hw_dim;             // [TREE_THREADS / 64]
-  const int i = blockIdx.x, j = blockIdx.y, tid = threadIdx.x;
-  for (int f = tid; f < d; f += TREE_THREADS) x[f] = zT[(size_t)i * d + f];
-  for (int f = tid; f < phi_dim; f += TREE_THREADS) x[d + f] = phi_s[(size_t)i * phi_dim + f];
-  for (int f = tid; f < hw_dim; f += TREE_THREADS) x[d + phi_dim + f] = hw[(size_t)j * hw_dim + f];
+  const int F = d + phi_dim + hw_dim;
+  float* x = tsm;                                      // [TREE_CPB][F]
+  float* red = tsm + TREE_CPB * F;                     // [TREE_THREADS / 64][TREE_CPB]
+  const int i0 = blockIdx.x * TREE_CPB, j = blockIdx.y, tid = threadIdx.x;
+  const int nc = min(TREE_CPB, B - i0);
+  for (int q = tid; q < TREE_CPB * F; q += TREE_THREADS) {
+    const int c = q / F, f = q - c * F;
+    const int i = i0 + (c < nc ? c : 0);               // rows past the batch repeat the first
+    float v;
+    if (f < d) v = zT[(size_t)i * d + f];
+    else if (f < d + phi_dim) v = phi_s[(size_t)i * phi_dim + (f - d)];
+    else v = hw[(size_t)j * hw_dim + (f - d - phi_dim)];
+    x[q] = v;
+  }
   __syncthreads();
   const int n_int = (1 << depth) - 1;
-  float acc = 0.0f;
+  float acc[TREE_CPB];
+#pragma unroll
+  for (int c = 0; c < TREE_CPB; ++c) acc[c] = 0.0f;
   for (int t = tid; t < NT; t += TREE_THREADS) {
     const int2* tn = nodes + (size_t)t * n_int;
-    int node = 0;
+    int node[TREE_CPB];
+#pragma unroll
+    for (int c = 0; c < TREE_CPB; ++c) node[c] = 0;
     for (int l = 0; l < depth; ++l) {
-      const int2 nd = tn[node];
-      node = 2 * node + (x[nd.x] < __int_as_float(nd.y) ? 1 : 2);
+#pragma unroll
+      for (int c = 0; c < TREE_CPB; ++c) {
+        const int2 nd = tn[node[c]];
+        node[c] = 2 * node[c] + (x[c * F + nd.x] < __int_as_float(nd.y) ? 1 : 2);
+      }
     }
-    acc += leaves[(size_t)t * (n_int + 1) + (node - n_int)];
+    const float* tl = leaves + (size_t)t * (n_int + 1);
+#pragma unroll
+    for (int c = 0; c < TREE_CPB; ++c) acc[c] += tl[node[c] - n_int];
   }
-  acc = wave_sum(acc);
-  if ((tid & 63) == 0) red[tid >> 6] = acc;
+#pragma unroll
+  for (int c = 0; c < TREE_CPB; ++c) {
+    const float v = wave_sum(acc[c]);
+    if ((tid & 63) == 0) red[(tid >> 6) * TREE_CPB + c] = v;
+  }
   __syncthreads();
-  if (tid == 0) {
+  if (tid < nc) {
     float y = base;
 #pragma unroll
-    for (int w = 0; w < TREE_THREADS / 64; ++w) y += red[w];
-    scores[(size_t)j * B + i] = y;
+    for (int w = 0; w < TREE_THREADS / 64; ++w) y += red[w * TREE_CPB + tid];
+    scores[(size_t)j * B + i0 + tid] = y;
   }
 }
 
@@ -2310,8 +2333,14 @@ hipError_t launch_score_trees(const DevForest& f, const float* zT, int32_t d, co
                               int32_t phi_dim, int32_t B, const float* hw, int32_t n_hw,
                               int32_t hw_dim, float* scores, hipStream_t st) {
   if (B == 0) return hipSuccess;
-  const int lds = (d + phi_dim + hw_dim + TREE_THREADS / 64) * (int)sizeof(float);
-  hipLaunchKernelGGL(score_trees_kernel, dim3(B, n_hw), dim3(TREE_THREADS), lds, st, f.nodes,
+  const int lds = (TREE_CPB * (d + phi_dim + hw_dim) + (TREE_THREADS / 64) * TREE_CPB) * (int)sizeof(float);
+  hipError_t e = hipFuncSetAttribute((const void*)score_trees_kernel,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
+  }
+  hipLaunchKernelGGL(score_trees_kernel, dim3((B + TREE_CPB - 1) / TREE_CPB, n_hw), dim3(TREE_THREADS), lds, st, f.nodes,
                      f.leaves, f.n_trees, f.depth, f.base, zT, d, phi_s, phi_dim, hw, hw_dim, B,
                      scores);
   return hipGetLastError();
