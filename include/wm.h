@@ -243,6 +243,52 @@ wm_status wm_evaluate_trees(const wm_model* model, const wm_forest* forest, cons
                             float* scores, float* zT, int32_t* idx, float* val,
                             void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Rollout loss and its gradients (training the transition, Sec. 3.4) --
+ * The transition (residual form, WM_NORM_NONE) is trained on rollouts: from
+ * z0 it is applied over each candidate's action sequence, and at every valid
+ * step t the predicted state p_t = z_{t+1} is compared with a target state
+ * z*_t (the encoded observed next state) and with n_neg negative states:
+ *
+ *   match_t = |p_t - z*_t|^2
+ *   rank_t  = max(0, |p_t - z*_t| - min_n |p_t - z-_{t,n}| + gamma)
+ *   loss_i  = sum_{t < len_i} lam * match_t + (1 - lam) * rank_t
+ *
+ * (|.| Euclidean; the hardest negative is the nearest, the first one on
+ * ties; at the hinge and at a zero distance the gradient taken is 0).  The
+ * gradients are those of L = sum_i loss_i with respect to the transition
+ * weights, the action embedding and each candidate's initial state, by the
+ * chain rule backwards through all steps.  In WM_BF16 every matrix product
+ * of the forward and of the backward takes bfloat16-rounded operands with
+ * float32 accumulation (the rounding is passed through unchanged).
+ * Gradients are sums in a fixed order: repeated calls give identical bits. */
+typedef struct wm_grads {
+  float *w1, *b1;             /* [H][d+e], [H] */
+  float *w2, *b2;             /* [d][H], [d] */
+  float *type_emb;            /* [n_kinds][e] */
+  float *param_w, *param_b;   /* [e][n_params], [e] */
+  float *z0;                  /* [B][d]: per candidate (may be NULL) */
+} wm_grads;
+
+/* Workspace bytes of wm_rollout_loss for B candidates with padded width
+ * T_max (0 on a bad argument).  Same ownership and error-word rules as
+ * wm_workspace_bytes (zero once before first use).  It holds the step
+ * activations of the backward pass, about 4 (2 H + 3 d + 2 e + 1) bytes per
+ * (candidate, step) slot, plus partial gradient sums. */
+size_t wm_loss_workspace_bytes(const wm_model* model, int32_t B, int32_t T_max);
+
+/* Rollout loss (definition above).  Inputs as in wm_rollout, plus
+ *   targets   [B][T_max][d] float32: z*_t for the state after step t
+ *   negatives [B][T_max][n_neg][d] float32, n_neg >= 1
+ *   (entries at t >= lens[i] are never read);
+ * outputs: loss [B] float32 (required), total (1 float, may be NULL),
+ * grads (may be NULL: loss only; else every pointer but z0 is required).
+ * Needs a WM_NORM_NONE model with d <= 256 (UNSUPPORTED otherwise). */
+wm_status wm_rollout_loss(const wm_model* model, const float* z0, const int32_t* seg_off, int32_t S,
+                          const int32_t* types, const int32_t* params, const int32_t* lens,
+                          int32_t B, int32_t T_max, const float* targets, const float* negatives,
+                          int32_t n_neg, float lam, float gamma, float* loss, float* total,
+                          const wm_grads* grads, void* ws, size_t ws_bytes, void* stream);
+
 /* Synchronise `stream`, read and clear the workspace's device error word.
  * Returns WM_OK, or WM_ERR_INPUT_RANGE with wm_last_error() naming the
  * violation(s); WM_ERR_DEVICE if the stream reports a failure. */
@@ -254,7 +300,8 @@ const char* wm_last_error(void);
 /* Kernel timing with HIP events recorded on the launch stream around each
  * launch of one kernel family (for benchmarks).  Ids: 0 rollout, 1 score,
  * 2 top-k, 3 bucketing, 4 action features, 5 encoder, 6 structured action
- * features, 7 tree-ensemble scores.  Enabling resets the
+ * features, 7 tree-ensemble scores, 8 loss forward steps, 9 step losses,
+ * 10 loss backward steps, 11 weight-gradient sums.  Enabling resets the
  * counters; reading synchronises on the recorded events.  At most 8192
  * launches per kernel are recorded while enabled. */
 wm_status wm_timing_enable(int32_t on);

@@ -22,7 +22,8 @@ WM_NORM_NONE, WM_NORM_L2 = 0, 1
 PRECISIONS = {"fp32": WM_FP32, "bf16": WM_BF16}
 NORMS = {"none": WM_NORM_NONE, "l2": WM_NORM_L2}
 KERNELS = {"rollout": 0, "score": 1, "topk": 2, "bucket": 3, "phi": 4, "encode": 5,
-           "phi_struct": 6, "trees": 7}
+           "phi_struct": 6, "trees": 7, "loss_fwd": 8, "loss_steps": 9, "loss_bwd": 10,
+           "loss_grads": 11}
 
 # Exported symbols (kept in step with include/wm.h).
 SYMBOLS = (
@@ -30,6 +31,7 @@ SYMBOLS = (
     "wm_rollout", "wm_score", "wm_topk", "wm_evaluate", "wm_device_status",
     "wm_last_error", "wm_timing_enable", "wm_timing_read", "wm_forest_create",
     "wm_forest_destroy", "wm_phi_struct", "wm_score_trees", "wm_evaluate_trees",
+    "wm_loss_workspace_bytes", "wm_rollout_loss",
 )
 
 
@@ -58,6 +60,13 @@ class Weights(ctypes.Structure):
         ("wh", _FP),
     ]
 
+
+class Grads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "w1", "b1", "w2", "b2", "type_emb", "param_w", "param_b", "z0")]
+
+
+GRAD_KEYS = ("w1", "b1", "w2", "b2", "type_emb", "param_w", "param_b")
 
 _lib = None
 
@@ -110,6 +119,12 @@ def load_library(path: str = LIB_PATH):
     lib.wm_evaluate_trees.argtypes = [vp, vp, vp, i32, vp, i32, vp, vp, vp, i32, i32, vp, i32, i32,
                                       vp, vp, vp, vp, vp, sz, vp]
     lib.wm_evaluate_trees.restype = i32
+    lib.wm_loss_workspace_bytes.argtypes = [vp, i32, i32]
+    lib.wm_loss_workspace_bytes.restype = sz
+    lib.wm_rollout_loss.argtypes = [vp, vp, vp, i32, vp, vp, vp, i32, i32, vp, vp, i32,
+                                    ctypes.c_float, ctypes.c_float, vp, vp, ctypes.POINTER(Grads),
+                                    vp, sz, vp]
+    lib.wm_rollout_loss.restype = i32
     _lib = lib
     return lib
 
@@ -279,6 +294,62 @@ def evaluate(model: Model, init, seg_off, types, params, lens, hw, k, *, init_is
     else:
         _check(load_library().wm_evaluate_trees(model.handle, forest.handle, *args))
     return {"idx": idx, "val": val, "scores": scores, "zT": zT, "ws": ws}
+
+
+def grad_shapes(model: Model) -> Dict[str, tuple]:
+    """Shapes of the weight gradients of a model (PyTorch Linear layout)."""
+    d = model.dims
+    return {"w1": (d["H"], d["d"] + d["e"]), "b1": (d["H"],), "w2": (d["d"], d["H"]),
+            "b2": (d["d"],), "type_emb": (d["n_kinds"], d["e"]),
+            "param_w": (d["e"], d["n_params"]), "param_b": (d["e"],)}
+
+
+def loss_workspace(model: Model, B: int, T_max: int, device="cuda"):
+    """Zero-filled workspace tensor (uint8) for rollout_loss."""
+    import torch
+    n = int(load_library().wm_loss_workspace_bytes(model.handle, B, T_max))
+    return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def rollout_loss(model: Model, z0, seg_off, types, params, lens, targets, negatives, lam: float,
+                 gamma: float, *, grads=True, dz0=True, loss=None, total=None, out=None, ws=None,
+                 stream=None):
+    """Rollout loss and its gradients (wm_rollout_loss) on device tensors.
+
+    targets [B][T_max][d], negatives [B][T_max][n_neg][d].  Returns a dict
+    with loss [B], total [1] and, when grads is true, the weight gradients
+    (keys of grad_shapes) and z0 [B][d] (when dz0 is true).  `out` may hold
+    preallocated gradient tensors under the same keys.
+    """
+    import torch
+    seg, segp = _host_i32(seg_off)
+    S = len(seg) - 1
+    B, T_max = types.shape[0], types.shape[1]
+    dev = types.device
+    if loss is None:
+        loss = torch.empty(B, dtype=torch.float32, device=dev)
+    if total is None:
+        total = torch.empty(1, dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = loss_workspace(model, B, T_max, device=dev)
+    res = {"loss": loss, "total": total, "ws": ws}
+    gp = None
+    if grads:
+        out = dict(out or {})
+        for k, shp in grad_shapes(model).items():
+            if k not in out:
+                out[k] = torch.empty(shp, dtype=torch.float32, device=dev)
+        if dz0 and "z0" not in out:
+            out["z0"] = torch.empty((B, model.dims["d"]), dtype=torch.float32, device=dev)
+        g = Grads(**{k: _ptr(v).value for k, v in out.items() if k in dict(Grads._fields_)})
+        gp = ctypes.byref(g)
+        res.update(out)
+    _check(load_library().wm_rollout_loss(
+        model.handle, _ptr(z0), segp, S, _ptr(types), _ptr(params), _ptr(lens), B, T_max,
+        _ptr(targets), _ptr(negatives), negatives.shape[2] if negatives.dim() == 4 else 0,
+        float(lam), float(gamma), _ptr(loss), _ptr(total), gp, _ptr(ws), ws.numel(),
+        _stream(stream)))
+    return res
 
 
 def device_status(ws, stream=None) -> int:

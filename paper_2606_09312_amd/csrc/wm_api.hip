@@ -3,6 +3,7 @@
 // workspace carving, kernel orchestration, device error word, event timing.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -103,6 +104,34 @@ void pack_transition(const wm_dims& dm, const wm_weights& w, std::vector<uint8_t
   }
 }
 
+// Transposed transition chunks for the rollout-loss backward (see TransT).
+template <class Gm>
+void pack_transposed(const wm_dims& dm, const wm_weights& w, std::vector<uint8_t>& w2t,
+                     std::vector<uint8_t>& w1t) {
+  const int D = dm.d, E = dm.embed_dim, H = dm.trans_hidden, IN = D + E;
+  const int B2 = TransT<Gm>::w2t_bytes(D), B1 = TransT<Gm>::w1t_bytes(D, E);
+  const int NZ = TransT<Gm>::nk2t(D), NF2 = 32 / Gm::KF;
+  w2t.assign((size_t)(H / 32) * B2, 0);
+  w1t.assign((size_t)(H / 32) * B1, 0);
+  for (int c = 0; c < H / 32; ++c) {
+    for (int kf = 0; kf < NZ; ++kf)
+      for (int L = 0; L < 64; ++L)
+        for (int j = 0; j < Gm::SL; ++j) {
+          const int m = L & 31, h = L >> 5;
+          const int feat = x_feature<Gm>(D, kf, h, j);
+          put<Gm>(w2t, (size_t)c * B2, kf, L, j, w.w2[(size_t)feat * H + 32 * c + m]);
+        }
+    for (int ob = 0; ob < IN / 32; ++ob)
+      for (int f = 0; f < NF2; ++f)
+        for (int L = 0; L < 64; ++L)
+          for (int j = 0; j < Gm::SL; ++j) {
+            const int m = L & 31, h = L >> 5;
+            const int hid = 32 * c + g_feature<Gm>(f, h, j);
+            put<Gm>(w1t, (size_t)c * B1, ob * NF2 + f, L, j, w.w1[(size_t)hid * IN + 32 * ob + m]);
+          }
+  }
+}
+
 // Cost chunks: for cost hidden chunk c, [Wc1 fragments][bc1 tail][wc2 tail].
 template <class Gm>
 std::vector<uint8_t> pack_cost(const wm_dims& dm, const wm_weights& w) {
@@ -161,6 +190,44 @@ WsLayout ws_layout(const DevModel& m, int B, int T_max, int S, int n_hw) {
   L.phi = o; o = align256(o + (size_t)B * m.dims.embed_dim * 4);
   L.phi_s = o; o = align256(o + (size_t)B * phi_struct_dim(m.dims.n_kinds, m.dims.n_params) * 4);
   L.scores = o; o = align256(o + (size_t)n_hw * B * 4);
+  L.total = o;
+  return L;
+}
+
+// Rollout-loss workspace: bucketing, step activations (rows i * T_max + t),
+// per-candidate step losses, partial gradient sums.
+struct LossLayout {
+  size_t err, perm, hist, X, A, G, P, SD, DE, lrow, pw1, pw2, pb1, pb2, pemb, ppb, total;
+  int splits, rows_per_split;
+};
+
+LossLayout loss_layout(const DevModel& m, int B, int T_max) {
+  const wm_dims& dm = m.dims;
+  const size_t D = dm.d, E = dm.embed_dim, H = dm.trans_hidden;
+  const size_t K = dm.n_kinds, P = dm.n_params;
+  const long long rows = (long long)B * T_max;
+  const size_t R = (size_t)rows;
+  LossLayout L;
+  L.splits = train_splits(rows);
+  L.rows_per_split = train_rows_per_split(rows);
+  const size_t S = (size_t)L.splits;
+  size_t o = 0;
+  L.err = o; o += 256;
+  L.perm = o; o = align256(o + (size_t)B * sizeof(int2));
+  L.hist = o; o = align256(o + (size_t)bucket_groups(B) * (size_t)(T_max + 1) * 4);
+  L.X = o; o = align256(o + R * (D + E) * 4);
+  L.A = o; o = align256(o + R * H * 4);
+  L.G = o; o = align256(o + R * H * 4);
+  L.P = o; o = align256(o + R * D * 4);
+  L.SD = o; o = align256(o + R * D * 4);
+  L.DE = o; o = align256(o + R * E * 4);
+  L.lrow = o; o = align256(o + R * 4);
+  L.pw1 = o; o = align256(o + S * H * (D + E) * 4);
+  L.pw2 = o; o = align256(o + S * D * H * 4);
+  L.pb1 = o; o = align256(o + S * H * 4);
+  L.pb2 = o; o = align256(o + S * D * 4);
+  L.pemb = o; o = align256(o + S * (K * E + E * P) * 4);
+  L.ppb = o; o = align256(o + S * E * 4);
   L.total = o;
   return L;
 }
@@ -260,10 +327,11 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.dims = dm;
   m.prec = dm.precision;
   const int D = dm.d, E = dm.embed_dim, K = dm.n_kinds, P = dm.n_params, HW = dm.hw_dim;
-  std::vector<uint8_t> tw1, tw2, cost, twh;
+  std::vector<uint8_t> tw1, tw2, cost, twh, tw2t, tw1t;
   const bool l2 = dm.norm == WM_NORM_L2;
   if (m.prec == WM_BF16) {
     pack_transition<GeomBF16>(dm, *w, tw1, tw2);
+    if ((D + E) % 32 == 0) pack_transposed<GeomBF16>(dm, *w, tw2t, tw1t);
     cost = pack_cost<GeomBF16>(dm, *w);
     if (l2) twh = pack_hyper<GeomBF16>(dm, *w);
     m.w1_chunk_bytes = TransChunk<GeomBF16>::w1_bytes(D, E);
@@ -272,6 +340,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   } else {
     if ((D + E + HW) % 8 != 0) return fail(WM_ERR_UNSUPPORTED, "fp32 needs d + embed_dim + hw_dim % 8 == 0");
     pack_transition<GeomF32>(dm, *w, tw1, tw2);
+    if ((D + E) % 32 == 0) pack_transposed<GeomF32>(dm, *w, tw2t, tw1t);
     cost = pack_cost<GeomF32>(dm, *w);
     if (l2) twh = pack_hyper<GeomF32>(dm, *w);
     m.w1_chunk_bytes = TransChunk<GeomF32>::w1_bytes(D, E);
@@ -318,6 +387,8 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   const size_t o_tw2 = off; off = align256(off + tw2.size());
   const size_t o_cost = off; off = align256(off + cost.size());
   const size_t o_wh = off; off = align256(off + twh.size());
+  const size_t o_w2t = off; off = align256(off + tw2t.size());
+  const size_t o_w1t = off; off = align256(off + tw1t.size());
   const size_t o_tab = off; off = align256(off + tab.size() * 4);
   const size_t o_enc = off; off = align256(off + enc.size() * 4);
   void* dev = nullptr;
@@ -330,6 +401,8 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   if (e == hipSuccess) e = hipMemcpy(base + o_tw2, tw2.data(), tw2.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_cost, cost.data(), cost.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess && !twh.empty()) e = hipMemcpy(base + o_wh, twh.data(), twh.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess && !tw2t.empty()) e = hipMemcpy(base + o_w2t, tw2t.data(), tw2t.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess && !tw1t.empty()) e = hipMemcpy(base + o_w1t, tw1t.data(), tw1t.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_tab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess && !enc.empty()) e = hipMemcpy(base + o_enc, enc.data(), enc.size() * 4, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
@@ -341,6 +414,8 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.trans_w2 = base + o_tw2;
   m.cost = base + o_cost;
   m.trans_wh = twh.empty() ? nullptr : base + o_wh;
+  m.trans_w2t = tw2t.empty() ? nullptr : base + o_w2t;
+  m.trans_w1t = tw1t.empty() ? nullptr : base + o_w1t;
   m.roll_tab = reinterpret_cast<const float*>(base + o_tab);
   m.emb_nat = m.roll_tab;
   const float* encp = reinterpret_cast<const float*>(base + o_enc);
@@ -613,6 +688,63 @@ wm_status wm_evaluate_trees(const wm_model* model, const wm_forest* forest, cons
   WM_TIMED(TK_PHI_STRUCT, st, launch_phi_struct(types, params, lens, B, T_max, dm.n_kinds, dm.n_params, phs, st));
   WM_TIMED(TK_TREES, st, launch_score_trees(forest->df, zTo, dm.d, phs, phi_dim, B, hw, n_hw, dm.hw_dim, sc, st));
   WM_TIMED(TK_TOPK, st, launch_topk(sc, n_hw, B, seg, k, idx, val, st));
+  return ok();
+}
+
+size_t wm_loss_workspace_bytes(const wm_model* model, int32_t B, int32_t T_max) {
+  if (!model || B < 0 || T_max < 0 || T_max > WM_MAX_T) return 0;
+  return loss_layout(model->dm, B, T_max).total;
+}
+
+wm_status wm_rollout_loss(const wm_model* model, const float* z0, const int32_t* seg_off, int32_t S,
+                          const int32_t* types, const int32_t* params, const int32_t* lens,
+                          int32_t B, int32_t T_max, const float* targets, const float* negatives,
+                          int32_t n_neg, float lam, float gamma, float* loss, float* total,
+                          const wm_grads* grads, void* ws, size_t ws_bytes, void* stream) {
+  wm_status s = check_rollout_args(model, z0, types, params, lens, B, T_max, reinterpret_cast<float*>(1));
+  if (s != WM_OK) return s;
+  const DevModel& m = model->dm;
+  if (m.dims.norm != WM_NORM_NONE)
+    return fail(WM_ERR_UNSUPPORTED, "the rollout loss is implemented for the residual transition (WM_NORM_NONE)");
+  if (!have_train_kernels(m.prec, m.dims.d, m.dims.embed_dim) || !m.trans_w1t || !m.trans_w2t)
+    return fail(WM_ERR_UNSUPPORTED, "no rollout-loss kernels for this (precision, d, embed_dim)");
+  if (n_neg < 1) return fail(WM_ERR_INVALID_ARGUMENT, "n_neg must be >= 1");
+  if (!std::isfinite(lam) || !std::isfinite(gamma)) return fail(WM_ERR_INVALID_ARGUMENT, "lam and gamma must be finite");
+  SegTable seg;
+  int32_t min_seg = 0;
+  if ((s = check_segments(seg_off, S, B, &seg, &min_seg)) != WM_OK) return s;
+  if (!loss) return fail(WM_ERR_INVALID_ARGUMENT, "loss is NULL");
+  if (B > 0 && T_max > 0 && (!targets || !negatives))
+    return fail(WM_ERR_INVALID_ARGUMENT, "targets/negatives is NULL");
+  if (grads && (!grads->w1 || !grads->b1 || !grads->w2 || !grads->b2 || !grads->type_emb ||
+                !grads->param_w || !grads->param_b))
+    return fail(WM_ERR_INVALID_ARGUMENT, "null gradient pointer");
+  if (!ws) return fail(WM_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  const LossLayout L = loss_layout(m, B, T_max);
+  if (ws_bytes < L.total) return fail(WM_ERR_INVALID_ARGUMENT, "workspace too small");
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* w8 = static_cast<uint8_t*>(ws);
+  auto fptr = [&](size_t off) { return reinterpret_cast<float*>(w8 + off); };
+  TrainIO io;
+  io.z0 = z0; io.perm = reinterpret_cast<int2*>(w8 + L.perm); io.types = types; io.params = params;
+  io.lens = lens; io.X = fptr(L.X); io.A = fptr(L.A); io.G = fptr(L.G); io.P = fptr(L.P);
+  io.SD = fptr(L.SD); io.DE = fptr(L.DE); io.dz0 = grads ? grads->z0 : nullptr;
+  io.err = reinterpret_cast<int32_t*>(w8 + L.err); io.B = B; io.T_max = T_max;
+  if (B > 0) {
+    WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, const_cast<int2*>(io.perm),
+                                          reinterpret_cast<int32_t*>(w8 + L.hist), io.err, st));
+    WM_TIMED(TK_TRAIN_FWD, st, launch_train_fwd(m, io, st));
+  }
+  WM_TIMED(TK_LOSS, st, launch_step_loss(io.P, targets, negatives, n_neg, lens, B, T_max, m.dims.d, lam,
+                                          gamma, io.SD, fptr(L.lrow), loss, total, st));
+  if (!grads) return ok();
+  if (B > 0) WM_TIMED(TK_TRAIN_BWD, st, launch_train_bwd(m, io, st));
+  GradParts gp;
+  gp.w1 = fptr(L.pw1); gp.w2 = fptr(L.pw2); gp.b1 = fptr(L.pb1); gp.b2 = fptr(L.pb2);
+  gp.emb = fptr(L.pemb); gp.pb = fptr(L.ppb); gp.splits = L.splits; gp.rows_per_split = L.rows_per_split;
+  WM_TIMED(TK_GRADS, st, launch_weight_grads(m, io, gp, grads->w1, grads->b1, grads->w2, grads->b2,
+                                             grads->type_emb, grads->param_w, grads->param_b, st));
   return ok();
 }
 

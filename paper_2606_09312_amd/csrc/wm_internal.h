@@ -107,6 +107,25 @@ struct CostChunk {
   static constexpr int bytes(int D, int E, int HW) { return ngroups(D, E, HW) * 1024 + 256; }
 };
 
+// Transposed transition weights for the backward pass of the rollout loss.
+//   W2^T chunk c: A fragments of dG^T[chunk] = W2^T[chunk] . Delta^T, rows =
+//     the chunk's 32 hidden units, contraction over the latent in the same
+//     slot order as the z part of X (x_feature), so Delta in accumulator
+//     layout feeds it like z feeds the first product: nk2t = D / KF
+//     fragments.
+//   W1^T chunk c: for every 32-row output block of the (d + e) inputs
+//     (latent blocks first, then embedding blocks), fragments over the
+//     chunk's hidden units in GELU-operand order (g_feature), so dA^T feeds
+//     it like G feeds the second product: ((D + E) / 32) x (32 / KF)
+//     fragments.  Output row i of block b is input feature 32b + i.
+template <class Gm>
+struct TransT {
+  static constexpr int nk2t(int D) { return D / Gm::KF; }
+  static constexpr int w2t_bytes(int D) { return nk2t(D) / Gm::G * 1024; }
+  static constexpr int nk1t(int D, int E) { return ((D + E) / 32) * (32 / Gm::KF); }
+  static constexpr int w1t_bytes(int D, int E) { return nk1t(D, E) / Gm::G * 1024; }
+};
+
 // Hyperplane-normal map Wh [d][e] of the paper-form transition, packed as
 // A-operand fragments of the product V^T = Wh . E^T: block b (rows
 // [32b, 32b+32) of Wh, i.e. features of the latent in accumulator layout)
@@ -165,6 +184,8 @@ struct DevModel {
   const uint8_t* trans_w2;  // H/32 transition chunks, W2 part
   const uint8_t* cost;      // C/32 cost chunks
   const uint8_t* trans_wh;  // Wh fragments (WM_NORM_L2 only)
+  const uint8_t* trans_w2t; // H/32 chunks of W2^T (rollout-loss backward)
+  const uint8_t* trans_w1t; // H/32 chunks of W1^T (rollout-loss backward)
   const float* roll_tab;    // type_emb [K][E + 4] (padded rows), param_w^T [PMAX][E] (zero rows past P), param_b [E], b2 (acc order) [D]
   const float* emb_nat;     // the first three parts of roll_tab
   const float* enc_w1t;     // We1^T [F][Fh] (bf16-rounded values in bf16 mode)
@@ -216,6 +237,44 @@ hipError_t launch_score_trees(const DevForest& f, const float* zT, int32_t d, co
                               int32_t phi_dim, int32_t B, const float* hw, int32_t n_hw,
                               int32_t hw_dim, float* scores, hipStream_t st);
 
+// Rollout loss (training objective of the transition): device buffers of
+// one call, rows r = i * T_max + t (see the kernels for their contents).
+struct TrainIO {
+  const float* z0;          // [S][D]
+  const int2* perm;         // length-sorted (candidate, subgraph)
+  const int32_t* types;
+  const int32_t* params;
+  const int32_t* lens;
+  float *X, *A, *G, *P, *SD, *DE;
+  float* dz0;               // [B][D] or null
+  int32_t* err;
+  int B, T_max;
+};
+// Weight-gradient partial sums: `splits` row ranges of rows_per_split rows
+// (a multiple of 16) each, added in order afterwards.
+struct GradParts {
+  float *w1, *w2, *b1, *b2, *emb, *pb;
+  int splits, rows_per_split;
+};
+inline int train_rows_per_split(long long rows) {
+  long long r = (rows + 63) / 64;
+  if (r < 256) r = 256;
+  return (int)((r + 15) / 16 * 16);
+}
+inline int train_splits(long long rows) {
+  const int r = train_rows_per_split(rows);
+  return rows == 0 ? 0 : (int)((rows + r - 1) / r);
+}
+bool have_train_kernels(int prec, int d, int e);
+hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st);
+hipError_t launch_step_loss(const float* P, const float* targets, const float* negatives, int NN,
+                            const int32_t* lens, int B, int T_max, int D, float lam, float gamma,
+                            float* SD, float* lrow, float* loss, float* total, hipStream_t st);
+hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st);
+hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradParts& parts,
+                               float* gw1, float* gb1, float* gw2, float* gb2, float* gtemb,
+                               float* gpw, float* gpb, hipStream_t st);
+
 // Whether a (precision, d, e) combination has rollout/score kernels.
 bool have_kernels(int prec, int d, int e);
 // LDS bytes the rollout kernel needs for a model (0 if unsupported).
@@ -223,7 +282,8 @@ int rollout_lds_bytes(const DevModel& m);
 
 // Kernel-family timing hooks (wm_api.hip).
 enum TimedKernel { TK_ROLLOUT = 0, TK_SCORE = 1, TK_TOPK = 2, TK_BUCKET = 3, TK_PHI = 4, TK_ENCODE = 5,
-                   TK_PHI_STRUCT = 6, TK_TREES = 7, TK_COUNT = 8 };
+                   TK_PHI_STRUCT = 6, TK_TREES = 7, TK_TRAIN_FWD = 8, TK_LOSS = 9,
+                   TK_TRAIN_BWD = 10, TK_GRADS = 11, TK_COUNT = 12 };
 void timing_begin(int kernel, hipStream_t st);
 void timing_end(int kernel, hipStream_t st);
 

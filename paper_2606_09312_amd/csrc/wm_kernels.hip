@@ -1727,6 +1727,549 @@ __global__ __launch_bounds__(TREE_THREADS) void score_trees_kernel(
 }
 
 // ==========================================================================
+// Rollout loss and its gradients (the transition's training objective,
+// Sec. 3.4).  Step activations live in dense rows r = i * T_max + t of the
+// workspace (rows with t >= len_i are never read: the gradient products and
+// sums mask them).
+//
+// train_fwd_kernel: one wavefront per 32-candidate tile (length-sorted),
+// the residual-MLP step with the weight groups streamed from L2 into a
+// register ring.  Per valid step it stores the product operands X = [z; e]
+// (with the value the products see), the pre-activations A, the GELU outputs
+// G (product-operand value) and the predicted state P = z_{t+1}.
+
+struct TrainArgs {
+  const uint8_t* w1;        // packed transition chunks (forward)
+  const uint8_t* w2;
+  const uint8_t* w2t;       // packed transposed chunks (backward)
+  const uint8_t* w1t;
+  const float* tab;         // rollout table
+  const float* z0;          // [S][D]
+  const int2* perm;
+  const int32_t* types;
+  const int32_t* params;
+  const int32_t* lens;
+  float* X;                 // [R][D+E]
+  float* A;                 // [R][H]   pre-activations; the backward overwrites them with dA
+  float* G;                 // [R][H]
+  float* P;                 // [R][D]   predicted states
+  float* SD;                // [R][D]   dL/dp seeds; the backward overwrites them with delta_{t+1}
+  float* DE;                // [R][E]   gradient reaching the step's embedding
+  float* dz0;               // [B][D]   (may be null)
+  int32_t* err;
+  int B, T_max, P_, K, H, tab_bytes;
+};
+
+template <class PR>
+__device__ __forceinline__ float op_value(float v) {   // the value a product operand takes
+  if constexpr (PR::G == 1) return (float)(__bf16)v;
+  else return v;
+}
+
+// d/dx [x Phi(x)] = Phi(x) + x phi(x), with erf from the same Abramowitz &
+// Stegun 7.1.26 form as gelu() and phi(x) = exp(-x^2/2) / sqrt(2 pi).
+__device__ __forceinline__ float gelu_grad(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.70710678118654752f, ax, 1.0f));
+  float p = fmaf(1.061405429f, t, -1.453152027f);
+  p = fmaf(p, t, 1.421413741f);
+  p = fmaf(p, t, -0.284496736f);
+  p = fmaf(p, t, 0.254829592f);
+  const float ex = __builtin_amdgcn_exp2f((x * x) * (-0.5f * 1.4426950408889634f));
+  const float erf_a = fmaf(-(p * t), ex, 1.0f);
+  return fmaf(0.5f, copysignf(erf_a, x), 0.5f) + x * ex * 0.3989422804014327f;
+}
+
+// 16 accumulator values of one 32-row block <-> a row in natural order
+// (rows acc_row(h, 4q .. 4q+3) are consecutive: four 16-byte accesses).
+__device__ __forceinline__ void store_acc(float* row, const f32x16& v, int h) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const f32x4 x = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+    *reinterpret_cast<f32x4*>(row + acc_row(h, 4 * q)) = x;
+  }
+}
+__device__ __forceinline__ f32x16 load_acc(const float* row, int h) {
+  f32x16 v;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const f32x4 x = *reinterpret_cast<const f32x4*>(row + acc_row(h, 4 * q));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[4 * q + i] = x[i];
+  }
+  return v;
+}
+
+template <class PR, int D, int E>
+struct TrainGeom {
+  using R = Roll<PR, D, E>;
+  static constexpr int G = PR::G;
+  static constexpr int N1 = R::NK1 / G, N2 = R::NK2 / G, NIF = N1 + N2;    // forward groups per chunk
+  static constexpr int NW2T = TransT<PR>::nk2t(D) / G;                    // backward: W2^T groups
+  static constexpr int NW1T = TransT<PR>::nk1t(D, E) / G;                 // backward: W1^T groups
+  static constexpr int NIB = NW2T + NW1T;
+  static constexpr int NBE = E / 32;                                       // embedding output blocks
+  // ring depth: a divisor of the groups per chunk, so the ring wraps from
+  // one chunk (and step) into the next with every group in a fixed slot
+  static constexpr int ring(int n) {
+    const int cap = G == 1 ? 8 : 12;
+    for (int r = cap; r > 1; --r)
+      if (n % r == 0) return r;
+    return 1;
+  }
+  static constexpr int RDF = ring(NIF), RDB = ring(NIB);
+  static_assert(E % 32 == 0, "embedding blocks");
+};
+
+// Tile bookkeeping shared by the two step kernels.
+struct TileInfo {
+  int cand, seg, len, T_wg;
+  bool valid;
+};
+__device__ __forceinline__ TileInfo tile_info(const TrainArgs& a, int tile, int n) {
+  TileInfo ti;
+  const int pos = tile * 32 + n;
+  ti.valid = pos < a.B;
+  const int2 pc = ti.valid ? a.perm[pos] : make_int2(0, 0);
+  ti.cand = pc.x;
+  ti.seg = pc.y;
+  ti.len = ti.valid ? clampi(a.lens[pc.x], 0, a.T_max) : 0;
+  // candidates are sorted longest first: the tile's first one sets its steps
+  ti.T_wg = tile * 32 < a.B
+                ? __builtin_amdgcn_readfirstlane(clampi(a.lens[a.perm[tile * 32].x], 0, a.T_max))
+                : 0;
+  return ti;
+}
+
+template <class PR, int D, int E, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 1) void train_fwd_kernel(const TrainArgs a) {
+  using R = Roll<PR, D, E>;
+  using TG = TrainGeom<PR, D, E>;
+  using Frag = typename PR::Frag;
+  constexpr int KF = PR::KF, SL = PR::SL, G = PR::G;
+  constexpr int NZ = R::NZ, NE = R::NE, NF2 = R::NF2, NB = R::NB;
+  constexpr int W1B = R::W1B, W2B = R::W2B, N1 = TG::N1, NI = TG::NIF, RD = TG::RDF;
+  constexpr int NT = 64 * WAVES, IN = D + E;
+
+  extern __shared__ __attribute__((aligned(16))) float tab[];
+  const float* t_emb = tab;
+  const float* t_pw = tab + a.K * temb_stride(E);
+  const float* t_pb = t_pw + PMAX * E;
+  const float* t_b2 = t_pb + E;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, h = lane >> 5;
+  stage_to_lds(reinterpret_cast<const uint8_t*>(a.tab), reinterpret_cast<uint8_t*>(tab),
+               a.tab_bytes, tid, NT);
+
+  const TileInfo ti = tile_info(a, blockIdx.x * WAVES + wave, n);
+  const int cand = ti.cand, len = ti.len, T_wg = ti.T_wg;
+  const int NC = a.H / 32;
+
+  f32x16 zacc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) zacc[b] = load_acc(a.z0 + (size_t)ti.seg * D + 32 * b, h);
+  const int32_t* ty_row = a.types + (size_t)cand * a.T_max;
+  const int32_t* pa_row = a.params + (size_t)cand * a.T_max * a.P_;
+  int errbits = 0;
+
+  gu8* w1g = (gu8*)(a.w1) + lane * 16;
+  gu8* w2g = (gu8*)(a.w2) + lane * 16;
+  auto group_ptr = [&](int c, int i) -> gu32x4* {
+    return reinterpret_cast<gu32x4*>(i < N1 ? w1g + (size_t)c * W1B + (size_t)i * 1024
+                                            : w2g + (size_t)c * W2B + (size_t)(i - N1) * 1024);
+  };
+  u32x4 ring[RD];
+#pragma unroll
+  for (int i = 0; i < RD; ++i) ring[i] = *group_ptr(0, i);
+  wait_vm_then_barrier();
+
+  for (int t = 0; t < T_wg; ++t) {
+    const bool active = t < len;
+    const float actf = active ? 1.0f : 0.0f;
+    const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
+    const size_t row = (size_t)cand * a.T_max + t;
+    // the step's action: kind and log2 parameters (zero embedding when done)
+    int ty = 0;
+    float u[PMAX];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) u[p] = 0.0f;
+    if (active) {
+      const int tv = ty_row[t];
+      if (tv < 0 || tv >= a.K) errbits |= ERRBIT_TYPE;
+      else ty = tv;
+#pragma unroll
+      for (int p = 0; p < PMAX; ++p)
+        if (p < a.P_) {
+          const int pv = pa_row[(size_t)t * a.P_ + p];
+          if (pv < 1) errbits |= ERRBIT_PARAM;
+          u[p] = log2f((float)pv);
+        }
+    }
+    float* xrow = a.X + row * IN;
+    Frag xe[NE];
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      const int f0 = KF * q + SL * h;
+      float ev[SL], tmp[SL];
+      R::row(t_emb + ty * temb_stride(E) + f0, ev);
+#pragma unroll
+      for (int p = 0; p < PMAX; ++p) {
+        R::row(t_pw + p * E + f0, tmp);
+#pragma unroll
+        for (int j = 0; j < SL; ++j) ev[j] = fmaf(tmp[j], u[p], ev[j]);
+      }
+      R::row(t_pb + f0, tmp);
+#pragma unroll
+      for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * actf;
+      xe[q] = PR::cvt(ev);
+      if (active) {
+#pragma unroll
+        for (int j = 0; j < SL; ++j) xrow[D + f0 + j] = op_value<PR>(ev[j]);
+      }
+    }
+    Frag xz[NZ];
+#pragma unroll
+    for (int kf = 0; kf < NZ; ++kf) {
+      float v[SL];
+#pragma unroll
+      for (int j = 0; j < SL; ++j) v[j] = zacc[kf / NF2][(kf % NF2) * SL + j];
+      xz[kf] = PR::cvt(v);
+    }
+    if (active) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        f32x16 v;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = op_value<PR>(zacc[b][r]);
+        store_acc(xrow + 32 * b, v, h);
+      }
+    }
+    for (int c = 0; c < NC; ++c) {
+      const int cn = c + 1 < NC ? c + 1 : 0;
+      const float* b1g = reinterpret_cast<const float*>(a.w1 + (size_t)c * W1B + (W1B - 128)) + 16 * h;
+      f32x16 acc;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(b1g + 4 * q);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[4 * q + i] = v[i];
+      }
+      typename PR::Packed gp[8];
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const u32x4 grp = ring[i % RD];
+        ring[i % RD] = (i + RD < NI) ? *group_ptr(c, i + RD) : *group_ptr(cn, i + RD - NI);
+        if (i < N1) {
+#pragma unroll
+          for (int ww = 0; ww < G; ++ww) {
+            const int kf = i * G + ww;
+            acc = PR::mfma(PR::pick(grp, ww), kf < NZ ? xz[kf < NZ ? kf : 0] : xe[kf < NZ ? 0 : kf - NZ], acc);
+          }
+          if (i == N1 - 1) {
+            f32x16 gv;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) gv[r] = op_value<PR>(gelu(acc[r]));
+#pragma unroll
+            for (int q = 0; q < 8; ++q) gp[q] = PR::pack2(gv[2 * q], gv[2 * q + 1], amask);
+            if (active) {
+              store_acc(a.A + row * a.H + 32 * c, acc, h);
+              store_acc(a.G + row * a.H + 32 * c, gv, h);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int ww = 0; ww < G; ++ww) {
+            const int F = (i - N1) * G + ww;
+            zacc[F / NF2] = PR::mfma(PR::pick(grp, ww), PR::gfrag(gp, F % NF2), zacc[F / NF2]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) zacc[b][r] += t_b2[(b * 2 + h) * 16 + r] * actf;
+    if (active) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) store_acc(a.P + row * D + 32 * b, zacc[b], h);
+    }
+  }
+  if (errbits) atomicOr(a.err, errbits);
+}
+
+// Per-step loss and its gradient with respect to the prediction: one
+// wavefront per row (candidate, step), lanes over the latent.  The hardest
+// negative is the nearest (first one on ties); a zero distance contributes a
+// zero gradient.
+__global__ __launch_bounds__(256) void loss_kernel(const float* __restrict__ P,
+                                                   const float* __restrict__ targets,
+                                                   const float* __restrict__ negatives, int NN,
+                                                   const int32_t* __restrict__ lens, int B,
+                                                   int T_max, int D, float lam, float gamma,
+                                                   float* __restrict__ SD, float* __restrict__ lrow) {
+  const int lane = threadIdx.x & 63;
+  const long long row = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (row >= (long long)B * T_max) return;             // whole wavefront leaves together
+  const int i = (int)(row / T_max), t = (int)(row - (long long)i * T_max);
+  if (t >= clampi(lens[i], 0, T_max)) return;
+  const float* p = P + row * D;
+  const float* y = targets + row * D;
+  float m = 0.0f;
+  for (int f = lane; f < D; f += 64) { const float v = p[f] - y[f]; m = fmaf(v, v, m); }
+  const float match = wave_sum(m);
+  const float dpos = sqrtf(match);
+  float dmin = INFINITY;
+  int hard = 0;
+  for (int q = 0; q < NN; ++q) {
+    const float* ng = negatives + (row * NN + q) * D;
+    float s = 0.0f;
+    for (int f = lane; f < D; f += 64) { const float v = p[f] - ng[f]; s = fmaf(v, v, s); }
+    const float dq = sqrtf(wave_sum(s));
+    if (dq < dmin) { dmin = dq; hard = q; }
+  }
+  const float hinge = dpos - dmin + gamma;
+  const bool act = hinge > 0.0f;
+  if (lane == 0) lrow[row] = lam * match + (1.0f - lam) * (act ? hinge : 0.0f);
+  const float ip = dpos > 0.0f ? 1.0f / dpos : 0.0f;
+  const float in = dmin > 0.0f ? 1.0f / dmin : 0.0f;
+  const float* ng = negatives + (row * NN + hard) * D;
+  for (int f = lane; f < D; f += 64) {
+    const float diff = p[f] - y[f];
+    float g = lam * 2.0f * diff;
+    if (act) g += (1.0f - lam) * (diff * ip - (p[f] - ng[f]) * in);
+    SD[row * D + f] = g;
+  }
+}
+
+// Per-candidate loss: the sum of its steps' losses in step order.
+__global__ __launch_bounds__(256) void loss_sum_kernel(const float* __restrict__ lrow,
+                                                       const int32_t* __restrict__ lens, int B,
+                                                       int T_max, float* __restrict__ loss) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B) return;
+  const int L = clampi(lens[i], 0, T_max);
+  float s = 0.0f;
+  for (int t = 0; t < L; ++t) s += lrow[(size_t)i * T_max + t];
+  loss[i] = s;
+}
+
+// Sum of the per-candidate losses, one workgroup in a fixed order.
+__global__ __launch_bounds__(1024) void loss_total_kernel(const float* __restrict__ loss, int B,
+                                                          float* __restrict__ total) {
+  __shared__ float part[16];
+  float s = 0.0f;
+  for (int i = threadIdx.x; i < B; i += 1024) s += loss[i];
+  s = wave_sum(s);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float tot = 0.0f;
+    for (int w = 0; w < 16; ++w) tot += part[w];
+    *total = tot;
+  }
+}
+
+// train_bwd_kernel: one wavefront per tile, steps from the last to the first.
+// delta (accumulator layout) gains each step's seed and is stored as
+// delta_{t+1} (for dW2, db2); as the B operand (product-operand value) it
+// gives dG^T = W2^T . delta^T per hidden chunk; dA = dG * GELU'(A) (A is read
+// back and overwritten with dA); then dX^T = W1^T . dA^T, whose latent blocks
+// accumulate straight into delta (the residual path carries delta itself)
+// and whose embedding blocks are stored as dE.  Finished candidates have no
+// seed and a zero mask, so their delta passes through unchanged.
+template <class PR, int D, int E, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 1) void train_bwd_kernel(const TrainArgs a) {
+  using R = Roll<PR, D, E>;
+  using TG = TrainGeom<PR, D, E>;
+  using Frag = typename PR::Frag;
+  constexpr int SL = PR::SL, G = PR::G;
+  constexpr int NZ = R::NZ, NF2 = R::NF2, NB = R::NB, NBE = TG::NBE;
+  constexpr int NW2T = TG::NW2T, NI = TG::NIB, RD = TG::RDB;
+  constexpr int W2TB = TransT<PR>::w2t_bytes(D), W1TB = TransT<PR>::w1t_bytes(D, E);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, h = lane >> 5;
+  const TileInfo ti = tile_info(a, blockIdx.x * WAVES + wave, n);
+  const int cand = ti.cand, len = ti.len, T_wg = ti.T_wg;
+  const int NC = a.H / 32;
+
+  gu8* w2g = (gu8*)(a.w2t) + lane * 16;
+  gu8* w1g = (gu8*)(a.w1t) + lane * 16;
+  auto group_ptr = [&](int c, int i) -> gu32x4* {
+    return reinterpret_cast<gu32x4*>(i < NW2T ? w2g + (size_t)c * W2TB + (size_t)i * 1024
+                                              : w1g + (size_t)c * W1TB + (size_t)(i - NW2T) * 1024);
+  };
+  u32x4 ring[RD];
+#pragma unroll
+  for (int i = 0; i < RD; ++i) ring[i] = *group_ptr(0, i);
+
+  f32x16 dacc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) dacc[b] = f32x16{};
+  for (int t = T_wg - 1; t >= 0; --t) {
+    const bool active = t < len;
+    const float actf = active ? 1.0f : 0.0f;
+    const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
+    const size_t row = (size_t)cand * a.T_max + t;
+    if (active) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        float* sd = a.SD + row * D + 32 * b;
+        dacc[b] += load_acc(sd, h);
+        store_acc(sd, dacc[b], h);                    // delta_{t+1}
+      }
+    }
+    Frag dop[NZ];
+#pragma unroll
+    for (int kf = 0; kf < NZ; ++kf) {
+      float v[SL];
+#pragma unroll
+      for (int j = 0; j < SL; ++j) v[j] = dacc[kf / NF2][(kf % NF2) * SL + j];
+      dop[kf] = PR::cvt(v);
+    }
+    f32x16 deacc[NBE];
+#pragma unroll
+    for (int b = 0; b < NBE; ++b) deacc[b] = f32x16{};
+    for (int c = 0; c < NC; ++c) {
+      const int cn = c + 1 < NC ? c + 1 : 0;
+      float* arow = a.A + row * a.H + 32 * c;
+      const f32x16 av = active ? load_acc(arow, h) : f32x16{};
+      f32x16 acc = {};
+      typename PR::Packed dp[8];
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const u32x4 grp = ring[i % RD];
+        ring[i % RD] = (i + RD < NI) ? *group_ptr(c, i + RD) : *group_ptr(cn, i + RD - NI);
+        if (i < NW2T) {
+#pragma unroll
+          for (int ww = 0; ww < G; ++ww) acc = PR::mfma(PR::pick(grp, ww), dop[i * G + ww], acc);
+          if (i == NW2T - 1) {
+            f32x16 da;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) da[r] = acc[r] * gelu_grad(av[r]) * actf;
+            if (active) store_acc(arow, da, h);       // dA
+#pragma unroll
+            for (int q = 0; q < 8; ++q) dp[q] = PR::pack2(da[2 * q], da[2 * q + 1], amask);
+          }
+        } else {
+#pragma unroll
+          for (int ww = 0; ww < G; ++ww) {
+            const int F = (i - NW2T) * G + ww;          // output block F / NF2, fragment F % NF2
+            const int ob = F / NF2;
+            if (ob < NB) dacc[ob] = PR::mfma(PR::pick(grp, ww), PR::gfrag(dp, F % NF2), dacc[ob]);
+            else deacc[ob - NB] = PR::mfma(PR::pick(grp, ww), PR::gfrag(dp, F % NF2), deacc[ob - NB]);
+          }
+        }
+      }
+    }
+    if (active) {
+#pragma unroll
+      for (int b = 0; b < NBE; ++b) store_acc(a.DE + row * E + 32 * b, deacc[b], h);
+    }
+  }
+  if (ti.valid && a.dz0) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) store_acc(a.dz0 + (size_t)cand * D + 32 * b, dacc[b], h);
+  }
+}
+
+// Weight-gradient product over the valid rows: part[split][m][k] = sum over
+// the split's rows r of A[r][m] * Bm[r][k] (operands taken as product
+// operands), rows with t >= len contributing zero.  One wavefront per 32 x 32
+// output tile and row split; sum_splits_kernel adds the splits in order.
+template <class PR>
+__global__ __launch_bounds__(64) void grad_gemm_kernel(const float* __restrict__ A, int M,
+                                                        const float* __restrict__ Bm, int N,
+                                                        const int32_t* __restrict__ lens,
+                                                        int T_max, long long rows, int rows_per_split,
+                                                        float* __restrict__ part) {
+  constexpr int KF = PR::KF, SL = PR::SL;
+  const int lane = threadIdx.x, cm = lane & 31, h = lane >> 5;
+  const int tiles_n = N / 32;
+  const int m0 = (blockIdx.x / tiles_n) * 32, k0 = (blockIdx.x % tiles_n) * 32;
+  const long long r0 = (long long)blockIdx.y * rows_per_split;
+  const long long r1 = r0 + rows_per_split < rows ? r0 + rows_per_split : rows;
+  f32x16 acc = {};
+  for (long long rb = r0; rb < r1; rb += KF) {
+    float va[SL], vb[SL];
+#pragma unroll
+    for (int j = 0; j < SL; ++j) {
+      const long long r = rb + SL * h + j;
+      bool ok = r < r1;
+      if (ok) {
+        const int i = (int)(r / T_max), t = (int)(r - (long long)i * T_max);
+        ok = t < clampi(lens[i], 0, T_max);
+      }
+      va[j] = ok ? A[r * M + m0 + cm] : 0.0f;
+      vb[j] = ok ? Bm[r * N + k0 + cm] : 0.0f;
+    }
+    acc = PR::mfma(PR::cvt(va), PR::cvt(vb), acc);
+  }
+  float* o = part + (size_t)blockIdx.y * M * N;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) o[(size_t)(m0 + acc_row(h, r)) * N + k0 + cm] = acc[r];
+}
+
+// out[q] = sum over k of part[k * stride + q], k in order.
+__global__ __launch_bounds__(256) void sum_splits_kernel(const float* __restrict__ part, int splits,
+                                                         long long stride, long long n,
+                                                         float* __restrict__ out) {
+  const long long q = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= n) return;
+  float s = 0.0f;
+  for (int k = 0; k < splits; ++k) s += part[(size_t)k * stride + q];
+  out[q] = s;
+}
+
+// Column sums over one split of the valid rows: part[split][c] (bias
+// gradients).
+__global__ __launch_bounds__(256) void colsum_kernel(const float* __restrict__ X, int C,
+                                                     const int32_t* __restrict__ lens, int T_max,
+                                                     long long rows, int rows_per_split,
+                                                     float* __restrict__ part) {
+  const long long r0 = (long long)blockIdx.y * rows_per_split;
+  const long long r1 = r0 + rows_per_split < rows ? r0 + rows_per_split : rows;
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= C) return;
+  float s = 0.0f;
+  for (long long r = r0; r < r1; ++r) {
+    const int i = (int)(r / T_max), t = (int)(r - (long long)i * T_max);
+    if (t < clampi(lens[i], 0, T_max)) s += X[r * C + c];
+  }
+  part[(size_t)blockIdx.y * C + c] = s;
+}
+
+// Embedding gradients over one split of the valid rows:
+// part[split] = [ d type_emb (K x E) | d param_w (E x P) ].
+__global__ __launch_bounds__(256) void emb_grad_kernel(const float* __restrict__ DE, int E,
+                                                       const int32_t* __restrict__ types,
+                                                       const int32_t* __restrict__ params,
+                                                       int K, int P,
+                                                       const int32_t* __restrict__ lens, int T_max,
+                                                       long long rows, int rows_per_split,
+                                                       float* __restrict__ part) {
+  const long long r0 = (long long)blockIdx.y * rows_per_split;
+  const long long r1 = r0 + rows_per_split < rows ? r0 + rows_per_split : rows;
+  const int W = K * E + E * P;
+  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= W) return;
+  float s = 0.0f;
+  if (q < K * E) {
+    const int k = q / E, f = q - k * E;
+    for (long long r = r0; r < r1; ++r) {
+      const int i = (int)(r / T_max), t = (int)(r - (long long)i * T_max);
+      if (t < clampi(lens[i], 0, T_max) && types[r] == k) s += DE[r * E + f];
+    }
+  } else {
+    const int f = (q - K * E) / P, p = (q - K * E) - f * P;
+    for (long long r = r0; r < r1; ++r) {
+      const int i = (int)(r / T_max), t = (int)(r - (long long)i * T_max);
+      if (t < clampi(lens[i], 0, T_max)) s = fmaf(DE[r * E + f], log2f((float)params[r * P + p]), s);
+    }
+  }
+  part[(size_t)blockIdx.y * W + q] = s;
+}
+
+// ==========================================================================
 // Cost model.  Wavefront = 32 candidates (original order), workgroup walks
 // the 32-wide chunks of the cost hidden layer with Wc1 fragments staged in
 // LDS.  The [z_T; phi] product is shared by all hardware vectors; each vector
@@ -2390,6 +2933,155 @@ hipError_t launch_encode(const DevModel& m, const float* feats, int32_t S, float
   const int lds = (F + Fh) * (int)sizeof(float);
   hipLaunchKernelGGL(encode_kernel, dim3(S), dim3(256), lds, st, feats, m.enc_w1t, m.enc_b1,
                      m.enc_w2t, m.enc_b2, F, Fh, D, m.prec == WM_BF16 ? 1 : 0, z0);
+  return hipGetLastError();
+}
+
+// ---- rollout loss ----------------------------------------------------------
+
+namespace {
+
+// Training kernels are instantiated for the dims whose step state fits the
+// registers of one wavefront (d <= 256).
+#define WM_FOR_TRAIN_DE(CALL)               \
+  WM_CASE(WM_FP32, PF32, 64, 32, CALL)      \
+  WM_CASE(WM_FP32, PF32, 256, 64, CALL)     \
+  WM_CASE(WM_BF16, PBF16, 64, 32, CALL)     \
+  WM_CASE(WM_BF16, PBF16, 256, 64, CALL)
+
+TrainArgs train_args(const DevModel& m, const TrainIO& io) {
+  TrainArgs a;
+  a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.w2t = m.trans_w2t; a.w1t = m.trans_w1t;
+  a.tab = m.roll_tab; a.z0 = io.z0; a.perm = io.perm; a.types = io.types; a.params = io.params;
+  a.lens = io.lens; a.X = io.X; a.A = io.A; a.G = io.G; a.P = io.P; a.SD = io.SD; a.DE = io.DE;
+  a.dz0 = io.dz0; a.err = io.err; a.B = io.B; a.T_max = io.T_max;
+  a.P_ = m.dims.n_params; a.K = m.dims.n_kinds; a.H = m.dims.trans_hidden;
+  a.tab_bytes = m.roll_tab_bytes;
+  return a;
+}
+
+template <class PR, int D, int E, int WAVES>
+hipError_t launch_train_fwd_t(const DevModel& m, const TrainArgs& a, int blocks, hipStream_t st) {
+  const int lds = m.roll_tab_bytes;
+  auto kern = train_fwd_kernel<PR, D, E, WAVES>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
+  }
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * WAVES), lds, st, a);
+  return hipGetLastError();
+}
+
+template <class PR, int D, int E>
+hipError_t launch_train_bwd_t(const TrainArgs& a, int tiles, hipStream_t st) {
+  const int waves = pick_waves(tiles);
+  const int blocks = (tiles + waves - 1) / waves;
+  if (waves == 4) hipLaunchKernelGGL((train_bwd_kernel<PR, D, E, 4>), dim3(blocks), dim3(256), 0, st, a);
+  else if (waves == 2) hipLaunchKernelGGL((train_bwd_kernel<PR, D, E, 2>), dim3(blocks), dim3(128), 0, st, a);
+  else hipLaunchKernelGGL((train_bwd_kernel<PR, D, E, 1>), dim3(blocks), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool have_train_kernels(int prec, int d, int e) {
+#define WM_HAVE_T(PR, D, E) return true;
+  WM_FOR_TRAIN_DE(WM_HAVE_T)
+#undef WM_HAVE_T
+  return false;
+}
+
+hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st) {
+  if (io.B == 0) return hipSuccess;
+  const TrainArgs a = train_args(m, io);
+  const int tiles = (io.B + 31) / 32;
+  const int waves = pick_waves(tiles);
+  const int blocks = (tiles + waves - 1) / waves;
+  const int prec = m.prec, d = m.dims.d, e = m.dims.embed_dim;
+#define WM_TFWD(PR, D, E)                                                          \
+  return waves == 4 ? launch_train_fwd_t<PR, D, E, 4>(m, a, blocks, st)              \
+       : waves == 2 ? launch_train_fwd_t<PR, D, E, 2>(m, a, blocks, st)              \
+                    : launch_train_fwd_t<PR, D, E, 1>(m, a, blocks, st);
+  WM_FOR_TRAIN_DE(WM_TFWD)
+#undef WM_TFWD
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st) {
+  if (io.B == 0) return hipSuccess;
+  const TrainArgs a = train_args(m, io);
+  const int tiles = (io.B + 31) / 32;
+  const int prec = m.prec, d = m.dims.d, e = m.dims.embed_dim;
+#define WM_TBWD(PR, D, E) return launch_train_bwd_t<PR, D, E>(a, tiles, st);
+  WM_FOR_TRAIN_DE(WM_TBWD)
+#undef WM_TBWD
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_step_loss(const float* P, const float* targets, const float* negatives, int NN,
+                            const int32_t* lens, int B, int T_max, int D, float lam, float gamma,
+                            float* SD, float* lrow, float* loss, float* total, hipStream_t st) {
+  if (B == 0) {
+    if (total) hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(1024), 0, st, loss, 0, total);
+    return hipGetLastError();
+  }
+  const long long rows = (long long)B * T_max;
+  if (rows > 0)
+    hipLaunchKernelGGL(loss_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, P, targets,
+                       negatives, NN, lens, B, T_max, D, lam, gamma, SD, lrow);
+  hipLaunchKernelGGL(loss_sum_kernel, dim3((B + 255) / 256), dim3(256), 0, st, lrow, lens, B, T_max, loss);
+  if (total) hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(1024), 0, st, loss, B, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradParts& g,
+                               float* gw1, float* gb1, float* gw2, float* gb2, float* gtemb,
+                               float* gpw, float* gpb, hipStream_t st) {
+  const int D = m.dims.d, E = m.dims.embed_dim, H = m.dims.trans_hidden, IN = D + E;
+  const int K = m.dims.n_kinds, P = m.dims.n_params, W = K * E + E * P;
+  const long long rows = (long long)io.B * io.T_max;
+  const int S = g.splits;
+  auto sums = [&](const float* part, long long stride, long long n, float* out) {
+    hipLaunchKernelGGL(sum_splits_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, S,
+                       stride, n, out);
+  };
+  if (S == 0) {       // no rows: every gradient is zero (a sum over no splits)
+    sums(nullptr, 0, (long long)H * IN, gw1);
+    sums(nullptr, 0, H, gb1);
+    sums(nullptr, 0, (long long)D * H, gw2);
+    sums(nullptr, 0, D, gb2);
+    sums(nullptr, 0, (long long)K * E, gtemb);
+    sums(nullptr, 0, (long long)E * P, gpw);
+    sums(nullptr, 0, E, gpb);
+    return hipGetLastError();
+  }
+  const dim3 gw2_grid((D / 32) * (H / 32), S), gw1_grid((H / 32) * (IN / 32), S);
+  if (m.prec == WM_BF16) {
+    hipLaunchKernelGGL(grad_gemm_kernel<PBF16>, gw2_grid, dim3(64), 0, st, io.SD, D, io.G, H, io.lens,
+                       io.T_max, rows, g.rows_per_split, g.w2);
+    hipLaunchKernelGGL(grad_gemm_kernel<PBF16>, gw1_grid, dim3(64), 0, st, io.A, H, io.X, IN, io.lens,
+                       io.T_max, rows, g.rows_per_split, g.w1);
+  } else {
+    hipLaunchKernelGGL(grad_gemm_kernel<PF32>, gw2_grid, dim3(64), 0, st, io.SD, D, io.G, H, io.lens,
+                       io.T_max, rows, g.rows_per_split, g.w2);
+    hipLaunchKernelGGL(grad_gemm_kernel<PF32>, gw1_grid, dim3(64), 0, st, io.A, H, io.X, IN, io.lens,
+                       io.T_max, rows, g.rows_per_split, g.w1);
+  }
+  hipLaunchKernelGGL(colsum_kernel, dim3((H + 255) / 256, S), dim3(256), 0, st, io.A, H, io.lens,
+                     io.T_max, rows, g.rows_per_split, g.b1);
+  hipLaunchKernelGGL(colsum_kernel, dim3((D + 255) / 256, S), dim3(256), 0, st, io.SD, D, io.lens,
+                     io.T_max, rows, g.rows_per_split, g.b2);
+  hipLaunchKernelGGL(colsum_kernel, dim3((E + 255) / 256, S), dim3(256), 0, st, io.DE, E, io.lens,
+                     io.T_max, rows, g.rows_per_split, g.pb);
+  hipLaunchKernelGGL(emb_grad_kernel, dim3((W + 255) / 256, S), dim3(256), 0, st, io.DE, E, io.types,
+                     io.params, K, P, io.lens, io.T_max, rows, g.rows_per_split, g.emb);
+  sums(g.w1, (long long)H * IN, (long long)H * IN, gw1);
+  sums(g.w2, (long long)D * H, (long long)D * H, gw2);
+  sums(g.b1, H, H, gb1);
+  sums(g.b2, D, D, gb2);
+  sums(g.pb, E, E, gpb);
+  sums(g.emb, W, (long long)K * E, gtemb);
+  sums(g.emb + (size_t)K * E, W, (long long)E * P, gpw);
   return hipGetLastError();
 }
 

@@ -114,3 +114,14 @@ def test_forest_create_validates_before_device_work():
     assert lib.wm_score_trees(None, None, 0, None, 0, 0, None, 1, 0, None, None) == B.WM_ERR_INVALID_ARGUMENT
     assert lib.wm_phi_struct(None, None, None, 4, 8, 33, 2, None, None) == B.WM_ERR_UNSUPPORTED
     assert lib.wm_phi_struct(None, None, None, -1, 8, 4, 2, None, None) == B.WM_ERR_INVALID_ARGUMENT
+
+
+def test_rollout_loss_rejects_before_device_work():
+    lib = wm.load_library()
+    assert lib.wm_loss_workspace_bytes(None, 4, 4) == 0
+    fake = ctypes.c_void_p(256)   # never dereferenced: validation fails first
+    arr, p = _seg([0, 4])
+    st = lib.wm_rollout_loss(None, fake, p, 1, fake, fake, fake, 4, 4, fake, fake, 2, 0.5, 0.3,
+                             fake, None, None, fake, 1 << 20, None)
+    assert st == B.WM_ERR_INVALID_ARGUMENT
+    assert "model" in lib.wm_last_error().decode()
