@@ -7,6 +7,7 @@ persistent rollout) from HIP events recorded on its launch stream, and the
 CPU oracle's throughput on a bounded sample of the same workload.
 
   python bench.py [--workload ansor_round] [--precision bf16] [--steps K] [--warmup W]
+  python bench.py --loss [...]     (rollout loss + gradients instead)
 """
 from __future__ import annotations
 
@@ -130,6 +131,109 @@ def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none", forest=None
                       f"+top-k, {total_t:.1f} s)"}
 
 
+def cpu_baseline_loss(w, W, I, tgt, neg, prec, lam, gamma, budget_s: float):
+    """Oracle throughput of the rollout loss with gradients on a bounded
+    random sample of the batch."""
+    from oracle import loss as LO
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    rng = np.random.default_rng(0)
+    n = min(w.B, 32)
+    seg_of = np.searchsorted(I["seg_off"], np.arange(w.B), side="right") - 1
+    total_c, total_t = 0, 0.0
+    while True:
+        pick = rng.choice(w.B, n, replace=False)
+        sub = {"types": I["types"][pick], "params": I["params"][pick], "lens": I["lens"][pick],
+               "z0": I["z0"][seg_of[pick]], "seg_off": np.arange(n + 1)}
+        t0 = time.perf_counter()
+        LO.loss_and_grad(W, sub, tgt[pick], neg[pick], lam, gamma, prec)
+        total_t += time.perf_counter() - t0
+        total_c += n
+        if total_t >= budget_s:
+            break
+        n = min(2 * n, w.B)
+    return {"value": total_c / total_t, "unit": "candidates/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{total_c} randomly drawn candidates of the {w.B}-candidate batch "
+                      f"(float64 NumPy oracle, rollout loss + gradients, {total_t:.1f} s)"}
+
+
+def run_loss_bench(args, w, prec):
+    """One step = one wm_rollout_loss call with gradients over the batch."""
+    import torch
+    import paper_2606_09312_amd as wm
+    if w.feat_dim:
+        raise SystemExit("--loss takes workloads with given initial latents")
+    dev = torch.device("cuda:0")
+    W = synth.make_weights(w, 1000)
+    I = synth.make_inputs(w, 2000)
+    tgt, neg = synth.make_loss_targets(w, 2100, args.n_neg, I["lens"])
+    lam, gamma = 0.5, 0.3
+    model = wm.Model(wm.model_dims(w), W, precision=prec)
+    t = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in I.items() if k != "seg_off"}
+    targets = torch.from_numpy(tgt).to(dev)
+    negatives = torch.from_numpy(neg).to(dev)
+    ws = wm.loss_workspace(model, w.B, w.T_max, device=dev)
+    out = {k: torch.empty(s, dtype=torch.float32, device=dev) for k, s in wm.grad_shapes(model).items()}
+    out["z0"] = torch.empty((w.B, w.d), dtype=torch.float32, device=dev)
+    loss = torch.empty(w.B, dtype=torch.float32, device=dev)
+    total = torch.empty(1, dtype=torch.float32, device=dev)
+
+    def step():
+        wm.rollout_loss(model, t["z0"], I["seg_off"], t["types"], t["params"], t["lens"], targets,
+                        negatives, lam, gamma, loss=loss, total=total, out=out, ws=ws)
+
+    for _ in range(args.warmup):
+        step()
+    wm.device_status(ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    wm.device_status(ws)
+    wm.timing_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    kern = {}
+    for name in ("bucket", "loss_fwd", "loss_steps", "loss_bwd", "loss_grads"):
+        ms, n = wm.timing_read(name)
+        if n:
+            kern[name] = {"avg_ms": ms / n, "launches": n}
+    wm.timing_enable(False)
+    steps_valid = int(I["lens"].astype(np.int64).sum())
+    flops = steps_valid * step_flops(w)          # per phase: forward, backward, weight gradients
+    dom = max(("loss_fwd", "loss_bwd", "loss_grads"), key=lambda k: kern[k]["avg_ms"])
+    achieved = flops / (kern[dom]["avg_ms"] / 1e3) / 1e12
+    peak = PEAK_TFLOPS[prec]
+    res = {
+        "metric": "candidate rollouts trained/sec (rollout loss + gradients)",
+        "value": w.B * args.steps / elapsed,
+        "unit": "candidates/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": prec, "data": "synthetic",
+        "config": {"workload": f"{w.name}: B={w.B} candidates, d={w.d}, e={w.e}, H={w.H}, "
+                               f"T_max={w.T_max}, {args.n_neg} negatives per step, "
+                               f"lambda={lam}, gamma={gamma}", "precision": prec,
+                   "global_batch": w.B, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak,
+                     "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                     "flop_per_launch": flops},
+        "kernels_avg_ms": {k: v["avg_ms"] for k, v in kern.items()},
+        "whole_path_tflops": 3 * flops * args.steps / elapsed / 1e12,
+    }
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline_loss(w, W, I, tgt, neg, prec, lam, gamma, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     global PREC
     ap = argparse.ArgumentParser()
@@ -144,6 +248,10 @@ def main():
     ap.add_argument("--ranker", default="mlp", choices=["mlp", "trees"],
                     help="cost model: the MLP on the mean action embedding, or the paper's "
                          "tree ensemble on structured action features")
+    ap.add_argument("--loss", action="store_true",
+                    help="time the rollout loss with gradients (training the transition) "
+                         "instead of the evaluator")
+    ap.add_argument("--n-neg", type=int, default=4, help="negatives per step (--loss)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -157,6 +265,9 @@ def main():
     w = synth.workload(args.workload)
     prec = args.precision or w.precisions[-1]
     PREC = prec
+    if args.loss:
+        run_loss_bench(args, w, prec)
+        return
 
     import torch
     import paper_2606_09312_amd as wm

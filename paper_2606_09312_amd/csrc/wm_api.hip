@@ -197,8 +197,8 @@ WsLayout ws_layout(const DevModel& m, int B, int T_max, int S, int n_hw) {
 // Rollout-loss workspace: bucketing, step activations (rows i * T_max + t),
 // per-candidate step losses, partial gradient sums.
 struct LossLayout {
-  size_t err, perm, hist, X, A, G, P, SD, DE, lrow, pw1, pw2, pb1, pb2, pemb, ppb, total;
-  int splits, rows_per_split;
+  size_t err, perm, hist, off, row_src, X, A, G, P, SD, DE, lrow, pw1, pw2, pb1, pb2, pemb, total;
+  int splits;
 };
 
 LossLayout loss_layout(const DevModel& m, int B, int T_max) {
@@ -209,12 +209,13 @@ LossLayout loss_layout(const DevModel& m, int B, int T_max) {
   const size_t R = (size_t)rows;
   LossLayout L;
   L.splits = train_splits(rows);
-  L.rows_per_split = train_rows_per_split(rows);
   const size_t S = (size_t)L.splits;
   size_t o = 0;
   L.err = o; o += 256;
   L.perm = o; o = align256(o + (size_t)B * sizeof(int2));
   L.hist = o; o = align256(o + (size_t)bucket_groups(B) * (size_t)(T_max + 1) * 4);
+  L.off = o; o = align256(o + ((size_t)B + 1) * 4);
+  L.row_src = o; o = align256(o + R * 4);
   L.X = o; o = align256(o + R * (D + E) * 4);
   L.A = o; o = align256(o + R * H * 4);
   L.G = o; o = align256(o + R * H * 4);
@@ -226,8 +227,7 @@ LossLayout loss_layout(const DevModel& m, int B, int T_max) {
   L.pw2 = o; o = align256(o + S * D * H * 4);
   L.pb1 = o; o = align256(o + S * H * 4);
   L.pb2 = o; o = align256(o + S * D * 4);
-  L.pemb = o; o = align256(o + S * (K * E + E * P) * 4);
-  L.ppb = o; o = align256(o + S * E * 4);
+  L.pemb = o; o = align256(o + S * (K * E + E * P + E) * 4);
   L.total = o;
   return L;
 }
@@ -728,21 +728,26 @@ wm_status wm_rollout_loss(const wm_model* model, const float* z0, const int32_t*
   auto fptr = [&](size_t off) { return reinterpret_cast<float*>(w8 + off); };
   TrainIO io;
   io.z0 = z0; io.perm = reinterpret_cast<int2*>(w8 + L.perm); io.types = types; io.params = params;
-  io.lens = lens; io.X = fptr(L.X); io.A = fptr(L.A); io.G = fptr(L.G); io.P = fptr(L.P);
+  io.lens = lens; io.off = reinterpret_cast<int32_t*>(w8 + L.off);
+  io.row_src = reinterpret_cast<int32_t*>(w8 + L.row_src);
+  io.X = fptr(L.X); io.A = fptr(L.A); io.G = fptr(L.G); io.P = fptr(L.P);
   io.SD = fptr(L.SD); io.DE = fptr(L.DE); io.dz0 = grads ? grads->z0 : nullptr;
   io.err = reinterpret_cast<int32_t*>(w8 + L.err); io.B = B; io.T_max = T_max;
   if (B > 0) {
     WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, const_cast<int2*>(io.perm),
                                           reinterpret_cast<int32_t*>(w8 + L.hist), io.err, st));
+    WM_TIMED(TK_BUCKET, st, launch_row_offsets(lens, B, T_max, io.off, st));
     WM_TIMED(TK_TRAIN_FWD, st, launch_train_fwd(m, io, st));
+  } else {
+    WM_TIMED(TK_BUCKET, st, launch_row_offsets(lens, 0, T_max, io.off, st));
   }
-  WM_TIMED(TK_LOSS, st, launch_step_loss(io.P, targets, negatives, n_neg, lens, B, T_max, m.dims.d, lam,
-                                          gamma, io.SD, fptr(L.lrow), loss, total, st));
+  WM_TIMED(TK_LOSS, st, launch_step_loss(io.P, targets, negatives, n_neg, lens, io.off, B, T_max,
+                                          m.dims.d, lam, gamma, io.SD, fptr(L.lrow), loss, total, st));
   if (!grads) return ok();
   if (B > 0) WM_TIMED(TK_TRAIN_BWD, st, launch_train_bwd(m, io, st));
   GradParts gp;
   gp.w1 = fptr(L.pw1); gp.w2 = fptr(L.pw2); gp.b1 = fptr(L.pb1); gp.b2 = fptr(L.pb2);
-  gp.emb = fptr(L.pemb); gp.pb = fptr(L.ppb); gp.splits = L.splits; gp.rows_per_split = L.rows_per_split;
+  gp.emb = fptr(L.pemb); gp.splits = L.splits;
   WM_TIMED(TK_GRADS, st, launch_weight_grads(m, io, gp, grads->w1, grads->b1, grads->w2, grads->b2,
                                              grads->type_emb, grads->param_w, grads->param_b, st));
   return ok();

@@ -238,38 +238,38 @@ hipError_t launch_score_trees(const DevForest& f, const float* zT, int32_t d, co
                               int32_t hw_dim, float* scores, hipStream_t st);
 
 // Rollout loss (training objective of the transition): device buffers of
-// one call, rows r = i * T_max + t (see the kernels for their contents).
+// one call.  Step activations are compact rows r = off[i] + t (see the
+// kernels for their contents); their arrays are sized for B * T_max rows.
 struct TrainIO {
   const float* z0;          // [S][D]
   const int2* perm;         // length-sorted (candidate, subgraph)
   const int32_t* types;
   const int32_t* params;
   const int32_t* lens;
+  int32_t* off;             // [B+1] row offsets (written by launch_row_offsets)
+  int32_t* row_src;         // [rows] i * T_max + t of each row
   float *X, *A, *G, *P, *SD, *DE;
   float* dz0;               // [B][D] or null
   int32_t* err;
   int B, T_max;
 };
-// Weight-gradient partial sums: `splits` row ranges of rows_per_split rows
-// (a multiple of 16) each, added in order afterwards.
+// Weight-gradient partial sums of `splits` equal shares of the rows, added
+// in order afterwards.
 struct GradParts {
-  float *w1, *w2, *b1, *b2, *emb, *pb;
-  int splits, rows_per_split;
+  float *w1, *w2, *b1, *b2, *emb;
+  int splits;
 };
-inline int train_rows_per_split(long long rows) {
-  long long r = (rows + 63) / 64;
-  if (r < 256) r = 256;
-  return (int)((r + 15) / 16 * 16);
-}
-inline int train_splits(long long rows) {
-  const int r = train_rows_per_split(rows);
-  return rows == 0 ? 0 : (int)((rows + r - 1) / r);
+inline int train_splits(long long rows_bound) {
+  const long long s = (rows_bound + 2047) / 2048;
+  return (int)(s < 1 ? 1 : (s > 32 ? 32 : s));
 }
 bool have_train_kernels(int prec, int d, int e);
+hipError_t launch_row_offsets(const int32_t* lens, int B, int T_max, int32_t* off, hipStream_t st);
 hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st);
 hipError_t launch_step_loss(const float* P, const float* targets, const float* negatives, int NN,
-                            const int32_t* lens, int B, int T_max, int D, float lam, float gamma,
-                            float* SD, float* lrow, float* loss, float* total, hipStream_t st);
+                            const int32_t* lens, const int32_t* off, int B, int T_max, int D,
+                            float lam, float gamma, float* SD, float* lrow, float* loss,
+                            float* total, hipStream_t st);
 hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st);
 hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradParts& parts,
                                float* gw1, float* gb1, float* gw2, float* gb2, float* gtemb,

@@ -14,6 +14,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "wm_internal.h"
 
 namespace wm {
@@ -1728,9 +1730,10 @@ __global__ __launch_bounds__(TREE_THREADS) void score_trees_kernel(
 
 // ==========================================================================
 // Rollout loss and its gradients (the transition's training objective,
-// Sec. 3.4).  Step activations live in dense rows r = i * T_max + t of the
-// workspace (rows with t >= len_i are never read: the gradient products and
-// sums mask them).
+// Sec. 3.4).  Step activations live in compact rows r = off[i] + t of the
+// workspace, off the exclusive prefix sum of the (clamped) lengths, so the
+// valid steps of all candidates are rows [0, off[B]) with no padding;
+// row_src[r] = i * T_max + t locates a row's action in the caller's tensors.
 //
 // train_fwd_kernel: one wavefront per 32-candidate tile (length-sorted),
 // the residual-MLP step with the weight groups streamed from L2 into a
@@ -1749,6 +1752,8 @@ struct TrainArgs {
   const int32_t* types;
   const int32_t* params;
   const int32_t* lens;
+  const int32_t* off;       // [B+1] row offsets
+  int32_t* row_src;         // [R]  i * T_max + t of each row
   float* X;                 // [R][D+E]
   float* A;                 // [R][H]   pre-activations; the backward overwrites them with dA
   float* G;                 // [R][H]
@@ -1864,6 +1869,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_fwd_kernel(const TrainArg
   const TileInfo ti = tile_info(a, blockIdx.x * WAVES + wave, n);
   const int cand = ti.cand, len = ti.len, T_wg = ti.T_wg;
   const int NC = a.H / 32;
+  const size_t row0 = ti.valid ? (size_t)a.off[cand] : 0;
 
   f32x16 zacc[NB];
 #pragma unroll
@@ -1887,7 +1893,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_fwd_kernel(const TrainArg
     const bool active = t < len;
     const float actf = active ? 1.0f : 0.0f;
     const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
-    const size_t row = (size_t)cand * a.T_max + t;
+    const size_t row = row0 + t;
+    if (active && h == 0) a.row_src[row] = cand * a.T_max + t;
     // the step's action: kind and log2 parameters (zero embedding when done)
     int ty = 0;
     float u[PMAX];
@@ -1998,22 +2005,25 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_fwd_kernel(const TrainArg
 }
 
 // Per-step loss and its gradient with respect to the prediction: one
-// wavefront per row (candidate, step), lanes over the latent.  The hardest
+// wavefront per (candidate, step) slot, lanes over the latent.  The hardest
 // negative is the nearest (first one on ties); a zero distance contributes a
-// zero gradient.
+// zero gradient.  targets / negatives are indexed by slot, P / SD / lrow by
+// compact row.
 __global__ __launch_bounds__(256) void loss_kernel(const float* __restrict__ P,
                                                    const float* __restrict__ targets,
                                                    const float* __restrict__ negatives, int NN,
-                                                   const int32_t* __restrict__ lens, int B,
+                                                   const int32_t* __restrict__ lens,
+                                                   const int32_t* __restrict__ off, int B,
                                                    int T_max, int D, float lam, float gamma,
                                                    float* __restrict__ SD, float* __restrict__ lrow) {
   const int lane = threadIdx.x & 63;
-  const long long row = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  if (row >= (long long)B * T_max) return;             // whole wavefront leaves together
-  const int i = (int)(row / T_max), t = (int)(row - (long long)i * T_max);
+  const long long slot = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (slot >= (long long)B * T_max) return;            // whole wavefront leaves together
+  const int i = (int)(slot / T_max), t = (int)(slot - (long long)i * T_max);
   if (t >= clampi(lens[i], 0, T_max)) return;
+  const size_t row = (size_t)off[i] + t;
   const float* p = P + row * D;
-  const float* y = targets + row * D;
+  const float* y = targets + slot * D;
   float m = 0.0f;
   for (int f = lane; f < D; f += 64) { const float v = p[f] - y[f]; m = fmaf(v, v, m); }
   const float match = wave_sum(m);
@@ -2021,7 +2031,7 @@ __global__ __launch_bounds__(256) void loss_kernel(const float* __restrict__ P,
   float dmin = INFINITY;
   int hard = 0;
   for (int q = 0; q < NN; ++q) {
-    const float* ng = negatives + (row * NN + q) * D;
+    const float* ng = negatives + (slot * NN + q) * D;
     float s = 0.0f;
     for (int f = lane; f < D; f += 64) { const float v = p[f] - ng[f]; s = fmaf(v, v, s); }
     const float dq = sqrtf(wave_sum(s));
@@ -2032,7 +2042,7 @@ __global__ __launch_bounds__(256) void loss_kernel(const float* __restrict__ P,
   if (lane == 0) lrow[row] = lam * match + (1.0f - lam) * (act ? hinge : 0.0f);
   const float ip = dpos > 0.0f ? 1.0f / dpos : 0.0f;
   const float in = dmin > 0.0f ? 1.0f / dmin : 0.0f;
-  const float* ng = negatives + (row * NN + hard) * D;
+  const float* ng = negatives + (slot * NN + hard) * D;
   for (int f = lane; f < D; f += 64) {
     const float diff = p[f] - y[f];
     float g = lam * 2.0f * diff;
@@ -2043,14 +2053,30 @@ __global__ __launch_bounds__(256) void loss_kernel(const float* __restrict__ P,
 
 // Per-candidate loss: the sum of its steps' losses in step order.
 __global__ __launch_bounds__(256) void loss_sum_kernel(const float* __restrict__ lrow,
-                                                       const int32_t* __restrict__ lens, int B,
-                                                       int T_max, float* __restrict__ loss) {
+                                                       const int32_t* __restrict__ off, int B,
+                                                       float* __restrict__ loss) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= B) return;
-  const int L = clampi(lens[i], 0, T_max);
   float s = 0.0f;
-  for (int t = 0; t < L; ++t) s += lrow[(size_t)i * T_max + t];
+  for (int r = off[i]; r < off[i + 1]; ++r) s += lrow[r];
   loss[i] = s;
+}
+
+// Row offsets: off[i] = sum over j < i of clamp(lens[j], 0, T_max), i <= B.
+// One workgroup; each thread sums a contiguous run, then a workgroup scan.
+__global__ __launch_bounds__(1024) void row_offsets_kernel(const int32_t* __restrict__ lens, int B,
+                                                           int T_max, int32_t* __restrict__ off) {
+  __shared__ int wsum[16];
+  const int per = (B + 1023) / 1024;
+  const int i0 = threadIdx.x * per, i1 = min(B, i0 + per);
+  int s = 0;
+  for (int i = i0; i < i1; ++i) s += clampi(lens[i], 0, T_max);
+  int run = block_exclusive_scan(s, wsum);
+  for (int i = i0; i < i1; ++i) {
+    off[i] = run;
+    run += clampi(lens[i], 0, T_max);
+  }
+  if (threadIdx.x == 1023) off[B] = run;
 }
 
 // Sum of the per-candidate losses, one workgroup in a fixed order.
@@ -2091,6 +2117,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_bwd_kernel(const TrainArg
   const TileInfo ti = tile_info(a, blockIdx.x * WAVES + wave, n);
   const int cand = ti.cand, len = ti.len, T_wg = ti.T_wg;
   const int NC = a.H / 32;
+  const size_t row0 = ti.valid ? (size_t)a.off[cand] : 0;
 
   gu8* w2g = (gu8*)(a.w2t) + lane * 16;
   gu8* w1g = (gu8*)(a.w1t) + lane * 16;
@@ -2109,7 +2136,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_bwd_kernel(const TrainArg
     const bool active = t < len;
     const float actf = active ? 1.0f : 0.0f;
     const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
-    const size_t row = (size_t)cand * a.T_max + t;
+    const size_t row = row0 + t;
     if (active) {
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
@@ -2172,41 +2199,159 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_bwd_kernel(const TrainArg
   }
 }
 
-// Weight-gradient product over the valid rows: part[split][m][k] = sum over
-// the split's rows r of A[r][m] * Bm[r][k] (operands taken as product
-// operands), rows with t >= len contributing zero.  One wavefront per 32 x 32
-// output tile and row split; sum_splits_kernel adds the splits in order.
+// Row range of one split of the compact rows [0, off[B]): equal shares,
+// multiples of 32 rows.
+__device__ __forceinline__ void split_rows(const int32_t* off, int B, int splits, int split,
+                                           int& r0, int& r1) {
+  const int Rv = off[B];
+  const int rps = ((Rv + splits - 1) / splits + 31) & ~31;
+  r0 = min(Rv, split * rps);
+  r1 = min(Rv, r0 + rps);
+}
+
+// Weight gradients as split-K products over the compact rows, two problems
+// per launch (dW2 = sum R(delta) (x) g, dW1 = sum R(dA) (x) x):
+//   part[split][m][n] = sum over the split's rows r of op(A[r][m]) * op(B[r][n])
+// with the column sums of A (unrounded: db2, db1) on the side.  Workgroup =
+// 4 wavefronts on a 128 x 128 output tile, each wavefront 64 x 64 (2 x 2
+// matrix-core tiles); 32 rows per stage: every thread loads 8 consecutive
+// rows of one column (coalesced across the wavefront), rounds them as
+// product operands and writes them to LDS transposed (column-major, rows
+// contiguous), so each lane's operand fragment is one 16-byte LDS read.  The
+// next stage's loads are in flight during the current stage's products.
+struct WgradProblem {
+  const float* A;           // [rows][M]
+  const float* Bm;          // [rows][N]
+  float* part;              // [splits][M][N]
+  float* colsum;            // [splits][M]
+  int M, N, tiles_n, tiles;
+};
+struct WgradArgs {
+  WgradProblem p0, p1;
+  const int32_t* off;
+  int B, splits;
+};
+constexpr int WG_T = 128, WG_KC = 32;
+
 template <class PR>
-__global__ __launch_bounds__(64) void grad_gemm_kernel(const float* __restrict__ A, int M,
-                                                        const float* __restrict__ Bm, int N,
-                                                        const int32_t* __restrict__ lens,
-                                                        int T_max, long long rows, int rows_per_split,
-                                                        float* __restrict__ part) {
+__global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   constexpr int KF = PR::KF, SL = PR::SL;
-  const int lane = threadIdx.x, cm = lane & 31, h = lane >> 5;
-  const int tiles_n = N / 32;
-  const int m0 = (blockIdx.x / tiles_n) * 32, k0 = (blockIdx.x % tiles_n) * 32;
-  const long long r0 = (long long)blockIdx.y * rows_per_split;
-  const long long r1 = r0 + rows_per_split < rows ? r0 + rows_per_split : rows;
-  f32x16 acc = {};
-  for (long long rb = r0; rb < r1; rb += KF) {
-    float va[SL], vb[SL];
+  constexpr bool BF = PR::G == 1;
+  using Elem = typename std::conditional<BF, __bf16, float>::type;
+  constexpr int LDW = WG_KC + (BF ? 8 : 4);               // padded LDS row (elements)
+  __shared__ __attribute__((aligned(16))) Elem As[WG_T * LDW];
+  __shared__ __attribute__((aligned(16))) Elem Bs[WG_T * LDW];
+  __shared__ float csum[WG_T];
+  const bool second = (int)blockIdx.x >= a.p0.tiles;
+  const float* A = second ? a.p1.A : a.p0.A;
+  const float* Bm = second ? a.p1.Bm : a.p0.Bm;
+  float* part = second ? a.p1.part : a.p0.part;
+  float* colsum = second ? a.p1.colsum : a.p0.colsum;
+  const int M = second ? a.p1.M : a.p0.M, N = second ? a.p1.N : a.p0.N;
+  const int tiles_n = second ? a.p1.tiles_n : a.p0.tiles_n;
+  const int tile = (int)blockIdx.x - (second ? a.p0.tiles : 0);
+  const int m0 = (tile / tiles_n) * WG_T, n0 = (tile % tiles_n) * WG_T;
+  const int split = blockIdx.y;
+  int r0, r1;
+  split_rows(a.off, a.B, a.splits, split, r0, r1);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = tid & (WG_T - 1), rg = tid >> 7;          // loader: column, row group (0, 1)
+  const bool okA = m0 + c < M, okB = n0 + c < N;
+  float va[2][8], vb[2][8];
+  float cs = 0.0f;
+  auto load = [&](int rb) {
 #pragma unroll
-    for (int j = 0; j < SL; ++j) {
-      const long long r = rb + SL * h + j;
-      bool ok = r < r1;
-      if (ok) {
-        const int i = (int)(r / T_max), t = (int)(r - (long long)i * T_max);
-        ok = t < clampi(lens[i], 0, T_max);
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int r = rb + (rg + 2 * q) * 8 + j;
+        const bool rv = r < r1;
+        va[q][j] = (rv && okA) ? A[(size_t)r * M + m0 + c] : 0.0f;
+        vb[q][j] = (rv && okB) ? Bm[(size_t)r * N + n0 + c] : 0.0f;
       }
-      va[j] = ok ? A[r * M + m0 + cm] : 0.0f;
-      vb[j] = ok ? Bm[r * N + k0 + cm] : 0.0f;
-    }
-    acc = PR::mfma(PR::cvt(va), PR::cvt(vb), acc);
-  }
-  float* o = part + (size_t)blockIdx.y * M * N;
+  };
+  auto store = [&]() {
 #pragma unroll
-  for (int r = 0; r < 16; ++r) o[(size_t)(m0 + acc_row(h, r)) * N + k0 + cm] = acc[r];
+    for (int q = 0; q < 2; ++q) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) cs += va[q][j];
+      Elem* da = As + c * LDW + (rg + 2 * q) * 8;
+      Elem* db = Bs + c * LDW + (rg + 2 * q) * 8;
+      if constexpr (BF) {
+        bf16x8 ea, eb;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          ea[j] = (__bf16)va[q][j];
+          eb[j] = (__bf16)vb[q][j];
+        }
+        *reinterpret_cast<bf16x8*>(da) = ea;
+        *reinterpret_cast<bf16x8*>(db) = eb;
+      } else {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const f32x4 xa = {va[q][4 * k], va[q][4 * k + 1], va[q][4 * k + 2], va[q][4 * k + 3]};
+          const f32x4 xb = {vb[q][4 * k], vb[q][4 * k + 1], vb[q][4 * k + 2], vb[q][4 * k + 3]};
+          *reinterpret_cast<f32x4*>(da + 4 * k) = xa;
+          *reinterpret_cast<f32x4*>(db + 4 * k) = xb;
+        }
+      }
+    }
+  };
+
+  const int wm = wave & 1, wn = wave >> 1;
+  const int cl = lane & 31, h = lane >> 5;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+  if (r0 < r1) load(r0);
+  for (int rb = r0; rb < r1; rb += WG_KC) {
+    __syncthreads();                      // the previous stage's reads are done
+    store();
+    __syncthreads();
+    if (rb + WG_KC < r1) load(rb + WG_KC);
+#pragma unroll
+    for (int ks = 0; ks < WG_KC / KF; ++ks) {
+      typename PR::Frag fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const Elem* pa = As + (wm * 64 + i * 32 + cl) * LDW + ks * KF + h * SL;
+        const Elem* pb = Bs + (wn * 64 + i * 32 + cl) * LDW + ks * KF + h * SL;
+        if constexpr (BF) {
+          fa[i] = *reinterpret_cast<const typename PR::Frag*>(pa);
+          fb[i] = *reinterpret_cast<const typename PR::Frag*>(pb);
+        } else {
+          fa[i] = *pa;
+          fb[i] = *pb;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = PR::mfma(fa[i], fb[j], acc[i][j]);
+    }
+  }
+  float* o = part + (size_t)split * M * N;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int n = n0 + wn * 64 + j * 32 + cl;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 64 + i * 32 + acc_row(h, r);
+        if (m < M && n < N) o[(size_t)m * N + n] = acc[i][j][r];
+      }
+    }
+  // column sums of A: the two row groups, in order (first column tile only)
+  if (n0 == 0) {
+    __syncthreads();
+    if (rg == 1) csum[c] = cs;
+    __syncthreads();
+    if (rg == 0 && okA) colsum[(size_t)split * M + m0 + c] = cs + csum[c];
+  }
 }
 
 // out[q] = sum over k of part[k * stride + q], k in order.
@@ -2220,53 +2365,45 @@ __global__ __launch_bounds__(256) void sum_splits_kernel(const float* __restrict
   out[q] = s;
 }
 
-// Column sums over one split of the valid rows: part[split][c] (bias
-// gradients).
-__global__ __launch_bounds__(256) void colsum_kernel(const float* __restrict__ X, int C,
-                                                     const int32_t* __restrict__ lens, int T_max,
-                                                     long long rows, int rows_per_split,
-                                                     float* __restrict__ part) {
-  const long long r0 = (long long)blockIdx.y * rows_per_split;
-  const long long r1 = r0 + rows_per_split < rows ? r0 + rows_per_split : rows;
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= C) return;
-  float s = 0.0f;
-  for (long long r = r0; r < r1; ++r) {
-    const int i = (int)(r / T_max), t = (int)(r - (long long)i * T_max);
-    if (t < clampi(lens[i], 0, T_max)) s += X[r * C + c];
+// Embedding gradients over one split of the compact rows:
+// part[split] = [ d type_emb (K x E) | d param_w (E x P) | d param_b (E) ].
+// Thread (row group g, feature f) walks rows g, g + RG, ... of the split
+// with per-kind bins in LDS (each thread owns its feature's column), then
+// the row groups are added in order.
+constexpr int EMB_THREADS = 256;
+__global__ __launch_bounds__(EMB_THREADS) void emb_grad_kernel(const float* __restrict__ DE, int E,
+                                                               const int32_t* __restrict__ row_src,
+                                                               const int32_t* __restrict__ types,
+                                                               const int32_t* __restrict__ params,
+                                                               int K, int P,
+                                                               const int32_t* __restrict__ off, int B,
+                                                               int splits, float* __restrict__ part) {
+  extern __shared__ float bins[];                          // [RG][K + P + 1][E]
+  const int RG = EMB_THREADS / E;
+  const int f = threadIdx.x % E, g = threadIdx.x / E;
+  const int W = K * E + E * P + E;
+  int r0, r1;
+  split_rows(off, B, splits, blockIdx.x, r0, r1);
+  float* mine = bins + (size_t)g * (K + P + 1) * E;
+  for (int k = 0; k < K + P + 1; ++k) mine[k * E + f] = 0.0f;
+  for (int r = r0 + g; r < r1; r += RG) {
+    const float v = DE[(size_t)r * E + f];
+    const int src = row_src[r];
+    const int ty = types[src];
+    if (ty >= 0 && ty < K) mine[ty * E + f] += v;
+    for (int p = 0; p < P; ++p) mine[(K + p) * E + f] = fmaf(v, log2f((float)params[(size_t)src * P + p]), mine[(K + p) * E + f]);
+    mine[(K + P) * E + f] += v;
   }
-  part[(size_t)blockIdx.y * C + c] = s;
-}
-
-// Embedding gradients over one split of the valid rows:
-// part[split] = [ d type_emb (K x E) | d param_w (E x P) ].
-__global__ __launch_bounds__(256) void emb_grad_kernel(const float* __restrict__ DE, int E,
-                                                       const int32_t* __restrict__ types,
-                                                       const int32_t* __restrict__ params,
-                                                       int K, int P,
-                                                       const int32_t* __restrict__ lens, int T_max,
-                                                       long long rows, int rows_per_split,
-                                                       float* __restrict__ part) {
-  const long long r0 = (long long)blockIdx.y * rows_per_split;
-  const long long r1 = r0 + rows_per_split < rows ? r0 + rows_per_split : rows;
-  const int W = K * E + E * P;
-  const int q = blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= W) return;
-  float s = 0.0f;
-  if (q < K * E) {
-    const int k = q / E, f = q - k * E;
-    for (long long r = r0; r < r1; ++r) {
-      const int i = (int)(r / T_max), t = (int)(r - (long long)i * T_max);
-      if (t < clampi(lens[i], 0, T_max) && types[r] == k) s += DE[r * E + f];
-    }
-  } else {
-    const int f = (q - K * E) / P, p = (q - K * E) - f * P;
-    for (long long r = r0; r < r1; ++r) {
-      const int i = (int)(r / T_max), t = (int)(r - (long long)i * T_max);
-      if (t < clampi(lens[i], 0, T_max)) s = fmaf(DE[r * E + f], log2f((float)params[r * P + p]), s);
-    }
+  __syncthreads();
+  if (g != 0) return;
+  float* o = part + (size_t)blockIdx.x * W;
+  for (int k = 0; k < K + P + 1; ++k) {
+    float s = 0.0f;
+    for (int q = 0; q < RG; ++q) s += bins[((size_t)q * (K + P + 1) + k) * E + f];
+    if (k < K) o[k * E + f] = s;                            // type_emb [K][E]
+    else if (k < K + P) o[K * E + f * P + (k - K)] = s;     // param_w [E][P]
+    else o[K * E + E * P + f] = s;                          // param_b [E]
   }
-  part[(size_t)blockIdx.y * W + q] = s;
 }
 
 // ==========================================================================
@@ -2952,7 +3089,8 @@ TrainArgs train_args(const DevModel& m, const TrainIO& io) {
   TrainArgs a;
   a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.w2t = m.trans_w2t; a.w1t = m.trans_w1t;
   a.tab = m.roll_tab; a.z0 = io.z0; a.perm = io.perm; a.types = io.types; a.params = io.params;
-  a.lens = io.lens; a.X = io.X; a.A = io.A; a.G = io.G; a.P = io.P; a.SD = io.SD; a.DE = io.DE;
+  a.lens = io.lens; a.off = io.off; a.row_src = io.row_src;
+  a.X = io.X; a.A = io.A; a.G = io.G; a.P = io.P; a.SD = io.SD; a.DE = io.DE;
   a.dz0 = io.dz0; a.err = io.err; a.B = io.B; a.T_max = io.T_max;
   a.P_ = m.dims.n_params; a.K = m.dims.n_kinds; a.H = m.dims.trans_hidden;
   a.tab_bytes = m.roll_tab_bytes;
@@ -3018,18 +3156,21 @@ hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st
   return hipErrorInvalidValue;
 }
 
+hipError_t launch_row_offsets(const int32_t* lens, int B, int T_max, int32_t* off, hipStream_t st) {
+  hipLaunchKernelGGL(row_offsets_kernel, dim3(1), dim3(1024), 0, st, lens, B, T_max, off);
+  return hipGetLastError();
+}
+
 hipError_t launch_step_loss(const float* P, const float* targets, const float* negatives, int NN,
-                            const int32_t* lens, int B, int T_max, int D, float lam, float gamma,
-                            float* SD, float* lrow, float* loss, float* total, hipStream_t st) {
-  if (B == 0) {
-    if (total) hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(1024), 0, st, loss, 0, total);
-    return hipGetLastError();
-  }
-  const long long rows = (long long)B * T_max;
-  if (rows > 0)
-    hipLaunchKernelGGL(loss_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, P, targets,
-                       negatives, NN, lens, B, T_max, D, lam, gamma, SD, lrow);
-  hipLaunchKernelGGL(loss_sum_kernel, dim3((B + 255) / 256), dim3(256), 0, st, lrow, lens, B, T_max, loss);
+                            const int32_t* lens, const int32_t* off, int B, int T_max, int D,
+                            float lam, float gamma, float* SD, float* lrow, float* loss,
+                            float* total, hipStream_t st) {
+  const long long slots = (long long)B * T_max;
+  if (slots > 0)
+    hipLaunchKernelGGL(loss_kernel, dim3((unsigned)((slots + 3) / 4)), dim3(256), 0, st, P, targets,
+                       negatives, NN, lens, off, B, T_max, D, lam, gamma, SD, lrow);
+  if (B > 0)
+    hipLaunchKernelGGL(loss_sum_kernel, dim3((B + 255) / 256), dim3(256), 0, st, lrow, off, B, loss);
   if (total) hipLaunchKernelGGL(loss_total_kernel, dim3(1), dim3(1024), 0, st, loss, B, total);
   return hipGetLastError();
 }
@@ -3038,50 +3179,42 @@ hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradP
                                float* gw1, float* gb1, float* gw2, float* gb2, float* gtemb,
                                float* gpw, float* gpb, hipStream_t st) {
   const int D = m.dims.d, E = m.dims.embed_dim, H = m.dims.trans_hidden, IN = D + E;
-  const int K = m.dims.n_kinds, P = m.dims.n_params, W = K * E + E * P;
-  const long long rows = (long long)io.B * io.T_max;
+  const int K = m.dims.n_kinds, P = m.dims.n_params, W = K * E + E * P + E;
   const int S = g.splits;
   auto sums = [&](const float* part, long long stride, long long n, float* out) {
     hipLaunchKernelGGL(sum_splits_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, S,
                        stride, n, out);
   };
-  if (S == 0) {       // no rows: every gradient is zero (a sum over no splits)
-    sums(nullptr, 0, (long long)H * IN, gw1);
-    sums(nullptr, 0, H, gb1);
-    sums(nullptr, 0, (long long)D * H, gw2);
-    sums(nullptr, 0, D, gb2);
-    sums(nullptr, 0, (long long)K * E, gtemb);
-    sums(nullptr, 0, (long long)E * P, gpw);
-    sums(nullptr, 0, E, gpb);
-    return hipGetLastError();
+  WgradArgs a;
+  auto prob = [](const float* A, int M, const float* Bm, int N, float* part, float* colsum) {
+    WgradProblem p;
+    p.A = A; p.Bm = Bm; p.part = part; p.colsum = colsum; p.M = M; p.N = N;
+    p.tiles_n = (N + WG_T - 1) / WG_T;
+    p.tiles = ((M + WG_T - 1) / WG_T) * p.tiles_n;
+    return p;
+  };
+  a.p0 = prob(io.SD, D, io.G, H, g.w2, g.b2);      // dW2 [D][H], db2
+  a.p1 = prob(io.A, H, io.X, IN, g.w1, g.b1);      // dW1 [H][IN], db1
+  a.off = io.off; a.B = io.B; a.splits = S;
+  const dim3 grid(a.p0.tiles + a.p1.tiles, S);
+  if (m.prec == WM_BF16) hipLaunchKernelGGL(wgrad_kernel<PBF16>, grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL(wgrad_kernel<PF32>, grid, dim3(256), 0, st, a);
+  if (E > EMB_THREADS || EMB_THREADS % E) return hipErrorInvalidValue;
+  const int lds = (EMB_THREADS / E) * (K + P + 1) * E * (int)sizeof(float);
+  hipError_t e = hipFuncSetAttribute((const void*)emb_grad_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
   }
-  const dim3 gw2_grid((D / 32) * (H / 32), S), gw1_grid((H / 32) * (IN / 32), S);
-  if (m.prec == WM_BF16) {
-    hipLaunchKernelGGL(grad_gemm_kernel<PBF16>, gw2_grid, dim3(64), 0, st, io.SD, D, io.G, H, io.lens,
-                       io.T_max, rows, g.rows_per_split, g.w2);
-    hipLaunchKernelGGL(grad_gemm_kernel<PBF16>, gw1_grid, dim3(64), 0, st, io.A, H, io.X, IN, io.lens,
-                       io.T_max, rows, g.rows_per_split, g.w1);
-  } else {
-    hipLaunchKernelGGL(grad_gemm_kernel<PF32>, gw2_grid, dim3(64), 0, st, io.SD, D, io.G, H, io.lens,
-                       io.T_max, rows, g.rows_per_split, g.w2);
-    hipLaunchKernelGGL(grad_gemm_kernel<PF32>, gw1_grid, dim3(64), 0, st, io.A, H, io.X, IN, io.lens,
-                       io.T_max, rows, g.rows_per_split, g.w1);
-  }
-  hipLaunchKernelGGL(colsum_kernel, dim3((H + 255) / 256, S), dim3(256), 0, st, io.A, H, io.lens,
-                     io.T_max, rows, g.rows_per_split, g.b1);
-  hipLaunchKernelGGL(colsum_kernel, dim3((D + 255) / 256, S), dim3(256), 0, st, io.SD, D, io.lens,
-                     io.T_max, rows, g.rows_per_split, g.b2);
-  hipLaunchKernelGGL(colsum_kernel, dim3((E + 255) / 256, S), dim3(256), 0, st, io.DE, E, io.lens,
-                     io.T_max, rows, g.rows_per_split, g.pb);
-  hipLaunchKernelGGL(emb_grad_kernel, dim3((W + 255) / 256, S), dim3(256), 0, st, io.DE, E, io.types,
-                     io.params, K, P, io.lens, io.T_max, rows, g.rows_per_split, g.emb);
+  hipLaunchKernelGGL(emb_grad_kernel, dim3(S), dim3(EMB_THREADS), lds, st, io.DE, E, io.row_src,
+                     io.types, io.params, K, P, io.off, io.B, S, g.emb);
   sums(g.w1, (long long)H * IN, (long long)H * IN, gw1);
   sums(g.w2, (long long)D * H, (long long)D * H, gw2);
   sums(g.b1, H, H, gb1);
   sums(g.b2, D, D, gb2);
-  sums(g.pb, E, E, gpb);
   sums(g.emb, W, (long long)K * E, gtemb);
   sums(g.emb + (size_t)K * E, W, (long long)E * P, gpw);
+  sums(g.emb + (size_t)K * E + (size_t)E * P, W, E, gpb);
   return hipGetLastError();
 }
 

@@ -20,7 +20,7 @@ import numpy as np
 
 __all__ = [
     "Workload", "WORKLOADS", "workload", "make_weights", "make_inputs",
-    "scaled", "WEIGHT_ORDER", "make_forest",
+    "scaled", "WEIGHT_ORDER", "make_forest", "make_loss_targets",
 ]
 
 
@@ -243,3 +243,19 @@ def make_forest(w: Workload, seed: int, n_trees: Optional[int] = None, depth: Op
     leaf = 0.1 * rng.standard_normal((NT, n_int + 1))
     return {"feat": feat, "thr": thr.astype(np.float32), "leaf": leaf.astype(np.float32),
             "base": np.float32(0.5)}
+
+
+def make_loss_targets(w: Workload, seed: int, n_neg: int, lens=None):
+    """Rollout-loss inputs of the batch's shape: targets [B][T_max][d] and
+    negatives [B][T_max][n_neg][d], N(0,1) float32 (a stand-in for encoded
+    observed next states and sampled negative states); entries at
+    t >= lens[i] are NaN when lens is given (a correct loss never reads them).
+    """
+    rng = np.random.default_rng(seed)
+    tgt = rng.standard_normal((w.B, w.T_max, w.d), dtype=np.float32)
+    neg = rng.standard_normal((w.B, w.T_max, n_neg, w.d), dtype=np.float32)
+    if lens is not None:
+        pad = np.arange(w.T_max)[None, :] >= np.asarray(lens)[:, None]
+        tgt[pad] = np.nan
+        neg[pad] = np.nan
+    return tgt, neg
