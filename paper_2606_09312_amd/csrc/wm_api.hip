@@ -198,7 +198,7 @@ WsLayout ws_layout(const DevModel& m, int B, int T_max, int S, int n_hw) {
 // per-candidate step losses, partial gradient sums.
 struct LossLayout {
   size_t err, perm, hist, off, row_src, X, A, G, P, SD, DE, lrow, pw1, pw2, pb1, pb2, pemb, total;
-  int splits;
+  int splits, emb_blocks;
 };
 
 LossLayout loss_layout(const DevModel& m, int B, int T_max) {
@@ -209,6 +209,7 @@ LossLayout loss_layout(const DevModel& m, int B, int T_max) {
   const size_t R = (size_t)rows;
   LossLayout L;
   L.splits = train_splits(rows);
+  L.emb_blocks = emb_blocks(rows);
   const size_t S = (size_t)L.splits;
   size_t o = 0;
   L.err = o; o += 256;
@@ -227,7 +228,7 @@ LossLayout loss_layout(const DevModel& m, int B, int T_max) {
   L.pw2 = o; o = align256(o + S * D * H * 4);
   L.pb1 = o; o = align256(o + S * H * 4);
   L.pb2 = o; o = align256(o + S * D * 4);
-  L.pemb = o; o = align256(o + S * (K * E + E * P + E) * 4);
+  L.pemb = o; o = align256(o + (size_t)L.emb_blocks * (K * E + E * P + E) * 4);
   L.total = o;
   return L;
 }
@@ -747,7 +748,7 @@ wm_status wm_rollout_loss(const wm_model* model, const float* z0, const int32_t*
   if (B > 0) WM_TIMED(TK_TRAIN_BWD, st, launch_train_bwd(m, io, st));
   GradParts gp;
   gp.w1 = fptr(L.pw1); gp.w2 = fptr(L.pw2); gp.b1 = fptr(L.pb1); gp.b2 = fptr(L.pb2);
-  gp.emb = fptr(L.pemb); gp.splits = L.splits;
+  gp.emb = fptr(L.pemb); gp.splits = L.splits; gp.emb_blocks = L.emb_blocks;
   WM_TIMED(TK_GRADS, st, launch_weight_grads(m, io, gp, grads->w1, grads->b1, grads->w2, grads->b2,
                                              grads->type_emb, grads->param_w, grads->param_b, st));
   return ok();

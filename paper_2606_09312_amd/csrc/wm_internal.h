@@ -257,11 +257,16 @@ struct TrainIO {
 // in order afterwards.
 struct GradParts {
   float *w1, *w2, *b1, *b2, *emb;
-  int splits;
+  int splits, emb_blocks;
 };
 inline int train_splits(long long rows_bound) {
   const long long s = (rows_bound + 2047) / 2048;
   return (int)(s < 1 ? 1 : (s > 32 ? 32 : s));
+}
+// Row blocks of the embedding-gradient kernel (about 256 rows each).
+inline int emb_blocks(long long rows_bound) {
+  const long long s = (rows_bound + 255) / 256;
+  return (int)(s < 1 ? 1 : (s > 512 ? 512 : s));
 }
 bool have_train_kernels(int prec, int d, int e);
 hipError_t launch_row_offsets(const int32_t* lens, int B, int T_max, int32_t* off, hipStream_t st);

@@ -2354,23 +2354,30 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   }
 }
 
-// out[q] = sum over k of part[k * stride + q], k in order.
+// out[q] = sum over k of part[k * stride + q] in a fixed order: eight
+// running sums (k mod 8, so the loads are independent), then a fixed tree.
 __global__ __launch_bounds__(256) void sum_splits_kernel(const float* __restrict__ part, int splits,
                                                          long long stride, long long n,
                                                          float* __restrict__ out) {
   const long long q = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (q >= n) return;
-  float s = 0.0f;
-  for (int k = 0; k < splits; ++k) s += part[(size_t)k * stride + q];
-  out[q] = s;
+  float s[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+  int k = 0;
+  for (; k + 8 <= splits; k += 8) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s[j] += part[(size_t)(k + j) * stride + q];
+  }
+  for (int j = 0; k + j < splits; ++j) s[j] += part[(size_t)(k + j) * stride + q];
+  out[q] = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
 }
 
-// Embedding gradients over one split of the compact rows:
-// part[split] = [ d type_emb (K x E) | d param_w (E x P) | d param_b (E) ].
-// Thread (row group g, feature f) walks rows g, g + RG, ... of the split
-// with per-kind bins in LDS (each thread owns its feature's column), then
-// the row groups are added in order.
-constexpr int EMB_THREADS = 256;
+// Embedding gradients over one block of the compact rows:
+// part[block] = [ d type_emb (K x E) | d param_w (E x P) | d param_b (E) ].
+// Rows are taken 64 at a time: their action kinds and log2 parameters are
+// staged in LDS (one thread per row), then thread (row group g, feature f)
+// walks rows g, g + RG, ... of the batch with per-kind bins in LDS (each
+// thread owns its feature's column); the row groups are added in order.
+constexpr int EMB_THREADS = 256, EMB_ROWS = 64;
 __global__ __launch_bounds__(EMB_THREADS) void emb_grad_kernel(const float* __restrict__ DE, int E,
                                                                const int32_t* __restrict__ row_src,
                                                                const int32_t* __restrict__ types,
@@ -2379,6 +2386,8 @@ __global__ __launch_bounds__(EMB_THREADS) void emb_grad_kernel(const float* __re
                                                                const int32_t* __restrict__ off, int B,
                                                                int splits, float* __restrict__ part) {
   extern __shared__ float bins[];                          // [RG][K + P + 1][E]
+  __shared__ int s_ty[EMB_ROWS];
+  __shared__ float s_u[EMB_ROWS][PMAX];
   const int RG = EMB_THREADS / E;
   const int f = threadIdx.x % E, g = threadIdx.x / E;
   const int W = K * E + E * P + E;
@@ -2386,13 +2395,22 @@ __global__ __launch_bounds__(EMB_THREADS) void emb_grad_kernel(const float* __re
   split_rows(off, B, splits, blockIdx.x, r0, r1);
   float* mine = bins + (size_t)g * (K + P + 1) * E;
   for (int k = 0; k < K + P + 1; ++k) mine[k * E + f] = 0.0f;
-  for (int r = r0 + g; r < r1; r += RG) {
-    const float v = DE[(size_t)r * E + f];
-    const int src = row_src[r];
-    const int ty = types[src];
-    if (ty >= 0 && ty < K) mine[ty * E + f] += v;
-    for (int p = 0; p < P; ++p) mine[(K + p) * E + f] = fmaf(v, log2f((float)params[(size_t)src * P + p]), mine[(K + p) * E + f]);
-    mine[(K + P) * E + f] += v;
+  for (int rb = r0; rb < r1; rb += EMB_ROWS) {
+    const int nr = min(EMB_ROWS, r1 - rb);
+    __syncthreads();
+    if ((int)threadIdx.x < nr) {
+      const int src = row_src[rb + threadIdx.x];
+      s_ty[threadIdx.x] = types[src];
+      for (int p = 0; p < P; ++p) s_u[threadIdx.x][p] = log2f((float)params[(size_t)src * P + p]);
+    }
+    __syncthreads();
+    for (int q = g; q < nr; q += RG) {
+      const float v = DE[(size_t)(rb + q) * E + f];
+      const int ty = s_ty[q];
+      if (ty >= 0 && ty < K) mine[ty * E + f] += v;
+      for (int p = 0; p < P; ++p) mine[(K + p) * E + f] = fmaf(v, s_u[q][p], mine[(K + p) * E + f]);
+      mine[(K + P) * E + f] += v;
+    }
   }
   __syncthreads();
   if (g != 0) return;
@@ -3206,15 +3224,19 @@ hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradP
     (void)hipGetLastError();
     return e;
   }
-  hipLaunchKernelGGL(emb_grad_kernel, dim3(S), dim3(EMB_THREADS), lds, st, io.DE, E, io.row_src,
-                     io.types, io.params, K, P, io.off, io.B, S, g.emb);
+  hipLaunchKernelGGL(emb_grad_kernel, dim3(g.emb_blocks), dim3(EMB_THREADS), lds, st, io.DE, E,
+                     io.row_src, io.types, io.params, K, P, io.off, io.B, g.emb_blocks, g.emb);
   sums(g.w1, (long long)H * IN, (long long)H * IN, gw1);
   sums(g.w2, (long long)D * H, (long long)D * H, gw2);
   sums(g.b1, H, H, gb1);
   sums(g.b2, D, D, gb2);
-  sums(g.emb, W, (long long)K * E, gtemb);
-  sums(g.emb + (size_t)K * E, W, (long long)E * P, gpw);
-  sums(g.emb + (size_t)K * E + (size_t)E * P, W, E, gpb);
+  auto sums_emb = [&](const float* part, long long n, float* out) {
+    hipLaunchKernelGGL(sum_splits_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part,
+                       g.emb_blocks, (long long)W, n, out);
+  };
+  sums_emb(g.emb, (long long)K * E, gtemb);
+  sums_emb(g.emb + (size_t)K * E, (long long)E * P, gpw);
+  sums_emb(g.emb + (size_t)K * E + (size_t)E * P, E, gpb);
   return hipGetLastError();
 }
 
