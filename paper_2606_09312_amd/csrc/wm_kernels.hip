@@ -112,6 +112,32 @@ __device__ __forceinline__ float gelu(float x) {
   return 0.5f * fmaf(ax, erf_a, x);
 }
 
+template <class PR>
+__device__ __forceinline__ float op_value(float v) {   // the value a product operand takes
+  if constexpr (PR::G == 1) return (float)(__bf16)v;
+  else return v;
+}
+
+// 16 accumulator values of one 32-row block <-> a row in natural order
+// (rows acc_row(h, 4q .. 4q+3) are consecutive: four 16-byte accesses).
+__device__ __forceinline__ void store_acc(float* row, const f32x16& v, int h) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const f32x4 x = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+    *reinterpret_cast<f32x4*>(row + acc_row(h, 4 * q)) = x;
+  }
+}
+__device__ __forceinline__ f32x16 load_acc(const float* row, int h) {
+  f32x16 v;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const f32x4 x = *reinterpret_cast<const f32x4*>(row + acc_row(h, 4 * q));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[4 * q + i] = x[i];
+  }
+  return v;
+}
+
 __device__ __forceinline__ u32x4 lds_group(const uint8_t* base, int group, int lane) {
   return *reinterpret_cast<const u32x4*>(base + group * 1024 + lane * 16);
 }
@@ -328,6 +354,11 @@ struct RollArgs {
   float* zT;                // [B][D]
   int32_t* err;
   int B, T_max, P, K, H, tab_bytes;
+  // training forward of the rollout loss (row-owned kernel only): the
+  // activations of every valid step in compact rows off[i] + t
+  float *X, *A, *G, *Pz;    // [R][D+E], [R][H], [R][H], [R][D]
+  const int32_t* off;
+  int32_t* row_src;
 };
 
 // Copies of the next weight chunk (its W1 and/or W2 part) into LDS, issued
@@ -1195,8 +1226,9 @@ struct RowsGeom {
   static constexpr int XE_BYTES = NEG * 1024;
 };
 
-template <class PR, int D, int E, int NC, int W, bool NORM>
+template <class PR, int D, int E, int NC, int W, bool NORM, bool TRAIN = false>
 __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs a) {
+  static_assert(!(TRAIN && NORM), "the training forward is the residual form");
   using R = Roll<PR, D, E>;
   using RG = RowsGeom<PR, D, E, NC, W>;
   using Frag = typename PR::Frag;
@@ -1232,6 +1264,8 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
   const int len = valid ? clampi(a.lens[cand], 0, a.T_max) : 0;
   const int T_wg = __builtin_amdgcn_readfirstlane(
       clampi(a.lens[a.perm[blockIdx.x * 32].x], 0, a.T_max));
+  constexpr int IN = D + E;
+  const size_t row0 = (TRAIN && valid) ? (size_t)a.off[cand] : 0;
 
   // owned latent blocks (fp32) and the full X operand
   const float* zs = a.z0 + (size_t)pc.y * D;
@@ -1288,9 +1322,9 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     }
   };
   // embedding fragment q (features KF*q + SL*h + j)
-  auto embed_frag = [&](int ty, const float (&u)[PMAX], float af, int q) -> Frag {
+  auto embed_vals = [&](int ty, const float (&u)[PMAX], float af, int q, float (&ev)[SL]) {
     const int f0 = KF * q + SL * h;
-    float ev[SL], tmp[SL];
+    float tmp[SL];
     R::row(t_emb + ty * temb_stride(E) + f0, ev);
 #pragma unroll
     for (int p = 0; p < PMAX; ++p) {
@@ -1301,6 +1335,10 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     R::row(t_pb + f0, tmp);
 #pragma unroll
     for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * af;
+  };
+  auto embed_frag = [&](int ty, const float (&u)[PMAX], float af, int q) -> Frag {
+    float ev[SL];
+    embed_vals(ty, u, af, q, ev);
     return PR::cvt(ev);
   };
   // all fragments in this wavefront (paper form: the normal map needs them
@@ -1323,7 +1361,16 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 #pragma unroll
       for (int k = 0; k < G; ++k) {
         const int q = gq * G + k;
-        *reinterpret_cast<Frag*>(xebuf + frag_offset<PR>(q, lane, 0)) = embed_frag(ty, u, af, q);
+        float ev[SL];
+        embed_vals(ty, u, af, q, ev);
+        *reinterpret_cast<Frag*>(xebuf + frag_offset<PR>(q, lane, 0)) = PR::cvt(ev);
+        if constexpr (TRAIN) {
+          if (s < len) {
+            float* xo = a.X + (row0 + s) * IN + D + KF * q + SL * h;
+#pragma unroll
+            for (int j = 0; j < SL; ++j) xo[j] = op_value<PR>(ev[j]);
+          }
+        }
       }
     }
   };
@@ -1434,6 +1481,19 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     gu8* pA = baseA;
     gu8* pB = baseB;
     asm volatile("" : "+v"(pA), "+v"(pB));
+    const size_t row = row0 + t;
+    if constexpr (TRAIN) {
+      if (active) {            // X = [z; e]: the owned latent blocks (e: embed_share)
+#pragma unroll
+        for (int bq = 0; bq < NBW; ++bq) {
+          f32x16 v;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) v[r] = op_value<PR>(zq[bq][r]);
+          store_acc(a.X + row * IN + 32 * (w * NBW + bq), v, h);
+        }
+        if (w == 0 && h == 0) a.row_src[row] = cand * a.T_max + t;
+      }
+    }
 
     f32x16 acc = {};
     f32x4 b1v[4];
@@ -1468,8 +1528,20 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
           for (int r4 = 0; r4 < 4; ++r4)
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc[4 * r4 + j] += b1v[r4][j];
+          if constexpr (TRAIN) {
+            f32x16 gv;
 #pragma unroll
-          for (int q = 0; q < 8; ++q) gp[q] = PR::pack2(gelu(acc[2 * q]), gelu(acc[2 * q + 1]), amask);
+            for (int r = 0; r < 16; ++r) gv[r] = op_value<PR>(gelu(acc[r]));
+#pragma unroll
+            for (int q = 0; q < 8; ++q) gp[q] = PR::pack2(gv[2 * q], gv[2 * q + 1], amask);
+            if (active) {
+              store_acc(a.A + row * a.H + 32 * c, acc, h);
+              store_acc(a.G + row * a.H + 32 * c, gv, h);
+            }
+          } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) gp[q] = PR::pack2(gelu(acc[2 * q]), gelu(acc[2 * q + 1]), amask);
+          }
 #pragma unroll
           for (int f = 0; f < NF2; ++f)
             *reinterpret_cast<Frag*>(gbuf + frag_offset<PR>(c * NF2 + f, lane, 0)) = PR::gfrag(gp, f);
@@ -1512,6 +1584,9 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
       const int b = w * NBW + bq;
 #pragma unroll
       for (int r = 0; r < 16; ++r) zq[bq][r] += dz[bq][r] + t_b2[(b * 2 + h) * 16 + r] * actf;
+      if constexpr (TRAIN) {
+        if (active) store_acc(a.Pz + row * D + 32 * b, zq[bq], h);
+      }
     }
     if constexpr (NORM) {
       embed_step(t + 1, xe);
@@ -1522,7 +1597,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     exchange_x();
   }
   if (errbits) atomicOr(a.err, errbits);
-  if (valid) {
+  if (valid && !TRAIN) {
     float* zo = a.zT + (size_t)cand * D;
 #pragma unroll
     for (int bq = 0; bq < NBW; ++bq)
@@ -1765,12 +1840,6 @@ struct TrainArgs {
   int B, T_max, P_, K, H, tab_bytes;
 };
 
-template <class PR>
-__device__ __forceinline__ float op_value(float v) {   // the value a product operand takes
-  if constexpr (PR::G == 1) return (float)(__bf16)v;
-  else return v;
-}
-
 // d/dx [x Phi(x)] = Phi(x) + x phi(x), with erf from the same Abramowitz &
 // Stegun 7.1.26 form as gelu() and phi(x) = exp(-x^2/2) / sqrt(2 pi).
 __device__ __forceinline__ float gelu_grad(float x) {
@@ -1783,26 +1852,6 @@ __device__ __forceinline__ float gelu_grad(float x) {
   const float ex = __builtin_amdgcn_exp2f((x * x) * (-0.5f * 1.4426950408889634f));
   const float erf_a = fmaf(-(p * t), ex, 1.0f);
   return fmaf(0.5f, copysignf(erf_a, x), 0.5f) + x * ex * 0.3989422804014327f;
-}
-
-// 16 accumulator values of one 32-row block <-> a row in natural order
-// (rows acc_row(h, 4q .. 4q+3) are consecutive: four 16-byte accesses).
-__device__ __forceinline__ void store_acc(float* row, const f32x16& v, int h) {
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const f32x4 x = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-    *reinterpret_cast<f32x4*>(row + acc_row(h, 4 * q)) = x;
-  }
-}
-__device__ __forceinline__ f32x16 load_acc(const float* row, int h) {
-  f32x16 v;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const f32x4 x = *reinterpret_cast<const f32x4*>(row + acc_row(h, 4 * q));
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[4 * q + i] = x[i];
-  }
-  return v;
 }
 
 template <class PR, int D, int E>
@@ -2986,7 +3035,7 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
 hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
                           int32_t B, int32_t T_max, float* zT, int32_t* err, hipStream_t st) {
-  RollArgs a;
+  RollArgs a{};
   a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.wh = m.trans_wh; a.tab = m.roll_tab; a.z0 = z0; a.perm = perm; a.types = types;
   a.params = params; a.lens = lens; a.zT = zT; a.err = err; a.B = B; a.T_max = T_max;
   a.P = m.dims.n_params; a.K = m.dims.n_kinds; a.H = m.dims.trans_hidden;
@@ -3147,10 +3196,37 @@ bool have_train_kernels(int prec, int d, int e) {
   return false;
 }
 
+// Training forward in the row-owned form (one workgroup per tile; d = 256).
+template <class PR, int NC, int W>
+hipError_t launch_train_fwd_rows(const DevModel& m, const TrainIO& io, int tiles, hipStream_t st) {
+  RollArgs a{};
+  a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.wh = nullptr; a.tab = m.roll_tab; a.z0 = io.z0;
+  a.perm = io.perm; a.types = io.types; a.params = io.params; a.lens = io.lens; a.zT = nullptr;
+  a.err = io.err; a.B = io.B; a.T_max = io.T_max; a.P = m.dims.n_params; a.K = m.dims.n_kinds;
+  a.H = m.dims.trans_hidden; a.tab_bytes = m.roll_tab_bytes;
+  a.X = io.X; a.A = io.A; a.G = io.G; a.Pz = io.P; a.off = io.off; a.row_src = io.row_src;
+  using RG = RowsGeom<PR, 256, 64, NC, W>;
+  const int lds = m.roll_tab_bytes + RG::GELU_BYTES + RG::X_BYTES + RG::XE_BYTES;
+  auto kern = rollout_rows_kernel<PR, 256, 64, NC, W, false, true>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
+  }
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * W), lds, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st) {
   if (io.B == 0) return hipSuccess;
   const TrainArgs a = train_args(m, io);
   const int tiles = (io.B + 31) / 32;
+  if (m.dims.d == 256 && m.dims.embed_dim == 64) {
+    const int NC = m.dims.trans_hidden / 32;
+    if (m.prec == WM_BF16 && NC == 16) return launch_train_fwd_rows<PBF16, 16, 8>(m, io, tiles, st);
+    if (m.prec == WM_BF16 && NC == 32) return launch_train_fwd_rows<PBF16, 32, 8>(m, io, tiles, st);
+    if (m.prec == WM_FP32 && NC == 16) return launch_train_fwd_rows<PF32, 16, 4>(m, io, tiles, st);
+  }
   const int waves = pick_waves(tiles);
   const int blocks = (tiles + waves - 1) / waves;
   const int prec = m.prec, d = m.dims.d, e = m.dims.embed_dim;
