@@ -2258,6 +2258,208 @@ __device__ __forceinline__ void split_rows(const int32_t* off, int B, int splits
   r1 = min(Rv, r0 + rps);
 }
 
+// Row-owned backward (d = 256, one workgroup of W wavefronts per tile), the
+// mirror of the row-owned forward.  Per step, from the last to the first:
+//  * wavefront w owns latent blocks [w*NBW, (w+1)*NBW) of delta: it adds the
+//    step's seed, stores delta_{t+1}, and publishes the blocks as operand
+//    fragments in LDS; after a barrier every wavefront reads all of delta;
+//  * phase 1, for its chunks c = w, w+W, ...: dG^T = W2^T[c] . delta^T,
+//    dA = dG * GELU'(A) (stored), dA as fragments into LDS, and the
+//    embedding outputs dE^T += W1^T[c][e blocks] . dA^T (a partial over its
+//    chunks, summed across wavefronts through LDS in a fixed order);
+//  * phase 2, for its own latent blocks over every chunk:
+//    delta += W1^T[c][block] . dA^T[c] (dA fragments from LDS).
+// Weight groups stream from L2 through a register ring that wraps from step
+// to step.
+template <class PR, int D, int E, int NC, int W>
+struct BwdRowsGeom {
+  using R = Roll<PR, D, E>;
+  static constexpr int G = PR::G, NF2 = R::NF2, NB = R::NB, NBE = E / 32;
+  static constexpr int NBW = NB / W, NCW = NC / W;
+  static constexpr int GF = NF2 / G;                      // W1^T groups per (chunk, output block)
+  static constexpr int N2T = TransT<PR>::nk2t(D) / G;     // W2^T groups per chunk
+  static constexpr int NP1 = N2T + NBE * GF;              // phase-1 groups per chunk
+  static constexpr int NA = NCW * NP1;                    // phase-1 items
+  static constexpr int NI = NA + NC * NBW * GF;           // items per step
+  static constexpr int ring_depth() {
+    const int cap = G == 1 ? 8 : 12;
+    for (int r = cap; r > 1; --r)
+      if (NI % r == 0) return r;
+    return 1;
+  }
+  static constexpr int RD = ring_depth();
+  static_assert(NB % W == 0 && NC % W == 0 && NF2 % G == 0, "even split");
+  // LDS: [table-free] [dA fragments: NC * GF KiB][delta fragments: NZ / G KiB]
+  //      [dE partials: W * NBE * 4 KiB]
+  static constexpr int DA_BYTES = NC * GF * 1024;
+  static constexpr int DL_BYTES = (R::NZ / G) * 1024;
+  static constexpr int DE_BYTES = W * NBE * 4096;
+  static constexpr int LDS = DA_BYTES + DL_BYTES + DE_BYTES;
+};
+
+template <class PR, int D, int E, int NC, int W>
+__global__ __launch_bounds__(64 * W, 1) void train_bwd_rows_kernel(const TrainArgs a) {
+  using R = Roll<PR, D, E>;
+  using BG = BwdRowsGeom<PR, D, E, NC, W>;
+  using Frag = typename PR::Frag;
+  constexpr int SL = PR::SL, G = PR::G;
+  constexpr int NZ = R::NZ, NF2 = R::NF2, NB = R::NB, NBE = BG::NBE;
+  constexpr int NBW = BG::NBW, NCW = BG::NCW, GF = BG::GF, N2T = BG::N2T, NP1 = BG::NP1;
+  constexpr int NA = BG::NA, NI = BG::NI, RD = BG::RD;
+  constexpr int W2TB = TransT<PR>::w2t_bytes(D), W1TB = TransT<PR>::w1t_bytes(D, E);
+
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  uint8_t* dabuf = lds;                                   // dA fragments, chunk-major
+  uint8_t* dlbuf = lds + BG::DA_BYTES;                    // delta fragments
+  float* debuf = reinterpret_cast<float*>(lds + BG::DA_BYTES + BG::DL_BYTES);  // [W][NBE][2][16][32]
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int n = lane & 31, h = lane >> 5;
+  const TileInfo ti = tile_info(a, blockIdx.x, n);
+  const int cand = ti.cand, len = ti.len, T_wg = ti.T_wg;
+  const size_t row0 = ti.valid ? (size_t)a.off[cand] : 0;
+
+  // item i -> weight group (compile-time offsets after unrolling)
+  auto item_ptr = [&](gu8* p2, gu8* p1, int i) -> gu32x4* {
+    if (i < NA) {
+      const int cw = i / NP1, k = i % NP1, c = w + cw * W;
+      if (k < N2T) return reinterpret_cast<gu32x4*>(p2 + (size_t)c * W2TB + (size_t)k * 1024);
+      const int q = (k - N2T) / GF, fg = (k - N2T) % GF;
+      return reinterpret_cast<gu32x4*>(p1 + (size_t)c * W1TB + (size_t)((NB + q) * GF + fg) * 1024);
+    }
+    const int j = i - NA, c = j / (NBW * GF), bq = (j / GF) % NBW, fg = j % GF;
+    return reinterpret_cast<gu32x4*>(p1 + (size_t)c * W1TB + (size_t)((w * NBW + bq) * GF + fg) * 1024);
+  };
+  gu8* base2 = ((gu8*)(a.w2t)) + lane * 16;
+  gu8* base1 = ((gu8*)(a.w1t)) + lane * 16;
+  u32x4 ring[RD];
+#pragma unroll
+  for (int i = 0; i < RD; ++i) ring[i] = *item_ptr(base2, base1, i);
+
+  f32x16 dq[NBW];
+#pragma unroll
+  for (int bq = 0; bq < NBW; ++bq) dq[bq] = f32x16{};
+
+  for (int t = T_wg - 1; t >= 0; --t) {
+    const bool active = t < len;
+    const float actf = active ? 1.0f : 0.0f;
+    const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
+    const size_t row = row0 + t;
+    gu8* p2 = base2;
+    gu8* p1 = base1;
+    asm volatile("" : "+v"(p2), "+v"(p1));
+    // ---- owned delta blocks: seed, delta_{t+1}, operand fragments in LDS
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq) {
+      const int b = w * NBW + bq;
+      if (active) {
+        float* sd = a.SD + row * D + 32 * b;
+        dq[bq] += load_acc(sd, h);
+        store_acc(sd, dq[bq], h);
+      }
+#pragma unroll
+      for (int f = 0; f < NF2; ++f) {
+        float v[SL];
+#pragma unroll
+        for (int j = 0; j < SL; ++j) v[j] = dq[bq][f * SL + j];
+        *reinterpret_cast<Frag*>(dlbuf + frag_offset<PR>(b * NF2 + f, lane, 0)) = PR::cvt(v);
+      }
+    }
+    // pre-activations of the own chunks (read early, used after W2^T)
+    f32x16 av[NCW];
+#pragma unroll
+    for (int cw = 0; cw < NCW; ++cw)
+      av[cw] = active ? load_acc(a.A + row * a.H + 32 * (w + cw * W), h) : f32x16{};
+    __syncthreads();
+    Frag dop[NZ];
+#pragma unroll
+    for (int kf = 0; kf < NZ; ++kf) dop[kf] = *reinterpret_cast<const Frag*>(dlbuf + frag_offset<PR>(kf, lane, 0));
+
+    f32x16 acc = {};
+    f32x16 deacc[NBE];
+#pragma unroll
+    for (int q = 0; q < NBE; ++q) deacc[q] = f32x16{};
+    typename PR::Packed dp[8];
+    constexpr int GB = NF2 / G;
+    u32x4 dcur[GB], dnext[GB];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const u32x4 grp = ring[i % RD];
+      ring[i % RD] = *item_ptr(p2, p1, (i + RD) % NI);   // wraps into the next step
+      if (i < NA) {
+        const int cw = i / NP1, k = i % NP1, c = w + cw * W;
+        if (k < N2T) {
+          if (k == 0) acc = f32x16{};
+#pragma unroll
+          for (int ww = 0; ww < G; ++ww) acc = PR::mfma(PR::pick(grp, ww), dop[k * G + ww], acc);
+          if (k == N2T - 1) {
+            f32x16 da;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) da[r] = acc[r] * gelu_grad(av[cw][r]) * actf;
+            if (active) store_acc(a.A + row * a.H + 32 * c, da, h);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) dp[q] = PR::pack2(da[2 * q], da[2 * q + 1], amask);
+#pragma unroll
+            for (int f = 0; f < NF2; ++f)
+              *reinterpret_cast<Frag*>(dabuf + frag_offset<PR>(c * NF2 + f, lane, 0)) = PR::gfrag(dp, f);
+          }
+        } else {
+          const int q = (k - N2T) / GF, fg = (k - N2T) % GF;
+#pragma unroll
+          for (int ww = 0; ww < G; ++ww)
+            deacc[q] = PR::mfma(PR::pick(grp, ww), PR::gfrag(dp, fg * G + ww), deacc[q]);
+        }
+        if (i == NA - 1) {
+          // embedding partials into LDS, then every chunk's dA is published
+#pragma unroll
+          for (int q = 0; q < NBE; ++q)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) debuf[(((w * NBE + q) * 2 + h) * 16 + r) * 32 + n] = deacc[q][r];
+          __syncthreads();
+          if (w < NBE) {            // dE block w: the partials in wavefront order
+            f32x16 e = {};
+#pragma unroll
+            for (int ww = 0; ww < W; ++ww)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) e[r] += debuf[(((ww * NBE + w) * 2 + h) * 16 + r) * 32 + n];
+            if (active) store_acc(a.DE + row * E + 32 * w, e, h);
+          }
+#pragma unroll
+          for (int gg = 0; gg < GB; ++gg) dcur[gg] = lds_group(dabuf, gg, lane);
+#pragma unroll
+          for (int gg = 0; gg < GB; ++gg) dnext[gg] = lds_group(dabuf, (NC > 1 ? GB : 0) + gg, lane);
+        }
+      } else {
+        const int j = i - NA, c = j / (NBW * GF), bq = (j / GF) % NBW, fg = j % GF;
+#pragma unroll
+        for (int ww = 0; ww < G; ++ww) {
+          const int f = fg * G + ww;
+          const u32x4 gf = dcur[(f * SL * PR::ES) / 16];
+          Frag b;
+          if constexpr (G == 1) b = PR::pick(gf, 0);
+          else b = PR::pick(gf, f % G);
+          dq[bq] = PR::mfma(PR::pick(grp, ww), b, dq[bq]);
+        }
+        if (bq == NBW - 1 && fg == GF - 1) {
+#pragma unroll
+          for (int gg = 0; gg < GB; ++gg) dcur[gg] = dnext[gg];
+          if (c + 2 < NC) {
+#pragma unroll
+            for (int gg = 0; gg < GB; ++gg) dnext[gg] = lds_group(dabuf, (c + 2) * GB + gg, lane);
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();                // dA / dE buffers are read before the next step writes them
+  }
+  if (ti.valid && a.dz0) {
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq) store_acc(a.dz0 + (size_t)cand * D + 32 * (w * NBW + bq), dq[bq], h);
+  }
+}
+
 // Weight gradients as split-K products over the compact rows, two problems
 // per launch (dW2 = sum R(delta) (x) g, dW1 = sum R(dA) (x) x):
 //   part[split][m][n] = sum over the split's rows r of op(A[r][m]) * op(B[r][n])
@@ -3177,6 +3379,19 @@ hipError_t launch_train_fwd_t(const DevModel& m, const TrainArgs& a, int blocks,
   return hipGetLastError();
 }
 
+template <class PR, int NC, int W>
+hipError_t launch_train_bwd_rows(const TrainArgs& a, int tiles, hipStream_t st) {
+  using BG = BwdRowsGeom<PR, 256, 64, NC, W>;
+  auto kern = train_bwd_rows_kernel<PR, 256, 64, NC, W>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, BG::LDS);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
+  }
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * W), BG::LDS, st, a);
+  return hipGetLastError();
+}
+
 template <class PR, int D, int E>
 hipError_t launch_train_bwd_t(const TrainArgs& a, int tiles, hipStream_t st) {
   const int waves = pick_waves(tiles);
@@ -3243,6 +3458,12 @@ hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st
   if (io.B == 0) return hipSuccess;
   const TrainArgs a = train_args(m, io);
   const int tiles = (io.B + 31) / 32;
+  if (m.dims.d == 256 && m.dims.embed_dim == 64) {
+    const int NC = m.dims.trans_hidden / 32;
+    if (m.prec == WM_BF16 && NC == 16) return launch_train_bwd_rows<PBF16, 16, 8>(a, tiles, st);
+    if (m.prec == WM_BF16 && NC == 32) return launch_train_bwd_rows<PBF16, 32, 8>(a, tiles, st);
+    if (m.prec == WM_FP32 && NC == 16) return launch_train_bwd_rows<PF32, 16, 4>(a, tiles, st);
+  }
   const int prec = m.prec, d = m.dims.d, e = m.dims.embed_dim;
 #define WM_TBWD(PR, D, E) return launch_train_bwd_t<PR, D, E>(a, tiles, st);
   WM_FOR_TRAIN_DE(WM_TBWD)
