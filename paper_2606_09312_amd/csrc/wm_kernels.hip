@@ -2054,10 +2054,13 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_fwd_kernel(const TrainArg
 }
 
 // Per-step loss and its gradient with respect to the prediction: one
-// wavefront per (candidate, step) slot, lanes over the latent.  The hardest
-// negative is the nearest (first one on ties); a zero distance contributes a
-// zero gradient.  targets / negatives are indexed by slot, P / SD / lrow by
+// wavefront per (candidate, step) slot; lane L holds features 4L..4L+3 (and
+// +256, ...), so the prediction, the target and up to LOSS_NEG negatives
+// are read in one pass of independent 16-byte loads.  The hardest negative
+// is the nearest (first one on ties); a zero distance contributes a zero
+// gradient.  targets / negatives are indexed by slot, P / SD / lrow by
 // compact row.
+constexpr int LOSS_NEG = 8;          // negatives per pass
 __global__ __launch_bounds__(256) void loss_kernel(const float* __restrict__ P,
                                                    const float* __restrict__ targets,
                                                    const float* __restrict__ negatives, int NN,
@@ -2071,32 +2074,57 @@ __global__ __launch_bounds__(256) void loss_kernel(const float* __restrict__ P,
   const int i = (int)(slot / T_max), t = (int)(slot - (long long)i * T_max);
   if (t >= clampi(lens[i], 0, T_max)) return;
   const size_t row = (size_t)off[i] + t;
-  const float* p = P + row * D;
-  const float* y = targets + slot * D;
+  const f32x4* p4 = reinterpret_cast<const f32x4*>(P + row * D);
+  const f32x4* y4 = reinterpret_cast<const f32x4*>(targets + slot * D);
+  const int D4 = D / 4;
   float m = 0.0f;
-  for (int f = lane; f < D; f += 64) { const float v = p[f] - y[f]; m = fmaf(v, v, m); }
+  for (int c = lane; c < D4; c += 64) {
+    const f32x4 v = p4[c] - y4[c];
+    m += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+  }
   const float match = wave_sum(m);
   const float dpos = sqrtf(match);
   float dmin = INFINITY;
   int hard = 0;
-  for (int q = 0; q < NN; ++q) {
-    const float* ng = negatives + (slot * NN + q) * D;
-    float s = 0.0f;
-    for (int f = lane; f < D; f += 64) { const float v = p[f] - ng[f]; s = fmaf(v, v, s); }
-    const float dq = sqrtf(wave_sum(s));
-    if (dq < dmin) { dmin = dq; hard = q; }
+  for (int q0 = 0; q0 < NN; q0 += LOSS_NEG) {
+    float sq[LOSS_NEG];
+#pragma unroll
+    for (int q = 0; q < LOSS_NEG; ++q) sq[q] = 0.0f;
+    for (int c = lane; c < D4; c += 64) {
+      const f32x4 pv = p4[c];
+#pragma unroll
+      for (int q = 0; q < LOSS_NEG; ++q) {
+        if (q0 + q < NN) {
+          const f32x4 v = pv - reinterpret_cast<const f32x4*>(negatives + (slot * NN + q0 + q) * D)[c];
+          sq[q] += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < LOSS_NEG; ++q) {
+      if (q0 + q < NN) {
+        const float dq = sqrtf(wave_sum(sq[q]));
+        if (dq < dmin) { dmin = dq; hard = q0 + q; }
+      }
+    }
   }
   const float hinge = dpos - dmin + gamma;
   const bool act = hinge > 0.0f;
   if (lane == 0) lrow[row] = lam * match + (1.0f - lam) * (act ? hinge : 0.0f);
   const float ip = dpos > 0.0f ? 1.0f / dpos : 0.0f;
   const float in = dmin > 0.0f ? 1.0f / dmin : 0.0f;
-  const float* ng = negatives + (slot * NN + hard) * D;
-  for (int f = lane; f < D; f += 64) {
-    const float diff = p[f] - y[f];
-    float g = lam * 2.0f * diff;
-    if (act) g += (1.0f - lam) * (diff * ip - (p[f] - ng[f]) * in);
-    SD[row * D + f] = g;
+  const f32x4* n4 = reinterpret_cast<const f32x4*>(negatives + (slot * NN + hard) * D);
+  f32x4* g4 = reinterpret_cast<f32x4*>(SD + row * D);
+  const float wr = act ? (1.0f - lam) : 0.0f;
+  for (int c = lane; c < D4; c += 64) {
+    const f32x4 pv = p4[c], diff = pv - y4[c], dn = pv - n4[c];
+    f32x4 g;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      g[k] = lam * 2.0f * diff[k];
+      if (act) g[k] += wr * (diff[k] * ip - dn[k] * in);
+    }
+    g4[c] = g;
   }
 }
 
