@@ -131,6 +131,20 @@ def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none", forest=None
                       f"+top-k, {total_t:.1f} s)"}
 
 
+def step_percentiles(torch, step, n: int) -> dict:
+    """Median, 10th and 90th percentile of n steps, each bracketed by HIP
+    events on the current stream (the stream the library launches on)."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for a, b in ev:
+        a.record()
+        step()
+        b.record()
+    torch.cuda.synchronize()
+    d = np.array([a.elapsed_time(b) for a, b in ev])
+    return {"median": float(np.median(d)), "p10": float(np.percentile(d, 10)),
+            "p90": float(np.percentile(d, 90)), "runs": n}
+
+
 def cpu_baseline_loss(w, W, I, tgt, neg, prec, lam, gamma, budget_s: float):
     """Oracle throughput of the rollout loss with gradients on a bounded
     random sample of the batch."""
@@ -196,6 +210,7 @@ def run_loss_bench(args, w, prec):
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     wm.device_status(ws)
+    step_ms = step_percentiles(torch, step, args.steps)
     wm.timing_enable(True)
     for _ in range(args.steps):
         step()
@@ -227,6 +242,7 @@ def run_loss_bench(args, w, prec):
                      "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
                      "flop_per_launch": flops},
         "kernels_avg_ms": {k: v["avg_ms"] for k, v in kern.items()},
+        "step_ms": step_ms,
         "whole_path_tflops": 3 * flops * args.steps / elapsed / 1e12,
     }
     if not args.no_cpu:
@@ -304,6 +320,9 @@ def main():
     elapsed = time.perf_counter() - t0
     wm.device_status(ws)
 
+    # per-step durations (HIP events around each call on the launch stream)
+    step_ms = step_percentiles(torch, step, args.steps)
+
     # per-kernel durations: HIP events recorded by the library around each
     # launch, on the stream the kernel runs on
     wm.timing_enable(True)
@@ -361,6 +380,7 @@ def main():
                      "flop_per_launch": flops_roll,
                      "algorithmic_bytes_per_launch": rollout_bytes(w, lens, args.norm)},
         "kernels_avg_ms": {k: v["avg_ms"] for k, v in kern.items()},
+        "step_ms": step_ms,
         "whole_path_tflops": total_flops * args.steps / elapsed / 1e12,
     }
     if not args.no_cpu:

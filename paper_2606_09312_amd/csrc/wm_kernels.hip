@@ -2521,16 +2521,23 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   __shared__ __attribute__((aligned(16))) Elem As[WG_T * LDW];
   __shared__ __attribute__((aligned(16))) Elem Bs[WG_T * LDW];
   __shared__ float csum[WG_T];
-  const bool second = (int)blockIdx.x >= a.p0.tiles;
+  // Workgroups are dealt to the 8 XCDs in turn: every tile of split s runs
+  // on XCD s mod 8, so the split's rows come from HBM once per XCD and the
+  // other tiles' re-reads hit that XCD's L2.
+  const int tiles_all = a.p0.tiles + a.p1.tiles;
+  const int xcd = blockIdx.x % 8, k8 = blockIdx.x / 8;
+  const int tile_id = k8 % tiles_all;
+  const int split = (k8 / tiles_all) * 8 + xcd;
+  if (split >= a.splits) return;
+  const bool second = tile_id >= a.p0.tiles;
   const float* A = second ? a.p1.A : a.p0.A;
   const float* Bm = second ? a.p1.Bm : a.p0.Bm;
   float* part = second ? a.p1.part : a.p0.part;
   float* colsum = second ? a.p1.colsum : a.p0.colsum;
   const int M = second ? a.p1.M : a.p0.M, N = second ? a.p1.N : a.p0.N;
   const int tiles_n = second ? a.p1.tiles_n : a.p0.tiles_n;
-  const int tile = (int)blockIdx.x - (second ? a.p0.tiles : 0);
+  const int tile = tile_id - (second ? a.p0.tiles : 0);
   const int m0 = (tile / tiles_n) * WG_T, n0 = (tile % tiles_n) * WG_T;
-  const int split = blockIdx.y;
   int r0, r1;
   split_rows(a.off, a.B, a.splits, split, r0, r1);
 
@@ -3539,7 +3546,7 @@ hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradP
   a.p0 = prob(io.SD, D, io.G, H, g.w2, g.b2);      // dW2 [D][H], db2
   a.p1 = prob(io.A, H, io.X, IN, g.w1, g.b1);      // dW1 [H][IN], db1
   a.off = io.off; a.B = io.B; a.splits = S;
-  const dim3 grid(a.p0.tiles + a.p1.tiles, S);
+  const dim3 grid((a.p0.tiles + a.p1.tiles) * ((S + 7) / 8) * 8);
   if (m.prec == WM_BF16) hipLaunchKernelGGL(wgrad_kernel<PBF16>, grid, dim3(256), 0, st, a);
   else hipLaunchKernelGGL(wgrad_kernel<PF32>, grid, dim3(256), 0, st, a);
   if (E > EMB_THREADS || EMB_THREADS % E) return hipErrorInvalidValue;
