@@ -145,7 +145,7 @@ def step_percentiles(torch, step, n: int) -> dict:
             "p90": float(np.percentile(d, 90)), "runs": n}
 
 
-def cpu_baseline_loss(w, W, I, tgt, neg, prec, lam, gamma, budget_s: float):
+def cpu_baseline_loss(w, W, I, tgt, neg, prec, lam, gamma, budget_s: float, norm: str = "none"):
     """Oracle throughput of the rollout loss with gradients on a bounded
     random sample of the batch."""
     from oracle import loss as LO
@@ -163,7 +163,7 @@ def cpu_baseline_loss(w, W, I, tgt, neg, prec, lam, gamma, budget_s: float):
         sub = {"types": I["types"][pick], "params": I["params"][pick], "lens": I["lens"][pick],
                "z0": I["z0"][seg_of[pick]], "seg_off": np.arange(n + 1)}
         t0 = time.perf_counter()
-        LO.loss_and_grad(W, sub, tgt[pick], neg[pick], lam, gamma, prec)
+        LO.loss_and_grad(W, sub, tgt[pick], neg[pick], lam, gamma, prec, norm=norm)
         total_t += time.perf_counter() - t0
         total_c += n
         if total_t >= budget_s:
@@ -186,7 +186,7 @@ def run_loss_bench(args, w, prec):
     I = synth.make_inputs(w, 2000)
     tgt, neg = synth.make_loss_targets(w, 2100, args.n_neg, I["lens"])
     lam, gamma = 0.5, 0.3
-    model = wm.Model(wm.model_dims(w), W, precision=prec)
+    model = wm.Model(wm.model_dims(w), W, precision=prec, norm=args.norm)
     t = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in I.items() if k != "seg_off"}
     targets = torch.from_numpy(tgt).to(dev)
     negatives = torch.from_numpy(neg).to(dev)
@@ -222,7 +222,7 @@ def run_loss_bench(args, w, prec):
             kern[name] = {"avg_ms": ms / n, "launches": n}
     wm.timing_enable(False)
     steps_valid = int(I["lens"].astype(np.int64).sum())
-    flops = steps_valid * step_flops(w)          # per phase: forward, backward, weight gradients
+    flops = steps_valid * step_flops(w, args.norm)   # per phase: forward, backward, weight gradients
     dom = max(("loss_fwd", "loss_bwd", "loss_grads"), key=lambda k: kern[k]["avg_ms"])
     achieved = flops / (kern[dom]["avg_ms"] / 1e3) / 1e12
     peak = PEAK_TFLOPS[prec]
@@ -237,6 +237,8 @@ def run_loss_bench(args, w, prec):
         "config": {"workload": f"{w.name}: B={w.B} candidates, d={w.d}, e={w.e}, H={w.H}, "
                                f"T_max={w.T_max}, {args.n_neg} negatives per step, "
                                f"lambda={lam}, gamma={gamma}", "precision": prec,
+                   "transition": "residual MLP" if args.norm == "none" else
+                                 "hyperplane projection + residual MLP + unit length",
                    "global_batch": w.B, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak,
                      "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
@@ -246,7 +248,8 @@ def run_loss_bench(args, w, prec):
         "whole_path_tflops": 3 * flops * args.steps / elapsed / 1e12,
     }
     if not args.no_cpu:
-        res["cpu_baseline"] = cpu_baseline_loss(w, W, I, tgt, neg, prec, lam, gamma, args.cpu_budget)
+        res["cpu_baseline"] = cpu_baseline_loss(w, W, I, tgt, neg, prec, lam, gamma, args.cpu_budget,
+                                                args.norm)
     print(json.dumps(res), flush=True)
 
 

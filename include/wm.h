@@ -254,26 +254,31 @@ wm_status wm_evaluate_trees(const wm_model* model, const wm_forest* forest, cons
  *   loss_i  = sum_{t < len_i} lam * match_t + (1 - lam) * rank_t
  *
  * (|.| Euclidean; the hardest negative is the nearest, the first one on
- * ties; at the hinge and at a zero distance the gradient taken is 0).  The
- * gradients are those of L = sum_i loss_i with respect to the transition
- * weights, the action embedding and each candidate's initial state, by the
- * chain rule backwards through all steps.  In WM_BF16 every matrix product
- * of the forward and of the backward takes bfloat16-rounded operands with
- * float32 accumulation (the rounding is passed through unchanged).
- * Gradients are sums in a fixed order: repeated calls give identical bits. */
+ * ties; at the hinge, at a zero distance and at a zero hyperplane normal the
+ * gradient taken is 0).  The gradients are those of L = sum_i loss_i with
+ * respect to the transition weights (with Wh for WM_NORM_L2), the action
+ * embedding and each candidate's initial state, by the chain rule backwards
+ * through all steps.  With WM_NORM_L2 the predictions p_t are the unit-length
+ * states of the paper's form, so both terms live in the normalised space as
+ * in Sec. 3.4.  In WM_BF16 every matrix product of the forward and of the
+ * backward takes bfloat16-rounded operands with float32 accumulation (the
+ * rounding is passed through unchanged).  Gradients are sums in a fixed
+ * order: repeated calls give identical bits. */
 typedef struct wm_grads {
   float *w1, *b1;             /* [H][d+e], [H] */
   float *w2, *b2;             /* [d][H], [d] */
   float *type_emb;            /* [n_kinds][e] */
   float *param_w, *param_b;   /* [e][n_params], [e] */
   float *z0;                  /* [B][d]: per candidate (may be NULL) */
+  float *wh;                  /* [d][e]: the normal map (WM_NORM_L2 models; ignored otherwise) */
 } wm_grads;
 
 /* Workspace bytes of wm_rollout_loss for B candidates with padded width
  * T_max (0 on a bad argument).  Same ownership and error-word rules as
  * wm_workspace_bytes (zero once before first use).  It holds the step
- * activations of the backward pass, about 4 (2 H + 3 d + 2 e + 1) bytes per
- * (candidate, step) slot, plus partial gradient sums. */
+ * activations of the backward pass, about 4 (2 H + 3 d + 2 e + 2) bytes per
+ * (candidate, step) slot (4 (2 d + 4) more for WM_NORM_L2), plus partial
+ * gradient sums. */
 size_t wm_loss_workspace_bytes(const wm_model* model, int32_t B, int32_t T_max);
 
 /* Rollout loss (definition above).  Inputs as in wm_rollout, plus
@@ -281,8 +286,8 @@ size_t wm_loss_workspace_bytes(const wm_model* model, int32_t B, int32_t T_max);
  *   negatives [B][T_max][n_neg][d] float32, n_neg >= 1
  *   (entries at t >= lens[i] are never read);
  * outputs: loss [B] float32 (required), total (1 float, may be NULL),
- * grads (may be NULL: loss only; else every pointer but z0 is required).
- * Needs a WM_NORM_NONE model with d <= 256 (UNSUPPORTED otherwise). */
+ * grads (may be NULL: loss only; else every pointer but z0 is required, and
+ * wh for a WM_NORM_L2 model).  Needs d <= 256 (UNSUPPORTED otherwise). */
 wm_status wm_rollout_loss(const wm_model* model, const float* z0, const int32_t* seg_off, int32_t S,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
                           int32_t B, int32_t T_max, const float* targets, const float* negatives,

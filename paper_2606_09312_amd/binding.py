@@ -63,7 +63,7 @@ class Weights(ctypes.Structure):
 
 class Grads(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
-        "w1", "b1", "w2", "b2", "type_emb", "param_w", "param_b", "z0")]
+        "w1", "b1", "w2", "b2", "type_emb", "param_w", "param_b", "z0", "wh")]
 
 
 GRAD_KEYS = ("w1", "b1", "w2", "b2", "type_emb", "param_w", "param_b")
@@ -299,9 +299,12 @@ def evaluate(model: Model, init, seg_off, types, params, lens, hw, k, *, init_is
 def grad_shapes(model: Model) -> Dict[str, tuple]:
     """Shapes of the weight gradients of a model (PyTorch Linear layout)."""
     d = model.dims
-    return {"w1": (d["H"], d["d"] + d["e"]), "b1": (d["H"],), "w2": (d["d"], d["H"]),
-            "b2": (d["d"],), "type_emb": (d["n_kinds"], d["e"]),
-            "param_w": (d["e"], d["n_params"]), "param_b": (d["e"],)}
+    shapes = {"w1": (d["H"], d["d"] + d["e"]), "b1": (d["H"],), "w2": (d["d"], d["H"]),
+              "b2": (d["d"],), "type_emb": (d["n_kinds"], d["e"]),
+              "param_w": (d["e"], d["n_params"]), "param_b": (d["e"],)}
+    if model.norm == "l2":
+        shapes["wh"] = (d["d"], d["e"])
+    return shapes
 
 
 def loss_workspace(model: Model, B: int, T_max: int, device="cuda"):

@@ -132,6 +132,23 @@ void pack_transposed(const wm_dims& dm, const wm_weights& w, std::vector<uint8_t
   }
 }
 
+// Transposed normal map: embedding block ob, fragment kf over the latent (z
+// operand order) -> rows 32 ob + L%32 of Wh^T, i.e. Wh[feature][32 ob + m].
+template <class Gm>
+std::vector<uint8_t> pack_hyper_t(const wm_dims& dm, const wm_weights& w) {
+  const int D = dm.d, E = dm.embed_dim, NZ = D / Gm::KF;
+  std::vector<uint8_t> blk((size_t)HyperT<Gm>::bytes(D, E), 0);
+  for (int ob = 0; ob < E / 32; ++ob)
+    for (int kf = 0; kf < NZ; ++kf)
+      for (int L = 0; L < 64; ++L)
+        for (int j = 0; j < Gm::SL; ++j) {
+          const int m = L & 31, h = L >> 5;
+          const int feat = x_feature<Gm>(D, kf, h, j);
+          put<Gm>(blk, 0, ob * NZ + kf, L, j, w.wh[(size_t)feat * E + 32 * ob + m]);
+        }
+  return blk;
+}
+
 // Cost chunks: for cost hidden chunk c, [Wc1 fragments][bc1 tail][wc2 tail].
 template <class Gm>
 std::vector<uint8_t> pack_cost(const wm_dims& dm, const wm_weights& w) {
@@ -197,7 +214,8 @@ WsLayout ws_layout(const DevModel& m, int B, int T_max, int S, int n_hw) {
 // Rollout-loss workspace: bucketing, step activations (rows i * T_max + t),
 // per-candidate step losses, partial gradient sums.
 struct LossLayout {
-  size_t err, perm, hist, off, row_src, X, A, G, P, SD, DE, lrow, pw1, pw2, pb1, pb2, pemb, total;
+  size_t err, perm, hist, off, row_src, X, A, G, P, SD, DE, V, SC, DV, lrow, pw1, pw2, pb1, pb2,
+      pemb, pwh, total;
   int splits, emb_blocks;
 };
 
@@ -223,12 +241,17 @@ LossLayout loss_layout(const DevModel& m, int B, int T_max) {
   L.P = o; o = align256(o + R * D * 4);
   L.SD = o; o = align256(o + R * D * 4);
   L.DE = o; o = align256(o + R * E * 4);
+  const bool l2 = dm.norm == WM_NORM_L2;
+  L.V = o; o = align256(o + (l2 ? R * D * 4 : 0));
+  L.SC = o; o = align256(o + (l2 ? R * 16 : 0));
+  L.DV = o; o = align256(o + (l2 ? R * D * 4 : 0));
   L.lrow = o; o = align256(o + R * 4);
   L.pw1 = o; o = align256(o + S * H * (D + E) * 4);
   L.pw2 = o; o = align256(o + S * D * H * 4);
   L.pb1 = o; o = align256(o + S * H * 4);
   L.pb2 = o; o = align256(o + S * D * 4);
   L.pemb = o; o = align256(o + (size_t)L.emb_blocks * (K * E + E * P + E) * 4);
+  L.pwh = o; o = align256(o + (l2 ? S * D * E * 4 : 0));
   L.total = o;
   return L;
 }
@@ -328,13 +351,14 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.dims = dm;
   m.prec = dm.precision;
   const int D = dm.d, E = dm.embed_dim, K = dm.n_kinds, P = dm.n_params, HW = dm.hw_dim;
-  std::vector<uint8_t> tw1, tw2, cost, twh, tw2t, tw1t;
+  std::vector<uint8_t> tw1, tw2, cost, twh, tw2t, tw1t, twht;
   const bool l2 = dm.norm == WM_NORM_L2;
   if (m.prec == WM_BF16) {
     pack_transition<GeomBF16>(dm, *w, tw1, tw2);
     if ((D + E) % 32 == 0) pack_transposed<GeomBF16>(dm, *w, tw2t, tw1t);
     cost = pack_cost<GeomBF16>(dm, *w);
     if (l2) twh = pack_hyper<GeomBF16>(dm, *w);
+    if (l2 && E % 32 == 0) twht = pack_hyper_t<GeomBF16>(dm, *w);
     m.w1_chunk_bytes = TransChunk<GeomBF16>::w1_bytes(D, E);
     m.w2_chunk_bytes = TransChunk<GeomBF16>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomBF16>::bytes(D, E, HW);
@@ -344,6 +368,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
     if ((D + E) % 32 == 0) pack_transposed<GeomF32>(dm, *w, tw2t, tw1t);
     cost = pack_cost<GeomF32>(dm, *w);
     if (l2) twh = pack_hyper<GeomF32>(dm, *w);
+    if (l2 && E % 32 == 0) twht = pack_hyper_t<GeomF32>(dm, *w);
     m.w1_chunk_bytes = TransChunk<GeomF32>::w1_bytes(D, E);
     m.w2_chunk_bytes = TransChunk<GeomF32>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomF32>::bytes(D, E, HW);
@@ -390,6 +415,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   const size_t o_wh = off; off = align256(off + twh.size());
   const size_t o_w2t = off; off = align256(off + tw2t.size());
   const size_t o_w1t = off; off = align256(off + tw1t.size());
+  const size_t o_wht = off; off = align256(off + twht.size());
   const size_t o_tab = off; off = align256(off + tab.size() * 4);
   const size_t o_enc = off; off = align256(off + enc.size() * 4);
   void* dev = nullptr;
@@ -404,6 +430,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   if (e == hipSuccess && !twh.empty()) e = hipMemcpy(base + o_wh, twh.data(), twh.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess && !tw2t.empty()) e = hipMemcpy(base + o_w2t, tw2t.data(), tw2t.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess && !tw1t.empty()) e = hipMemcpy(base + o_w1t, tw1t.data(), tw1t.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess && !twht.empty()) e = hipMemcpy(base + o_wht, twht.data(), twht.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_tab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess && !enc.empty()) e = hipMemcpy(base + o_enc, enc.data(), enc.size() * 4, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
@@ -417,6 +444,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.trans_wh = twh.empty() ? nullptr : base + o_wh;
   m.trans_w2t = tw2t.empty() ? nullptr : base + o_w2t;
   m.trans_w1t = tw1t.empty() ? nullptr : base + o_w1t;
+  m.trans_wht = twht.empty() ? nullptr : base + o_wht;
   m.roll_tab = reinterpret_cast<const float*>(base + o_tab);
   m.emb_nat = m.roll_tab;
   const float* encp = reinterpret_cast<const float*>(base + o_enc);
@@ -705,9 +733,9 @@ wm_status wm_rollout_loss(const wm_model* model, const float* z0, const int32_t*
   wm_status s = check_rollout_args(model, z0, types, params, lens, B, T_max, reinterpret_cast<float*>(1));
   if (s != WM_OK) return s;
   const DevModel& m = model->dm;
-  if (m.dims.norm != WM_NORM_NONE)
-    return fail(WM_ERR_UNSUPPORTED, "the rollout loss is implemented for the residual transition (WM_NORM_NONE)");
-  if (!have_train_kernels(m.prec, m.dims.d, m.dims.embed_dim) || !m.trans_w1t || !m.trans_w2t)
+  const bool l2 = m.dims.norm == WM_NORM_L2;
+  if (!have_train_kernels(m.prec, m.dims.d, m.dims.embed_dim) || !m.trans_w1t || !m.trans_w2t ||
+      (l2 && !m.trans_wht))
     return fail(WM_ERR_UNSUPPORTED, "no rollout-loss kernels for this (precision, d, embed_dim)");
   if (n_neg < 1) return fail(WM_ERR_INVALID_ARGUMENT, "n_neg must be >= 1");
   if (!std::isfinite(lam) || !std::isfinite(gamma)) return fail(WM_ERR_INVALID_ARGUMENT, "lam and gamma must be finite");
@@ -718,7 +746,7 @@ wm_status wm_rollout_loss(const wm_model* model, const float* z0, const int32_t*
   if (B > 0 && T_max > 0 && (!targets || !negatives))
     return fail(WM_ERR_INVALID_ARGUMENT, "targets/negatives is NULL");
   if (grads && (!grads->w1 || !grads->b1 || !grads->w2 || !grads->b2 || !grads->type_emb ||
-                !grads->param_w || !grads->param_b))
+                !grads->param_w || !grads->param_b || (l2 && !grads->wh)))
     return fail(WM_ERR_INVALID_ARGUMENT, "null gradient pointer");
   if (!ws) return fail(WM_ERR_INVALID_ARGUMENT, "workspace is NULL");
   const LossLayout L = loss_layout(m, B, T_max);
@@ -733,6 +761,7 @@ wm_status wm_rollout_loss(const wm_model* model, const float* z0, const int32_t*
   io.row_src = reinterpret_cast<int32_t*>(w8 + L.row_src);
   io.X = fptr(L.X); io.A = fptr(L.A); io.G = fptr(L.G); io.P = fptr(L.P);
   io.SD = fptr(L.SD); io.DE = fptr(L.DE); io.dz0 = grads ? grads->z0 : nullptr;
+  io.V = l2 ? fptr(L.V) : nullptr; io.SC = l2 ? fptr(L.SC) : nullptr; io.DV = l2 ? fptr(L.DV) : nullptr;
   io.err = reinterpret_cast<int32_t*>(w8 + L.err); io.B = B; io.T_max = T_max;
   if (B > 0) {
     WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, const_cast<int2*>(io.perm),
@@ -748,9 +777,11 @@ wm_status wm_rollout_loss(const wm_model* model, const float* z0, const int32_t*
   if (B > 0) WM_TIMED(TK_TRAIN_BWD, st, launch_train_bwd(m, io, st));
   GradParts gp;
   gp.w1 = fptr(L.pw1); gp.w2 = fptr(L.pw2); gp.b1 = fptr(L.pb1); gp.b2 = fptr(L.pb2);
-  gp.emb = fptr(L.pemb); gp.splits = L.splits; gp.emb_blocks = L.emb_blocks;
+  gp.emb = fptr(L.pemb); gp.wh = l2 ? fptr(L.pwh) : nullptr;
+  gp.splits = L.splits; gp.emb_blocks = L.emb_blocks;
   WM_TIMED(TK_GRADS, st, launch_weight_grads(m, io, gp, grads->w1, grads->b1, grads->w2, grads->b2,
-                                             grads->type_emb, grads->param_w, grads->param_b, st));
+                                             grads->type_emb, grads->param_w, grads->param_b,
+                                             l2 ? grads->wh : nullptr, st));
   return ok();
 }
 

@@ -136,6 +136,15 @@ struct HyperGeom {
   static constexpr int groups_per_block(int E) { return E / Gm::KF / Gm::G; }
   static constexpr int bytes(int D, int E) { return (D / 32) * groups_per_block(E) * 1024; }
 };
+// Transposed normal map for the paper-form loss backward: de += Wh^T . dv,
+// with A fragments per 32-row block of the embedding and contraction over the
+// latent in the z operand's slot order (x_feature), so dv in accumulator
+// layout is the B operand: (E / 32) x (D / KF) fragments.
+template <class Gm>
+struct HyperT {
+  static constexpr int groups_per_block(int D) { return D / Gm::KF / Gm::G; }
+  static constexpr int bytes(int D, int E) { return (E / 32) * groups_per_block(D) * 1024; }
+};
 // The rollout kernel keeps Wh in LDS when the double-buffered chunks leave
 // room for it (and for the embedding table), otherwise streams it from L2.
 constexpr int WH_LDS_LIMIT = 112 * 1024;
@@ -186,6 +195,7 @@ struct DevModel {
   const uint8_t* trans_wh;  // Wh fragments (WM_NORM_L2 only)
   const uint8_t* trans_w2t; // H/32 chunks of W2^T (rollout-loss backward)
   const uint8_t* trans_w1t; // H/32 chunks of W1^T (rollout-loss backward)
+  const uint8_t* trans_wht; // Wh^T fragments (paper-form rollout-loss backward)
   const float* roll_tab;    // type_emb [K][E + 4] (padded rows), param_w^T [PMAX][E] (zero rows past P), param_b [E], b2 (acc order) [D]
   const float* emb_nat;     // the first three parts of roll_tab
   const float* enc_w1t;     // We1^T [F][Fh] (bf16-rounded values in bf16 mode)
@@ -249,6 +259,7 @@ struct TrainIO {
   int32_t* off;             // [B+1] row offsets (written by launch_row_offsets)
   int32_t* row_src;         // [rows] i * T_max + t of each row
   float *X, *A, *G, *P, *SD, *DE;
+  float *V, *SC, *DV;       // paper form: Wh e [rows][D], (v.z, v.v, |u|, 0) [rows][4], dL/dv [rows][D]
   float* dz0;               // [B][D] or null
   int32_t* err;
   int B, T_max;
@@ -256,7 +267,7 @@ struct TrainIO {
 // Weight-gradient partial sums of `splits` equal shares of the rows, added
 // in order afterwards.
 struct GradParts {
-  float *w1, *w2, *b1, *b2, *emb;
+  float *w1, *w2, *b1, *b2, *emb, *wh;
   int splits, emb_blocks;
 };
 inline int train_splits(long long rows_bound) {
@@ -278,7 +289,7 @@ hipError_t launch_step_loss(const float* P, const float* targets, const float* n
 hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st);
 hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradParts& parts,
                                float* gw1, float* gb1, float* gw2, float* gb2, float* gtemb,
-                               float* gpw, float* gpb, hipStream_t st);
+                               float* gpw, float* gpb, float* gwh, hipStream_t st);
 
 // Whether a (precision, d, e) combination has rollout/score kernels.
 bool have_kernels(int prec, int d, int e);

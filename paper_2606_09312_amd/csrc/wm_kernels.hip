@@ -1835,6 +1835,11 @@ struct TrainArgs {
   float* P;                 // [R][D]   predicted states
   float* SD;                // [R][D]   dL/dp seeds; the backward overwrites them with delta_{t+1}
   float* DE;                // [R][E]   gradient reaching the step's embedding
+  const uint8_t* wh;        // paper form: packed normal map, and its transpose
+  const uint8_t* wht;
+  float* V;                 // [R][D]   Wh e
+  float* SC;                // [R][4]   v.z, v.v, |u|, 0
+  float* DV;                // [R][D]   dL/dv
   float* dz0;               // [B][D]   (may be null)
   int32_t* err;
   int B, T_max, P_, K, H, tab_bytes;
@@ -1895,7 +1900,7 @@ __device__ __forceinline__ TileInfo tile_info(const TrainArgs& a, int tile, int 
   return ti;
 }
 
-template <class PR, int D, int E, int WAVES>
+template <class PR, int D, int E, int WAVES, bool NORM>
 __global__ __launch_bounds__(64 * WAVES, 1) void train_fwd_kernel(const TrainArgs a) {
   using R = Roll<PR, D, E>;
   using TG = TrainGeom<PR, D, E>;
@@ -1983,6 +1988,43 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_fwd_kernel(const TrainArg
         for (int j = 0; j < SL; ++j) xrow[D + f0 + j] = op_value<PR>(ev[j]);
       }
     }
+    // paper form: z' = z - (v.z / v.v) v with v = Wh e (two passes of V^T =
+    // Wh . E^T on the matrix cores: the dots, then the projection)
+    float s_vz = 0.0f, s_vv = 0.0f;
+    if constexpr (NORM) {
+      using HY = Hyper<PR, D, E>;
+      constexpr int GPB = HY::GPB;
+      gu8* whb = (gu8*)(a.wh) + lane * 16;
+      auto vblock = [&](int b) -> f32x16 {
+        f32x16 vb = {};
+#pragma unroll
+        for (int k = 0; k < GPB; ++k) {
+          const u32x4 grp = *reinterpret_cast<gu32x4*>(whb + (size_t)(b * GPB + k) * 1024);
+#pragma unroll
+          for (int ww = 0; ww < G; ++ww) vb = PR::mfma(PR::pick(grp, ww), xe[k * G + ww], vb);
+        }
+        return vb;
+      };
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const f32x16 vb = vblock(b);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s_vz = fmaf(vb[r], zacc[b][r], s_vz);
+          s_vv = fmaf(vb[r], vb[r], s_vv);
+        }
+        if (active) store_acc(a.V + row * D + 32 * b, vb, h);
+      }
+      s_vz = HY::pair_sum(s_vz);
+      s_vv = HY::pair_sum(s_vv);
+      const float al = s_vv > 0.0f ? s_vz / s_vv : 0.0f;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const f32x16 vb = vblock(b);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) zacc[b][r] -= al * vb[r];
+      }
+    }
     Frag xz[NZ];
 #pragma unroll
     for (int kf = 0; kf < NZ; ++kf) {
@@ -2045,6 +2087,24 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_fwd_kernel(const TrainArg
     for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) zacc[b][r] += t_b2[(b * 2 + h) * 16 + r] * actf;
+    if constexpr (NORM) {            // z_{t+1} = u / |u| (finished candidates stay as they are)
+      float uu = 0.0f;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) uu = fmaf(zacc[b][r], zacc[b][r], uu);
+      uu = uu + __shfl_xor(uu, 32);
+      const float nu = sqrtf(uu);
+      const float sc = (active && nu > 0.0f) ? 1.0f / nu : 1.0f;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) zacc[b][r] *= sc;
+      if (active && h == 0) {
+        const f32x4 sv = {s_vz, s_vv, nu, 0.0f};
+        *reinterpret_cast<f32x4*>(a.SC + row * 4) = sv;
+      }
+    }
     if (active) {
 #pragma unroll
       for (int b = 0; b < NB; ++b) store_acc(a.P + row * D + 32 * b, zacc[b], h);
@@ -2180,7 +2240,7 @@ __global__ __launch_bounds__(1024) void loss_total_kernel(const float* __restric
 // accumulate straight into delta (the residual path carries delta itself)
 // and whose embedding blocks are stored as dE.  Finished candidates have no
 // seed and a zero mask, so their delta passes through unchanged.
-template <class PR, int D, int E, int WAVES>
+template <class PR, int D, int E, int WAVES, bool NORM>
 __global__ __launch_bounds__(64 * WAVES, 1) void train_bwd_kernel(const TrainArgs a) {
   using R = Roll<PR, D, E>;
   using TG = TrainGeom<PR, D, E>;
@@ -2216,11 +2276,33 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_bwd_kernel(const TrainArg
     const size_t row = row0 + t;
     if (active) {
 #pragma unroll
+      for (int b = 0; b < NB; ++b) dacc[b] += load_acc(a.SD + row * D + 32 * b, h);
+    }
+    f32x4 sc = {0.0f, 0.0f, 0.0f, 0.0f};
+    if constexpr (NORM) {
+      // through z_{t+1} = u / |u|: du = (delta - (delta . z) z) / |u|
+      if (active) sc = *reinterpret_cast<const f32x4*>(a.SC + row * 4);
+      float dz = 0.0f;
+#pragma unroll
       for (int b = 0; b < NB; ++b) {
-        float* sd = a.SD + row * D + 32 * b;
-        dacc[b] += load_acc(sd, h);
-        store_acc(sd, dacc[b], h);                    // delta_{t+1}
+        const f32x16 zb = active ? load_acc(a.P + row * D + 32 * b, h) : f32x16{};
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dz = fmaf(dacc[b][r], zb[r], dz);
       }
+      dz = dz + __shfl_xor(dz, 32);
+      const bool nrm = active && sc[2] > 0.0f;
+      const float inu = nrm ? 1.0f / sc[2] : 1.0f;
+      const float cz = nrm ? dz : 0.0f;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const f32x16 zb = nrm ? load_acc(a.P + row * D + 32 * b, h) : f32x16{};
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dacc[b][r] = (dacc[b][r] - cz * zb[r]) * inu;
+      }
+    }
+    if (active) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) store_acc(a.SD + row * D + 32 * b, dacc[b], h);   // du (delta_{t+1} in the residual form)
     }
     Frag dop[NZ];
 #pragma unroll
@@ -2261,6 +2343,51 @@ __global__ __launch_bounds__(64 * WAVES, 1) void train_bwd_kernel(const TrainArg
             const int ob = F / NF2;
             if (ob < NB) dacc[ob] = PR::mfma(PR::pick(grp, ww), PR::gfrag(dp, F % NF2), dacc[ob]);
             else deacc[ob - NB] = PR::mfma(PR::pick(grp, ww), PR::gfrag(dp, F % NF2), deacc[ob - NB]);
+          }
+        }
+      }
+    }
+    if constexpr (NORM) {
+      // through z' = z - (w . z) w, w = v / |v|: dz = dz' - (w . dz') w,
+      // dv = (dw - (w . dw) w) / |v| with dw = -((w . z) dz' + (w . dz') z),
+      // where w . dw = -2 (w . z)(w . dz'); de += R(Wh)^T R(dv)
+      const bool prj = active && sc[1] > 0.0f;
+      const float inv = prj ? rsqrtf(sc[1]) : 0.0f;
+      const float wz = sc[0] * inv;
+      float wdz = 0.0f;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const f32x16 vb = prj ? load_acc(a.V + row * D + 32 * b, h) : f32x16{};
+#pragma unroll
+        for (int r = 0; r < 16; ++r) wdz = fmaf(vb[r], dacc[b][r], wdz);
+      }
+      wdz = (wdz + __shfl_xor(wdz, 32)) * inv;
+      const float* zin = t > 0 ? a.P + (row - 1) * D : a.z0 + (size_t)ti.seg * D;
+      gu8* whtb = (gu8*)(a.wht) + lane * 16;
+      constexpr int NZG = NZ / G;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const f32x16 vb = prj ? load_acc(a.V + row * D + 32 * b, h) : f32x16{};
+        const f32x16 zb = prj ? load_acc(zin + 32 * b, h) : f32x16{};
+        f32x16 dv;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float wr = vb[r] * inv;
+          dv[r] = (-(wz * dacc[b][r] + wdz * zb[r]) + 2.0f * wz * wdz * wr) * inv;
+          dacc[b][r] -= wdz * wr;
+        }
+        if (active) store_acc(a.DV + row * D + 32 * b, dv, h);
+#pragma unroll
+        for (int f = 0; f < NF2; ++f) {
+          float v[SL];
+#pragma unroll
+          for (int j = 0; j < SL; ++j) v[j] = dv[f * SL + j];
+          const Frag dvf = PR::cvt(v);
+          const int kf = b * NF2 + f;
+#pragma unroll
+          for (int ob = 0; ob < NBE; ++ob) {
+            const u32x4 grp = *reinterpret_cast<gu32x4*>(whtb + (size_t)(ob * NZG + kf / G) * 1024);
+            deacc[ob] = PR::mfma(PR::pick(grp, kf % G), dvf, deacc[ob]);
           }
         }
       }
@@ -2499,14 +2626,14 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_rows_kernel(const TrainAr
 // contiguous), so each lane's operand fragment is one 16-byte LDS read.  The
 // next stage's loads are in flight during the current stage's products.
 struct WgradProblem {
-  const float* A;           // [rows][M]
-  const float* Bm;          // [rows][N]
+  const float* A;           // [rows][lda], columns [0, M)
+  const float* Bm;          // [rows][ldb], columns [0, N)
   float* part;              // [splits][M][N]
-  float* colsum;            // [splits][M]
-  int M, N, tiles_n, tiles;
+  float* colsum;            // [splits][M] (may be null)
+  int M, N, lda, ldb, tiles_n, tiles;
 };
 struct WgradArgs {
-  WgradProblem p0, p1;
+  WgradProblem p0, p1, p2;  // p2.tiles may be 0
   const int32_t* off;
   int B, splits;
 };
@@ -2524,19 +2651,20 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   // Workgroups are dealt to the 8 XCDs in turn: every tile of split s runs
   // on XCD s mod 8, so the split's rows come from HBM once per XCD and the
   // other tiles' re-reads hit that XCD's L2.
-  const int tiles_all = a.p0.tiles + a.p1.tiles;
+  const int tiles_all = a.p0.tiles + a.p1.tiles + a.p2.tiles;
   const int xcd = blockIdx.x % 8, k8 = blockIdx.x / 8;
   const int tile_id = k8 % tiles_all;
   const int split = (k8 / tiles_all) * 8 + xcd;
   if (split >= a.splits) return;
-  const bool second = tile_id >= a.p0.tiles;
-  const float* A = second ? a.p1.A : a.p0.A;
-  const float* Bm = second ? a.p1.Bm : a.p0.Bm;
-  float* part = second ? a.p1.part : a.p0.part;
-  float* colsum = second ? a.p1.colsum : a.p0.colsum;
-  const int M = second ? a.p1.M : a.p0.M, N = second ? a.p1.N : a.p0.N;
-  const int tiles_n = second ? a.p1.tiles_n : a.p0.tiles_n;
-  const int tile = tile_id - (second ? a.p0.tiles : 0);
+  const int which = tile_id < a.p0.tiles ? 0 : (tile_id < a.p0.tiles + a.p1.tiles ? 1 : 2);
+  const WgradProblem& pr = which == 0 ? a.p0 : (which == 1 ? a.p1 : a.p2);
+  const float* A = pr.A;
+  const float* Bm = pr.Bm;
+  float* part = pr.part;
+  float* colsum = pr.colsum;
+  const int M = pr.M, N = pr.N, lda = pr.lda, ldb = pr.ldb;
+  const int tiles_n = pr.tiles_n;
+  const int tile = tile_id - (which == 0 ? 0 : (which == 1 ? a.p0.tiles : a.p0.tiles + a.p1.tiles));
   const int m0 = (tile / tiles_n) * WG_T, n0 = (tile % tiles_n) * WG_T;
   int r0, r1;
   split_rows(a.off, a.B, a.splits, split, r0, r1);
@@ -2553,8 +2681,8 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
       for (int j = 0; j < 8; ++j) {
         const int r = rb + (rg + 2 * q) * 8 + j;
         const bool rv = r < r1;
-        va[q][j] = (rv && okA) ? A[(size_t)r * M + m0 + c] : 0.0f;
-        vb[q][j] = (rv && okB) ? Bm[(size_t)r * N + n0 + c] : 0.0f;
+        va[q][j] = (rv && okA) ? A[(size_t)r * lda + m0 + c] : 0.0f;
+        vb[q][j] = (rv && okB) ? Bm[(size_t)r * ldb + n0 + c] : 0.0f;
       }
   };
   auto store = [&]() {
@@ -2632,7 +2760,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
       }
     }
   // column sums of A: the two row groups, in order (first column tile only)
-  if (n0 == 0) {
+  if (n0 == 0 && colsum) {
     __syncthreads();
     if (rg == 1) csum[c] = cs;
     __syncthreads();
@@ -3395,16 +3523,17 @@ TrainArgs train_args(const DevModel& m, const TrainIO& io) {
   a.tab = m.roll_tab; a.z0 = io.z0; a.perm = io.perm; a.types = io.types; a.params = io.params;
   a.lens = io.lens; a.off = io.off; a.row_src = io.row_src;
   a.X = io.X; a.A = io.A; a.G = io.G; a.P = io.P; a.SD = io.SD; a.DE = io.DE;
+  a.wh = m.trans_wh; a.wht = m.trans_wht; a.V = io.V; a.SC = io.SC; a.DV = io.DV;
   a.dz0 = io.dz0; a.err = io.err; a.B = io.B; a.T_max = io.T_max;
   a.P_ = m.dims.n_params; a.K = m.dims.n_kinds; a.H = m.dims.trans_hidden;
   a.tab_bytes = m.roll_tab_bytes;
   return a;
 }
 
-template <class PR, int D, int E, int WAVES>
+template <class PR, int D, int E, int WAVES, bool NORM>
 hipError_t launch_train_fwd_t(const DevModel& m, const TrainArgs& a, int blocks, hipStream_t st) {
   const int lds = m.roll_tab_bytes;
-  auto kern = train_fwd_kernel<PR, D, E, WAVES>;
+  auto kern = train_fwd_kernel<PR, D, E, WAVES, NORM>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -3427,13 +3556,13 @@ hipError_t launch_train_bwd_rows(const TrainArgs& a, int tiles, hipStream_t st) 
   return hipGetLastError();
 }
 
-template <class PR, int D, int E>
+template <class PR, int D, int E, bool NORM>
 hipError_t launch_train_bwd_t(const TrainArgs& a, int tiles, hipStream_t st) {
   const int waves = pick_waves(tiles);
   const int blocks = (tiles + waves - 1) / waves;
-  if (waves == 4) hipLaunchKernelGGL((train_bwd_kernel<PR, D, E, 4>), dim3(blocks), dim3(256), 0, st, a);
-  else if (waves == 2) hipLaunchKernelGGL((train_bwd_kernel<PR, D, E, 2>), dim3(blocks), dim3(128), 0, st, a);
-  else hipLaunchKernelGGL((train_bwd_kernel<PR, D, E, 1>), dim3(blocks), dim3(64), 0, st, a);
+  if (waves == 4) hipLaunchKernelGGL((train_bwd_kernel<PR, D, E, 4, NORM>), dim3(blocks), dim3(256), 0, st, a);
+  else if (waves == 2) hipLaunchKernelGGL((train_bwd_kernel<PR, D, E, 2, NORM>), dim3(blocks), dim3(128), 0, st, a);
+  else hipLaunchKernelGGL((train_bwd_kernel<PR, D, E, 1, NORM>), dim3(blocks), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 
@@ -3471,7 +3600,8 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
   if (io.B == 0) return hipSuccess;
   const TrainArgs a = train_args(m, io);
   const int tiles = (io.B + 31) / 32;
-  if (m.dims.d == 256 && m.dims.embed_dim == 64) {
+  const bool norm = m.dims.norm == WM_NORM_L2;
+  if (m.dims.d == 256 && m.dims.embed_dim == 64 && !norm) {
     const int NC = m.dims.trans_hidden / 32;
     if (m.prec == WM_BF16 && NC == 16) return launch_train_fwd_rows<PBF16, 16, 8>(m, io, tiles, st);
     if (m.prec == WM_BF16 && NC == 32) return launch_train_fwd_rows<PBF16, 32, 8>(m, io, tiles, st);
@@ -3480,10 +3610,13 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
   const int waves = pick_waves(tiles);
   const int blocks = (tiles + waves - 1) / waves;
   const int prec = m.prec, d = m.dims.d, e = m.dims.embed_dim;
-#define WM_TFWD(PR, D, E)                                                          \
-  return waves == 4 ? launch_train_fwd_t<PR, D, E, 4>(m, a, blocks, st)              \
-       : waves == 2 ? launch_train_fwd_t<PR, D, E, 2>(m, a, blocks, st)              \
-                    : launch_train_fwd_t<PR, D, E, 1>(m, a, blocks, st);
+#define WM_TFWD(PR, D, E)                                                                      \
+  if (norm) return waves == 4 ? launch_train_fwd_t<PR, D, E, 4, true>(m, a, blocks, st)          \
+                 : waves == 2 ? launch_train_fwd_t<PR, D, E, 2, true>(m, a, blocks, st)          \
+                              : launch_train_fwd_t<PR, D, E, 1, true>(m, a, blocks, st);         \
+  return waves == 4 ? launch_train_fwd_t<PR, D, E, 4, false>(m, a, blocks, st)                   \
+       : waves == 2 ? launch_train_fwd_t<PR, D, E, 2, false>(m, a, blocks, st)                   \
+                    : launch_train_fwd_t<PR, D, E, 1, false>(m, a, blocks, st);
   WM_FOR_TRAIN_DE(WM_TFWD)
 #undef WM_TFWD
   return hipErrorInvalidValue;
@@ -3493,14 +3626,16 @@ hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st
   if (io.B == 0) return hipSuccess;
   const TrainArgs a = train_args(m, io);
   const int tiles = (io.B + 31) / 32;
-  if (m.dims.d == 256 && m.dims.embed_dim == 64) {
+  const bool norm = m.dims.norm == WM_NORM_L2;
+  if (m.dims.d == 256 && m.dims.embed_dim == 64 && !norm) {
     const int NC = m.dims.trans_hidden / 32;
     if (m.prec == WM_BF16 && NC == 16) return launch_train_bwd_rows<PBF16, 16, 8>(a, tiles, st);
     if (m.prec == WM_BF16 && NC == 32) return launch_train_bwd_rows<PBF16, 32, 8>(a, tiles, st);
     if (m.prec == WM_FP32 && NC == 16) return launch_train_bwd_rows<PF32, 16, 4>(a, tiles, st);
   }
   const int prec = m.prec, d = m.dims.d, e = m.dims.embed_dim;
-#define WM_TBWD(PR, D, E) return launch_train_bwd_t<PR, D, E>(a, tiles, st);
+#define WM_TBWD(PR, D, E) \
+  return norm ? launch_train_bwd_t<PR, D, E, true>(a, tiles, st) : launch_train_bwd_t<PR, D, E, false>(a, tiles, st);
   WM_FOR_TRAIN_DE(WM_TBWD)
 #undef WM_TBWD
   return hipErrorInvalidValue;
@@ -3527,7 +3662,7 @@ hipError_t launch_step_loss(const float* P, const float* targets, const float* n
 
 hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradParts& g,
                                float* gw1, float* gb1, float* gw2, float* gb2, float* gtemb,
-                               float* gpw, float* gpb, hipStream_t st) {
+                               float* gpw, float* gpb, float* gwh, hipStream_t st) {
   const int D = m.dims.d, E = m.dims.embed_dim, H = m.dims.trans_hidden, IN = D + E;
   const int K = m.dims.n_kinds, P = m.dims.n_params, W = K * E + E * P + E;
   const int S = g.splits;
@@ -3536,17 +3671,20 @@ hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradP
                        stride, n, out);
   };
   WgradArgs a;
-  auto prob = [](const float* A, int M, const float* Bm, int N, float* part, float* colsum) {
+  auto prob = [](const float* A, int M, int lda, const float* Bm, int N, int ldb, float* part,
+                 float* colsum) {
     WgradProblem p;
-    p.A = A; p.Bm = Bm; p.part = part; p.colsum = colsum; p.M = M; p.N = N;
+    p.A = A; p.Bm = Bm; p.part = part; p.colsum = colsum; p.M = M; p.N = N; p.lda = lda; p.ldb = ldb;
     p.tiles_n = (N + WG_T - 1) / WG_T;
     p.tiles = ((M + WG_T - 1) / WG_T) * p.tiles_n;
     return p;
   };
-  a.p0 = prob(io.SD, D, io.G, H, g.w2, g.b2);      // dW2 [D][H], db2
-  a.p1 = prob(io.A, H, io.X, IN, g.w1, g.b1);      // dW1 [H][IN], db1
+  a.p0 = prob(io.SD, D, D, io.G, H, H, g.w2, g.b2);         // dW2 [D][H], db2
+  a.p1 = prob(io.A, H, H, io.X, IN, IN, g.w1, g.b1);        // dW1 [H][IN], db1
+  a.p2 = gwh ? prob(io.DV, D, D, io.X + D, E, IN, g.wh, nullptr)   // dWh [D][E] = sum R(dv) R(e)^T
+             : WgradProblem{};
   a.off = io.off; a.B = io.B; a.splits = S;
-  const dim3 grid((a.p0.tiles + a.p1.tiles) * ((S + 7) / 8) * 8);
+  const dim3 grid((a.p0.tiles + a.p1.tiles + a.p2.tiles) * ((S + 7) / 8) * 8);
   if (m.prec == WM_BF16) hipLaunchKernelGGL(wgrad_kernel<PBF16>, grid, dim3(256), 0, st, a);
   else hipLaunchKernelGGL(wgrad_kernel<PF32>, grid, dim3(256), 0, st, a);
   if (E > EMB_THREADS || EMB_THREADS % E) return hipErrorInvalidValue;
@@ -3560,6 +3698,7 @@ hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradP
                      io.row_src, io.types, io.params, K, P, io.off, io.B, g.emb_blocks, g.emb);
   sums(g.w1, (long long)H * IN, (long long)H * IN, gw1);
   sums(g.w2, (long long)D * H, (long long)D * H, gw2);
+  if (gwh) sums(g.wh, (long long)D * E, (long long)D * E, gwh);
   sums(g.b1, H, H, gb1);
   sums(g.b2, D, D, gb2);
   auto sums_emb = [&](const float* part, long long n, float* out) {

@@ -29,7 +29,9 @@ The GPU's float32 accumulation perturbs the computation at that level
 sequence length from 1 to 32).  So long sequences are held to the per-tensor
 and per-row rules in fp32, and in bf16 to the per-tensor rule with the bound
 max(2e-2, 2 s), s the largest of the oracle's own per-tensor changes under
-three such weight perturbations (seeded).
+three such weight perturbations (seeded).  The paper's form (unit-length
+states) is well conditioned: there every case is held to the per-tensor and
+per-row rules in both precisions, whatever the sequence length.
 """
 import numpy as np
 import pytest
@@ -59,16 +61,16 @@ def wm():
 _models = {}
 
 
-def model_for(wm, name, prec):
-    key = (name, prec)
+def model_for(wm, name, prec, norm="none", W=None, tag=""):
+    key = (name, prec, norm, tag)
     if key not in _models:
         w = synth.workload(name)
-        W = synth.make_weights(w, 1000)
-        _models[key] = (wm.Model(wm.model_dims(w), W, precision=prec), W)
+        W = synth.make_weights(w, 1000) if W is None else W
+        _models[key] = (wm.Model(wm.model_dims(w), W, precision=prec, norm=norm), W)
     return _models[key]
 
 
-def margin_targets(W, I, prec, n_neg, seed, gamma, mode="mixed"):
+def margin_targets(W, I, prec, n_neg, seed, gamma, mode="mixed", norm="none"):
     """targets [B][T][d], negatives [B][T][n_neg][d] around the oracle's
     predicted states p_t: z* = p + a u and z-_q = p + b_q v_q (u, v_q random
     unit vectors), so d(p, z*) = a and d(p, z-_q) = b_q.  With the scale
@@ -80,7 +82,7 @@ def margin_targets(W, I, prec, n_neg, seed, gamma, mode="mixed"):
     rng = np.random.default_rng(seed)
     Wd = O.prepare(W, prec)
     _, _, traj = O.rollout(Wd, I["z0"], I["seg_off"], I["types"], I["params"], I["lens"], prec,
-                           trajectory=True)
+                           trajectory=True, norm=norm)
     B, T = I["types"].shape
     d = Wd["w2"].shape[0]
     tgt = np.full((B, T, d), np.nan, dtype=np.float32)
@@ -125,28 +127,31 @@ def rel_rms(g, o):
     return np.abs(g - o) / np.maximum(np.abs(o), max(rms, 1e-30))
 
 
-def check_against_oracle(g, W, I, tgt, neg, lam, gamma, prec, rows=None, elems=False):
+def check_against_oracle(g, W, I, tgt, neg, lam, gamma, prec, rows=None, elems=False,
+                         norm="none"):
     """Compare one GPU result with the oracle (rules in the module docstring);
     rows / elems: apply the per-row (default: in fp32) / per-element rule.
     Without the per-row rule in bf16, the per-tensor bound widens to twice
     the oracle's own change under 1e-7 relative noise on the weights."""
     rows = prec == "fp32" if rows is None else rows
-    L, per, G = LO.loss_and_grad(W, I, tgt, neg, lam, gamma, prec)
+    L, per, G = LO.loss_and_grad(W, I, tgt, neg, lam, gamma, prec, norm=norm)
     tol = TOL[prec]
     lr = rel_rms(g["loss"], per)
     assert lr.max() <= tol, f"loss rel err {lr.max():.3e}"
     assert abs(g["total"][0] - L) <= tol * max(abs(L), 1e-30)
     report = {"loss": lr.max()}
-    bound = {k: tol for k in KEYS + ("z0",)}
+    keys = KEYS + ("z0",) + (("wh",) if norm == "l2" else ())
+    row_max = 0.0
+    bound = {k: tol for k in keys}
     if prec == "bf16" and not rows:
         rng = np.random.default_rng(12345)
         for _ in range(3):
             Wp = {k: np.asarray(v, dtype=np.float64) * (1.0 + 1e-7 * rng.standard_normal(np.shape(v)))
                   for k, v in W.items()}
-            _, _, Gp = LO.loss_and_grad(Wp, I, tgt, neg, lam, gamma, prec)
+            _, _, Gp = LO.loss_and_grad(Wp, I, tgt, neg, lam, gamma, prec, norm=norm)
             for k in bound:
                 bound[k] = max(bound[k], 2.0 * fro_rel(Gp[k], G[k]))
-    for k in KEYS + ("z0",):
+    for k in keys:
         o, x = G[k], g[k]
         fro = fro_rel(x, o)
         rr = rows_rel(x, o).max() if rows and o.ndim > 1 else 0.0
@@ -154,6 +159,9 @@ def check_against_oracle(g, W, I, tgt, neg, lam, gamma, prec, rows=None, elems=F
         assert fro <= bound[k] and max(rr, el) <= tol, \
             f"{k}: frobenius rel {fro:.3e} (bound {bound[k]:.1e}), row rel {rr:.3e}, element rel {el:.3e}"
         report[k] = fro
+        row_max = max(row_max, rr)
+    if rows:
+        report["rows"] = row_max
     return report
 
 
@@ -267,3 +275,72 @@ def test_loss_all_empty_sequences(wm):
     g = run_loss(wm, model, I, tgt, neg, 0.5, 0.3)
     for k in ("loss", "total", "z0") + KEYS:
         np.testing.assert_array_equal(g[k], 0.0, err_msg=k)
+
+
+# ---- the paper form (hyperplane projection, unit-length states; the loss
+# compares unit-length predictions, Sec. 3.4)
+
+L2_CASES = [
+    ("tiny", "fp32", 300, 1),
+    ("tiny", "bf16", 300, 1),
+    ("ansor_round", "fp32", 200, 1),
+    ("ansor_round", "bf16", 4 * 61, 4),
+    ("long_schedule", "bf16", 150, 1),
+]
+
+
+@pytest.mark.parametrize("name,prec,B,S", L2_CASES)
+def test_l2_loss_parity_scaled(wm, name, prec, B, S):
+    base = synth.workload(name)
+    w = synth.scaled(base, B=B, S=S)
+    print(f"[l2 loss parity] {name} {prec} B={B} S={S}", flush=True)
+    model, W = model_for(wm, name, prec, norm="l2")
+    I = synth.make_inputs(w, 5100 + B, pad="garbage")
+    I["lens"][:3] = 0
+    tgt, neg = margin_targets(W, I, prec, 3, 81, 0.3, norm="l2")
+    g = run_loss(wm, model, I, tgt, neg, 0.5, 0.3)
+    rep = check_against_oracle(g, W, I, tgt, neg, 0.5, 0.3, prec, rows=True, norm="l2")
+    np.testing.assert_array_equal(g["loss"][:3], 0.0)
+    np.testing.assert_array_equal(g["z0"][:3], 0.0)
+    print("  " + ", ".join(f"{k} {v:.1e}" for k, v in rep.items()), flush=True)
+
+
+@pytest.mark.parametrize("name,prec,B", [("ansor_round", "bf16", 250), ("ansor_round", "fp32", 130),
+                                         ("tiny", "bf16", 200)])
+def test_l2_loss_short_sequences_rowwise(wm, name, prec, B):
+    w = synth.scaled(synth.workload(name), B=B, lengths="uniform", len_lo=0, len_hi=2)
+    print(f"[l2 loss short] {name} {prec} B={B}", flush=True)
+    model, W = model_for(wm, name, prec, norm="l2")
+    I = synth.make_inputs(w, 7100 + B, pad="garbage")
+    tgt, neg = margin_targets(W, I, prec, 3, 83, 0.3, norm="l2")
+    g = run_loss(wm, model, I, tgt, neg, 0.5, 0.3)
+    rep = check_against_oracle(g, W, I, tgt, neg, 0.5, 0.3, prec, rows=True,
+                               elems=prec == "fp32", norm="l2")
+    print("  " + ", ".join(f"{k} {v:.1e}" for k, v in rep.items()), flush=True)
+
+
+def test_l2_loss_full_size_ansor(wm):
+    w = synth.workload("ansor_round")
+    print(f"[l2 loss full] ansor_round bf16 B={w.B}", flush=True)
+    model, W = model_for(wm, "ansor_round", "bf16", norm="l2")
+    I = synth.make_inputs(w, 93)
+    tgt, neg = margin_targets(W, I, "bf16", 4, 17, 0.3, norm="l2")
+    g = run_loss(wm, model, I, tgt, neg, 0.5, 0.3)
+    rep = check_against_oracle(g, W, I, tgt, neg, 0.5, 0.3, "bf16", rows=True, norm="l2")
+    print("  " + ", ".join(f"{k} {v:.1e}" for k, v in rep.items()), flush=True)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_l2_loss_zero_normal_map(wm, prec):
+    """Wh = 0: no hyperplane anywhere; the normal map's gradient is the
+    subgradient 0 and the rest follows the plain step with unit length."""
+    base = synth.workload("ansor_round")
+    W = dict(synth.make_weights(base, 1000))
+    W["wh"] = np.zeros_like(W["wh"])
+    model, W = model_for(wm, "ansor_round", prec, norm="l2", W=W, tag="wh0")
+    w = synth.scaled(base, B=100, lengths="uniform", len_lo=0, len_hi=4)
+    I = synth.make_inputs(w, 47, pad="garbage")
+    tgt, neg = margin_targets(W, I, prec, 2, 7, 0.3, norm="l2")
+    g = run_loss(wm, model, I, tgt, neg, 0.5, 0.3)
+    check_against_oracle(g, W, I, tgt, neg, 0.5, 0.3, prec, rows=True, norm="l2")
+    np.testing.assert_array_equal(g["wh"], 0.0)
