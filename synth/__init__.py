@@ -20,7 +20,8 @@ import numpy as np
 
 __all__ = [
     "Workload", "WORKLOADS", "workload", "make_weights", "make_inputs",
-    "scaled", "WEIGHT_ORDER", "make_forest", "make_loss_targets",
+    "scaled", "WEIGHT_ORDER", "make_forest", "make_loss_targets", "TextWorkload",
+    "TEXT_WORKLOADS", "TEXT_WEIGHT_ORDER", "make_text_weights", "make_programs",
 ]
 
 
@@ -259,3 +260,76 @@ def make_loss_targets(w: Workload, seed: int, n_neg: int, lens=None):
         tgt[pad] = np.nan
         neg[pad] = np.nan
     return tgt, neg
+
+
+# ---- chunked transformer state encoder (Sec. 3.3) -------------------------
+
+@dataclass(frozen=True)
+class TextWorkload:
+    """Shape of the chunked transformer encoder and of a batch of programs.
+
+    vocab/hidden/heads/ffn/layers: the backbone (the CodeBERT shape is
+    RoBERTa-base); window/stride: the sliding-window chunks; d: the latent
+    width of the projection head; S programs with token counts uniform in
+    [len_lo, len_hi].
+    """
+    name: str
+    S: int
+    vocab: int
+    hidden: int
+    heads: int
+    ffn: int
+    layers: int
+    window: int
+    stride: int
+    d: int
+    len_lo: int
+    len_hi: int
+
+
+TEXT_WORKLOADS: Dict[str, TextWorkload] = {
+    # small backbone for whole-batch parity checks
+    "tiny_text": TextWorkload(name="tiny_text", S=6, vocab=1000, hidden=128, heads=4, ffn=256,
+                              layers=2, window=64, stride=32, d=64, len_lo=0, len_hi=200),
+    # CodeBERT (RoBERTa-base) backbone, 512-token windows with half overlap,
+    # 32 programs of 256..2048 tokens, projected to the 256-d latent
+    "codebert": TextWorkload(name="codebert", S=32, vocab=50265, hidden=768, heads=12, ffn=3072,
+                             layers=12, window=512, stride=256, d=256, len_lo=256, len_hi=2048),
+}
+
+TEXT_WEIGHT_ORDER = ("tok_emb", "pos_emb", "ln0_g", "ln0_b", "wqkv", "bqkv", "wo", "bo", "ln1_g",
+                     "ln1_b", "w1", "b1", "w2", "b2", "ln2_g", "ln2_b", "wp", "bp")
+
+
+def make_text_weights(w: TextWorkload, seed: int) -> Dict[str, np.ndarray]:
+    """Random encoder weights, float32: matrices, embeddings and biases
+    N(0, 0.02^2) (the usual initialisation of this backbone family), LayerNorm
+    gains 1 + N(0, 0.02^2) and shifts N(0, 0.02^2); the projection head
+    N(0, 1/hidden).  Layers are stacked on a leading axis."""
+    rng = np.random.default_rng(seed)
+    H, F, L = w.hidden, w.ffn, w.layers
+    shapes = {
+        "tok_emb": (w.vocab, H), "pos_emb": (w.window, H), "ln0_g": (H,), "ln0_b": (H,),
+        "wqkv": (L, 3 * H, H), "bqkv": (L, 3 * H), "wo": (L, H, H), "bo": (L, H),
+        "ln1_g": (L, H), "ln1_b": (L, H), "w1": (L, F, H), "b1": (L, F), "w2": (L, H, F),
+        "b2": (L, H), "ln2_g": (L, H), "ln2_b": (L, H), "wp": (w.d, H), "bp": (w.d,),
+    }
+    out = {}
+    for k in TEXT_WEIGHT_ORDER:
+        std = 1.0 / np.sqrt(H) if k in ("wp", "bp") else 0.02
+        a = rng.standard_normal(shapes[k], dtype=np.float32) * np.float32(std)
+        if k.endswith("_g"):
+            a += np.float32(1.0)
+        out[k] = a
+    return out
+
+
+def make_programs(w: TextWorkload, seed: int):
+    """S programs of token ids (int32, uniform over the vocabulary) with
+    lengths uniform in [len_lo, len_hi]; returns (tokens [N_total],
+    tok_off [S+1])."""
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(w.len_lo, w.len_hi + 1, size=w.S)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    tokens = rng.integers(0, w.vocab, size=int(off[-1])).astype(np.int32)
+    return tokens, off
