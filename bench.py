@@ -8,6 +8,7 @@ CPU oracle's throughput on a bounded sample of the same workload.
 
   python bench.py [--workload ansor_round] [--precision bf16] [--steps K] [--warmup W]
   python bench.py --loss [...]     (rollout loss + gradients instead)
+  python bench.py --encoder [...]  (chunked transformer state encoder instead)
 """
 from __future__ import annotations
 
@@ -253,6 +254,103 @@ def run_loss_bench(args, w, prec):
     print(json.dumps(res), flush=True)
 
 
+def run_text_bench(args, prec):
+    """One step = one wm_encode_text call over a batch of programs."""
+    import torch
+    import paper_2606_09312_amd as wm
+    from oracle import text_encoder as TE  # noqa: F401  (cpu baseline below)
+    w = synth.TEXT_WORKLOADS[args.text_workload]
+    dev = torch.device("cuda:0")
+    W = synth.make_text_weights(w, 500)
+    tokens, off = synth.make_programs(w, 600)
+    model = wm.TextModel(w, W, precision=prec)
+    t = torch.from_numpy(tokens).to(dev)
+    ws = model.workspace(off, device=dev)
+    z0 = torch.empty((w.S, w.d), dtype=torch.float32, device=dev)
+    n_chunks = model.chunks(off)
+
+    def step():
+        wm.encode_text(model, t, off, z0=z0, ws=ws)
+
+    for _ in range(args.warmup):
+        step()
+    wm.device_status(ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    wm.device_status(ws)
+    step_ms = step_percentiles(torch, step, args.steps)
+    wm.timing_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    kern = {}
+    for name in ("text_gemm", "text_attn", "text_other"):
+        ms, n = wm.timing_read(name)
+        if n:
+            kern[name] = {"total_ms": ms / args.steps, "launches": n // args.steps}
+    wm.timing_enable(False)
+    # algorithmic work: token positions of the chunks (padding excluded)
+    chunk_tokens = 0
+    for s in range(w.S):
+        n = int(off[s + 1] - off[s])
+        chunk_tokens += sum(b - a for a, b in TE.chunk_bounds(n, w.window, w.stride)) if n else 0
+    H, F = w.hidden, w.ffn
+    dense_flops = 2 * chunk_tokens * (3 * H * H + H * H + 2 * H * F) * w.layers
+    gemm_s = kern["text_gemm"]["total_ms"] / 1e3
+    achieved = dense_flops / gemm_s / 1e12
+    peak = PEAK_TFLOPS[prec]
+    res = {
+        "metric": "programs encoded/sec (chunked transformer state encoder)",
+        "value": w.S * args.steps / elapsed,
+        "unit": "programs/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": prec, "data": "synthetic",
+        "config": {"workload": f"{w.name}: S={w.S} programs, {int(off[-1])} tokens, {n_chunks} chunks "
+                               f"of {w.window} (stride {w.stride}), {w.layers} layers, hidden {H}, "
+                               f"{w.heads} heads, ffn {F}, d={w.d}", "precision": prec,
+                   "global_batch": w.S, "parallelism": "single GPU"},
+        "tokens_per_s": int(off[-1]) * args.steps / elapsed,
+        "roofline": {"bound": "mfma", "kernel": "text_gemm (dense products, all launches of a step)",
+                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": None, "flop_per_launch": dense_flops},
+        "kernels_ms_per_step": {k: v["total_ms"] for k, v in kern.items()},
+        "step_ms": step_ms,
+    }
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline_text(w, W, tokens, off, prec, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline_text(w, W, tokens, off, prec, budget_s: float):
+    """Oracle throughput of the encoder, one program at a time until the budget."""
+    from oracle import text_encoder as TE
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    Wd = TE.prepare(W, prec)
+    done, total_t, toks = 0, 0.0, 0
+    for s in range(w.S):
+        ids = tokens[off[s]:off[s + 1]]
+        t0 = time.perf_counter()
+        TE.encode_program(Wd, ids, w.window, w.stride, w.heads, prec)
+        total_t += time.perf_counter() - t0
+        done += 1
+        toks += len(ids)
+        if total_t >= budget_s:
+            break
+    return {"value": done / total_t, "unit": "programs/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"the first {done} programs of the batch ({toks} tokens; float64 NumPy oracle, "
+                      f"{total_t:.1f} s)"}
+
+
 def main():
     global PREC
     ap = argparse.ArgumentParser()
@@ -271,6 +369,9 @@ def main():
                     help="time the rollout loss with gradients (training the transition) "
                          "instead of the evaluator")
     ap.add_argument("--n-neg", type=int, default=4, help="negatives per step (--loss)")
+    ap.add_argument("--encoder", action="store_true",
+                    help="time the chunked transformer state encoder instead of the evaluator")
+    ap.add_argument("--text-workload", default="codebert", choices=sorted(synth.TEXT_WORKLOADS))
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -281,6 +382,9 @@ def main():
                           "(the batch would shard by candidates across GPUs with one small "
                           "top-k exchange, which is not built)"}))
         sys.exit(2)
+    if args.encoder:
+        run_text_bench(args, args.precision or "bf16")
+        return
     w = synth.workload(args.workload)
     prec = args.precision or w.precisions[-1]
     PREC = prec

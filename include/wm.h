@@ -294,6 +294,72 @@ wm_status wm_rollout_loss(const wm_model* model, const float* z0, const int32_t*
                           int32_t n_neg, float lam, float gamma, float* loss, float* total,
                           const wm_grads* grads, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Chunked transformer state encoder (the paper's E, Sec. 3.3) --------
+ * E maps a program's token sequence to its initial latent: the tokens are cut
+ * into overlapping chunks by a sliding window (window W, stride Sd: chunk c
+ * holds tokens [c Sd, min(c Sd + W, N)); 1 + ceil((N - W) / Sd) chunks when
+ * N > W, one when 0 < N <= W, none when N = 0), every chunk is encoded on its
+ * own by a post-LayerNorm transformer backbone (the CodeBERT / RoBERTa
+ * shape), each chunk's outputs are mean-pooled over its tokens, a program's
+ * chunk vectors are averaged (zero for an empty program) and projected:
+ *
+ *   h = LN(tok_emb[id] + pos_emb[p])              p = position in the chunk
+ *   per layer: [q k v] = h Wqkv^T + bqkv;  per head o = softmax(q k^T / sqrt(dh)) v
+ *              h = LN(h + o Wo^T + bo);  h = LN(h + GELU(h W1^T + b1) W2^T + b2)
+ *   z = Wp mean_c(mean_p h) + bp
+ *
+ * LN(x) = (x - mean) / sqrt(var + 1e-5) * gamma + beta.  In WM_BF16 the weight
+ * matrices and every activation entering a matrix product are rounded to
+ * bfloat16 (float32 accumulation); embeddings, biases, LayerNorm, softmax,
+ * residual sums and pooling stay float32. */
+#define WM_TEXT_MAX_PROGRAMS 256   /* programs per call */
+
+/* vocab, hidden width, heads (hidden / heads = head width), feed-forward
+ * width, layers, window, stride, latent width d, precision (wm_precision).
+ * Supported: hidden, ffn, window and the head width multiples of 32,
+ * hidden <= 1024, window <= 1024, 1 <= stride <= window. */
+typedef struct wm_text_dims {
+  int32_t vocab, hidden, heads, ffn, layers, window, stride, d, precision;
+} wm_text_dims;
+
+/* HOST float32, PyTorch layouts, layers stacked on the leading axis:
+ * tok_emb [vocab][hidden], pos_emb [window][hidden], ln0_g/ln0_b [hidden],
+ * wqkv [L][3 hidden][hidden] (rows q, k, v), bqkv [L][3 hidden],
+ * wo [L][hidden][hidden], bo [L][hidden], ln1_g/ln1_b [L][hidden],
+ * w1 [L][ffn][hidden], b1 [L][ffn], w2 [L][hidden][ffn], b2 [L][hidden],
+ * ln2_g/ln2_b [L][hidden], wp [d][hidden], bp [d]. */
+typedef struct wm_text_weights {
+  const float *tok_emb, *pos_emb, *ln0_g, *ln0_b;
+  const float *wqkv, *bqkv, *wo, *bo, *ln1_g, *ln1_b, *w1, *b1, *w2, *b2, *ln2_g, *ln2_b;
+  const float *wp, *bp;
+} wm_text_weights;
+
+typedef struct wm_text_model wm_text_model;
+
+/* Copy the encoder to the current device (matrices rounded to bfloat16 in
+ * WM_BF16).  Synchronous.  Errors: INVALID_ARGUMENT, UNSUPPORTED,
+ * OUT_OF_MEMORY, DEVICE. */
+wm_status wm_text_model_create(const wm_text_dims* dims, const wm_text_weights* weights,
+                               wm_text_model** out);
+void wm_text_model_destroy(wm_text_model* model);
+
+/* Total chunks of S programs given HOST token offsets tok_off [S+1]
+ * (0 = tok_off[0] <= ... ); -1 on a bad argument. */
+int32_t wm_text_chunks(const wm_text_model* model, const int32_t* tok_off, int32_t S);
+
+/* Workspace bytes of wm_encode_text for a batch of n_chunks chunks (caller
+ * allocated, 256-byte aligned, zeroed once; same error-word rules as
+ * wm_workspace_bytes).  About 4 (6 hidden + ffn + heads window) bytes per
+ * chunk position. */
+size_t wm_text_workspace_bytes(const wm_text_model* model, int32_t n_chunks);
+
+/* z0 [S][d] float32 out, from the concatenated token ids tokens [tok_off[S]]
+ * int32 (device) of S programs, tok_off HOST [S+1], 1 <= S <= 256.  A token
+ * id outside [0, vocab) sets the device error word (read it with
+ * wm_device_status).  The result can feed wm_evaluate as its z0. */
+wm_status wm_encode_text(const wm_text_model* model, const int32_t* tokens, const int32_t* tok_off,
+                         int32_t S, float* z0, void* ws, size_t ws_bytes, void* stream);
+
 /* Synchronise `stream`, read and clear the workspace's device error word.
  * Returns WM_OK, or WM_ERR_INPUT_RANGE with wm_last_error() naming the
  * violation(s); WM_ERR_DEVICE if the stream reports a failure. */
@@ -306,7 +372,8 @@ const char* wm_last_error(void);
  * launch of one kernel family (for benchmarks).  Ids: 0 rollout, 1 score,
  * 2 top-k, 3 bucketing, 4 action features, 5 encoder, 6 structured action
  * features, 7 tree-ensemble scores, 8 loss forward steps, 9 step losses,
- * 10 loss backward steps, 11 weight-gradient sums.  Enabling resets the
+ * 10 loss backward steps, 11 weight-gradient sums, 12 encoder dense
+ * products, 13 encoder attention, 14 other encoder kernels.  Enabling resets the
  * counters; reading synchronises on the recorded events.  At most 8192
  * launches per kernel are recorded while enabled. */
 wm_status wm_timing_enable(int32_t on);

@@ -23,7 +23,7 @@ PRECISIONS = {"fp32": WM_FP32, "bf16": WM_BF16}
 NORMS = {"none": WM_NORM_NONE, "l2": WM_NORM_L2}
 KERNELS = {"rollout": 0, "score": 1, "topk": 2, "bucket": 3, "phi": 4, "encode": 5,
            "phi_struct": 6, "trees": 7, "loss_fwd": 8, "loss_steps": 9, "loss_bwd": 10,
-           "loss_grads": 11}
+           "loss_grads": 11, "text_gemm": 12, "text_attn": 13, "text_other": 14}
 
 # Exported symbols (kept in step with include/wm.h).
 SYMBOLS = (
@@ -31,7 +31,8 @@ SYMBOLS = (
     "wm_rollout", "wm_score", "wm_topk", "wm_evaluate", "wm_device_status",
     "wm_last_error", "wm_timing_enable", "wm_timing_read", "wm_forest_create",
     "wm_forest_destroy", "wm_phi_struct", "wm_score_trees", "wm_evaluate_trees",
-    "wm_loss_workspace_bytes", "wm_rollout_loss",
+    "wm_loss_workspace_bytes", "wm_rollout_loss", "wm_text_model_create", "wm_text_model_destroy",
+    "wm_text_chunks", "wm_text_workspace_bytes", "wm_encode_text",
 )
 
 
@@ -67,6 +68,19 @@ class Grads(ctypes.Structure):
 
 
 GRAD_KEYS = ("w1", "b1", "w2", "b2", "type_emb", "param_w", "param_b")
+
+
+class TextDims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "vocab", "hidden", "heads", "ffn", "layers", "window", "stride", "d", "precision")]
+
+
+TEXT_WEIGHT_KEYS = ("tok_emb", "pos_emb", "ln0_g", "ln0_b", "wqkv", "bqkv", "wo", "bo", "ln1_g",
+                    "ln1_b", "w1", "b1", "w2", "b2", "ln2_g", "ln2_b", "wp", "bp")
+
+
+class TextWeights(ctypes.Structure):
+    _fields_ = [(n, _FP) for n in TEXT_WEIGHT_KEYS]
 
 _lib = None
 
@@ -125,6 +139,17 @@ def load_library(path: str = LIB_PATH):
                                     ctypes.c_float, ctypes.c_float, vp, vp, ctypes.POINTER(Grads),
                                     vp, sz, vp]
     lib.wm_rollout_loss.restype = i32
+    lib.wm_text_model_create.argtypes = [ctypes.POINTER(TextDims), ctypes.POINTER(TextWeights),
+                                         ctypes.POINTER(vp)]
+    lib.wm_text_model_create.restype = i32
+    lib.wm_text_model_destroy.argtypes = [vp]
+    lib.wm_text_model_destroy.restype = None
+    lib.wm_text_chunks.argtypes = [vp, vp, i32]
+    lib.wm_text_chunks.restype = i32
+    lib.wm_text_workspace_bytes.argtypes = [vp, i32]
+    lib.wm_text_workspace_bytes.restype = sz
+    lib.wm_encode_text.argtypes = [vp, vp, vp, i32, vp, vp, sz, vp]
+    lib.wm_encode_text.restype = i32
     _lib = lib
     return lib
 
@@ -353,6 +378,62 @@ def rollout_loss(model: Model, z0, seg_off, types, params, lens, targets, negati
         float(lam), float(gamma), _ptr(loss), _ptr(total), gp, _ptr(ws), ws.numel(),
         _stream(stream)))
     return res
+
+
+class TextModel:
+    """Device copy of the chunked transformer state encoder (wm_text_model_create)."""
+
+    def __init__(self, w, weights: Dict[str, np.ndarray], precision: str = "bf16"):
+        """w: object with vocab, hidden, heads, ffn, layers, window, stride, d."""
+        lib = load_library()
+        self.w = w
+        self.precision = precision
+        d = TextDims(vocab=w.vocab, hidden=w.hidden, heads=w.heads, ffn=w.ffn, layers=w.layers,
+                     window=w.window, stride=w.stride, d=w.d, precision=PRECISIONS[precision])
+        self._keep = {k: np.ascontiguousarray(weights[k], dtype=np.float32) for k in TEXT_WEIGHT_KEYS}
+        tw = TextWeights(**{k: self._keep[k].ctypes.data_as(_FP) for k in TEXT_WEIGHT_KEYS})
+        h = ctypes.c_void_p()
+        _check(lib.wm_text_model_create(ctypes.byref(d), ctypes.byref(tw), ctypes.byref(h)))
+        self.handle = h
+        self._keep = None           # copied to the device
+
+    def close(self):
+        if getattr(self, "handle", None):
+            load_library().wm_text_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def chunks(self, tok_off) -> int:
+        off, offp = _host_i32(tok_off)
+        n = int(load_library().wm_text_chunks(self.handle, offp, len(off) - 1))
+        if n < 0:
+            raise WMError(WM_ERR_INVALID_ARGUMENT, "bad tok_off")
+        return n
+
+    def workspace(self, tok_off, device="cuda"):
+        import torch
+        n = int(load_library().wm_text_workspace_bytes(self.handle, self.chunks(tok_off)))
+        return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def encode_text(model: TextModel, tokens, tok_off, z0=None, ws=None, stream=None):
+    """z0 [S][d] from concatenated token ids (device int32) and HOST tok_off [S+1]."""
+    import torch
+    off, offp = _host_i32(tok_off)
+    S = len(off) - 1
+    dev = tokens.device
+    if z0 is None:
+        z0 = torch.empty((S, model.w.d), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = model.workspace(off, device=dev)
+    _check(load_library().wm_encode_text(model.handle, _ptr(tokens), offp, S, _ptr(z0), _ptr(ws),
+                                         ws.numel(), _stream(stream)))
+    return {"z0": z0, "ws": ws}
 
 
 def device_status(ws, stream=None) -> int:

@@ -308,6 +308,8 @@ void timing_end(int k, hipStream_t st) {
   (void)hipEventRecord(g_timing.stop[k][i], st);
   g_timing.count[k] = i + 1;
 }
+wm_status set_error(wm_status st, const std::string& msg) { return fail(st, msg); }
+wm_status clear_error() { return ok(); }
 }  // namespace wm
 
 #define WM_TIMED(K, ST, CALL)                                              \
@@ -797,6 +799,7 @@ wm_status wm_device_status(void* ws, size_t ws_bytes, void* stream) {
   if (word & ERRBIT_LEN) msg += " a length outside [0, T_max];";
   if (word & ERRBIT_TYPE) msg += " an action type outside [0, n_kinds);";
   if (word & ERRBIT_PARAM) msg += " an action parameter < 1;";
+  if (word & ERRBIT_TOKEN) msg += " a token id outside [0, vocab);";
   return fail(WM_ERR_INPUT_RANGE, msg);
 }
 

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
 #include "../../include/wm.h"
 
 namespace wm {
@@ -177,7 +179,7 @@ inline int bucket_groups(int B) {
 }
 
 // Device error bits (workspace error word).
-enum : int { ERRBIT_LEN = 1, ERRBIT_TYPE = 2, ERRBIT_PARAM = 4 };
+enum : int { ERRBIT_LEN = 1, ERRBIT_TYPE = 2, ERRBIT_PARAM = 4, ERRBIT_TOKEN = 8 };
 
 struct SegTable {
   int32_t n;                              // S
@@ -299,8 +301,13 @@ int rollout_lds_bytes(const DevModel& m);
 // Kernel-family timing hooks (wm_api.hip).
 enum TimedKernel { TK_ROLLOUT = 0, TK_SCORE = 1, TK_TOPK = 2, TK_BUCKET = 3, TK_PHI = 4, TK_ENCODE = 5,
                    TK_PHI_STRUCT = 6, TK_TREES = 7, TK_TRAIN_FWD = 8, TK_LOSS = 9,
-                   TK_TRAIN_BWD = 10, TK_GRADS = 11, TK_COUNT = 12 };
+                   TK_TRAIN_BWD = 10, TK_GRADS = 11, TK_TEXT_GEMM = 12, TK_TEXT_ATTN = 13,
+                   TK_TEXT_OTHER = 14, TK_COUNT = 15 };
 void timing_begin(int kernel, hipStream_t st);
 void timing_end(int kernel, hipStream_t st);
+
+// Thread-local last-error message of the C ABI (wm_api.hip).
+wm_status set_error(wm_status st, const std::string& msg);
+wm_status clear_error();
 
 }  // namespace wm
