@@ -372,6 +372,139 @@ __global__ __launch_bounds__(256) void softmax_kernel(float* __restrict__ s, con
   }
 }
 
+// Fused attention of one (chunk, head) per workgroup, bf16: wavefront w
+// takes queries [32 w, 32 w + 32).  K and V of the chunk are staged in LDS
+// once (K row-major, V transposed with its keys permuted into accumulator
+// order); the scores are computed transposed, S^T = K . Q^T, so a query is a
+// lane's column and its softmax statistics are per-lane sums completed across
+// the lane pair (L, L^32).  Pass 1 forms the row maximum and sum online over
+// 32-key blocks; pass 2 recomputes the scores, normalises them (the
+// probabilities exactly as defined, rounded as product operands) and
+// accumulates O^T = V^T . P with P straight from the accumulators (its key
+// order is the one V was permuted into).
+template <int DH>
+__global__ __launch_bounds__(1024) void attention_kernel(const float* __restrict__ qkv,
+                                                         float* __restrict__ ctx, const TTable tt,
+                                                         int window, int stride, int heads, int H,
+                                                         float scale) {
+  constexpr int KS = DH / 16;                 // 16-deep steps over the head width
+  constexpr int DB = DH / 32;                 // 32-row blocks of the head width
+  constexpr int KW = DH + 8;                  // padded K row (bf16)
+  extern __shared__ __attribute__((aligned(16))) __bf16 lds_att[];
+  const int VW = window + 8;                  // padded V^T row (bf16)
+  __bf16* Ks = lds_att;                       // [window][KW]
+  __bf16* Vt = lds_att + (size_t)window * KW; // [DH][VW]
+  const int c = blockIdx.x / heads, head = blockIdx.x % heads;
+  int first, len;
+  chunk_span(tt, c, window, stride, first, len);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nt = blockDim.x;
+  const int cl = lane & 31, h = lane >> 5;
+  const float* base = qkv + (size_t)c * window * 3 * H + head * DH;
+  const int nkb = (len + 31) / 32;
+
+  // stage K (row-major) and V (transposed, keys in accumulator order per block)
+  for (int u = tid; u < nkb * 32 * (DH / 4); u += nt) {
+    const int key = u / (DH / 4), d4 = (u % (DH / 4)) * 4;
+    f32x4 kv = {0.0f, 0.0f, 0.0f, 0.0f}, vv = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (key < len) {
+      kv = *reinterpret_cast<const f32x4*>(base + (size_t)key * 3 * H + H + d4);
+      vv = *reinterpret_cast<const f32x4*>(base + (size_t)key * 3 * H + 2 * H + d4);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) Ks[key * KW + d4 + i] = (__bf16)kv[i];
+    // key = 32 kb + acc_row(hh, 8 f + j)  ->  position 32 kb + 16 f + 8 hh + j
+    const int kb = key >> 5, kr = key & 31;
+    const int hh = (kr >> 2) & 1, rr = ((kr >> 3) << 2) | (kr & 3);
+    const int pos = kb * 32 + (rr >> 3) * 16 + hh * 8 + (rr & 7);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) Vt[(d4 + i) * VW + pos] = (__bf16)vv[i];
+  }
+  // this wavefront's queries as B operands: Q[q][16 kk + 8 h + j]
+  const int q = wave * 32 + cl;
+  bf16x8 qf[KS];
+  {
+    const float* qrow = base + (size_t)min(q, window - 1) * 3 * H;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const f32x4 a = *reinterpret_cast<const f32x4*>(qrow + 16 * kk + 8 * h);
+      const f32x4 b = *reinterpret_cast<const f32x4*>(qrow + 16 * kk + 8 * h + 4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        qf[kk][i] = (__bf16)a[i];
+        qf[kk][4 + i] = (__bf16)b[i];
+      }
+    }
+  }
+  __syncthreads();
+  if (wave * 32 >= len) return;               // no valid query in this wavefront
+
+  auto scores = [&](int kb) -> f32x16 {
+    f32x16 sacc = {};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const bf16x8 kfrag = *reinterpret_cast<const bf16x8*>(Ks + (kb * 32 + cl) * KW + 16 * kk + 8 * h);
+      sacc = BF::mfma(kfrag, qf[kk], sacc);
+    }
+    return sacc;
+  };
+  // pass 1: running maximum and sum of exp over the valid keys
+  float mx = -INFINITY, sum = 0.0f;
+  for (int kb = 0; kb < nkb; ++kb) {
+    const f32x16 sacc = scores(kb);
+    float bm = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (kb * 32 + acc_row(h, r) < len) bm = fmaxf(bm, sacc[r] * scale);
+    const float nm = fmaxf(mx, bm);
+    float bs = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (kb * 32 + acc_row(h, r) < len) bs += __expf(sacc[r] * scale - nm);
+    sum = (mx == -INFINITY ? 0.0f : sum * __expf(mx - nm)) + bs;
+    mx = nm;
+  }
+  {
+    const float mo = __shfl_xor(mx, 32), so = __shfl_xor(sum, 32);
+    const float m2 = fmaxf(mx, mo);
+    sum = (mx == -INFINITY ? 0.0f : sum * __expf(mx - m2)) + (mo == -INFINITY ? 0.0f : so * __expf(mo - m2));
+    mx = m2;
+  }
+  const float inv = 1.0f / sum;
+  // pass 2: probabilities and O^T = V^T . P
+  f32x16 oacc[DB];
+#pragma unroll
+  for (int b = 0; b < DB; ++b) oacc[b] = f32x16{};
+  for (int kb = 0; kb < nkb; ++kb) {
+    const f32x16 sacc = scores(kb);
+    bf16x8 pf[2];
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int r = 8 * f + j;
+        const float pv = kb * 32 + acc_row(h, r) < len ? __expf(sacc[r] * scale - mx) * inv : 0.0f;
+        pf[f][j] = (__bf16)pv;
+      }
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int f = 0; f < 2; ++f) {
+        const bf16x8 vfrag = *reinterpret_cast<const bf16x8*>(Vt + (b * 32 + cl) * VW + kb * 32 + 16 * f + 8 * h);
+        oacc[b] = BF::mfma(vfrag, pf[f], oacc[b]);
+      }
+  }
+  if (q < window) {
+    float* orow = ctx + ((size_t)c * window + q) * H + head * DH;
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const f32x4 v = {oacc[b][4 * r4], oacc[b][4 * r4 + 1], oacc[b][4 * r4 + 2], oacc[b][4 * r4 + 3]};
+        *reinterpret_cast<f32x4*>(orow + 32 * b + acc_row(h, 4 * r4)) = v;
+      }
+  }
+}
+
 // Mean of each chunk's rows over its tokens.  One workgroup per chunk.
 __global__ __launch_bounds__(256) void pool_kernel(const float* __restrict__ h, const TTable tt,
                                                    int window, int stride, int H,
@@ -595,6 +728,8 @@ wm_status wm_encode_text(const wm_text_model* m, const int32_t* tokens, const in
   const int H = d.hidden, F = d.ffn, W = d.window, nh = d.heads, dh = H / nh;
   const int rows = n_chunks * W;
   const bool bf = d.precision == WM_BF16;
+  // fused attention: bf16, head width 32 or 64, K and V of a window in LDS
+  const bool fused = bf && (dh == 32 || dh == 64) && W <= 512;
   auto gemm = [&](const GemmArgs& g, int batch, bool bt) {
     return bf ? launch_gemm<BF>(g, batch, bt, st) : launch_gemm<FP>(g, batch, bt, st);
   };
@@ -615,6 +750,17 @@ wm_status wm_encode_text(const wm_text_model* m, const int32_t* tokens, const in
       // q, k, v
       WM_TT(TK_TEXT_GEMM, gemm(dense(h, rows, H, m->wqkv + lH * 3 * H, 3 * H, qkv, m->bqkv + 3 * lH,
                                      nullptr, 0), 1, false));
+      if (fused) {               // bf16: one fused kernel per (chunk, head)
+        const int lds = (W * (dh + 8) + dh * (W + 8)) * 2;
+        auto kern = dh == 64 ? attention_kernel<64> : attention_kernel<32>;
+        WM_TT(TK_TEXT_ATTN, [&]() {
+          hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+          if (e != hipSuccess) { (void)hipGetLastError(); return e; }
+          hipLaunchKernelGGL(kern, dim3(n_chunks * nh), dim3(64 * (W / 32)), lds, st, qkv, ctx, tt, W,
+                             d.stride, nh, H, 1.0f / std::sqrt((float)dh));
+          return hipGetLastError();
+        }());
+      } else {
       // scores per (chunk, head): q k^T / sqrt(dh)
       GemmArgs s{};
       s.A = qkv; s.B = qkv + H; s.C = sc; s.M = W; s.N = W; s.K = dh;
@@ -635,6 +781,7 @@ wm_status wm_encode_text(const wm_text_model* m, const int32_t* tokens, const in
       pv.sC1 = (long long)W * H; pv.sC2 = dh;
       pv.alpha = 1.0f;
       WM_TT(TK_TEXT_ATTN, gemm(pv, n_chunks * nh, true));
+      }
       // h = LN(h + ctx Wo^T + bo)
       WM_TT(TK_TEXT_GEMM, gemm(dense(ctx, rows, H, m->wo + lH * H, H, y, m->bo + lH, h, 0), 1, false));
       WM_TT(TK_TEXT_OTHER, [&]() { hipLaunchKernelGGL(ln_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, y,
