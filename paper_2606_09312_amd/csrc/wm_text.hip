@@ -30,6 +30,7 @@ struct wm_text_model {
   const float *tok_emb, *pos_emb, *ln0_g, *ln0_b;
   const float *wqkv, *bqkv, *wo, *bo, *ln1_g, *ln1_b, *w1, *b1, *w2, *b2, *ln2_g, *ln2_b;
   const float *wp, *bp;
+  const __bf16 *wqkv16, *wo16, *w116, *w216;   // WM_BF16: the layer matrices as bf16
 };
 
 namespace wm {
@@ -119,7 +120,7 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int32_t* __restrict
                                                        const float* __restrict__ g,
                                                        const float* __restrict__ b, int H, int vocab,
                                                        int rows, float* __restrict__ h,
-                                                       int32_t* err) {
+                                                       __bf16* __restrict__ hb, int32_t* err) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= rows) return;
@@ -128,7 +129,10 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int32_t* __restrict
   chunk_span(tt, c, window, stride, first, len);
   float* out = h + (size_t)r * H;
   if (p >= len) {
-    for (int f = lane; f < H; f += 64) out[f] = 0.0f;
+    for (int f = lane; f < H; f += 64) {
+      out[f] = 0.0f;
+      if (hb) hb[(size_t)r * H + f] = (__bf16)0.0f;
+    }
     return;
   }
   int id = tokens[first + p];
@@ -155,7 +159,11 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int32_t* __restrict
 #pragma unroll
   for (int i = 0; i < LN_MAX_PER_LANE; ++i) {
     const int f = lane + 64 * i;
-    if (f < H) out[f] = (x[i] - mean) * rs * g[f] + b[f];
+    if (f < H) {
+      const float o = (x[i] - mean) * rs * g[f] + b[f];
+      out[f] = o;
+      if (hb) hb[(size_t)r * H + f] = (__bf16)o;
+    }
   }
 }
 
@@ -163,7 +171,7 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int32_t* __restrict
 __global__ __launch_bounds__(256) void ln_kernel(const float* __restrict__ y,
                                                  const float* __restrict__ g,
                                                  const float* __restrict__ b, int H, int rows,
-                                                 float* __restrict__ h) {
+                                                 float* __restrict__ h, __bf16* __restrict__ hb) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= rows) return;
@@ -188,7 +196,11 @@ __global__ __launch_bounds__(256) void ln_kernel(const float* __restrict__ y,
 #pragma unroll
   for (int i = 0; i < LN_MAX_PER_LANE; ++i) {
     const int f = lane + 64 * i;
-    if (f < H) out[f] = (x[i] - mean) * rs * g[f] + b[f];
+    if (f < H) {
+      const float o = (x[i] - mean) * rs * g[f] + b[f];
+      out[f] = o;
+      if (hb) hb[(size_t)r * H + f] = (__bf16)o;
+    }
   }
 }
 
@@ -336,6 +348,97 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs g) {
     }
 }
 
+// bf16 dense product with operands stored as bf16 (the product-operand
+// values themselves):  C = epi(A . W^T), A [M][K] and W [N][K] row-major,
+// epilogue + bias[n], GELU, + residual R[m][n] (fp32), C fp32 or bf16.
+// Workgroup = 8 wavefronts on a 256 x 128 tile (each 64 x 64, 2 x 2
+// matrix-core tiles); 32-deep stages, 16-byte loads straight into LDS rows
+// (contraction contiguous), the next stage's loads in flight meanwhile.
+struct Gemm16Args {
+  const __bf16* A;
+  const __bf16* W;
+  void* C;
+  const float* bias;
+  const float* res;
+  int M, N, K, tiles_n, gelu;
+};
+constexpr int G16_BM = 256, G16_BN = 128, G16_LDW = GK + 8;
+
+template <bool OUT16>
+__global__ __launch_bounds__(512) void gemm16_kernel(const Gemm16Args g) {
+  __shared__ __attribute__((aligned(16))) __bf16 As[G16_BM * G16_LDW];
+  __shared__ __attribute__((aligned(16))) __bf16 Bs[G16_BN * G16_LDW];
+  const int m0 = (blockIdx.x / g.tiles_n) * G16_BM, n0 = (blockIdx.x % g.tiles_n) * G16_BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // A: 2 units of 8 bf16 per thread, B: 1 unit
+  bf16x8 ra[2], rb;
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int u = tid + 512 * i, row = u >> 2, q = u & 3;
+      ra[i] = m0 + row < g.M ? *reinterpret_cast<const bf16x8*>(g.A + (size_t)(m0 + row) * g.K + k0 + 8 * q)
+                             : bf16x8{};
+    }
+    const int row = tid >> 2, q = tid & 3;
+    rb = n0 + row < g.N ? *reinterpret_cast<const bf16x8*>(g.W + (size_t)(n0 + row) * g.K + k0 + 8 * q)
+                        : bf16x8{};
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int u = tid + 512 * i, row = u >> 2, q = u & 3;
+      *reinterpret_cast<bf16x8*>(As + row * G16_LDW + 8 * q) = ra[i];
+    }
+    const int row = tid >> 2, q = tid & 3;
+    *reinterpret_cast<bf16x8*>(Bs + row * G16_LDW + 8 * q) = rb;
+  };
+  const int wm = wave & 3, wn = wave >> 2;
+  const int cl = lane & 31, h = lane >> 5;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+  load(0);
+  for (int k0 = 0; k0 < g.K; k0 += GK) {
+    __syncthreads();
+    store();
+    __syncthreads();
+    if (k0 + GK < g.K) load(k0 + GK);
+#pragma unroll
+    for (int ks = 0; ks < GK / 16; ++ks) {
+      bf16x8 fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[i] = *reinterpret_cast<const bf16x8*>(As + (wm * 64 + i * 32 + cl) * G16_LDW + ks * 16 + h * 8);
+        fb[i] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + i * 32 + cl) * G16_LDW + ks * 16 + h * 8);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = BF::mfma(fa[i], fb[j], acc[i][j]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int n = n0 + wn * 64 + j * 32 + cl;
+      if (n >= g.N) continue;
+      const float bn = g.bias ? g.bias[n] : 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 64 + i * 32 + acc_row(h, r);
+        if (m >= g.M) continue;
+        float v = acc[i][j][r] + bn;
+        if (g.gelu) v = gelu(v);
+        if (g.res) v += g.res[(size_t)m * g.N + n];
+        if constexpr (OUT16) reinterpret_cast<__bf16*>(g.C)[(size_t)m * g.N + n] = (__bf16)v;
+        else reinterpret_cast<float*>(g.C)[(size_t)m * g.N + n] = v;
+      }
+    }
+}
+
 // Row softmax of the attention scores, keys past the chunk's tokens masked.
 // One wavefront per row (chunk c, head, query); in place.
 constexpr int SM_MAX_PER_LANE = 16;               // window <= 1024
@@ -383,8 +486,8 @@ __global__ __launch_bounds__(256) void softmax_kernel(float* __restrict__ s, con
 // accumulates O^T = V^T . P with P straight from the accumulators (its key
 // order is the one V was permuted into).
 template <int DH>
-__global__ __launch_bounds__(1024) void attention_kernel(const float* __restrict__ qkv,
-                                                         float* __restrict__ ctx, const TTable tt,
+__global__ __launch_bounds__(1024) void attention_kernel(const __bf16* __restrict__ qkv,
+                                                         __bf16* __restrict__ ctx, const TTable tt,
                                                          int window, int stride, int heads, int H,
                                                          float scale) {
   constexpr int KS = DH / 16;                 // 16-deep steps over the head width
@@ -399,41 +502,32 @@ __global__ __launch_bounds__(1024) void attention_kernel(const float* __restrict
   chunk_span(tt, c, window, stride, first, len);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nt = blockDim.x;
   const int cl = lane & 31, h = lane >> 5;
-  const float* base = qkv + (size_t)c * window * 3 * H + head * DH;
+  const __bf16* base = qkv + (size_t)c * window * 3 * H + head * DH;
   const int nkb = (len + 31) / 32;
 
   // stage K (row-major) and V (transposed, keys in accumulator order per block)
-  for (int u = tid; u < nkb * 32 * (DH / 4); u += nt) {
-    const int key = u / (DH / 4), d4 = (u % (DH / 4)) * 4;
-    f32x4 kv = {0.0f, 0.0f, 0.0f, 0.0f}, vv = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int u = tid; u < nkb * 32 * (DH / 8); u += nt) {
+    const int key = u / (DH / 8), d8 = (u % (DH / 8)) * 8;
+    bf16x8 kv = {}, vv = {};
     if (key < len) {
-      kv = *reinterpret_cast<const f32x4*>(base + (size_t)key * 3 * H + H + d4);
-      vv = *reinterpret_cast<const f32x4*>(base + (size_t)key * 3 * H + 2 * H + d4);
+      kv = *reinterpret_cast<const bf16x8*>(base + (size_t)key * 3 * H + H + d8);
+      vv = *reinterpret_cast<const bf16x8*>(base + (size_t)key * 3 * H + 2 * H + d8);
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) Ks[key * KW + d4 + i] = (__bf16)kv[i];
+    *reinterpret_cast<bf16x8*>(Ks + key * KW + d8) = kv;
     // key = 32 kb + acc_row(hh, 8 f + j)  ->  position 32 kb + 16 f + 8 hh + j
     const int kb = key >> 5, kr = key & 31;
     const int hh = (kr >> 2) & 1, rr = ((kr >> 3) << 2) | (kr & 3);
     const int pos = kb * 32 + (rr >> 3) * 16 + hh * 8 + (rr & 7);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) Vt[(d4 + i) * VW + pos] = (__bf16)vv[i];
+    for (int i = 0; i < 8; ++i) Vt[(d8 + i) * VW + pos] = vv[i];
   }
   // this wavefront's queries as B operands: Q[q][16 kk + 8 h + j]
   const int q = wave * 32 + cl;
   bf16x8 qf[KS];
   {
-    const float* qrow = base + (size_t)min(q, window - 1) * 3 * H;
+    const __bf16* qrow = base + (size_t)min(q, window - 1) * 3 * H;
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      const f32x4 a = *reinterpret_cast<const f32x4*>(qrow + 16 * kk + 8 * h);
-      const f32x4 b = *reinterpret_cast<const f32x4*>(qrow + 16 * kk + 8 * h + 4);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        qf[kk][i] = (__bf16)a[i];
-        qf[kk][4 + i] = (__bf16)b[i];
-      }
-    }
+    for (int kk = 0; kk < KS; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qrow + 16 * kk + 8 * h);
   }
   __syncthreads();
   if (wave * 32 >= len) return;               // no valid query in this wavefront
@@ -493,15 +587,12 @@ __global__ __launch_bounds__(1024) void attention_kernel(const float* __restrict
         oacc[b] = BF::mfma(vfrag, pf[f], oacc[b]);
       }
   }
-  if (q < window) {
-    float* orow = ctx + ((size_t)c * window + q) * H + head * DH;
+  if (q < window) {             // the output as the next product's operand
+    __bf16* orow = ctx + ((size_t)c * window + q) * H + head * DH;
 #pragma unroll
     for (int b = 0; b < DB; ++b)
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const f32x4 v = {oacc[b][4 * r4], oacc[b][4 * r4 + 1], oacc[b][4 * r4 + 2], oacc[b][4 * r4 + 3]};
-        *reinterpret_cast<f32x4*>(orow + 32 * b + acc_row(h, 4 * r4)) = v;
-      }
+      for (int r = 0; r < 16; ++r) orow[32 * b + acc_row(h, r)] = (__bf16)oacc[b][r];
   }
 }
 
@@ -560,22 +651,35 @@ int n_chunks_of(int n_tokens, int window, int stride) {
   return 1 + (n_tokens - window + stride - 1) / stride;
 }
 
+// bf16 with a fused-attention head width and window: operands stored as bf16
+bool bf16_path(const wm_text_dims& d) {
+  const int dh = d.hidden / d.heads;
+  return d.precision == WM_BF16 && (dh == 32 || dh == 64) && d.window <= 512;
+}
+
 struct TextLayout {
-  size_t err, h, qkv, sc, ctx, y, f, pooled, total;
+  size_t err, h, qkv, sc, ctx, y, f, pooled, hb, qkvb, ctxb, fb, total;
 };
 
 TextLayout text_layout(const wm_text_dims& dm, int n_chunks) {
   const size_t rows = (size_t)n_chunks * dm.window, H = dm.hidden;
+  const bool bf = bf16_path(dm);
   TextLayout L;
   size_t o = 0;
   L.err = o; o += 256;
   L.h = o; o = al256(o + rows * H * 4);
-  L.qkv = o; o = al256(o + rows * 3 * H * 4);
-  L.sc = o; o = al256(o + (size_t)n_chunks * dm.heads * dm.window * dm.window * 4);
-  L.ctx = o; o = al256(o + rows * H * 4);
+  L.qkv = o; o = al256(o + (bf ? 0 : rows * 3 * H * 4));
+  L.sc = o; o = al256(o + (bf ? 0 : (size_t)n_chunks * dm.heads * dm.window * dm.window * 4));
+  L.ctx = o; o = al256(o + (bf ? 0 : rows * H * 4));
   L.y = o; o = al256(o + rows * H * 4);
-  L.f = o; o = al256(o + rows * (size_t)dm.ffn * 4);
+  L.f = o; o = al256(o + (bf ? 0 : rows * (size_t)dm.ffn * 4));
   L.pooled = o; o = al256(o + (size_t)n_chunks * H * 4);
+  // bf16: the product operands (the fp32 qkv, scores, context and hidden
+  // buffers above are then unused and sized zero)
+  L.hb = o; o = al256(o + (bf ? rows * H * 2 : 0));
+  L.qkvb = o; o = al256(o + (bf ? rows * 3 * H * 2 : 0));
+  L.ctxb = o; o = al256(o + (bf ? rows * H * 2 : 0));
+  L.fb = o; o = al256(o + (bf ? rows * (size_t)dm.ffn * 2 : 0));
   L.total = o;
   return L;
 }
@@ -644,6 +748,11 @@ wm_status wm_text_model_create(const wm_text_dims* dims, const wm_text_weights* 
       {w->wp, (size_t)d.d * H, true, 0}, {w->bp, (size_t)d.d, false, 0}};
   size_t total = 0;
   for (auto& p : parts) { p.off = total; total = al256(total + p.n * 4); }
+  // bf16 copies of wqkv, wo, w1, w2 (parts 4, 6, 10, 12)
+  const int mats[4] = {4, 6, 10, 12};
+  size_t off16[4] = {0, 0, 0, 0};
+  if (bf)
+    for (int i = 0; i < 4; ++i) { off16[i] = total; total = al256(total + parts[mats[i]].n * 2); }
   void* dev = nullptr;
   if (hipMalloc(&dev, total) != hipSuccess) {
     (void)hipGetLastError();
@@ -661,6 +770,19 @@ wm_status wm_text_model_create(const wm_text_dims* dims, const wm_text_weights* 
       return set_error(WM_ERR_DEVICE, "hipMemcpy of the encoder weights failed");
     }
   }
+  if (bf) {
+    std::vector<__bf16> t16;
+    for (int i = 0; i < 4; ++i) {
+      const Part& p = parts[mats[i]];
+      if (p.n == 0) continue;
+      t16.resize(p.n);
+      for (size_t j = 0; j < p.n; ++j) t16[j] = (__bf16)p.src[j];
+      if (hipMemcpy(base + off16[i], t16.data(), p.n * 2, hipMemcpyHostToDevice) != hipSuccess) {
+        (void)hipFree(dev);
+        return set_error(WM_ERR_DEVICE, "hipMemcpy of the encoder weights failed");
+      }
+    }
+  }
   wm_text_model* m = new (std::nothrow) wm_text_model;
   if (!m) {
     (void)hipFree(dev);
@@ -672,6 +794,8 @@ wm_status wm_text_model_create(const wm_text_dims* dims, const wm_text_weights* 
                          &m->bo, &m->ln1_g, &m->ln1_b, &m->w1, &m->b1, &m->w2, &m->b2, &m->ln2_g,
                          &m->ln2_b, &m->wp, &m->bp};
   for (size_t i = 0; i < parts.size(); ++i) *dst[i] = reinterpret_cast<const float*>(base + parts[i].off);
+  const __bf16** dst16[] = {&m->wqkv16, &m->wo16, &m->w116, &m->w216};
+  for (int i = 0; i < 4; ++i) *dst16[i] = bf ? reinterpret_cast<const __bf16*>(base + off16[i]) : nullptr;
   *out = m;
   return clear_error();
 }
@@ -728,8 +852,9 @@ wm_status wm_encode_text(const wm_text_model* m, const int32_t* tokens, const in
   const int H = d.hidden, F = d.ffn, W = d.window, nh = d.heads, dh = H / nh;
   const int rows = n_chunks * W;
   const bool bf = d.precision == WM_BF16;
-  // fused attention: bf16, head width 32 or 64, K and V of a window in LDS
-  const bool fused = bf && (dh == 32 || dh == 64) && W <= 512;
+  // bf16 operand path: fused attention (head width 32 or 64, K and V of a
+  // window in LDS) and products on bf16-stored operands
+  const bool fused = bf16_path(d);
   auto gemm = [&](const GemmArgs& g, int batch, bool bt) {
     return bf ? launch_gemm<BF>(g, batch, bt, st) : launch_gemm<FP>(g, batch, bt, st);
   };
@@ -741,26 +866,55 @@ wm_status wm_encode_text(const wm_text_model* m, const int32_t* tokens, const in
     if (e_ != hipSuccess) return set_error(WM_ERR_DEVICE, std::string("kernel launch: ") + hipGetErrorString(e_)); \
   } while (0)
 
+  auto g16 = [&](const __bf16* A, int M, int K, const __bf16* Wm, int N, void* C, const float* bias,
+                 const float* res, int gelu, bool out16) {
+    Gemm16Args g;
+    g.A = A; g.W = Wm; g.C = C; g.bias = bias; g.res = res; g.M = M; g.N = N; g.K = K; g.gelu = gelu;
+    g.tiles_n = (N + G16_BN - 1) / G16_BN;
+    const dim3 grid(((M + G16_BM - 1) / G16_BM) * g.tiles_n);
+    if (out16) hipLaunchKernelGGL(gemm16_kernel<true>, grid, dim3(512), 0, st, g);
+    else hipLaunchKernelGGL(gemm16_kernel<false>, grid, dim3(512), 0, st, g);
+    return hipGetLastError();
+  };
+  auto ln = [&](const float* yin, const float* gm, const float* bt, __bf16* hbo) {
+    hipLaunchKernelGGL(ln_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, yin, gm, bt, H, rows, h, hbo);
+    return hipGetLastError();
+  };
+  __bf16* hb = reinterpret_cast<__bf16*>(w8 + L.hb);
+  __bf16* qkvb = reinterpret_cast<__bf16*>(w8 + L.qkvb);
+  __bf16* ctxb = reinterpret_cast<__bf16*>(w8 + L.ctxb);
+  __bf16* fb = reinterpret_cast<__bf16*>(w8 + L.fb);
+
   if (n_chunks > 0) {
     WM_TT(TK_TEXT_OTHER, [&]() { hipLaunchKernelGGL(embed_ln_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, tokens,
                                              tt, W, d.stride, m->tok_emb, m->pos_emb, m->ln0_g, m->ln0_b,
-                                             H, d.vocab, rows, h, err); return hipGetLastError(); }());
+                                             H, d.vocab, rows, h, fused ? hb : nullptr, err); return hipGetLastError(); }());
     for (int l = 0; l < d.layers; ++l) {
       const size_t lH = (size_t)l * H;
-      // q, k, v
-      WM_TT(TK_TEXT_GEMM, gemm(dense(h, rows, H, m->wqkv + lH * 3 * H, 3 * H, qkv, m->bqkv + 3 * lH,
-                                     nullptr, 0), 1, false));
-      if (fused) {               // bf16: one fused kernel per (chunk, head)
+      if (fused) {
+        // bf16: every product operand is stored as bf16
+        WM_TT(TK_TEXT_GEMM, g16(hb, rows, H, m->wqkv16 + lH * 3 * H, 3 * H, qkvb, m->bqkv + 3 * lH,
+                                nullptr, 0, true));
         const int lds = (W * (dh + 8) + dh * (W + 8)) * 2;
         auto kern = dh == 64 ? attention_kernel<64> : attention_kernel<32>;
         WM_TT(TK_TEXT_ATTN, [&]() {
           hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
           if (e != hipSuccess) { (void)hipGetLastError(); return e; }
-          hipLaunchKernelGGL(kern, dim3(n_chunks * nh), dim3(64 * (W / 32)), lds, st, qkv, ctx, tt, W,
+          hipLaunchKernelGGL(kern, dim3(n_chunks * nh), dim3(64 * (W / 32)), lds, st, qkvb, ctxb, tt, W,
                              d.stride, nh, H, 1.0f / std::sqrt((float)dh));
           return hipGetLastError();
         }());
-      } else {
+        WM_TT(TK_TEXT_GEMM, g16(ctxb, rows, H, m->wo16 + lH * H, H, y, m->bo + lH, h, 0, false));
+        WM_TT(TK_TEXT_OTHER, ln(y, m->ln1_g + lH, m->ln1_b + lH, hb));
+        WM_TT(TK_TEXT_GEMM, g16(hb, rows, H, m->w116 + (size_t)l * F * H, F, fb, m->b1 + (size_t)l * F,
+                                nullptr, 1, true));
+        WM_TT(TK_TEXT_GEMM, g16(fb, rows, F, m->w216 + (size_t)l * H * F, H, y, m->b2 + lH, h, 0, false));
+        WM_TT(TK_TEXT_OTHER, ln(y, m->ln2_g + lH, m->ln2_b + lH, hb));
+        continue;
+      }
+      // q, k, v
+      WM_TT(TK_TEXT_GEMM, gemm(dense(h, rows, H, m->wqkv + lH * 3 * H, 3 * H, qkv, m->bqkv + 3 * lH,
+                                     nullptr, 0), 1, false));
       // scores per (chunk, head): q k^T / sqrt(dh)
       GemmArgs s{};
       s.A = qkv; s.B = qkv + H; s.C = sc; s.M = W; s.N = W; s.K = dh;
@@ -781,17 +935,14 @@ wm_status wm_encode_text(const wm_text_model* m, const int32_t* tokens, const in
       pv.sC1 = (long long)W * H; pv.sC2 = dh;
       pv.alpha = 1.0f;
       WM_TT(TK_TEXT_ATTN, gemm(pv, n_chunks * nh, true));
-      }
       // h = LN(h + ctx Wo^T + bo)
       WM_TT(TK_TEXT_GEMM, gemm(dense(ctx, rows, H, m->wo + lH * H, H, y, m->bo + lH, h, 0), 1, false));
-      WM_TT(TK_TEXT_OTHER, [&]() { hipLaunchKernelGGL(ln_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, y,
-                                               m->ln1_g + lH, m->ln1_b + lH, H, rows, h); return hipGetLastError(); }());
+      WM_TT(TK_TEXT_OTHER, ln(y, m->ln1_g + lH, m->ln1_b + lH, nullptr));
       // h = LN(h + GELU(h W1^T + b1) W2^T + b2)
       WM_TT(TK_TEXT_GEMM, gemm(dense(h, rows, H, m->w1 + (size_t)l * F * H, F, f, m->b1 + (size_t)l * F,
                                      nullptr, 1), 1, false));
       WM_TT(TK_TEXT_GEMM, gemm(dense(f, rows, F, m->w2 + (size_t)l * H * F, H, y, m->b2 + lH, h, 0), 1, false));
-      WM_TT(TK_TEXT_OTHER, [&]() { hipLaunchKernelGGL(ln_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, y,
-                                               m->ln2_g + lH, m->ln2_b + lH, H, rows, h); return hipGetLastError(); }());
+      WM_TT(TK_TEXT_OTHER, ln(y, m->ln2_g + lH, m->ln2_b + lH, nullptr));
     }
     WM_TT(TK_TEXT_OTHER, [&]() { hipLaunchKernelGGL(pool_kernel, dim3(n_chunks), dim3(256), 0, st, h, tt, W,
                                              d.stride, H, pooled); return hipGetLastError(); }());
