@@ -132,6 +132,44 @@ def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none", forest=None
                       f"+top-k, {total_t:.1f} s)"}
 
 
+def measure_peaks(torch) -> dict:
+    """Achievable peaks on this GPU, for context beside the published ones:
+    a large bf16 and fp32 matrix product through torch (hipBLASLt / rocBLAS)
+    and a 2 GiB device-to-device copy, best of several timed runs."""
+    dev = torch.device("cuda:0")
+    out = {}
+    for name, dt, n in (("bf16_tflops", torch.bfloat16, 8192), ("fp32_tflops", torch.float32, 8192)):
+        a = torch.randn(n, n, device=dev, dtype=dt)
+        b = torch.randn(n, n, device=dev, dtype=dt)
+        c = a @ b
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            torch.matmul(a, b, out=c)
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1) / 1e3)
+        out[name] = 2.0 * n ** 3 / best / 1e12
+        del a, b, c
+    nb = 2 << 30
+    src = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    best = float("inf")
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1) / 1e3)
+    out["hbm_gbs"] = 2.0 * nb / best / 1e9          # bytes read + written
+    del src, dst
+    torch.cuda.empty_cache()
+    return out
+
+
 def step_percentiles(torch, step, n: int) -> dict:
     """Median, 10th and 90th percentile of n steps, each bracketed by HIP
     events on the current stream (the stream the library launches on)."""
@@ -374,6 +412,8 @@ def main():
     ap.add_argument("--text-workload", default="codebert", choices=sorted(synth.TEXT_WORKLOADS))
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the achievable-peak measurements (library matrix products, copy)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this size (counter calibration)")
     args = ap.parse_args()
@@ -490,6 +530,12 @@ def main():
         "step_ms": step_ms,
         "whole_path_tflops": total_flops * args.steps / elapsed / 1e12,
     }
+    if not args.no_peaks:
+        ach = measure_peaks(torch)
+        key = "bf16_tflops" if prec == "bf16" else "fp32_tflops"
+        out["achievable_peaks"] = ach
+        out["roofline"]["achievable_peak"] = ach[key]
+        out["roofline"]["frac_achievable"] = achieved / ach[key]
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(w, W, I, prec, args.cpu_budget, args.norm, forest_arrays)
     print(json.dumps(out), flush=True)
