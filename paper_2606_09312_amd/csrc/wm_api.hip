@@ -518,8 +518,10 @@ wm_status wm_rollout(const wm_model* model, const float* z0, const int32_t* seg_
   int32_t* err = reinterpret_cast<int32_t*>(w8 + L.err);
   int2* perm = reinterpret_cast<int2*>(w8 + L.perm);
   WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, reinterpret_cast<int32_t*>(w8 + L.hist), err, st));
-  WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zT, err, st));
-  if (phi) WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
+  bool phi_done = false;
+  WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zT, phi,
+                                          &phi_done, err, st));
+  if (phi && !phi_done) WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
   return ok();
 }
 
@@ -590,8 +592,10 @@ wm_status wm_evaluate(const wm_model* model, const float* init, int32_t init_is_
   float* phi = reinterpret_cast<float*>(w8 + L.phi);
   float* sc = scores ? scores : reinterpret_cast<float*>(w8 + L.scores);
   WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, reinterpret_cast<int32_t*>(w8 + L.hist), err, st));
-  WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zTo, err, st));
-  WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
+  bool phi_done = false;
+  WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zTo, phi,
+                                          &phi_done, err, st));
+  if (!phi_done) WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
   WM_TIMED(TK_SCORE, st, launch_score(model->dm, zTo, phi, B, hw, n_hw, sc, st));
   WM_TIMED(TK_TOPK, st, launch_topk(sc, n_hw, B, seg, k, idx, val, st));
   return ok();
@@ -715,7 +719,9 @@ wm_status wm_evaluate_trees(const wm_model* model, const wm_forest* forest, cons
   float* phs = reinterpret_cast<float*>(w8 + L.phi_s);
   float* sc = scores ? scores : reinterpret_cast<float*>(w8 + L.scores);
   WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, reinterpret_cast<int32_t*>(w8 + L.hist), err, st));
-  WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zTo, err, st));
+  bool phi_done = false;
+  WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zTo, nullptr,
+                                          &phi_done, err, st));
   WM_TIMED(TK_PHI_STRUCT, st, launch_phi_struct(types, params, lens, B, T_max, dm.n_kinds, dm.n_params, phs, st));
   WM_TIMED(TK_TREES, st, launch_score_trees(forest->df, zTo, dm.d, phs, phi_dim, B, hw, n_hw, dm.hw_dim, sc, st));
   WM_TIMED(TK_TOPK, st, launch_topk(sc, n_hw, B, seg, k, idx, val, st));

@@ -230,9 +230,12 @@ __host__ __device__ constexpr inline int phi_struct_dim(int K, int P) { return K
 // hist: bucket_groups(B) * (T_max + 1) ints of workspace (unused when 0)
 hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
                          int2* perm, int32_t* hist, int32_t* err, hipStream_t st);
+// phi (may be null): the kernel families that can also sum the action
+// features write them and set *phi_done; otherwise launch_phi computes them.
 hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
-                          int32_t B, int32_t T_max, float* zT, int32_t* err, hipStream_t st);
+                          int32_t B, int32_t T_max, float* zT, float* phi, bool* phi_done,
+                          int32_t* err, hipStream_t st);
 hipError_t launch_phi(const DevModel& m, const int32_t* types, const int32_t* params,
                       const int32_t* lens, int32_t B, int32_t T_max, float* phi, hipStream_t st);
 hipError_t launch_score(const DevModel& m, const float* zT, const float* phi, int32_t B,

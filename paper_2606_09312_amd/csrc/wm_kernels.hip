@@ -352,6 +352,7 @@ struct RollArgs {
   const int32_t* params;    // [B][T_max][P]
   const int32_t* lens;      // [B]
   float* zT;                // [B][D]
+  float* phi;               // [B][E] mean step embedding, or null (the phi kernel computes it)
   int32_t* err;
   int B, T_max, P, K, H, tab_bytes;
   // training forward of the rollout loss (row-owned kernel only): the
@@ -640,6 +641,17 @@ struct Hyper {
   }
 };
 
+// Whether the persistent kernel also sums the action features: d <= 256 and
+// its static chunk buffers, the table (at most 16 KiB) and the sums
+// (WAVES * 32 rows of E + 1 floats) fit the 160 KiB of LDS.
+template <class PR, int D, int E, int WAVES, bool NORM>
+constexpr bool persistent_phi_ok() {
+  constexpr int W1B = TransChunk<PR>::w1_bytes(D, E), W2B = TransChunk<PR>::w2_bytes(D);
+  constexpr int WHB = HyperGeom<PR>::bytes(D, E);
+  constexpr int stat = 2 * (W1B + W2B) + ((NORM && wh_in_lds(W1B, W2B, WHB)) ? WHB : 0);
+  return D <= 256 && stat + 16 * 1024 + WAVES * 32 * (E + 1) * 4 <= 160 * 1024;
+}
+
 template <class PR, int D, int E, int WAVES, bool NORM>
 __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a) {
   using R = Roll<PR, D, E>;
@@ -666,6 +678,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
   const float* t_pw = tab + a.K * temb_stride(E);              // [PMAX][E], zero rows past P
   const float* t_pb = t_pw + PMAX * E;            // [E]
   const float* t_b2 = t_pb + E;                   // [NB][2][16] accumulator order
+  // action features (d <= 256; the launcher adds the area): running sums of
+  // the step embeddings per candidate row, rows padded by one float
+  constexpr bool PHI_OK = persistent_phi_ok<PR, D, E, WAVES, NORM>();
+  const bool do_phi = PHI_OK && a.phi != nullptr;
+  float* phib = tab + a.tab_bytes / 4;             // [WAVES * 32][E + 1]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
@@ -678,6 +695,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
   stage_fixed<W2B, NT>(a.w2, w2a, tid);
   if constexpr (PIPE) stage_fixed<W1B, NT>(a.w1 + W1B, w1b, tid);
   if constexpr (WH_LDS) stage_fixed<HY::BYTES, NT>(a.wh, whs, tid);
+  if (do_phi)
+    for (int i = tid; i < WAVES * 32 * (E + 1); i += NT) phib[i] = 0.0f;
 
   const int pos = (blockIdx.x * WAVES + wave) * 32 + n;
   const bool valid = pos < a.B;
@@ -756,6 +775,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
 #pragma unroll
       for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * actf;
       xe[q] = PR::cvt(ev);
+      if (do_phi) {
+        float* ph = phib + (wave * 32 + n) * (E + 1) + f0;
+#pragma unroll
+        for (int j = 0; j < SL; ++j) ph[j] += ev[j];
+      }
     }
     if constexpr (NORM) {
       // unit length for the previous step's output, hyperplane projection for this step
@@ -836,6 +860,17 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
   if constexpr (NORM) HY::unit(zacc, T_wg > 0 && T_wg <= len);
   if (errbits) atomicOr(a.err, errbits);
 
+  if (do_phi && valid) {         // phi = sum / len (0 when empty); the lane pair holds all features
+    const float inv = len > 0 ? 1.0f / (float)len : 0.0f;
+    const float* ph = phib + (wave * 32 + n) * (E + 1);
+#pragma unroll
+    for (int q = 0; q < NE; ++q)
+#pragma unroll
+      for (int j = 0; j < SL; ++j) {
+        const int f = KF * q + SL * h + j;
+        a.phi[(size_t)cand * E + f] = ph[f] * inv;
+      }
+  }
   if (valid) {
     float* zo = a.zT + (size_t)cand * D;
 #pragma unroll
@@ -1250,12 +1285,18 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
   uint8_t* xbuf = gbuf + RG::GELU_BYTES;                            // X fragments
   uint8_t* xebuf = xbuf + RG::X_BYTES;                              // embedding fragments
   float* dots = reinterpret_cast<float*>(xebuf + RG::XE_BYTES);     // [W][3][32]
+  // action features: the running sum of each owned embedding fragment, per
+  // candidate row (rows padded by one float against bank conflicts)
+  float* phib = dots + (NORM ? W * 3 * 32 : 0);                      // [32][E + 1]
+  const bool do_phi = !TRAIN && a.phi != nullptr;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
 
   stage_to_lds(reinterpret_cast<const uint8_t*>(a.tab), reinterpret_cast<uint8_t*>(tab),
                a.tab_bytes, tid, NT);
+  if (do_phi)
+    for (int i = tid; i < 32 * (E + 1); i += NT) phib[i] = 0.0f;
 
   const int pos = blockIdx.x * 32 + n;
   const bool valid = pos < a.B;
@@ -1336,19 +1377,25 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 #pragma unroll
     for (int j = 0; j < SL; ++j) ev[j] = (ev[j] + tmp[j]) * af;
   };
-  auto embed_frag = [&](int ty, const float (&u)[PMAX], float af, int q) -> Frag {
-    float ev[SL];
-    embed_vals(ty, u, af, q, ev);
-    return PR::cvt(ev);
+  // running sum of fragment q's features (inactive steps add zero)
+  auto phi_add = [&](int q, const float (&ev)[SL]) {
+    float* ph = phib + n * (E + 1) + KF * q + SL * h;
+#pragma unroll
+    for (int j = 0; j < SL; ++j) ph[j] += ev[j];
   };
   // all fragments in this wavefront (paper form: the normal map needs them
-  // before the step's exchange)
+  // before the step's exchange); the owner of each fragment group sums it
   auto embed_step = [&](int s, Frag (&xe)[NE]) {
     int ty;
     float u[PMAX], af;
     decode(s, ty, u, af);
 #pragma unroll
-    for (int q = 0; q < NE; ++q) xe[q] = embed_frag(ty, u, af, q);
+    for (int q = 0; q < NE; ++q) {
+      float ev[SL];
+      embed_vals(ty, u, af, q, ev);
+      xe[q] = PR::cvt(ev);
+      if (do_phi && (q / G) % W == w) phi_add(q, ev);
+    }
   };
   // this wavefront's share of the fragment groups, into LDS (read back with X)
   auto embed_share = [&](int s) {
@@ -1364,6 +1411,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
         float ev[SL];
         embed_vals(ty, u, af, q, ev);
         *reinterpret_cast<Frag*>(xebuf + frag_offset<PR>(q, lane, 0)) = PR::cvt(ev);
+        if (do_phi) phi_add(q, ev);
         if constexpr (TRAIN) {
           if (s < len) {
             float* xo = a.X + (row0 + s) * IN + D + KF * q + SL * h;
@@ -1597,6 +1645,16 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     exchange_x();
   }
   if (errbits) atomicOr(a.err, errbits);
+  if (do_phi && valid) {         // phi = sum / len over the owned fragments (0 when empty)
+    const float inv = len > 0 ? 1.0f / (float)len : 0.0f;
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      if ((q / G) % W != w) continue;
+      const float* ph = phib + n * (E + 1) + KF * q + SL * h;
+#pragma unroll
+      for (int j = 0; j < SL; ++j) a.phi[(size_t)cand * E + KF * q + SL * h + j] = ph[j] * inv;
+    }
+  }
   if (valid && !TRAIN) {
     float* zo = a.zT + (size_t)cand * D;
 #pragma unroll
@@ -3259,7 +3317,9 @@ namespace {
 
 template <class PR, int D, int E, int WAVES, bool NORM>
 hipError_t launch_rollout_t(const DevModel& m, const RollArgs& a, int blocks, hipStream_t st) {
-  const int lds = m.roll_tab_bytes;   // the chunk buffers are static
+  // the chunk buffers are static; the table and the phi sums are dynamic
+  constexpr bool PHI_OK = persistent_phi_ok<PR, D, E, WAVES, NORM>();
+  const int lds = m.roll_tab_bytes + (PHI_OK && a.phi ? WAVES * 32 * (E + 1) * 4 : 0);
   auto kern = rollout_kernel<PR, D, E, WAVES, NORM>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
@@ -3357,7 +3417,7 @@ template <class PR, int D, int E, int NC, int W, bool NORM>
 hipError_t launch_rollout_rows_t(const DevModel& m, const RollArgs& a, int tiles, hipStream_t st) {
   using RG = RowsGeom<PR, D, E, NC, W>;
   const int lds = m.roll_tab_bytes + RG::GELU_BYTES + RG::X_BYTES + RG::XE_BYTES +
-                  (NORM ? W * 3 * 32 * 4 : 0);
+                  (NORM ? W * 3 * 32 * 4 : 0) + (a.phi ? 32 * (E + 1) * 4 : 0);
   auto kern = rollout_rows_kernel<PR, D, E, NC, W, NORM>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
@@ -3373,8 +3433,10 @@ hipError_t launch_rollout_rows_t(const DevModel& m, const RollArgs& a, int tiles
 // workgroup.
 template <class PR, int D, int E, bool NORM>
 hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, int blocks,
-                             int waves, bool split, hipStream_t st) {
+                             int waves, bool split, bool* phi_done, hipStream_t st) {
   // d = 256: row-owned form for the hidden widths it is instantiated for
+  // (it also sums the action features)
+  *phi_done = a.phi != nullptr;
   if constexpr (D == 256) {
     if (split) {
       const int NC = m.dims.trans_hidden / 32;
@@ -3386,11 +3448,28 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
       }
     }
   }
-  // fp32 at d = 256 does not fit the split kernel's registers
+  // fp32 at d = 256 does not fit the split kernel's registers; the split
+  // kernel leaves the action features to the phi kernel
   if constexpr (D <= 256 && (PR::G == 1 || D <= 64)) {
     constexpr int SPLIT = (D / 32) >= 4 ? 4 : (D / 32);
-    if (split && m.dims.trans_hidden / 32 >= SPLIT)
-      return launch_rollout_split_t<PR, D, E, SPLIT, NORM>(m, a, tiles, st);
+    if (split && m.dims.trans_hidden / 32 >= SPLIT) {
+      RollArgs b = a;
+      b.phi = nullptr;
+      *phi_done = false;
+      return launch_rollout_split_t<PR, D, E, SPLIT, NORM>(m, b, tiles, st);
+    }
+  }
+  // the persistent kernel sums the action features where they fit its LDS
+  const bool pok = waves == 4   ? persistent_phi_ok<PR, D, E, 4, NORM>()
+                   : waves == 2 ? persistent_phi_ok<PR, D, E, 2, NORM>()
+                                : persistent_phi_ok<PR, D, E, 1, NORM>();
+  if (!pok) {
+    RollArgs b = a;
+    b.phi = nullptr;
+    *phi_done = false;
+    if (waves == 4) return launch_rollout_t<PR, D, E, 4, NORM>(m, b, blocks, st);
+    if (waves == 2) return launch_rollout_t<PR, D, E, 2, NORM>(m, b, blocks, st);
+    return launch_rollout_t<PR, D, E, 1, NORM>(m, b, blocks, st);
   }
   if (waves == 4) return launch_rollout_t<PR, D, E, 4, NORM>(m, a, blocks, st);
   if (waves == 2) return launch_rollout_t<PR, D, E, 2, NORM>(m, a, blocks, st);
@@ -3399,10 +3478,11 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
 
 hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
-                          int32_t B, int32_t T_max, float* zT, int32_t* err, hipStream_t st) {
+                          int32_t B, int32_t T_max, float* zT, float* phi, bool* phi_done,
+                          int32_t* err, hipStream_t st) {
   RollArgs a{};
   a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.wh = m.trans_wh; a.tab = m.roll_tab; a.z0 = z0; a.perm = perm; a.types = types;
-  a.params = params; a.lens = lens; a.zT = zT; a.err = err; a.B = B; a.T_max = T_max;
+  a.params = params; a.lens = lens; a.zT = zT; a.phi = phi; a.err = err; a.B = B; a.T_max = T_max;
   a.P = m.dims.n_params; a.K = m.dims.n_kinds; a.H = m.dims.trans_hidden;
   a.tab_bytes = m.roll_tab_bytes;
   const int tiles = (B + 31) / 32;
@@ -3413,9 +3493,10 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
   // the compute unit's SIMDs instead (d <= 256: the partial updates fit LDS).
   const bool split = tiles <= SPLIT_MAX_TILES && d <= 256;
   const bool norm = m.dims.norm == WM_NORM_L2;
-#define WM_ROLL(PR, D, E)                                                                \
-  return norm ? launch_rollout_de<PR, D, E, true>(m, a, tiles, blocks, waves, split, st)  \
-              : launch_rollout_de<PR, D, E, false>(m, a, tiles, blocks, waves, split, st);
+  *phi_done = false;
+#define WM_ROLL(PR, D, E)                                                                          \
+  return norm ? launch_rollout_de<PR, D, E, true>(m, a, tiles, blocks, waves, split, phi_done, st)  \
+              : launch_rollout_de<PR, D, E, false>(m, a, tiles, blocks, waves, split, phi_done, st);
   WM_FOR_ALL_DE(WM_ROLL)
 #undef WM_ROLL
   return hipErrorInvalidValue;

@@ -315,3 +315,42 @@ def test_large_batch_bucketing(wm, lens_kind):
     rel = latent_rel(g["zT"], ref["zT"])
     assert rel.max() <= 1e-4, f"z_T rel err {rel.max():.3e}"
     check_topk_vs_oracle(g["idx"], ref["scores"], I["seg_off"], w.k, 1e-4)
+
+
+# The action features come from the rollout kernel itself (row-owned kernel,
+# and the persistent kernel where its LDS has room) or from the phi kernel
+# (split kernel, d = 512, fp32 at d = 256): every family against the oracle.
+PHI_CASES = [
+    ("tiny", "fp32", 200, "none"),            # split kernel + phi kernel
+    ("tiny", "fp32", 8224, "none"),           # persistent, sums in the kernel
+    ("ansor_round", "bf16", 300, "none"),     # row-owned
+    ("ansor_round", "bf16", 300, "l2"),       # row-owned, paper form
+    ("ansor_round", "bf16", 9000, "none"),    # persistent d = 256
+    ("ansor_round", "bf16", 9000, "l2"),      # persistent d = 256, paper form
+    ("ansor_round", "fp32", 9000, "none"),    # persistent fp32 d = 256 + phi kernel
+    ("large_latent", "bf16", 300, "none"),    # d = 512 + phi kernel
+]
+
+
+@pytest.mark.parametrize("name,prec,B,norm", PHI_CASES)
+def test_rollout_phi_every_kernel_family(wm, name, prec, B, norm):
+    w = synth.scaled(synth.workload(name), B=B, S=1)
+    print(f"[phi] {name} {prec} B={B} {norm}", flush=True)
+    W = synth.make_weights(w, 1000)
+    model = wm.Model(wm.model_dims(w), W, precision=prec, norm=norm)
+    I = synth.make_inputs(w, 4100 + B, pad="garbage")
+    I["lens"][:2] = 0
+    dev = "cuda"
+    t = to_dev(I, dev)
+    zT = torch.empty((w.B, w.d), device=dev)
+    phi = torch.full((w.B, w.e), float("nan"), device=dev)
+    ws = model.workspace(w.B, w.T_max, w.S, 1)
+    wm.rollout(model, t["z0"], I["seg_off"], t["types"], t["params"], t["lens"], zT, phi, ws)
+    wm.device_status(ws)
+    Wd = O.prepare(W, prec)
+    _, ref = O.rollout(Wd, I["z0"], I["seg_off"], I["types"], I["params"], I["lens"], prec, norm=norm)
+    got = phi.cpu().numpy().astype(np.float64)
+    assert np.isfinite(got).all()
+    np.testing.assert_array_equal(got[:2], 0.0)
+    err = np.abs(got - ref).max() / max(1.0, np.abs(ref).max())
+    assert err <= 1e-5, f"phi err {err:.3e}"
