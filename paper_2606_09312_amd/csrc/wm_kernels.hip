@@ -358,6 +358,7 @@ struct RollArgs {
   // training forward of the rollout loss (row-owned kernel only): the
   // activations of every valid step in compact rows off[i] + t
   float *X, *A, *G, *Pz;    // [R][D+E], [R][H], [R][H], [R][D]
+  float *V, *SC;            // paper form: [R][D] Wh e, [R][4] v.z, v.v, |u|, 0
   const int32_t* off;
   int32_t* row_src;
 };
@@ -1263,7 +1264,6 @@ struct RowsGeom {
 
 template <class PR, int D, int E, int NC, int W, bool NORM, bool TRAIN = false>
 __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs a) {
-  static_assert(!(TRAIN && NORM), "the training forward is the residual form");
   using R = Roll<PR, D, E>;
   using RG = RowsGeom<PR, D, E, NC, W>;
   using Frag = typename PR::Frag;
@@ -1395,6 +1395,13 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
       embed_vals(ty, u, af, q, ev);
       xe[q] = PR::cvt(ev);
       if (do_phi && (q / G) % W == w) phi_add(q, ev);
+      if constexpr (TRAIN) {
+        if ((q / G) % W == w && s < len) {
+          float* xo = a.X + (row0 + s) * IN + D + KF * q + SL * h;
+#pragma unroll
+          for (int j = 0; j < SL; ++j) xo[j] = op_value<PR>(ev[j]);
+        }
+      }
     }
   };
   // this wavefront's share of the fragment groups, into LDS (read back with X)
@@ -1429,7 +1436,9 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 #pragma unroll
     for (int i = 0; i < NBW * GPB; ++i) whq[i] = HY::group(a.wh, w * NBW * GPB + i, lane);
   }
-  auto boundary = [&](const Frag (&xe)[NE], bool renorm, bool project) {
+  // Training mode: the unit-length prediction of the finished step t and
+  // |u| go to row t, the next step's v, v.z and v.v to row t + 1.
+  auto boundary = [&](const Frag (&xe)[NE], bool renorm, bool project, int t) {
     f32x16 vq[NBW];
     float vz = 0.0f, vv = 0.0f, zz = 0.0f;
 #pragma unroll
@@ -1465,6 +1474,29 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
     }
     const float sc = (renorm && zz > 0.0f) ? rsqrtf(zz) : 1.0f;
     const float al = (project && vv > 0.0f) ? vz / vv : 0.0f;
+    if constexpr (TRAIN) {
+      if (renorm) {              // step t was active
+        const size_t rt = row0 + t;
+#pragma unroll
+        for (int bq = 0; bq < NBW; ++bq) {
+          f32x16 pv;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) pv[r] = zq[bq][r] * sc;
+          store_acc(a.Pz + rt * D + 32 * (w * NBW + bq), pv, h);
+        }
+        if (w == 0 && h == 0) a.SC[rt * 4 + 2] = sqrtf(zz);
+      }
+      if (project) {             // step t + 1 is active
+        const size_t rs = row0 + (t + 1);
+#pragma unroll
+        for (int bq = 0; bq < NBW; ++bq) store_acc(a.V + rs * D + 32 * (w * NBW + bq), vq[bq], h);
+        if (w == 0 && h == 0) {
+          a.SC[rs * 4 + 0] = vz * sc;
+          a.SC[rs * 4 + 1] = vv;
+          a.SC[rs * 4 + 3] = 0.0f;
+        }
+      }
+    }
 #pragma unroll
     for (int bq = 0; bq < NBW; ++bq)
 #pragma unroll
@@ -1514,7 +1546,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 
   if constexpr (NORM) {
     embed_step(0, xe);
-    boundary(xe, false, 0 < len);
+    boundary(xe, false, 0 < len, -1);
   } else {
     embed_share(0);
   }
@@ -1632,13 +1664,13 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
       const int b = w * NBW + bq;
 #pragma unroll
       for (int r = 0; r < 16; ++r) zq[bq][r] += dz[bq][r] + t_b2[(b * 2 + h) * 16 + r] * actf;
-      if constexpr (TRAIN) {
+      if constexpr (TRAIN && !NORM) {
         if (active) store_acc(a.Pz + row * D + 32 * b, zq[bq], h);
       }
     }
     if constexpr (NORM) {
       embed_step(t + 1, xe);
-      boundary(xe, active, t + 1 < len);
+      boundary(xe, active, t + 1 < len, t);
     } else {
       embed_share(t + 1);
     }
@@ -2510,7 +2542,7 @@ struct BwdRowsGeom {
   static constexpr int LDS = DA_BYTES + DL_BYTES + DE_BYTES;
 };
 
-template <class PR, int D, int E, int NC, int W>
+template <class PR, int D, int E, int NC, int W, bool NORM>
 __global__ __launch_bounds__(64 * W, 1) void train_bwd_rows_kernel(const TrainArgs a) {
   using R = Roll<PR, D, E>;
   using BG = BwdRowsGeom<PR, D, E, NC, W>;
@@ -2525,6 +2557,7 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_rows_kernel(const TrainAr
   uint8_t* dabuf = lds;                                   // dA fragments, chunk-major
   uint8_t* dlbuf = lds + BG::DA_BYTES;                    // delta fragments
   float* debuf = reinterpret_cast<float*>(lds + BG::DA_BYTES + BG::DL_BYTES);  // [W][NBE][2][16][32]
+  float* dots = reinterpret_cast<float*>(lds + BG::LDS);  // paper form: [2][W][32]
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
@@ -2561,15 +2594,42 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_rows_kernel(const TrainAr
     gu8* p2 = base2;
     gu8* p1 = base1;
     asm volatile("" : "+v"(p2), "+v"(p1));
-    // ---- owned delta blocks: seed, delta_{t+1}, operand fragments in LDS
+    // ---- owned delta blocks: seed, delta_{t+1} (paper form: du through the
+    // normalisation, du = (delta - (delta . z) z) / |u| with z the unit
+    // prediction), operand fragments in LDS
+    f32x4 sc = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (active) {
+#pragma unroll
+      for (int bq = 0; bq < NBW; ++bq) dq[bq] += load_acc(a.SD + row * D + 32 * (w * NBW + bq), h);
+    }
+    if constexpr (NORM) {
+      if (active) sc = *reinterpret_cast<const f32x4*>(a.SC + row * 4);
+      f32x16 pb[NBW];
+      float dz = 0.0f;
+#pragma unroll
+      for (int bq = 0; bq < NBW; ++bq) {
+        pb[bq] = active ? load_acc(a.P + row * D + 32 * (w * NBW + bq), h) : f32x16{};
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dz = fmaf(dq[bq][r], pb[bq][r], dz);
+      }
+      dz = dz + __shfl_xor(dz, 32);
+      if (h == 0) dots[w * 32 + n] = dz;
+      __syncthreads();
+      dz = 0.0f;
+#pragma unroll
+      for (int ww = 0; ww < W; ++ww) dz += dots[ww * 32 + n];
+      const bool nrm = active && sc[2] > 0.0f;
+      const float inu = nrm ? 1.0f / sc[2] : 1.0f;
+      const float cz = nrm ? dz : 0.0f;
+#pragma unroll
+      for (int bq = 0; bq < NBW; ++bq)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dq[bq][r] = (dq[bq][r] - cz * pb[bq][r]) * inu;
+    }
 #pragma unroll
     for (int bq = 0; bq < NBW; ++bq) {
       const int b = w * NBW + bq;
-      if (active) {
-        float* sd = a.SD + row * D + 32 * b;
-        dq[bq] += load_acc(sd, h);
-        store_acc(sd, dq[bq], h);
-      }
+      if (active) store_acc(a.SD + row * D + 32 * b, dq[bq], h);
 #pragma unroll
       for (int f = 0; f < NF2; ++f) {
         float v[SL];
@@ -2592,6 +2652,7 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_rows_kernel(const TrainAr
     f32x16 deacc[NBE];
 #pragma unroll
     for (int q = 0; q < NBE; ++q) deacc[q] = f32x16{};
+    f32x16 emlp = {};              // paper form: this wavefront's dE block, MLP part
     typename PR::Packed dp[8];
     constexpr int GB = NF2 / G;
     u32x4 dcur[GB], dnext[GB];
@@ -2636,7 +2697,8 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_rows_kernel(const TrainAr
             for (int ww = 0; ww < W; ++ww)
 #pragma unroll
               for (int r = 0; r < 16; ++r) e[r] += debuf[(((ww * NBE + w) * 2 + h) * 16 + r) * 32 + n];
-            if (active) store_acc(a.DE + row * E + 32 * w, e, h);
+            if constexpr (NORM) emlp = e;
+            else if (active) store_acc(a.DE + row * E + 32 * w, e, h);
           }
 #pragma unroll
           for (int gg = 0; gg < GB; ++gg) dcur[gg] = lds_group(dabuf, gg, lane);
@@ -2664,6 +2726,76 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_rows_kernel(const TrainAr
         }
       }
       __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (NORM) {
+      // through z' = z - (w . z) w, w = v / |v| (as in the one-wavefront
+      // kernel): dz = dz' - (w . dz') w, dv = (dw - (w . dw) w) / |v|,
+      // de += R(Wh)^T R(dv); the dot w . dz' and the dE partials of the
+      // owned blocks are summed across wavefronts through LDS
+      const bool prj = active && sc[1] > 0.0f;
+      const float inv = prj ? rsqrtf(sc[1]) : 0.0f;
+      const float wz = sc[0] * inv;
+      f32x16 vb[NBW];
+      float wdz = 0.0f;
+#pragma unroll
+      for (int bq = 0; bq < NBW; ++bq) {
+        vb[bq] = prj ? load_acc(a.V + row * D + 32 * (w * NBW + bq), h) : f32x16{};
+#pragma unroll
+        for (int r = 0; r < 16; ++r) wdz = fmaf(vb[bq][r], dq[bq][r], wdz);
+      }
+      wdz = wdz + __shfl_xor(wdz, 32);
+      if (h == 0) dots[(W + w) * 32 + n] = wdz;
+      __syncthreads();
+      wdz = 0.0f;
+#pragma unroll
+      for (int ww = 0; ww < W; ++ww) wdz += dots[(W + ww) * 32 + n];
+      wdz *= inv;
+      const float* zin = t > 0 ? a.P + (row - 1) * D : a.z0 + (size_t)ti.seg * D;
+      gu8* whtb = (gu8*)(a.wht) + lane * 16;
+      constexpr int NZG = NZ / G;
+      f32x16 den[NBE];
+#pragma unroll
+      for (int q = 0; q < NBE; ++q) den[q] = f32x16{};
+#pragma unroll
+      for (int bq = 0; bq < NBW; ++bq) {
+        const int b = w * NBW + bq;
+        const f32x16 zb = prj ? load_acc(zin + 32 * b, h) : f32x16{};
+        f32x16 dv;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float wr = vb[bq][r] * inv;
+          dv[r] = (-(wz * dq[bq][r] + wdz * zb[r]) + 2.0f * wz * wdz * wr) * inv;
+          dq[bq][r] -= wdz * wr;
+        }
+        if (active) store_acc(a.DV + row * D + 32 * b, dv, h);
+#pragma unroll
+        for (int f = 0; f < NF2; ++f) {
+          float v[SL];
+#pragma unroll
+          for (int j = 0; j < SL; ++j) v[j] = dv[f * SL + j];
+          const Frag dvf = PR::cvt(v);
+          const int kf = b * NF2 + f;
+#pragma unroll
+          for (int q = 0; q < NBE; ++q) {
+            const u32x4 grp = *reinterpret_cast<gu32x4*>(whtb + (size_t)(q * NZG + kf / G) * 1024);
+            den[q] = PR::mfma(PR::pick(grp, kf % G), dvf, den[q]);
+          }
+        }
+      }
+      // the MLP partials were read before this step's dot barrier
+#pragma unroll
+      for (int q = 0; q < NBE; ++q)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) debuf[(((w * NBE + q) * 2 + h) * 16 + r) * 32 + n] = den[q][r];
+      __syncthreads();
+      if (w < NBE) {
+        f32x16 e = emlp;
+#pragma unroll
+        for (int ww = 0; ww < W; ++ww)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) e[r] += debuf[(((ww * NBE + w) * 2 + h) * 16 + r) * 32 + n];
+        if (active) store_acc(a.DE + row * E + 32 * w, e, h);
+      }
     }
     __syncthreads();                // dA / dE buffers are read before the next step writes them
   }
@@ -3624,16 +3756,18 @@ hipError_t launch_train_fwd_t(const DevModel& m, const TrainArgs& a, int blocks,
   return hipGetLastError();
 }
 
-template <class PR, int NC, int W>
+template <class PR, int NC, int W, bool NORM>
 hipError_t launch_train_bwd_rows(const TrainArgs& a, int tiles, hipStream_t st) {
   using BG = BwdRowsGeom<PR, 256, 64, NC, W>;
-  auto kern = train_bwd_rows_kernel<PR, 256, 64, NC, W>;
-  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, BG::LDS);
+  constexpr int lds = BG::LDS + (NORM ? 2 * W * 32 * 4 : 0);
+  static_assert(lds <= 160 * 1024, "LDS");
+  auto kern = train_bwd_rows_kernel<PR, 256, 64, NC, W, NORM>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return e;
   }
-  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * W), BG::LDS, st, a);
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * W), lds, st, a);
   return hipGetLastError();
 }
 
@@ -3657,17 +3791,18 @@ bool have_train_kernels(int prec, int d, int e) {
 }
 
 // Training forward in the row-owned form (one workgroup per tile; d = 256).
-template <class PR, int NC, int W>
+template <class PR, int NC, int W, bool NORM>
 hipError_t launch_train_fwd_rows(const DevModel& m, const TrainIO& io, int tiles, hipStream_t st) {
   RollArgs a{};
-  a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.wh = nullptr; a.tab = m.roll_tab; a.z0 = io.z0;
+  a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.wh = NORM ? m.trans_wh : nullptr; a.tab = m.roll_tab; a.z0 = io.z0;
   a.perm = io.perm; a.types = io.types; a.params = io.params; a.lens = io.lens; a.zT = nullptr;
   a.err = io.err; a.B = io.B; a.T_max = io.T_max; a.P = m.dims.n_params; a.K = m.dims.n_kinds;
   a.H = m.dims.trans_hidden; a.tab_bytes = m.roll_tab_bytes;
   a.X = io.X; a.A = io.A; a.G = io.G; a.Pz = io.P; a.off = io.off; a.row_src = io.row_src;
+  a.V = io.V; a.SC = io.SC;
   using RG = RowsGeom<PR, 256, 64, NC, W>;
-  const int lds = m.roll_tab_bytes + RG::GELU_BYTES + RG::X_BYTES + RG::XE_BYTES;
-  auto kern = rollout_rows_kernel<PR, 256, 64, NC, W, false, true>;
+  const int lds = m.roll_tab_bytes + RG::GELU_BYTES + RG::X_BYTES + RG::XE_BYTES + (NORM ? W * 3 * 32 * 4 : 0);
+  auto kern = rollout_rows_kernel<PR, 256, 64, NC, W, NORM, true>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -3682,11 +3817,14 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
   const TrainArgs a = train_args(m, io);
   const int tiles = (io.B + 31) / 32;
   const bool norm = m.dims.norm == WM_NORM_L2;
-  if (m.dims.d == 256 && m.dims.embed_dim == 64 && !norm) {
+  if (m.dims.d == 256 && m.dims.embed_dim == 64) {
     const int NC = m.dims.trans_hidden / 32;
-    if (m.prec == WM_BF16 && NC == 16) return launch_train_fwd_rows<PBF16, 16, 8>(m, io, tiles, st);
-    if (m.prec == WM_BF16 && NC == 32) return launch_train_fwd_rows<PBF16, 32, 8>(m, io, tiles, st);
-    if (m.prec == WM_FP32 && NC == 16) return launch_train_fwd_rows<PF32, 16, 4>(m, io, tiles, st);
+#define WM_TFWD_ROWS(N)                                                                              \
+    if (m.prec == WM_BF16 && NC == 16) return launch_train_fwd_rows<PBF16, 16, 8, N>(m, io, tiles, st); \
+    if (m.prec == WM_BF16 && NC == 32) return launch_train_fwd_rows<PBF16, 32, 8, N>(m, io, tiles, st); \
+    if (m.prec == WM_FP32 && NC == 16) return launch_train_fwd_rows<PF32, 16, 4, N>(m, io, tiles, st);
+    if (norm) { WM_TFWD_ROWS(true) } else { WM_TFWD_ROWS(false) }
+#undef WM_TFWD_ROWS
   }
   const int waves = pick_waves(tiles);
   const int blocks = (tiles + waves - 1) / waves;
@@ -3708,11 +3846,14 @@ hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st
   const TrainArgs a = train_args(m, io);
   const int tiles = (io.B + 31) / 32;
   const bool norm = m.dims.norm == WM_NORM_L2;
-  if (m.dims.d == 256 && m.dims.embed_dim == 64 && !norm) {
+  if (m.dims.d == 256 && m.dims.embed_dim == 64) {
     const int NC = m.dims.trans_hidden / 32;
-    if (m.prec == WM_BF16 && NC == 16) return launch_train_bwd_rows<PBF16, 16, 8>(a, tiles, st);
-    if (m.prec == WM_BF16 && NC == 32) return launch_train_bwd_rows<PBF16, 32, 8>(a, tiles, st);
-    if (m.prec == WM_FP32 && NC == 16) return launch_train_bwd_rows<PF32, 16, 4>(a, tiles, st);
+#define WM_TBWD_ROWS(N)                                                                         \
+    if (m.prec == WM_BF16 && NC == 16) return launch_train_bwd_rows<PBF16, 16, 8, N>(a, tiles, st); \
+    if (m.prec == WM_BF16 && NC == 32) return launch_train_bwd_rows<PBF16, 32, 8, N>(a, tiles, st); \
+    if (m.prec == WM_FP32 && NC == 16) return launch_train_bwd_rows<PF32, 16, 4, N>(a, tiles, st);
+    if (norm) { WM_TBWD_ROWS(true) } else { WM_TBWD_ROWS(false) }
+#undef WM_TBWD_ROWS
   }
   const int prec = m.prec, d = m.dims.d, e = m.dims.embed_dim;
 #define WM_TBWD(PR, D, E) \
