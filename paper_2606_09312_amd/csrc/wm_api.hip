@@ -104,6 +104,37 @@ void pack_transition(const wm_dims& dm, const wm_weights& w, std::vector<uint8_t
   }
 }
 
+// Narrow-tile transition blob (bf16; layout at Narrow in wm_internal.h).
+std::vector<uint8_t> pack_transition_narrow(const wm_dims& dm, const wm_weights& w) {
+  const int D = dm.d, E = dm.embed_dim, H = dm.trans_hidden, IN = D + E, NK = IN / 32;
+  std::vector<uint8_t> blk(Narrow::bytes(D, E, H), 0);
+  auto put16 = [&](size_t group, int lane, int j, float v) {
+    const uint16_t b = f32_to_bf16(v);
+    std::memcpy(&blk[group * 1024 + (size_t)lane * 16 + (size_t)j * 2], &b, 2);
+  };
+  for (int c = 0; c < H / 32; ++c)
+    for (int kf = 0; kf < NK; ++kf)
+      for (int rb = 0; rb < 2; ++rb)
+        for (int L = 0; L < 64; ++L)
+          for (int j = 0; j < 8; ++j) {
+            const int hid = 32 * c + 16 * rb + (L & 15);
+            put16(((size_t)c * NK + kf) * 2 + rb, L, j,
+                  w.w1[(size_t)hid * IN + narrow_x_feature(D, kf, L >> 4, j)]);
+          }
+  const size_t g2 = Narrow::w1_groups(D, E, H);
+  for (int c = 0; c < H / 32; ++c)
+    for (int b = 0; b < D / 16; ++b)
+      for (int L = 0; L < 64; ++L)
+        for (int j = 0; j < 8; ++j) {
+          const int row = 16 * b + (L & 15), hid = 32 * c + narrow_g_feature(L >> 4, j);
+          put16(g2 + (size_t)c * (D / 16) + b, L, j, w.w2[(size_t)row * H + hid]);
+        }
+  const size_t tail = (g2 + Narrow::w2_groups(D, H)) * 1024;
+  std::memcpy(&blk[tail], w.b1, (size_t)H * 4);
+  std::memcpy(&blk[tail + (size_t)H * 4], w.b2, (size_t)D * 4);
+  return blk;
+}
+
 // Transposed transition chunks for the rollout-loss backward (see TransT).
 template <class Gm>
 void pack_transposed(const wm_dims& dm, const wm_weights& w, std::vector<uint8_t>& w2t,
@@ -353,7 +384,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.dims = dm;
   m.prec = dm.precision;
   const int D = dm.d, E = dm.embed_dim, K = dm.n_kinds, P = dm.n_params, HW = dm.hw_dim;
-  std::vector<uint8_t> tw1, tw2, cost, twh, tw2t, tw1t, twht;
+  std::vector<uint8_t> tw1, tw2, cost, twh, tw2t, tw1t, twht, tn;
   const bool l2 = dm.norm == WM_NORM_L2;
   if (m.prec == WM_BF16) {
     pack_transition<GeomBF16>(dm, *w, tw1, tw2);
@@ -361,6 +392,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
     cost = pack_cost<GeomBF16>(dm, *w);
     if (l2) twh = pack_hyper<GeomBF16>(dm, *w);
     if (l2 && E % 32 == 0) twht = pack_hyper_t<GeomBF16>(dm, *w);
+    if (D % 32 == 0 && E % 32 == 0) tn = pack_transition_narrow(dm, *w);
     m.w1_chunk_bytes = TransChunk<GeomBF16>::w1_bytes(D, E);
     m.w2_chunk_bytes = TransChunk<GeomBF16>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomBF16>::bytes(D, E, HW);
@@ -418,6 +450,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   const size_t o_w2t = off; off = align256(off + tw2t.size());
   const size_t o_w1t = off; off = align256(off + tw1t.size());
   const size_t o_wht = off; off = align256(off + twht.size());
+  const size_t o_tn = off; off = align256(off + tn.size());
   const size_t o_tab = off; off = align256(off + tab.size() * 4);
   const size_t o_enc = off; off = align256(off + enc.size() * 4);
   void* dev = nullptr;
@@ -433,6 +466,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   if (e == hipSuccess && !tw2t.empty()) e = hipMemcpy(base + o_w2t, tw2t.data(), tw2t.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess && !tw1t.empty()) e = hipMemcpy(base + o_w1t, tw1t.data(), tw1t.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess && !twht.empty()) e = hipMemcpy(base + o_wht, twht.data(), twht.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess && !tn.empty()) e = hipMemcpy(base + o_tn, tn.data(), tn.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_tab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess && !enc.empty()) e = hipMemcpy(base + o_enc, enc.data(), enc.size() * 4, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
@@ -447,6 +481,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.trans_w2t = tw2t.empty() ? nullptr : base + o_w2t;
   m.trans_w1t = tw1t.empty() ? nullptr : base + o_w1t;
   m.trans_wht = twht.empty() ? nullptr : base + o_wht;
+  m.trans_n = tn.empty() ? nullptr : base + o_tn;
   m.roll_tab = reinterpret_cast<const float*>(base + o_tab);
   m.emb_nat = m.roll_tab;
   const float* encp = reinterpret_cast<const float*>(base + o_enc);

@@ -154,6 +154,37 @@ constexpr bool wh_in_lds(int w1_chunk_bytes, int w2_chunk_bytes, int wh_bytes) {
   return 2 * (w1_chunk_bytes + w2_chunk_bytes) + wh_bytes <= WH_LDS_LIMIT;
 }
 
+// --------------------------------------------------------------------------
+// Narrow tiles (bf16, 16 candidates): v_mfma_f32_16x16x32_bf16.  Lane L of
+// the accumulator holds column L%16 and rows 4(L/16) + r, r < 4; operand
+// lane L holds row (A) or column (B) L%16 and 8 contraction slots of lane
+// group L/16.  As with the 32-wide products, the contraction order is free:
+//  * a z operand fragment kf (32 features) is made of the accumulators of
+//    latent blocks 2kf and 2kf+1 (16 features each): slot j of group g is
+//    feature 32kf + 16(j/4) + 4g + j%4, so z never leaves its lane;
+//  * the GELU outputs of a 32-unit hidden chunk (two 16-row output blocks)
+//    form one operand fragment of the second product in the same order;
+//  * embedding fragments use the natural order 32q + 8g + j.
+// Packed blob (pack_transition_narrow in wm_api.hip), 1 KiB A fragments:
+//   W1: chunk c, k-fragment kf, row block rb (16 hidden units 32c + 16rb..):
+//       group (c * NK + kf) * 2 + rb, NK = (D + E) / 32;
+//   W2: chunk c, latent block b (16 rows): group c * (D / 16) + b, after W1;
+//   then b1 (H floats) and b2 (D floats), natural order.
+// --------------------------------------------------------------------------
+__host__ __device__ constexpr inline int narrow_x_feature(int D, int kf, int g, int j) {
+  return kf < D / 32 ? 32 * kf + 16 * (j >> 2) + 4 * g + (j & 3) : D + 32 * (kf - D / 32) + 8 * g + j;
+}
+__host__ __device__ constexpr inline int narrow_g_feature(int g, int j) {
+  return 16 * (j >> 2) + 4 * g + (j & 3);
+}
+struct Narrow {
+  static constexpr size_t w1_groups(int D, int E, int H) { return (size_t)(H / 32) * ((D + E) / 32) * 2; }
+  static constexpr size_t w2_groups(int D, int H) { return (size_t)(H / 32) * (D / 16); }
+  static constexpr size_t bytes(int D, int E, int H) {
+    return (w1_groups(D, E, H) + w2_groups(D, H)) * 1024 + (size_t)(H + D) * 4;
+  }
+};
+
 // Action parameters per step are padded to PMAX in the embedding table
 // (zero weights), so the kernels loop over a fixed count.
 constexpr int PMAX = 8;
@@ -198,6 +229,7 @@ struct DevModel {
   const uint8_t* trans_w2t; // H/32 chunks of W2^T (rollout-loss backward)
   const uint8_t* trans_w1t; // H/32 chunks of W1^T (rollout-loss backward)
   const uint8_t* trans_wht; // Wh^T fragments (paper-form rollout-loss backward)
+  const uint8_t* trans_n;   // narrow-tile transition blob (bf16, d and e multiples of 32), or null
   const float* roll_tab;    // type_emb [K][E + 4] (padded rows), param_w^T [PMAX][E] (zero rows past P), param_b [E], b2 (acc order) [D]
   const float* emb_nat;     // the first three parts of roll_tab
   const float* enc_w1t;     // We1^T [F][Fh] (bf16-rounded values in bf16 mode)

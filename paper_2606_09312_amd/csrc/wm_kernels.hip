@@ -1702,6 +1702,258 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 }
 
 // ==========================================================================
+// Narrow-tile rollout (bf16; d = 32 W): one workgroup of W wavefronts per
+// tile of 16 candidates, on the 16x16x32 matrix-core product (layouts at
+// Narrow in wm_internal.h).  For batches that give at most one tile per
+// compute unit the kernel time is the longest tile's chain of steps, and a
+// step of 16 candidates is half the products and half the GELUs of a
+// 32-candidate step with the same number of exchanges.
+//  * wavefront w owns latent blocks 2w, 2w+1 (16 features each, 4 per lane),
+//    which together are operand fragment w of z: it publishes that fragment
+//    in LDS and, after a barrier, every wavefront reads all fragments of X;
+//  * first product, for its chunks c = w, w + W, ...: two 16-row output
+//    blocks per chunk over the NK fragments of X, bias, GELU, rounding, and
+//    the chunk's GELU fragment into LDS;
+//  * after a barrier, the update of its two latent blocks over every chunk.
+// Weight groups stream from L2 through a register ring that wraps from
+// step to step.  Wavefronts w < E/32 also embed the next step's action and
+// sum the action features.
+typedef float f32x4n __attribute__((ext_vector_type(4)));
+
+template <int D, int E, int NC, int W>
+struct NarrowGeom {
+  static constexpr int NB = D / 16, NBW = NB / W;          // latent blocks, per wavefront
+  static constexpr int NZ = D / 32, NE = E / 32, NK = NZ + NE;
+  static constexpr int NCW = NC / W;                       // first-product chunks per wavefront
+  static constexpr int NA = NCW * NK * 2;                  // first-product groups per step
+  static constexpr int NI = NA + NC * NBW;                 // groups per step
+  static constexpr int W1G = NC * NK * 2;                  // W1 groups in the blob
+  static constexpr int W2G = NC * NB;
+  static constexpr int ring_depth() {
+    for (int r = 12; r > 1; --r)
+      if (NI % r == 0) return r;
+    return 1;
+  }
+  static constexpr int RD = ring_depth();
+  static_assert(NBW == 2 && NZ == W, "wavefront w owns z fragment w");
+  static_assert(NC % W == 0 && NE <= W, "even split");
+  static constexpr int G_BYTES = NC * 1024, X_BYTES = NK * 1024;
+};
+
+template <int D, int E, int NC, int W>
+__global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArgs a) {
+  using NG = NarrowGeom<D, E, NC, W>;
+  constexpr int NK = NG::NK, NZ = NG::NZ, NE = NG::NE, NB = NG::NB, NBW = NG::NBW;
+  constexpr int NCW = NG::NCW, NA = NG::NA, NI = NG::NI, RD = NG::RD, NT = 64 * W;
+
+  extern __shared__ __attribute__((aligned(16))) float tab[];
+  const float* t_emb = tab;
+  const float* t_pw = tab + a.K * temb_stride(E);
+  const float* t_pb = t_pw + PMAX * E;
+  uint8_t* gbuf = reinterpret_cast<uint8_t*>(tab) + a.tab_bytes;     // GELU fragments [NC]
+  uint8_t* xbuf = gbuf + NG::G_BYTES;                                 // X fragments [NK]
+  float* phib = reinterpret_cast<float*>(xbuf + NG::X_BYTES);         // [16][E + 1]
+  const bool do_phi = a.phi != nullptr;
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int n = lane & 15, g = lane >> 4;
+  stage_to_lds(reinterpret_cast<const uint8_t*>(a.tab), reinterpret_cast<uint8_t*>(tab),
+               a.tab_bytes, tid, NT);
+  if (do_phi)
+    for (int i = tid; i < 16 * (E + 1); i += NT) phib[i] = 0.0f;
+
+  const int pos = blockIdx.x * 16 + n;
+  const bool valid = pos < a.B;
+  const int2 pc = valid ? a.perm[pos] : make_int2(0, 0);
+  const int cand = pc.x;
+  const int len = valid ? clampi(a.lens[cand], 0, a.T_max) : 0;
+  const int T_wg = __builtin_amdgcn_readfirstlane(
+      clampi(a.lens[a.perm[blockIdx.x * 16].x], 0, a.T_max));
+
+  const float* b1n = reinterpret_cast<const float*>(a.w1 + (size_t)(NG::W1G + NG::W2G) * 1024);
+  const float* b2n = b1n + NC * 32;
+  // owned latent blocks 2w + bq, their b2, and the b1 of the own chunks
+  const float* zs = a.z0 + (size_t)pc.y * D;
+  f32x4n zq[NBW], b2v[NBW], b1v[NCW][2];
+#pragma unroll
+  for (int bq = 0; bq < NBW; ++bq) {
+    zq[bq] = *reinterpret_cast<const f32x4n*>(zs + 16 * (w * NBW + bq) + 4 * g);
+    b2v[bq] = *reinterpret_cast<const f32x4n*>(b2n + 16 * (w * NBW + bq) + 4 * g);
+  }
+#pragma unroll
+  for (int cw = 0; cw < NCW; ++cw)
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+      b1v[cw][rb] = *reinterpret_cast<const f32x4n*>(b1n + 32 * (w + cw * W) + 16 * rb + 4 * g);
+
+  const int32_t* ty_row = a.types + (size_t)cand * a.T_max;
+  const int32_t* pa_row = a.params + (size_t)cand * a.T_max * a.P;
+  int nx_type = 0;
+  int nx_par[PMAX];
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p) nx_par[p] = 1;
+  if (0 < len) {
+    nx_type = ty_row[0];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[p];
+  }
+  int errbits = 0;
+
+  // embedding fragment q = w of step s (wavefronts w < NE): features
+  // 32q + 8g + j, into LDS as an operand fragment, summed for phi
+  auto embed_share = [&](int s) {
+    if (w >= NE) return;
+    const bool act = s < len;
+    const float af = act ? 1.0f : 0.0f;
+    const bool bad_type = act && (nx_type < 0 || nx_type >= a.K);
+    const int ty = (act && !bad_type) ? nx_type : 0;
+    bool bad_par = false;
+    float u[PMAX];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) {
+      bad_par |= act && nx_par[p] < 1;
+      u[p] = act ? log2f((float)nx_par[p]) : 0.0f;
+    }
+    errbits |= (bad_type ? ERRBIT_TYPE : 0) | (bad_par ? ERRBIT_PARAM : 0);
+    if (s + 1 < len) {
+      nx_type = ty_row[s + 1];
+#pragma unroll
+      for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(s + 1) * a.P + p];
+    }
+    const int f0 = 32 * w + 8 * g;
+    float ev[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ev[j] = t_emb[ty * temb_stride(E) + f0 + j];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ev[j] = fmaf(t_pw[p * E + f0 + j], u[p], ev[j]);
+    bf16x8 f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      ev[j] = (ev[j] + t_pb[f0 + j]) * af;
+      f[j] = (__bf16)ev[j];
+    }
+    *reinterpret_cast<bf16x8*>(xbuf + (NZ + w) * 1024 + lane * 16) = f;
+    if (do_phi) {
+      float* ph = phib + n * (E + 1) + f0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ph[j] += ev[j];
+    }
+  };
+  // publish z fragment w (blocks 2w, 2w+1), read back all of X
+  bf16x8 xf[NK];
+  auto exchange_x = [&]() {
+    bf16x8 f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      f[j] = (__bf16)zq[0][j];
+      f[4 + j] = (__bf16)zq[1][j];
+    }
+    *reinterpret_cast<bf16x8*>(xbuf + w * 1024 + lane * 16) = f;
+    __syncthreads();
+#pragma unroll
+    for (int kf = 0; kf < NK; ++kf) xf[kf] = *reinterpret_cast<const bf16x8*>(xbuf + kf * 1024 + lane * 16);
+  };
+
+  // weight group of stream item i, relative to the wavefront's two bases
+  auto item_off = [](int i) -> size_t {
+    if (i < NA) {
+      const int cw = i / (NK * 2), r = i % (NK * 2);
+      return ((size_t)cw * W * NK * 2 + r) * 1024;
+    }
+    const int j = i - NA;
+    return ((size_t)(j / NBW) * NB + (j % NBW)) * 1024;
+  };
+  gu8* baseA = ((gu8*)(a.w1)) + (size_t)(w * NK * 2) * 1024 + lane * 16;
+  gu8* baseB = ((gu8*)(a.w1)) + (size_t)(NG::W1G + w * NBW) * 1024 + lane * 16;
+  auto item_ptr = [&](gu8* pA, gu8* pB, int i) -> gu32x4* {
+    return reinterpret_cast<gu32x4*>((i < NA ? pA : pB) + item_off(i));
+  };
+  u32x4 ring[RD];
+#pragma unroll
+  for (int i = 0; i < RD; ++i) ring[i] = *item_ptr(baseA, baseB, i);
+
+  wait_vm_then_barrier();
+  embed_share(0);
+  exchange_x();
+
+  for (int t = 0; t < T_wg; ++t) {
+    const bool active = t < len;
+    const float actf = active ? 1.0f : 0.0f;
+    const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
+    gu8* pA = baseA;
+    gu8* pB = baseB;
+    asm volatile("" : "+v"(pA), "+v"(pB));
+    f32x4n acc[2], dz[NBW];
+    acc[0] = f32x4n{}; acc[1] = f32x4n{};
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq) dz[bq] = f32x4n{};
+    u32x4 gcur = {}, gnext = {};
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const u32x4 grp = ring[i % RD];
+      ring[i % RD] = *item_ptr(pA, pB, (i + RD) % NI);   // wraps into the next step
+      if (i < NA) {
+        const int cw = i / (NK * 2), kf = (i / 2) % NK, rb = i % 2;
+        acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, grp), xf[kf], acc[rb], 0, 0, 0);
+        if (kf == NK - 1 && rb == 1) {
+          // bias, GELU, rounding, mask -> the chunk's operand fragment in LDS
+          const int c = w + cw * W;
+          uint32_t gp[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int r0 = (2 * q) & 3, rb0 = (2 * q) >> 2;
+            typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+            const bf16x2 v = {(__bf16)gelu(acc[rb0][r0] + b1v[cw][rb0][r0]),
+                              (__bf16)gelu(acc[rb0][r0 + 1] + b1v[cw][rb0][r0 + 1])};
+            gp[q] = __builtin_bit_cast(uint32_t, v) & amask;
+          }
+          const u32x4 gf = {gp[0], gp[1], gp[2], gp[3]};
+          *reinterpret_cast<u32x4*>(gbuf + c * 1024 + lane * 16) = gf;
+          acc[0] = f32x4n{};
+          acc[1] = f32x4n{};
+        }
+        if (i == NA - 1) {
+          __syncthreads();           // every chunk's GELU fragment is in LDS
+          gcur = lds_group(gbuf, 0, lane);
+          gnext = lds_group(gbuf, NC > 1 ? 1 : 0, lane);
+        }
+      } else {
+        const int j = i - NA, c = j / NBW, bq = j % NBW;
+        dz[bq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, grp),
+                                                         __builtin_bit_cast(bf16x8, gcur), dz[bq], 0, 0, 0);
+        if (bq == NBW - 1) {
+          gcur = gnext;
+          if (c + 2 < NC) gnext = lds_group(gbuf, c + 2, lane);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) zq[bq][r] += dz[bq][r] + b2v[bq][r] * actf;
+    embed_share(t + 1);
+    exchange_x();
+  }
+  if (errbits) atomicOr(a.err, errbits);
+  if (do_phi && valid && w < NE) {   // phi = sum / len over the owned fragment (0 when empty)
+    const float inv = len > 0 ? 1.0f / (float)len : 0.0f;
+    const int f0 = 32 * w + 8 * g;
+    const float* ph = phib + n * (E + 1) + f0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) a.phi[(size_t)cand * E + f0 + j] = ph[j] * inv;
+  }
+  if (valid) {
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq)
+      *reinterpret_cast<f32x4n*>(a.zT + (size_t)cand * D + 16 * (w * NBW + bq) + 4 * g) = zq[bq];
+  }
+}
+
+// ==========================================================================
 // Action features: phi_i = (1/len_i) sum_t e_t.  The sum is regrouped by
 // what varies per step:  sum_t e_t = sum_k n_k type_emb[k] + param_w .
 // sum_t log2(params_t) + len_i param_b, with n_k the number of steps of
@@ -3608,6 +3860,24 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
   return launch_rollout_t<PR, D, E, 1, NORM>(m, a, blocks, st);
 }
 
+// Narrow tiles (16 candidates) for bf16 batches of at most one such tile per
+// compute unit, at d = 256, e = 64 and hidden widths 512 and 1024.
+constexpr int NARROW_MAX_TILES = 256;
+template <int NC>
+hipError_t launch_rollout_narrow(const DevModel& m, RollArgs a, int tiles, hipStream_t st) {
+  using NG = NarrowGeom<256, 64, NC, 8>;
+  a.w1 = m.trans_n;
+  const int lds = m.roll_tab_bytes + NG::G_BYTES + NG::X_BYTES + (a.phi ? 16 * (64 + 1) * 4 : 0);
+  auto kern = rollout_narrow_kernel<256, 64, NC, 8>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
+  }
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(512), lds, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
                           int32_t B, int32_t T_max, float* zT, float* phi, bool* phi_done,
@@ -3626,6 +3896,14 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
   const bool split = tiles <= SPLIT_MAX_TILES && d <= 256;
   const bool norm = m.dims.norm == WM_NORM_L2;
   *phi_done = false;
+  const int ntiles = (B + 15) / 16;
+  if (prec == WM_BF16 && d == 256 && e == 64 && !norm && m.trans_n && B > 0 && ntiles <= NARROW_MAX_TILES) {
+    const int NC = m.dims.trans_hidden / 32;
+    if (NC == 16 || NC == 32) {
+      *phi_done = phi != nullptr;
+      return NC == 16 ? launch_rollout_narrow<16>(m, a, ntiles, st) : launch_rollout_narrow<32>(m, a, ntiles, st);
+    }
+  }
 #define WM_ROLL(PR, D, E)                                                                          \
   return norm ? launch_rollout_de<PR, D, E, true>(m, a, tiles, blocks, waves, split, phi_done, st)  \
               : launch_rollout_de<PR, D, E, false>(m, a, tiles, blocks, waves, split, phi_done, st);

@@ -43,6 +43,7 @@ CASES = [
     ("tiny", "bf16", 300, 1),
     ("ansor_round", "fp32", 300, 1),
     ("ansor_round", "bf16", 300, 1),
+    ("ansor_round", "bf16", 5000, 1),        # 32-candidate tiles (over 256 16-candidate tiles)
     ("long_schedule", "bf16", 270, 1),
     ("large_latent", "bf16", 150, 1),
     ("multi_subgraph", "bf16", 4 * 70, 4),
@@ -323,7 +324,10 @@ def test_large_batch_bucketing(wm, lens_kind):
 PHI_CASES = [
     ("tiny", "fp32", 200, "none"),            # split kernel + phi kernel
     ("tiny", "fp32", 8224, "none"),           # persistent, sums in the kernel
-    ("ansor_round", "bf16", 300, "none"),     # row-owned
+    ("ansor_round", "bf16", 300, "none"),     # narrow tiles (16 candidates)
+    ("ansor_round", "bf16", 4096, "none"),    # narrow tiles, 256 full tiles
+    ("ansor_round", "bf16", 5000, "none"),    # row-owned, 32-candidate tiles
+    ("long_schedule", "bf16", 300, "none"),   # narrow tiles, hidden width 1024
     ("ansor_round", "bf16", 300, "l2"),       # row-owned, paper form
     ("ansor_round", "bf16", 9000, "none"),    # persistent d = 256
     ("ansor_round", "bf16", 9000, "l2"),      # persistent d = 256, paper form
