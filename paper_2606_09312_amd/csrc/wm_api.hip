@@ -107,7 +107,8 @@ void pack_transition(const wm_dims& dm, const wm_weights& w, std::vector<uint8_t
 // Narrow-tile transition blob (bf16; layout at Narrow in wm_internal.h).
 std::vector<uint8_t> pack_transition_narrow(const wm_dims& dm, const wm_weights& w) {
   const int D = dm.d, E = dm.embed_dim, H = dm.trans_hidden, IN = D + E, NK = IN / 32;
-  std::vector<uint8_t> blk(Narrow::bytes(D, E, H), 0);
+  const bool l2 = dm.norm == WM_NORM_L2;
+  std::vector<uint8_t> blk(Narrow::bytes(D, E, H) + (l2 ? Narrow::wh_bytes(D, E) : 0), 0);
   auto put16 = [&](size_t group, int lane, int j, float v) {
     const uint16_t b = f32_to_bf16(v);
     std::memcpy(&blk[group * 1024 + (size_t)lane * 16 + (size_t)j * 2], &b, 2);
@@ -132,6 +133,16 @@ std::vector<uint8_t> pack_transition_narrow(const wm_dims& dm, const wm_weights&
   const size_t tail = (g2 + Narrow::w2_groups(D, H)) * 1024;
   std::memcpy(&blk[tail], w.b1, (size_t)H * 4);
   std::memcpy(&blk[tail + (size_t)H * 4], w.b2, (size_t)D * 4);
+  if (l2) {
+    const size_t base = Narrow::bytes(D, E, H);           // 16-byte aligned: H + D is a multiple of 4
+    for (int b = 0; b < D / 16; ++b)
+      for (int q = 0; q < E / 32; ++q)
+        for (int L = 0; L < 64; ++L)
+          for (int j = 0; j < 8; ++j) {
+            const uint16_t v = f32_to_bf16(w.wh[(size_t)(16 * b + (L & 15)) * E + 32 * q + 8 * (L >> 4) + j]);
+            std::memcpy(&blk[base + ((size_t)b * (E / 32) + q) * 1024 + (size_t)L * 16 + (size_t)j * 2], &v, 2);
+          }
+  }
   return blk;
 }
 

@@ -169,7 +169,9 @@ constexpr bool wh_in_lds(int w1_chunk_bytes, int w2_chunk_bytes, int wh_bytes) {
 //   W1: chunk c, k-fragment kf, row block rb (16 hidden units 32c + 16rb..):
 //       group (c * NK + kf) * 2 + rb, NK = (D + E) / 32;
 //   W2: chunk c, latent block b (16 rows): group c * (D / 16) + b, after W1;
-//   then b1 (H floats) and b2 (D floats), natural order.
+//   then b1 (H floats) and b2 (D floats), natural order;
+//   paper form: then Wh, latent block b (16 rows), embedding fragment q:
+//       group b * (E / 32) + q, slot (g, j) = embedding feature 32q + 8g + j.
 // --------------------------------------------------------------------------
 __host__ __device__ constexpr inline int narrow_x_feature(int D, int kf, int g, int j) {
   return kf < D / 32 ? 32 * kf + 16 * (j >> 2) + 4 * g + (j & 3) : D + 32 * (kf - D / 32) + 8 * g + j;
@@ -183,6 +185,7 @@ struct Narrow {
   static constexpr size_t bytes(int D, int E, int H) {
     return (w1_groups(D, E, H) + w2_groups(D, H)) * 1024 + (size_t)(H + D) * 4;
   }
+  static constexpr size_t wh_bytes(int D, int E) { return (size_t)(D / 16) * (E / 32) * 1024; }
 };
 
 // Action parameters per step are padded to PMAX in the embedding table

@@ -1740,7 +1740,7 @@ struct NarrowGeom {
   static constexpr int G_BYTES = NC * 1024, X_BYTES = NK * 1024;
 };
 
-template <int D, int E, int NC, int W>
+template <int D, int E, int NC, int W, bool NORM>
 __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArgs a) {
   using NG = NarrowGeom<D, E, NC, W>;
   constexpr int NK = NG::NK, NZ = NG::NZ, NE = NG::NE, NB = NG::NB, NBW = NG::NBW;
@@ -1752,7 +1752,8 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
   const float* t_pb = t_pw + PMAX * E;
   uint8_t* gbuf = reinterpret_cast<uint8_t*>(tab) + a.tab_bytes;     // GELU fragments [NC]
   uint8_t* xbuf = gbuf + NG::G_BYTES;                                 // X fragments [NK]
-  float* phib = reinterpret_cast<float*>(xbuf + NG::X_BYTES);         // [16][E + 1]
+  float* dots = reinterpret_cast<float*>(xbuf + NG::X_BYTES);         // paper form: [W][3][16]
+  float* phib = dots + (NORM ? W * 3 * 16 : 0);                       // [16][E + 1]
   const bool do_phi = a.phi != nullptr;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -1799,16 +1800,14 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
   }
   int errbits = 0;
 
-  // embedding fragment q = w of step s (wavefronts w < NE): features
-  // 32q + 8g + j, into LDS as an operand fragment, summed for phi
-  auto embed_share = [&](int s) {
-    if (w >= NE) return;
+  // Embedding of step s: the action's kind and log2 parameters (error bits,
+  // prefetch of step s + 1), then fragment q (features 32q + 8g + j).
+  auto decode = [&](int s, int& ty, float (&u)[PMAX], float& af) {
     const bool act = s < len;
-    const float af = act ? 1.0f : 0.0f;
+    af = act ? 1.0f : 0.0f;
     const bool bad_type = act && (nx_type < 0 || nx_type >= a.K);
-    const int ty = (act && !bad_type) ? nx_type : 0;
+    ty = (act && !bad_type) ? nx_type : 0;
     bool bad_par = false;
-    float u[PMAX];
 #pragma unroll
     for (int p = 0; p < PMAX; ++p) {
       bad_par |= act && nx_par[p] < 1;
@@ -1820,7 +1819,10 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
 #pragma unroll
       for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(s + 1) * a.P + p];
     }
-    const int f0 = 32 * w + 8 * g;
+  };
+  // fragment q; the wavefront q also adds it to the phi sums
+  auto embed_frag = [&](int q, int ty, const float (&u)[PMAX], float af) -> bf16x8 {
+    const int f0 = 32 * q + 8 * g;
     float ev[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) ev[j] = t_emb[ty * temb_stride(E) + f0 + j];
@@ -1834,15 +1836,25 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
       ev[j] = (ev[j] + t_pb[f0 + j]) * af;
       f[j] = (__bf16)ev[j];
     }
-    *reinterpret_cast<bf16x8*>(xbuf + (NZ + w) * 1024 + lane * 16) = f;
-    if (do_phi) {
+    if (do_phi && q == w) {
       float* ph = phib + n * (E + 1) + f0;
 #pragma unroll
       for (int j = 0; j < 8; ++j) ph[j] += ev[j];
     }
+    return f;
   };
-  // publish z fragment w (blocks 2w, 2w+1), read back all of X
+  // residual form: wavefront w < NE embeds fragment w into LDS
+  auto embed_share = [&](int s) {
+    if (w >= NE) return;
+    int ty;
+    float u[PMAX], af;
+    decode(s, ty, u, af);
+    *reinterpret_cast<bf16x8*>(xbuf + (NZ + w) * 1024 + lane * 16) = embed_frag(w, ty, u, af);
+  };
+  // publish z fragment w (blocks 2w, 2w+1), read back all of X (paper
+  // form: every wavefront holds the embedding fragments itself)
   bf16x8 xf[NK];
+  bf16x8 xe[NORM ? NE : 1];
   auto exchange_x = [&]() {
     bf16x8 f;
 #pragma unroll
@@ -1853,7 +1865,73 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     *reinterpret_cast<bf16x8*>(xbuf + w * 1024 + lane * 16) = f;
     __syncthreads();
 #pragma unroll
-    for (int kf = 0; kf < NK; ++kf) xf[kf] = *reinterpret_cast<const bf16x8*>(xbuf + kf * 1024 + lane * 16);
+    for (int kf = 0; kf < NK; ++kf) {
+      if (NORM && kf >= NZ) xf[kf] = xe[NORM ? kf - NZ : 0];
+      else xf[kf] = *reinterpret_cast<const bf16x8*>(xbuf + kf * 1024 + lane * 16);
+    }
+  };
+  // Paper form (Sec. 3.4): at a step boundary the finished step's u is
+  // renormalised and, for an active next step, projected off the normal
+  // v = Wh e of its embedding: z' = (u - (v.u / v.v) v) / |u|.  The owned
+  // blocks' v come from the matrix cores (Wh groups in registers); the dots
+  // are summed over the candidate's four lane groups, then over the
+  // wavefronts through LDS.
+  u32x4 whq[NORM ? NBW * NE : 1];
+  if constexpr (NORM) {
+    const uint8_t* whb = a.w1 + Narrow::bytes(D, E, NC * 32);
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq)
+#pragma unroll
+      for (int q = 0; q < NE; ++q)
+        whq[bq * NE + q] = *reinterpret_cast<const u32x4*>(whb + ((size_t)(w * NBW + bq) * NE + q) * 1024 + lane * 16);
+  }
+  auto embed_all = [&](int s) {
+    int ty;
+    float u[PMAX], af;
+    decode(s, ty, u, af);
+#pragma unroll
+    for (int q = 0; q < NE; ++q) xe[NORM ? q : 0] = embed_frag(q, ty, u, af);
+  };
+  auto boundary = [&](bool renorm, bool project) {
+    f32x4n vq[NBW];
+    float vz = 0.0f, vv = 0.0f, zz = 0.0f;
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq) {
+      f32x4n v = {};
+#pragma unroll
+      for (int q = 0; q < NE; ++q)
+        v = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, whq[NORM ? bq * NE + q : 0]),
+                                                    xe[NORM ? q : 0], v, 0, 0, 0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        vz = fmaf(v[r], zq[bq][r], vz);
+        vv = fmaf(v[r], v[r], vv);
+        zz = fmaf(zq[bq][r], zq[bq][r], zz);
+      }
+      vq[bq] = v;
+    }
+    vz += __shfl_xor(vz, 16); vz += __shfl_xor(vz, 32);
+    vv += __shfl_xor(vv, 16); vv += __shfl_xor(vv, 32);
+    zz += __shfl_xor(zz, 16); zz += __shfl_xor(zz, 32);
+    if (g == 0) {
+      dots[(w * 3 + 0) * 16 + n] = vz;
+      dots[(w * 3 + 1) * 16 + n] = vv;
+      dots[(w * 3 + 2) * 16 + n] = zz;
+    }
+    __syncthreads();
+    vz = 0.0f; vv = 0.0f; zz = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < W; ++ww) {
+      vz += dots[(ww * 3 + 0) * 16 + n];
+      vv += dots[(ww * 3 + 1) * 16 + n];
+      zz += dots[(ww * 3 + 2) * 16 + n];
+    }
+    const float sc = (renorm && zz > 0.0f) ? rsqrtf(zz) : 1.0f;
+    const float al = (project && vv > 0.0f) ? vz / vv : 0.0f;
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) zq[bq][r] = (zq[bq][r] - al * vq[bq][r]) * sc;
   };
 
   // weight group of stream item i, relative to the wavefront's two bases
@@ -1875,7 +1953,12 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
   for (int i = 0; i < RD; ++i) ring[i] = *item_ptr(baseA, baseB, i);
 
   wait_vm_then_barrier();
-  embed_share(0);
+  if constexpr (NORM) {
+    embed_all(0);
+    boundary(false, 0 < len);
+  } else {
+    embed_share(0);
+  }
   exchange_x();
 
   for (int t = 0; t < T_wg; ++t) {
@@ -1935,7 +2018,12 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     for (int bq = 0; bq < NBW; ++bq)
 #pragma unroll
       for (int r = 0; r < 4; ++r) zq[bq][r] += dz[bq][r] + b2v[bq][r] * actf;
-    embed_share(t + 1);
+    if constexpr (NORM) {
+      embed_all(t + 1);
+      boundary(active, t + 1 < len);
+    } else {
+      embed_share(t + 1);
+    }
     exchange_x();
   }
   if (errbits) atomicOr(a.err, errbits);
@@ -3863,12 +3951,13 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
 // Narrow tiles (16 candidates) for bf16 batches of at most one such tile per
 // compute unit, at d = 256, e = 64 and hidden widths 512 and 1024.
 constexpr int NARROW_MAX_TILES = 256;
-template <int NC>
+template <int NC, bool NORM>
 hipError_t launch_rollout_narrow(const DevModel& m, RollArgs a, int tiles, hipStream_t st) {
   using NG = NarrowGeom<256, 64, NC, 8>;
   a.w1 = m.trans_n;
-  const int lds = m.roll_tab_bytes + NG::G_BYTES + NG::X_BYTES + (a.phi ? 16 * (64 + 1) * 4 : 0);
-  auto kern = rollout_narrow_kernel<256, 64, NC, 8>;
+  const int lds = m.roll_tab_bytes + NG::G_BYTES + NG::X_BYTES + (NORM ? 8 * 3 * 16 * 4 : 0) +
+                  (a.phi ? 16 * (64 + 1) * 4 : 0);
+  auto kern = rollout_narrow_kernel<256, 64, NC, 8, NORM>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -3897,11 +3986,15 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
   const bool norm = m.dims.norm == WM_NORM_L2;
   *phi_done = false;
   const int ntiles = (B + 15) / 16;
-  if (prec == WM_BF16 && d == 256 && e == 64 && !norm && m.trans_n && B > 0 && ntiles <= NARROW_MAX_TILES) {
+  if (prec == WM_BF16 && d == 256 && e == 64 && m.trans_n && B > 0 && ntiles <= NARROW_MAX_TILES) {
     const int NC = m.dims.trans_hidden / 32;
     if (NC == 16 || NC == 32) {
       *phi_done = phi != nullptr;
-      return NC == 16 ? launch_rollout_narrow<16>(m, a, ntiles, st) : launch_rollout_narrow<32>(m, a, ntiles, st);
+      if (norm)
+        return NC == 16 ? launch_rollout_narrow<16, true>(m, a, ntiles, st)
+                        : launch_rollout_narrow<32, true>(m, a, ntiles, st);
+      return NC == 16 ? launch_rollout_narrow<16, false>(m, a, ntiles, st)
+                      : launch_rollout_narrow<32, false>(m, a, ntiles, st);
     }
   }
 #define WM_ROLL(PR, D, E)                                                                          \

@@ -46,13 +46,16 @@ def _check_unit(g, lens, z0_of):
     np.testing.assert_array_equal(g["zT"][~pos], z0_of[~pos])
 
 
-# Scaled batches (one tile per compute unit or fewer: the split kernel at
-# d <= 256 except fp32 d = 256, the persistent kernel otherwise)
+# Scaled batches (one tile per compute unit or fewer): 16-candidate tiles
+# for bf16 d = 256 up to 4096 candidates, 32-candidate row-owned tiles for
+# d = 256 otherwise, the split kernel at d = 64, the persistent kernel at
+# d = 512
 CASES = [
     ("tiny", "fp32", 300, 1),
     ("tiny", "bf16", 300, 1),
     ("ansor_round", "fp32", 300, 1),
     ("ansor_round", "bf16", 300, 1),
+    ("ansor_round", "bf16", 5000, 1),
     ("long_schedule", "bf16", 270, 1),
     ("large_latent", "bf16", 150, 1),
     ("multi_subgraph", "bf16", 4 * 70, 4),
