@@ -104,44 +104,54 @@ void pack_transition(const wm_dims& dm, const wm_weights& w, std::vector<uint8_t
   }
 }
 
-// Narrow-tile transition blob (bf16; layout at Narrow in wm_internal.h).
+// Narrow-tile transition blob (layout at Narrow in wm_internal.h): bf16
+// (gpk = 1, 8 bf16 per lane and group) or fp32 (gpk = 2, 4 floats per lane
+// and group, slots 4hh .. 4hh + 3).
 std::vector<uint8_t> pack_transition_narrow(const wm_dims& dm, const wm_weights& w) {
   const int D = dm.d, E = dm.embed_dim, H = dm.trans_hidden, IN = D + E, NK = IN / 32;
-  const bool l2 = dm.norm == WM_NORM_L2;
-  std::vector<uint8_t> blk(Narrow::bytes(D, E, H) + (l2 ? Narrow::wh_bytes(D, E) : 0), 0);
-  auto put16 = [&](size_t group, int lane, int j, float v) {
-    const uint16_t b = f32_to_bf16(v);
-    std::memcpy(&blk[group * 1024 + (size_t)lane * 16 + (size_t)j * 2], &b, 2);
+  const bool bf = dm.precision == WM_BF16, l2 = dm.norm == WM_NORM_L2;
+  const int gpk = bf ? 1 : 2, per = 8 / gpk;                 // slots per lane and group
+  std::vector<uint8_t> blk(Narrow::bytes(D, E, H, gpk) + (l2 ? Narrow::wh_bytes(D, E, gpk) : 0), 0);
+  // slot j of the operand fragment starting at group frag_group0 (groups
+  // counted from byte `base`): group half j / per, position j % per
+  auto put_at = [&](size_t base, size_t frag_group0, int lane, int j, float v) {
+    const size_t off = base + (frag_group0 + (size_t)(j / per)) * 1024 + (size_t)lane * 16;
+    if (bf) {
+      const uint16_t b = f32_to_bf16(v);
+      std::memcpy(&blk[off + (size_t)(j % per) * 2], &b, 2);
+    } else {
+      std::memcpy(&blk[off + (size_t)(j % per) * 4], &v, 4);
+    }
   };
+  auto put = [&](size_t frag_group0, int lane, int j, float v) { put_at(0, frag_group0, lane, j, v); };
   for (int c = 0; c < H / 32; ++c)
     for (int kf = 0; kf < NK; ++kf)
       for (int rb = 0; rb < 2; ++rb)
         for (int L = 0; L < 64; ++L)
           for (int j = 0; j < 8; ++j) {
             const int hid = 32 * c + 16 * rb + (L & 15);
-            put16(((size_t)c * NK + kf) * 2 + rb, L, j,
-                  w.w1[(size_t)hid * IN + narrow_x_feature(D, kf, L >> 4, j)]);
+            put((((size_t)c * NK + kf) * 2 + rb) * gpk, L, j,
+                w.w1[(size_t)hid * IN + narrow_x_feature(D, kf, L >> 4, j)]);
           }
-  const size_t g2 = Narrow::w1_groups(D, E, H);
+  const size_t g2 = Narrow::w1_groups(D, E, H, gpk);
   for (int c = 0; c < H / 32; ++c)
     for (int b = 0; b < D / 16; ++b)
       for (int L = 0; L < 64; ++L)
         for (int j = 0; j < 8; ++j) {
           const int row = 16 * b + (L & 15), hid = 32 * c + narrow_g_feature(L >> 4, j);
-          put16(g2 + (size_t)c * (D / 16) + b, L, j, w.w2[(size_t)row * H + hid]);
+          put(g2 + ((size_t)c * (D / 16) + b) * gpk, L, j, w.w2[(size_t)row * H + hid]);
         }
-  const size_t tail = (g2 + Narrow::w2_groups(D, H)) * 1024;
+  const size_t tail = (g2 + Narrow::w2_groups(D, H, gpk)) * 1024;
   std::memcpy(&blk[tail], w.b1, (size_t)H * 4);
   std::memcpy(&blk[tail + (size_t)H * 4], w.b2, (size_t)D * 4);
   if (l2) {
-    const size_t base = Narrow::bytes(D, E, H);           // 16-byte aligned: H + D is a multiple of 4
+    const size_t base = Narrow::bytes(D, E, H, gpk);          // 16-byte aligned
     for (int b = 0; b < D / 16; ++b)
       for (int q = 0; q < E / 32; ++q)
         for (int L = 0; L < 64; ++L)
-          for (int j = 0; j < 8; ++j) {
-            const uint16_t v = f32_to_bf16(w.wh[(size_t)(16 * b + (L & 15)) * E + 32 * q + 8 * (L >> 4) + j]);
-            std::memcpy(&blk[base + ((size_t)b * (E / 32) + q) * 1024 + (size_t)L * 16 + (size_t)j * 2], &v, 2);
-          }
+          for (int j = 0; j < 8; ++j)
+            put_at(base, ((size_t)b * (E / 32) + q) * gpk, L, j,
+                w.wh[(size_t)(16 * b + (L & 15)) * E + 32 * q + 8 * (L >> 4) + j]);
   }
   return blk;
 }
@@ -403,7 +413,6 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
     cost = pack_cost<GeomBF16>(dm, *w);
     if (l2) twh = pack_hyper<GeomBF16>(dm, *w);
     if (l2 && E % 32 == 0) twht = pack_hyper_t<GeomBF16>(dm, *w);
-    if (D % 32 == 0 && E % 32 == 0) tn = pack_transition_narrow(dm, *w);
     m.w1_chunk_bytes = TransChunk<GeomBF16>::w1_bytes(D, E);
     m.w2_chunk_bytes = TransChunk<GeomBF16>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomBF16>::bytes(D, E, HW);
@@ -418,6 +427,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
     m.w2_chunk_bytes = TransChunk<GeomF32>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomF32>::bytes(D, E, HW);
   }
+  if (D % 32 == 0 && E % 32 == 0) tn = pack_transition_narrow(dm, *w);
   // rollout table: type_emb [K][E + 4], param_w^T [PMAX][E], param_b [E], b2 (accumulator order)
   std::vector<float> tab;
   tab.reserve((size_t)K * temb_stride(E) + (size_t)PMAX * E + E + D + 4);

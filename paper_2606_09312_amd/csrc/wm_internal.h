@@ -165,13 +165,16 @@ constexpr bool wh_in_lds(int w1_chunk_bytes, int w2_chunk_bytes, int wh_bytes) {
 //  * the GELU outputs of a 32-unit hidden chunk (two 16-row output blocks)
 //    form one operand fragment of the second product in the same order;
 //  * embedding fragments use the natural order 32q + 8g + j.
-// Packed blob (pack_transition_narrow in wm_api.hip), 1 KiB A fragments:
+// Packed blob (pack_transition_narrow in wm_api.hip), 1 KiB groups of A
+// operands, gpk groups per operand fragment (bf16: 1, one 16x16x32 product;
+// fp32: 2, four 16x16x4 products each, slots 4hh .. 4hh + 3 in half hh):
 //   W1: chunk c, k-fragment kf, row block rb (16 hidden units 32c + 16rb..):
-//       group (c * NK + kf) * 2 + rb, NK = (D + E) / 32;
-//   W2: chunk c, latent block b (16 rows): group c * (D / 16) + b, after W1;
+//       group ((c * NK + kf) * 2 + rb) * gpk + hh, NK = (D + E) / 32;
+//   W2: chunk c, latent block b (16 rows): group (c * (D / 16) + b) * gpk + hh,
+//       after W1;
 //   then b1 (H floats) and b2 (D floats), natural order;
 //   paper form: then Wh, latent block b (16 rows), embedding fragment q:
-//       group b * (E / 32) + q, slot (g, j) = embedding feature 32q + 8g + j.
+//       group (b * (E / 32) + q) * gpk + hh, slot j = embedding feature 32q + 8g + j.
 // --------------------------------------------------------------------------
 __host__ __device__ constexpr inline int narrow_x_feature(int D, int kf, int g, int j) {
   return kf < D / 32 ? 32 * kf + 16 * (j >> 2) + 4 * g + (j & 3) : D + 32 * (kf - D / 32) + 8 * g + j;
@@ -180,12 +183,12 @@ __host__ __device__ constexpr inline int narrow_g_feature(int g, int j) {
   return 16 * (j >> 2) + 4 * g + (j & 3);
 }
 struct Narrow {
-  static constexpr size_t w1_groups(int D, int E, int H) { return (size_t)(H / 32) * ((D + E) / 32) * 2; }
-  static constexpr size_t w2_groups(int D, int H) { return (size_t)(H / 32) * (D / 16); }
-  static constexpr size_t bytes(int D, int E, int H) {
-    return (w1_groups(D, E, H) + w2_groups(D, H)) * 1024 + (size_t)(H + D) * 4;
+  static constexpr size_t w1_groups(int D, int E, int H, int gpk) { return (size_t)(H / 32) * ((D + E) / 32) * 2 * gpk; }
+  static constexpr size_t w2_groups(int D, int H, int gpk) { return (size_t)(H / 32) * (D / 16) * gpk; }
+  static constexpr size_t bytes(int D, int E, int H, int gpk) {
+    return (w1_groups(D, E, H, gpk) + w2_groups(D, H, gpk)) * 1024 + (size_t)(H + D) * 4;
   }
-  static constexpr size_t wh_bytes(int D, int E) { return (size_t)(D / 16) * (E / 32) * 1024; }
+  static constexpr size_t wh_bytes(int D, int E, int gpk) { return (size_t)(D / 16) * (E / 32) * gpk * 1024; }
 };
 
 // Action parameters per step are padded to PMAX in the embedding table
@@ -232,7 +235,7 @@ struct DevModel {
   const uint8_t* trans_w2t; // H/32 chunks of W2^T (rollout-loss backward)
   const uint8_t* trans_w1t; // H/32 chunks of W1^T (rollout-loss backward)
   const uint8_t* trans_wht; // Wh^T fragments (paper-form rollout-loss backward)
-  const uint8_t* trans_n;   // narrow-tile transition blob (bf16, d and e multiples of 32), or null
+  const uint8_t* trans_n;   // narrow-tile transition blob (d and e multiples of 32), or null
   const float* roll_tab;    // type_emb [K][E + 4] (padded rows), param_w^T [PMAX][E] (zero rows past P), param_b [E], b2 (acc order) [D]
   const float* emb_nat;     // the first three parts of roll_tab
   const float* enc_w1t;     // We1^T [F][Fh] (bf16-rounded values in bf16 mode)

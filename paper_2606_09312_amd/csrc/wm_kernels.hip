@@ -1702,12 +1702,12 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 }
 
 // ==========================================================================
-// Narrow-tile rollout (bf16; d = 32 W): one workgroup of W wavefronts per
-// tile of 16 candidates, on the 16x16x32 matrix-core product (layouts at
-// Narrow in wm_internal.h).  For batches that give at most one tile per
-// compute unit the kernel time is the longest tile's chain of steps, and a
-// step of 16 candidates is half the products and half the GELUs of a
-// 32-candidate step with the same number of exchanges.
+// Narrow-tile rollout (d = 32 W): one workgroup of W wavefronts per tile of
+// 16 candidates, on the 16x16 matrix-core products (layouts at Narrow in
+// wm_internal.h).  For batches that give at most one tile per compute unit
+// the kernel time is the longest tile's chain of steps, and a step of 16
+// candidates is half the products and half the GELUs of a 32-candidate step
+// with the same number of exchanges.
 //  * wavefront w owns latent blocks 2w, 2w+1 (16 features each, 4 per lane),
 //    which together are operand fragment w of z: it publishes that fragment
 //    in LDS and, after a barrier, every wavefront reads all fragments of X;
@@ -1718,17 +1718,87 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 // Weight groups stream from L2 through a register ring that wraps from
 // step to step.  Wavefronts w < E/32 also embed the next step's action and
 // sum the action features.
+//
+// An operand fragment is 8 values per lane (32 contraction slots over the 4
+// lane groups).  bf16: one 16x16x32 product per fragment, one 1 KiB group of
+// A operands.  fp32: four 16x16x4 products per 1 KiB group, two groups per
+// fragment (slots 4hh .. 4hh + 3 in half hh); fragments in LDS as two 1 KiB
+// halves.
 typedef float f32x4n __attribute__((ext_vector_type(4)));
+typedef float f32x8n __attribute__((ext_vector_type(8)));
 
-template <int D, int E, int NC, int W>
+struct NarrowBF16 {
+  using XF = bf16x8;
+  static constexpr int GPK = 1;                 // 1 KiB groups per fragment
+  static __device__ __forceinline__ XF cvt(const float (&v)[8]) {
+    XF f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] = (__bf16)v[j];
+    return f;
+  }
+  static __device__ __forceinline__ f32x4n mma(u32x4 grp, int, const XF& x, f32x4n acc) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, grp), x, acc, 0, 0, 0);
+  }
+  static __device__ __forceinline__ void store(uint8_t* buf, int frag, int lane, const XF& x) {
+    *reinterpret_cast<XF*>(buf + frag * 1024 + lane * 16) = x;
+  }
+  static __device__ __forceinline__ XF load(const uint8_t* buf, int frag, int lane) {
+    return *reinterpret_cast<const XF*>(buf + frag * 1024 + lane * 16);
+  }
+  // GELU outputs (masked) as an operand fragment
+  static __device__ __forceinline__ XF gfrag(const float (&v)[8], uint32_t m) {
+    u32x4 u = __builtin_bit_cast(u32x4, cvt(v));
+    u &= m;
+    return __builtin_bit_cast(XF, u);
+  }
+};
+
+struct NarrowF32 {
+  using XF = f32x8n;
+  static constexpr int GPK = 2;
+  static __device__ __forceinline__ XF cvt(const float (&v)[8]) {
+    XF f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] = v[j];
+    return f;
+  }
+  static __device__ __forceinline__ f32x4n mma(u32x4 grp, int hh, const XF& x, f32x4n acc) {
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const uint32_t a = grp[jj];
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a), x[4 * hh + jj], acc, 0, 0, 0);
+    }
+    return acc;
+  }
+  static __device__ __forceinline__ void store(uint8_t* buf, int frag, int lane, const XF& x) {
+    const f32x4n lo = {x[0], x[1], x[2], x[3]}, hi = {x[4], x[5], x[6], x[7]};
+    *reinterpret_cast<f32x4n*>(buf + (2 * frag) * 1024 + lane * 16) = lo;
+    *reinterpret_cast<f32x4n*>(buf + (2 * frag + 1) * 1024 + lane * 16) = hi;
+  }
+  static __device__ __forceinline__ XF load(const uint8_t* buf, int frag, int lane) {
+    const f32x4n lo = *reinterpret_cast<const f32x4n*>(buf + (2 * frag) * 1024 + lane * 16);
+    const f32x4n hi = *reinterpret_cast<const f32x4n*>(buf + (2 * frag + 1) * 1024 + lane * 16);
+    const XF x = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return x;
+  }
+  static __device__ __forceinline__ XF gfrag(const float (&v)[8], uint32_t m) {
+    XF f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] = __uint_as_float(__float_as_uint(v[j]) & m);
+    return f;
+  }
+};
+
+template <class NP, int D, int E, int NC, int W>
 struct NarrowGeom {
+  static constexpr int GPK = NP::GPK;
   static constexpr int NB = D / 16, NBW = NB / W;          // latent blocks, per wavefront
   static constexpr int NZ = D / 32, NE = E / 32, NK = NZ + NE;
   static constexpr int NCW = NC / W;                       // first-product chunks per wavefront
-  static constexpr int NA = NCW * NK * 2;                  // first-product groups per step
-  static constexpr int NI = NA + NC * NBW;                 // groups per step
-  static constexpr int W1G = NC * NK * 2;                  // W1 groups in the blob
-  static constexpr int W2G = NC * NB;
+  static constexpr int NA = NCW * NK * 2 * GPK;            // first-product groups per step
+  static constexpr int NI = NA + NC * NBW * GPK;           // groups per step
+  static constexpr int W1G = NC * NK * 2 * GPK;            // W1 groups in the blob
+  static constexpr int W2G = NC * NB * GPK;
   static constexpr int ring_depth() {
     for (int r = 12; r > 1; --r)
       if (NI % r == 0) return r;
@@ -1737,13 +1807,14 @@ struct NarrowGeom {
   static constexpr int RD = ring_depth();
   static_assert(NBW == 2 && NZ == W, "wavefront w owns z fragment w");
   static_assert(NC % W == 0 && NE <= W, "even split");
-  static constexpr int G_BYTES = NC * 1024, X_BYTES = NK * 1024;
+  static constexpr int G_BYTES = NC * GPK * 1024, X_BYTES = NK * GPK * 1024;
 };
 
-template <int D, int E, int NC, int W, bool NORM>
+template <class NP, int D, int E, int NC, int W, bool NORM>
 __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArgs a) {
-  using NG = NarrowGeom<D, E, NC, W>;
-  constexpr int NK = NG::NK, NZ = NG::NZ, NE = NG::NE, NB = NG::NB, NBW = NG::NBW;
+  using NG = NarrowGeom<NP, D, E, NC, W>;
+  using XF = typename NP::XF;
+  constexpr int GPK = NG::GPK, NK = NG::NK, NZ = NG::NZ, NE = NG::NE, NB = NG::NB, NBW = NG::NBW;
   constexpr int NCW = NG::NCW, NA = NG::NA, NI = NG::NI, RD = NG::RD, NT = 64 * W;
 
   extern __shared__ __attribute__((aligned(16))) float tab[];
@@ -1821,7 +1892,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     }
   };
   // fragment q; the wavefront q also adds it to the phi sums
-  auto embed_frag = [&](int q, int ty, const float (&u)[PMAX], float af) -> bf16x8 {
+  auto embed_frag = [&](int q, int ty, const float (&u)[PMAX], float af) -> XF {
     const int f0 = 32 * q + 8 * g;
     float ev[8];
 #pragma unroll
@@ -1830,18 +1901,14 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     for (int p = 0; p < PMAX; ++p)
 #pragma unroll
       for (int j = 0; j < 8; ++j) ev[j] = fmaf(t_pw[p * E + f0 + j], u[p], ev[j]);
-    bf16x8 f;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      ev[j] = (ev[j] + t_pb[f0 + j]) * af;
-      f[j] = (__bf16)ev[j];
-    }
+    for (int j = 0; j < 8; ++j) ev[j] = (ev[j] + t_pb[f0 + j]) * af;
     if (do_phi && q == w) {
       float* ph = phib + n * (E + 1) + f0;
 #pragma unroll
       for (int j = 0; j < 8; ++j) ph[j] += ev[j];
     }
-    return f;
+    return NP::cvt(ev);
   };
   // residual form: wavefront w < NE embeds fragment w into LDS
   auto embed_share = [&](int s) {
@@ -1849,25 +1916,25 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     int ty;
     float u[PMAX], af;
     decode(s, ty, u, af);
-    *reinterpret_cast<bf16x8*>(xbuf + (NZ + w) * 1024 + lane * 16) = embed_frag(w, ty, u, af);
+    NP::store(xbuf, NZ + w, lane, embed_frag(w, ty, u, af));
   };
   // publish z fragment w (blocks 2w, 2w+1), read back all of X (paper
   // form: every wavefront holds the embedding fragments itself)
-  bf16x8 xf[NK];
-  bf16x8 xe[NORM ? NE : 1];
+  XF xf[NK];
+  XF xe[NORM ? NE : 1];
   auto exchange_x = [&]() {
-    bf16x8 f;
+    float v[8];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      f[j] = (__bf16)zq[0][j];
-      f[4 + j] = (__bf16)zq[1][j];
+      v[j] = zq[0][j];
+      v[4 + j] = zq[1][j];
     }
-    *reinterpret_cast<bf16x8*>(xbuf + w * 1024 + lane * 16) = f;
+    NP::store(xbuf, w, lane, NP::cvt(v));
     __syncthreads();
 #pragma unroll
     for (int kf = 0; kf < NK; ++kf) {
       if (NORM && kf >= NZ) xf[kf] = xe[NORM ? kf - NZ : 0];
-      else xf[kf] = *reinterpret_cast<const bf16x8*>(xbuf + kf * 1024 + lane * 16);
+      else xf[kf] = NP::load(xbuf, kf, lane);
     }
   };
   // Paper form (Sec. 3.4): at a step boundary the finished step's u is
@@ -1876,14 +1943,12 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
   // blocks' v come from the matrix cores (Wh groups in registers); the dots
   // are summed over the candidate's four lane groups, then over the
   // wavefronts through LDS.
-  u32x4 whq[NORM ? NBW * NE : 1];
+  u32x4 whq[NORM ? NBW * NE * GPK : 1];
   if constexpr (NORM) {
-    const uint8_t* whb = a.w1 + Narrow::bytes(D, E, NC * 32);
+    const uint8_t* whb = a.w1 + Narrow::bytes(D, E, NC * 32, GPK);
 #pragma unroll
-    for (int bq = 0; bq < NBW; ++bq)
-#pragma unroll
-      for (int q = 0; q < NE; ++q)
-        whq[bq * NE + q] = *reinterpret_cast<const u32x4*>(whb + ((size_t)(w * NBW + bq) * NE + q) * 1024 + lane * 16);
+    for (int i = 0; i < NBW * NE * GPK; ++i)
+      whq[i] = *reinterpret_cast<const u32x4*>(whb + ((size_t)w * NBW * NE * GPK + i) * 1024 + lane * 16);
   }
   auto embed_all = [&](int s) {
     int ty;
@@ -1900,8 +1965,9 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
       f32x4n v = {};
 #pragma unroll
       for (int q = 0; q < NE; ++q)
-        v = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, whq[NORM ? bq * NE + q : 0]),
-                                                    xe[NORM ? q : 0], v, 0, 0, 0);
+#pragma unroll
+        for (int hh = 0; hh < GPK; ++hh)
+          v = NP::mma(whq[NORM ? (bq * NE + q) * GPK + hh : 0], hh, xe[NORM ? q : 0], v);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         vz = fmaf(v[r], zq[bq][r], vz);
@@ -1937,14 +2003,15 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
   // weight group of stream item i, relative to the wavefront's two bases
   auto item_off = [](int i) -> size_t {
     if (i < NA) {
-      const int cw = i / (NK * 2), r = i % (NK * 2);
-      return ((size_t)cw * W * NK * 2 + r) * 1024;
+      const int cw = i / (NK * 2 * GPK), r = i % (NK * 2 * GPK);
+      return ((size_t)cw * W * NK * 2 * GPK + r) * 1024;
     }
-    const int j = i - NA;
-    return ((size_t)(j / NBW) * NB + (j % NBW)) * 1024;
+    const int j = i - NA;       // (chunk, own block, half)
+    const int c = j / (NBW * GPK), r = j % (NBW * GPK);
+    return ((size_t)c * NB * GPK + r) * 1024;
   };
-  gu8* baseA = ((gu8*)(a.w1)) + (size_t)(w * NK * 2) * 1024 + lane * 16;
-  gu8* baseB = ((gu8*)(a.w1)) + (size_t)(NG::W1G + w * NBW) * 1024 + lane * 16;
+  gu8* baseA = ((gu8*)(a.w1)) + (size_t)(w * NK * 2 * GPK) * 1024 + lane * 16;
+  gu8* baseB = ((gu8*)(a.w1)) + (size_t)(NG::W1G + w * NBW * GPK) * 1024 + lane * 16;
   auto item_ptr = [&](gu8* pA, gu8* pB, int i) -> gu32x4* {
     return reinterpret_cast<gu32x4*>((i < NA ? pA : pB) + item_off(i));
   };
@@ -1972,44 +2039,36 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     acc[0] = f32x4n{}; acc[1] = f32x4n{};
 #pragma unroll
     for (int bq = 0; bq < NBW; ++bq) dz[bq] = f32x4n{};
-    u32x4 gcur = {}, gnext = {};
+    XF gcur = {}, gnext = {};
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const u32x4 grp = ring[i % RD];
       ring[i % RD] = *item_ptr(pA, pB, (i + RD) % NI);   // wraps into the next step
       if (i < NA) {
-        const int cw = i / (NK * 2), kf = (i / 2) % NK, rb = i % 2;
-        acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, grp), xf[kf], acc[rb], 0, 0, 0);
-        if (kf == NK - 1 && rb == 1) {
+        const int cw = i / (NK * 2 * GPK), kf = (i / (2 * GPK)) % NK;
+        const int rb = (i / GPK) % 2, hh = i % GPK;
+        acc[rb] = NP::mma(grp, hh, xf[kf], acc[rb]);
+        if (kf == NK - 1 && rb == 1 && hh == GPK - 1) {
           // bias, GELU, rounding, mask -> the chunk's operand fragment in LDS
-          const int c = w + cw * W;
-          uint32_t gp[4];
+          float gv[8];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int r0 = (2 * q) & 3, rb0 = (2 * q) >> 2;
-            typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-            const bf16x2 v = {(__bf16)gelu(acc[rb0][r0] + b1v[cw][rb0][r0]),
-                              (__bf16)gelu(acc[rb0][r0 + 1] + b1v[cw][rb0][r0 + 1])};
-            gp[q] = __builtin_bit_cast(uint32_t, v) & amask;
-          }
-          const u32x4 gf = {gp[0], gp[1], gp[2], gp[3]};
-          *reinterpret_cast<u32x4*>(gbuf + c * 1024 + lane * 16) = gf;
+          for (int j = 0; j < 8; ++j) gv[j] = gelu(acc[j >> 2][j & 3] + b1v[cw][j >> 2][j & 3]);
+          NP::store(gbuf, w + cw * W, lane, NP::gfrag(gv, amask));
           acc[0] = f32x4n{};
           acc[1] = f32x4n{};
         }
         if (i == NA - 1) {
           __syncthreads();           // every chunk's GELU fragment is in LDS
-          gcur = lds_group(gbuf, 0, lane);
-          gnext = lds_group(gbuf, NC > 1 ? 1 : 0, lane);
+          gcur = NP::load(gbuf, 0, lane);
+          gnext = NP::load(gbuf, NC > 1 ? 1 : 0, lane);
         }
       } else {
-        const int j = i - NA, c = j / NBW, bq = j % NBW;
-        dz[bq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, grp),
-                                                         __builtin_bit_cast(bf16x8, gcur), dz[bq], 0, 0, 0);
-        if (bq == NBW - 1) {
+        const int j = i - NA, c = j / (NBW * GPK), bq = (j / GPK) % NBW, hh = j % GPK;
+        dz[bq] = NP::mma(grp, hh, gcur, dz[bq]);
+        if (bq == NBW - 1 && hh == GPK - 1) {
           gcur = gnext;
-          if (c + 2 < NC) gnext = lds_group(gbuf, c + 2, lane);
+          if (c + 2 < NC) gnext = NP::load(gbuf, c + 2, lane);
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -3948,16 +4007,17 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
   return launch_rollout_t<PR, D, E, 1, NORM>(m, a, blocks, st);
 }
 
-// Narrow tiles (16 candidates) for bf16 batches of at most one such tile per
-// compute unit, at d = 256, e = 64 and hidden widths 512 and 1024.
+// Narrow tiles (16 candidates) for batches of at most one such tile per
+// compute unit at d = 256, e = 64: bf16 with hidden widths 512 and 1024 (both
+// transition forms), fp32 with hidden width 512 (residual form).
 constexpr int NARROW_MAX_TILES = 256;
-template <int NC, bool NORM>
+template <class NP, int NC, bool NORM>
 hipError_t launch_rollout_narrow(const DevModel& m, RollArgs a, int tiles, hipStream_t st) {
-  using NG = NarrowGeom<256, 64, NC, 8>;
+  using NG = NarrowGeom<NP, 256, 64, NC, 8>;
   a.w1 = m.trans_n;
   const int lds = m.roll_tab_bytes + NG::G_BYTES + NG::X_BYTES + (NORM ? 8 * 3 * 16 * 4 : 0) +
                   (a.phi ? 16 * (64 + 1) * 4 : 0);
-  auto kern = rollout_narrow_kernel<256, 64, NC, 8, NORM>;
+  auto kern = rollout_narrow_kernel<NP, 256, 64, NC, 8, NORM>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -3986,15 +4046,19 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
   const bool norm = m.dims.norm == WM_NORM_L2;
   *phi_done = false;
   const int ntiles = (B + 15) / 16;
-  if (prec == WM_BF16 && d == 256 && e == 64 && m.trans_n && B > 0 && ntiles <= NARROW_MAX_TILES) {
+  if (d == 256 && e == 64 && m.trans_n && B > 0 && ntiles <= NARROW_MAX_TILES) {
     const int NC = m.dims.trans_hidden / 32;
-    if (NC == 16 || NC == 32) {
+    if (prec == WM_BF16 && (NC == 16 || NC == 32)) {
       *phi_done = phi != nullptr;
       if (norm)
-        return NC == 16 ? launch_rollout_narrow<16, true>(m, a, ntiles, st)
-                        : launch_rollout_narrow<32, true>(m, a, ntiles, st);
-      return NC == 16 ? launch_rollout_narrow<16, false>(m, a, ntiles, st)
-                      : launch_rollout_narrow<32, false>(m, a, ntiles, st);
+        return NC == 16 ? launch_rollout_narrow<NarrowBF16, 16, true>(m, a, ntiles, st)
+                        : launch_rollout_narrow<NarrowBF16, 32, true>(m, a, ntiles, st);
+      return NC == 16 ? launch_rollout_narrow<NarrowBF16, 16, false>(m, a, ntiles, st)
+                      : launch_rollout_narrow<NarrowBF16, 32, false>(m, a, ntiles, st);
+    }
+    if (prec == WM_FP32 && NC == 16 && !norm) {
+      *phi_done = phi != nullptr;
+      return launch_rollout_narrow<NarrowF32, 16, false>(m, a, ntiles, st);
     }
   }
 #define WM_ROLL(PR, D, E)                                                                          \

@@ -42,6 +42,7 @@ CASES = [
     ("tiny", "fp32", 300, 1),
     ("tiny", "bf16", 300, 1),
     ("ansor_round", "fp32", 300, 1),
+    ("ansor_round", "fp32", 5000, 1),        # 32-candidate tiles (over 256 16-candidate tiles)
     ("ansor_round", "bf16", 300, 1),
     ("ansor_round", "bf16", 5000, 1),        # 32-candidate tiles (over 256 16-candidate tiles)
     ("long_schedule", "bf16", 270, 1),
@@ -325,6 +326,7 @@ PHI_CASES = [
     ("tiny", "fp32", 200, "none"),            # split kernel + phi kernel
     ("tiny", "fp32", 8224, "none"),           # persistent, sums in the kernel
     ("ansor_round", "bf16", 300, "none"),     # narrow tiles (16 candidates)
+    ("ansor_round", "fp32", 300, "none"),     # narrow tiles, fp32
     ("ansor_round", "bf16", 4096, "none"),    # narrow tiles, 256 full tiles
     ("ansor_round", "bf16", 5000, "none"),    # row-owned, 32-candidate tiles
     ("long_schedule", "bf16", 300, "none"),   # narrow tiles, hidden width 1024
