@@ -3707,23 +3707,20 @@ __device__ __forceinline__ uint32_t score_key(float v) {
 constexpr int TOPK_THREADS = 1024;
 constexpr int TOPK_WAVES = TOPK_THREADS / 64;
 
-// Largest-first radix select over keys key(i) of the elements with pred(i):
-// returns the `need`-th largest key (1-based) and, in *rank_in_eq, how many
-// elements equal to it must be taken.
-template <class KeyF, class PredF>
-__device__ uint32_t radix_select(int n, int need, KeyF key, PredF pred, uint32_t* hist_w,
-                                 int* shared_int, int* rank_in_eq) {
+// Largest-first radix select over the keys that for_each(f) passes to f
+// (each thread its own elements): returns the `need`-th largest key (1-based)
+// and, in *rank_in_eq, how many elements equal to it must be taken.
+template <class ForEach>
+__device__ uint32_t radix_select(int need, ForEach for_each, uint32_t* hist_w, int* shared_int,
+                                 int* rank_in_eq) {
   const int tid = threadIdx.x, wave = tid >> 6;
   uint32_t prefix = 0, mask = 0;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int i = tid; i < TOPK_WAVES * 256; i += TOPK_THREADS) hist_w[i] = 0;
     __syncthreads();
-    for (int i = tid; i < n; i += TOPK_THREADS) {
-      if (pred(i)) {
-        const uint32_t kk = key(i);
-        if ((kk & mask) == prefix) atomicAdd(&hist_w[wave * 256 + ((kk >> shift) & 255)], 1u);
-      }
-    }
+    for_each([&](uint32_t kk) {
+      if ((kk & mask) == prefix) atomicAdd(&hist_w[wave * 256 + ((kk >> shift) & 255)], 1u);
+    });
     __syncthreads();
     // combine the per-wave histograms into the first
     for (int b = tid; b < 256; b += TOPK_THREADS) {
@@ -3772,6 +3769,10 @@ __device__ uint32_t radix_select(int n, int need, KeyF key, PredF pred, uint32_t
   return prefix;
 }
 
+// KPT > 0: the segment has at most KPT * TOPK_THREADS candidates and each
+// thread keeps its keys in registers across the passes; KPT = 0 reads the
+// scores again in every pass.
+template <int KPT>
 __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const float* __restrict__ scores,
                                                             int B, const SegTable seg, int k,
                                                             int P2, int32_t* __restrict__ idx,
@@ -3785,15 +3786,35 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const float* __restr
   const float* y = scores + (size_t)j * B + lo;
   const int tid = threadIdx.x;
 
+  uint32_t keys[KPT > 0 ? KPT : 1];
+  if constexpr (KPT > 0) {
+#pragma unroll
+    for (int q = 0; q < KPT; ++q) {
+      const int i = tid + q * TOPK_THREADS;
+      keys[q] = i < n ? score_key(y[i]) : 0u;
+    }
+  }
+  // f(key, local index) over this thread's candidates
+  auto each_key = [&](auto f) {
+    if constexpr (KPT > 0) {
+#pragma unroll
+      for (int q = 0; q < KPT; ++q) {
+        const int i = tid + q * TOPK_THREADS;
+        if (i < n) f(keys[q], i);
+      }
+    } else {
+      for (int i = tid; i < n; i += TOPK_THREADS) f(score_key(y[i]), i);
+    }
+  };
+
   int need_eq = 0;
   const uint32_t kstar = radix_select(
-      n, k, [&](int i) { return score_key(y[i]); }, [](int) { return true; }, hist_w, sh,
-      &need_eq);
+      k, [&](auto f) { each_key([&](uint32_t kk, int) { f(kk); }); }, hist_w, sh, &need_eq);
   // count of keys equal to K*
   if (tid == 0) { sh[2] = 0; sh[3] = 0; }
   __syncthreads();
   int my_eq = 0;
-  for (int i = tid; i < n; i += TOPK_THREADS) my_eq += (score_key(y[i]) == kstar);
+  each_key([&](uint32_t kk, int) { my_eq += (kk == kstar); });
   if (my_eq) atomicAdd(&sh[2], my_eq);
   __syncthreads();
   const int n_eq = sh[2];
@@ -3802,20 +3823,20 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const float* __restr
   if (need_eq < n_eq) {
     int dummy = 0;
     istar = radix_select(
-        n, need_eq, [](int i) { return ~(uint32_t)i; },
-        [&](int i) { return score_key(y[i]) == kstar; }, hist_w, sh, &dummy);
+        need_eq,
+        [&](auto f) { each_key([&](uint32_t kk, int i) { if (kk == kstar) f(~(uint32_t)i); }); },
+        hist_w, sh, &dummy);
   }
   const uint32_t ilimit = (need_eq < n_eq) ? ~istar : 0xFFFFFFFFu;  // keep local index <= ilimit
   if (tid == 0) sh[3] = 0;
   for (int i = tid; i < P2; i += TOPK_THREADS) sel[i] = 0ull;
   __syncthreads();
-  for (int i = tid; i < n; i += TOPK_THREADS) {
-    const uint32_t kk = score_key(y[i]);
+  each_key([&](uint32_t kk, int i) {
     if (kk > kstar || (kk == kstar && (uint32_t)i <= ilimit)) {
       const int slot = atomicAdd(&sh[3], 1);
       if (slot < k) sel[slot] = ((unsigned long long)kk << 32) | (unsigned long long)(~(uint32_t)i);
     }
-  }
+  });
   __syncthreads();
   // bitonic sort, descending
   for (int size = 2; size <= P2; size <<= 1) {
@@ -4139,8 +4160,15 @@ hipError_t launch_topk(const float* scores, int32_t n_hw, int32_t B, const SegTa
                        int32_t k, int32_t* idx, float* val, hipStream_t st) {
   int P2 = 1;
   while (P2 < k) P2 <<= 1;
-  hipLaunchKernelGGL(topk_kernel, dim3(n_hw * seg.n), dim3(TOPK_THREADS), 0, st, scores, B, seg,
-                     k, P2, idx, val);
+  int nmax = 0;
+  for (int s = 0; s < seg.n; ++s) nmax = seg.off[s + 1] - seg.off[s] > nmax ? seg.off[s + 1] - seg.off[s] : nmax;
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3(n_hw * seg.n), dim3(TOPK_THREADS), 0, st, scores, B, seg, k, P2, idx, val);
+  };
+  if (nmax <= 2 * TOPK_THREADS) go(topk_kernel<2>);
+  else if (nmax <= 8 * TOPK_THREADS) go(topk_kernel<8>);
+  else if (nmax <= 32 * TOPK_THREADS) go(topk_kernel<32>);
+  else go(topk_kernel<0>);
   return hipGetLastError();
 }
 

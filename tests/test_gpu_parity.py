@@ -291,6 +291,15 @@ def test_topk_entry_point_edge_scores(wm):
     ref3, rv3 = O.topk(y2.astype(np.float64), [0, 70000], 700)
     np.testing.assert_array_equal(idx3.cpu().numpy(), ref3)
     np.testing.assert_array_equal(val3.cpu().numpy(), rv3.astype(np.float32))
+    # segment sizes of each register-cached variant (up to 2, 8 and 32 keys
+    # per thread), with ties at the k-th score
+    for seg in ([0, 2000], [0, 3000], [0, 5000, 20000]):
+        n = seg[-1]
+        sc4 = torch.from_numpy(np.ascontiguousarray(y2[:, :n])).to(dev)
+        idx4 = torch.empty((2, len(seg) - 1, 300), dtype=torch.int32, device=dev)
+        wm.topk(sc4, seg, 300, idx4)
+        ref4, _ = O.topk(y2[:, :n].astype(np.float64), seg, 300)
+        np.testing.assert_array_equal(idx4.cpu().numpy(), ref4)
 
 
 @pytest.mark.parametrize("lens_kind", ["mixed", "all_max", "mostly_empty", "bad_length"])
