@@ -1730,6 +1730,7 @@ typedef float f32x8n __attribute__((ext_vector_type(8)));
 struct NarrowBF16 {
   using XF = bf16x8;
   static constexpr int GPK = 1;                 // 1 KiB groups per fragment
+  static __device__ __forceinline__ float op(float v) { return (float)(__bf16)v; }
   static __device__ __forceinline__ XF cvt(const float (&v)[8]) {
     XF f;
 #pragma unroll
@@ -1756,6 +1757,7 @@ struct NarrowBF16 {
 struct NarrowF32 {
   using XF = f32x8n;
   static constexpr int GPK = 2;
+  static __device__ __forceinline__ float op(float v) { return v; }
   static __device__ __forceinline__ XF cvt(const float (&v)[8]) {
     XF f;
 #pragma unroll
@@ -1810,8 +1812,13 @@ struct NarrowGeom {
   static constexpr int G_BYTES = NC * GPK * 1024, X_BYTES = NK * GPK * 1024;
 };
 
-template <class NP, int D, int E, int NC, int W, bool NORM>
+// TRAIN (residual form): the training forward of the rollout loss; stores,
+// per valid step in compact row off[i] + t, the operands X = [z; e], the
+// pre-activations A, the GELU outputs G and the prediction, as the 32-wide
+// row-owned kernel does.
+template <class NP, int D, int E, int NC, int W, bool NORM, bool TRAIN = false>
 __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArgs a) {
+  static_assert(!(TRAIN && NORM), "narrow training forward: residual form");
   using NG = NarrowGeom<NP, D, E, NC, W>;
   using XF = typename NP::XF;
   constexpr int GPK = NG::GPK, NK = NG::NK, NZ = NG::NZ, NE = NG::NE, NB = NG::NB, NBW = NG::NBW;
@@ -1825,10 +1832,11 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
   uint8_t* xbuf = gbuf + NG::G_BYTES;                                 // X fragments [NK]
   float* dots = reinterpret_cast<float*>(xbuf + NG::X_BYTES);         // paper form: [W][3][16]
   float* phib = dots + (NORM ? W * 3 * 16 : 0);                       // [16][E + 1]
-  const bool do_phi = a.phi != nullptr;
+  const bool do_phi = !TRAIN && a.phi != nullptr;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n = lane & 15, g = lane >> 4;
+  constexpr int IN = D + E;
   stage_to_lds(reinterpret_cast<const uint8_t*>(a.tab), reinterpret_cast<uint8_t*>(tab),
                a.tab_bytes, tid, NT);
   if (do_phi)
@@ -1841,6 +1849,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
   const int len = valid ? clampi(a.lens[cand], 0, a.T_max) : 0;
   const int T_wg = __builtin_amdgcn_readfirstlane(
       clampi(a.lens[a.perm[blockIdx.x * 16].x], 0, a.T_max));
+  const size_t row0 = (TRAIN && valid) ? (size_t)a.off[cand] : 0;
 
   const float* b1n = reinterpret_cast<const float*>(a.w1 + (size_t)(NG::W1G + NG::W2G) * 1024);
   const float* b2n = b1n + NC * 32;
@@ -1870,6 +1879,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[p];
   }
   int errbits = 0;
+  int s_cur = 0;                     // step of the embedding being built
 
   // Embedding of step s: the action's kind and log2 parameters (error bits,
   // prefetch of step s + 1), then fragment q (features 32q + 8g + j).
@@ -1903,6 +1913,15 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
       for (int j = 0; j < 8; ++j) ev[j] = fmaf(t_pw[p * E + f0 + j], u[p], ev[j]);
 #pragma unroll
     for (int j = 0; j < 8; ++j) ev[j] = (ev[j] + t_pb[f0 + j]) * af;
+    if constexpr (TRAIN) {
+      if (q == w && af != 0.0f) {     // the owner stores e of an active step
+        float* xo = a.X + (row0 + s_cur) * IN + D + f0;
+        const f32x4n lo = {NP::op(ev[0]), NP::op(ev[1]), NP::op(ev[2]), NP::op(ev[3])};
+        const f32x4n hi = {NP::op(ev[4]), NP::op(ev[5]), NP::op(ev[6]), NP::op(ev[7])};
+        *reinterpret_cast<f32x4n*>(xo) = lo;
+        *reinterpret_cast<f32x4n*>(xo + 4) = hi;
+      }
+    }
     if (do_phi && q == w) {
       float* ph = phib + n * (E + 1) + f0;
 #pragma unroll
@@ -1913,6 +1932,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
   // residual form: wavefront w < NE embeds fragment w into LDS
   auto embed_share = [&](int s) {
     if (w >= NE) return;
+    s_cur = s;
     int ty;
     float u[PMAX], af;
     decode(s, ty, u, af);
@@ -2035,6 +2055,17 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     gu8* pA = baseA;
     gu8* pB = baseB;
     asm volatile("" : "+v"(pA), "+v"(pB));
+    const size_t row = row0 + t;
+    if constexpr (TRAIN) {
+      if (active) {                  // X = [z; e]: the owned latent blocks (e: embed_share)
+#pragma unroll
+        for (int bq = 0; bq < NBW; ++bq) {
+          const f32x4n v = {NP::op(zq[bq][0]), NP::op(zq[bq][1]), NP::op(zq[bq][2]), NP::op(zq[bq][3])};
+          *reinterpret_cast<f32x4n*>(a.X + row * IN + 16 * (w * NBW + bq) + 4 * g) = v;
+        }
+        if (w == 0 && g == 0) a.row_src[row] = cand * a.T_max + t;
+      }
+    }
     f32x4n acc[2], dz[NBW];
     acc[0] = f32x4n{}; acc[1] = f32x4n{};
 #pragma unroll
@@ -2054,6 +2085,20 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
           float gv[8];
 #pragma unroll
           for (int j = 0; j < 8; ++j) gv[j] = gelu(acc[j >> 2][j & 3] + b1v[cw][j >> 2][j & 3]);
+          if constexpr (TRAIN) {
+            if (active) {
+              const int c = w + cw * W;
+#pragma unroll
+              for (int rb = 0; rb < 2; ++rb) {
+                const f32x4n av = {acc[rb][0] + b1v[cw][rb][0], acc[rb][1] + b1v[cw][rb][1],
+                                   acc[rb][2] + b1v[cw][rb][2], acc[rb][3] + b1v[cw][rb][3]};
+                const f32x4n gq = {NP::op(gv[4 * rb]), NP::op(gv[4 * rb + 1]), NP::op(gv[4 * rb + 2]),
+                                   NP::op(gv[4 * rb + 3])};
+                *reinterpret_cast<f32x4n*>(a.A + row * a.H + 32 * c + 16 * rb + 4 * g) = av;
+                *reinterpret_cast<f32x4n*>(a.G + row * a.H + 32 * c + 16 * rb + 4 * g) = gq;
+              }
+            }
+          }
           NP::store(gbuf, w + cw * W, lane, NP::gfrag(gv, amask));
           acc[0] = f32x4n{};
           acc[1] = f32x4n{};
@@ -2074,9 +2119,13 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
-    for (int bq = 0; bq < NBW; ++bq)
+    for (int bq = 0; bq < NBW; ++bq) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) zq[bq][r] += dz[bq][r] + b2v[bq][r] * actf;
+      if constexpr (TRAIN) {
+        if (active) *reinterpret_cast<f32x4n*>(a.Pz + row * D + 16 * (w * NBW + bq) + 4 * g) = zq[bq];
+      }
+    }
     if constexpr (NORM) {
       embed_all(t + 1);
       boundary(active, t + 1 < len);
@@ -2093,7 +2142,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
 #pragma unroll
     for (int j = 0; j < 8; ++j) a.phi[(size_t)cand * E + f0 + j] = ph[j] * inv;
   }
-  if (valid) {
+  if (valid && !TRAIN) {
 #pragma unroll
     for (int bq = 0; bq < NBW; ++bq)
       *reinterpret_cast<f32x4n*>(a.zT + (size_t)cand * D + 16 * (w * NBW + bq) + 4 * g) = zq[bq];
@@ -4032,13 +4081,13 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
 // compute unit at d = 256, e = 64: bf16 with hidden widths 512 and 1024 (both
 // transition forms), fp32 with hidden width 512 (residual form).
 constexpr int NARROW_MAX_TILES = 256;
-template <class NP, int NC, bool NORM>
+template <class NP, int NC, bool NORM, bool TRAIN = false>
 hipError_t launch_rollout_narrow(const DevModel& m, RollArgs a, int tiles, hipStream_t st) {
   using NG = NarrowGeom<NP, 256, 64, NC, 8>;
   a.w1 = m.trans_n;
   const int lds = m.roll_tab_bytes + NG::G_BYTES + NG::X_BYTES + (NORM ? 8 * 3 * 16 * 4 : 0) +
-                  (a.phi ? 16 * (64 + 1) * 4 : 0);
-  auto kern = rollout_narrow_kernel<NP, 256, 64, NC, 8, NORM>;
+                  (a.phi && !TRAIN ? 16 * (64 + 1) * 4 : 0);
+  auto kern = rollout_narrow_kernel<NP, 256, 64, NC, 8, NORM, TRAIN>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -4253,16 +4302,22 @@ bool have_train_kernels(int prec, int d, int e) {
   return false;
 }
 
-// Training forward in the row-owned form (one workgroup per tile; d = 256).
-template <class PR, int NC, int W, bool NORM>
-hipError_t launch_train_fwd_rows(const DevModel& m, const TrainIO& io, int tiles, hipStream_t st) {
+// Rollout arguments of the training forward (no z_T, no phi).
+RollArgs train_roll_args(const DevModel& m, const TrainIO& io, bool norm) {
   RollArgs a{};
-  a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.wh = NORM ? m.trans_wh : nullptr; a.tab = m.roll_tab; a.z0 = io.z0;
+  a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.wh = norm ? m.trans_wh : nullptr; a.tab = m.roll_tab; a.z0 = io.z0;
   a.perm = io.perm; a.types = io.types; a.params = io.params; a.lens = io.lens; a.zT = nullptr;
   a.err = io.err; a.B = io.B; a.T_max = io.T_max; a.P = m.dims.n_params; a.K = m.dims.n_kinds;
   a.H = m.dims.trans_hidden; a.tab_bytes = m.roll_tab_bytes;
   a.X = io.X; a.A = io.A; a.G = io.G; a.Pz = io.P; a.off = io.off; a.row_src = io.row_src;
   a.V = io.V; a.SC = io.SC;
+  return a;
+}
+
+// Training forward in the row-owned form (one workgroup per tile; d = 256).
+template <class PR, int NC, int W, bool NORM>
+hipError_t launch_train_fwd_rows(const DevModel& m, const TrainIO& io, int tiles, hipStream_t st) {
+  const RollArgs a = train_roll_args(m, io, NORM);
   using RG = RowsGeom<PR, 256, 64, NC, W>;
   const int lds = m.roll_tab_bytes + RG::GELU_BYTES + RG::X_BYTES + RG::XE_BYTES + (NORM ? W * 3 * 32 * 4 : 0);
   auto kern = rollout_rows_kernel<PR, 256, 64, NC, W, NORM, true>;
@@ -4280,6 +4335,15 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
   const TrainArgs a = train_args(m, io);
   const int tiles = (io.B + 31) / 32;
   const bool norm = m.dims.norm == WM_NORM_L2;
+  // residual form, at most one 16-candidate tile per compute unit: narrow tiles
+  const int ntiles = (io.B + 15) / 16;
+  if (m.dims.d == 256 && m.dims.embed_dim == 64 && !norm && m.trans_n && ntiles <= NARROW_MAX_TILES) {
+    const int NC = m.dims.trans_hidden / 32;
+    const RollArgs r = train_roll_args(m, io, false);
+    if (m.prec == WM_BF16 && NC == 16) return launch_rollout_narrow<NarrowBF16, 16, false, true>(m, r, ntiles, st);
+    if (m.prec == WM_BF16 && NC == 32) return launch_rollout_narrow<NarrowBF16, 32, false, true>(m, r, ntiles, st);
+    if (m.prec == WM_FP32 && NC == 16) return launch_rollout_narrow<NarrowF32, 16, false, true>(m, r, ntiles, st);
+  }
   if (m.dims.d == 256 && m.dims.embed_dim == 64) {
     const int NC = m.dims.trans_hidden / 32;
 #define WM_TFWD_ROWS(N)                                                                              \

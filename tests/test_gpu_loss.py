@@ -222,10 +222,17 @@ def test_loss_terms(wm, prec, lam, gamma, mode):
 
 
 @pytest.mark.parametrize("name,prec,B", [("tiny", "bf16", 300), ("ansor_round", "bf16", 250),
-                                         ("long_schedule", "bf16", 130), ("ansor_round", "fp32", 130)])
+                                         ("long_schedule", "bf16", 130), ("ansor_round", "fp32", 130),
+                                         ("ansor_round", "bf16", 5000), ("ansor_round", "fp32", 5000)])
 def test_loss_short_sequences_rowwise(wm, name, prec, B):
     """At most two steps: every gradient row (and, in fp32, element)
-    against the oracle's."""
+    against the oracle's.  Up to 4096 candidates the forward runs in
+    16-candidate tiles; 5000 candidates take the 32-candidate row-owned
+    tiles.  The per-element rule is for the small batches: an element of
+    a weight gradient over 5000 rows is an fp32 sum of 5000 terms of mixed
+    sign, whose rounding (about sqrt(rows) ulp of the terms) exceeds 1e-4 of
+    the element scale where the terms cancel; rows and the whole tensor
+    keep their bounds."""
     w = synth.scaled(synth.workload(name), B=B, lengths="uniform", len_lo=0, len_hi=2)
     print(f"[loss short] {name} {prec} B={B}", flush=True)
     model, W = model_for(wm, name, prec)
@@ -233,7 +240,7 @@ def test_loss_short_sequences_rowwise(wm, name, prec, B):
     tgt, neg = margin_targets(W, I, prec, 3, 79, 0.3)
     g = run_loss(wm, model, I, tgt, neg, 0.5, 0.3)
     rep = check_against_oracle(g, W, I, tgt, neg, 0.5, 0.3, prec, rows=True,
-                               elems=prec == "fp32")
+                               elems=prec == "fp32" and B <= 300)
     print("  " + ", ".join(f"{k} {v:.1e}" for k, v in rep.items()), flush=True)
 
 
