@@ -156,6 +156,41 @@ std::vector<uint8_t> pack_transition_narrow(const wm_dims& dm, const wm_weights&
   return blk;
 }
 
+// Transposed narrow-tile blob for the rollout-loss backward (Narrow::t_bytes).
+std::vector<uint8_t> pack_transposed_narrow(const wm_dims& dm, const wm_weights& w) {
+  const int D = dm.d, E = dm.embed_dim, H = dm.trans_hidden, IN = D + E;
+  const bool bf = dm.precision == WM_BF16;
+  const int gpk = bf ? 1 : 2, per = 8 / gpk;
+  std::vector<uint8_t> blk(Narrow::t_bytes(D, E, H, gpk), 0);
+  auto put = [&](size_t frag_group0, int lane, int j, float v) {
+    const size_t off = (frag_group0 + (size_t)(j / per)) * 1024 + (size_t)lane * 16;
+    if (bf) {
+      const uint16_t b = f32_to_bf16(v);
+      std::memcpy(&blk[off + (size_t)(j % per) * 2], &b, 2);
+    } else {
+      std::memcpy(&blk[off + (size_t)(j % per) * 4], &v, 4);
+    }
+  };
+  for (int c = 0; c < H / 32; ++c)
+    for (int kf = 0; kf < D / 32; ++kf)
+      for (int rb = 0; rb < 2; ++rb)
+        for (int L = 0; L < 64; ++L)
+          for (int j = 0; j < 8; ++j) {
+            const int hid = 32 * c + 16 * rb + (L & 15);
+            const int lat = narrow_x_feature(D, kf, L >> 4, j);
+            put((((size_t)c * (D / 32) + kf) * 2 + rb) * gpk, L, j, w.w2[(size_t)lat * H + hid]);
+          }
+  const size_t g1 = Narrow::w2t_groups(D, H, gpk);
+  for (int c = 0; c < H / 32; ++c)
+    for (int ob = 0; ob < IN / 16; ++ob)
+      for (int L = 0; L < 64; ++L)
+        for (int j = 0; j < 8; ++j) {
+          const int feat = 16 * ob + (L & 15), hid = 32 * c + narrow_g_feature(L >> 4, j);
+          put(g1 + ((size_t)c * (IN / 16) + ob) * gpk, L, j, w.w1[(size_t)hid * IN + feat]);
+        }
+  return blk;
+}
+
 // Transposed transition chunks for the rollout-loss backward (see TransT).
 template <class Gm>
 void pack_transposed(const wm_dims& dm, const wm_weights& w, std::vector<uint8_t>& w2t,
@@ -405,7 +440,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.dims = dm;
   m.prec = dm.precision;
   const int D = dm.d, E = dm.embed_dim, K = dm.n_kinds, P = dm.n_params, HW = dm.hw_dim;
-  std::vector<uint8_t> tw1, tw2, cost, twh, tw2t, tw1t, twht, tn;
+  std::vector<uint8_t> tw1, tw2, cost, twh, tw2t, tw1t, twht, tn, tnt;
   const bool l2 = dm.norm == WM_NORM_L2;
   if (m.prec == WM_BF16) {
     pack_transition<GeomBF16>(dm, *w, tw1, tw2);
@@ -427,7 +462,10 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
     m.w2_chunk_bytes = TransChunk<GeomF32>::w2_bytes(D);
     m.cost_chunk_bytes = CostChunk<GeomF32>::bytes(D, E, HW);
   }
-  if (D % 32 == 0 && E % 32 == 0) tn = pack_transition_narrow(dm, *w);
+  if (D % 32 == 0 && E % 32 == 0) {
+    tn = pack_transition_narrow(dm, *w);
+    tnt = pack_transposed_narrow(dm, *w);
+  }
   // rollout table: type_emb [K][E + 4], param_w^T [PMAX][E], param_b [E], b2 (accumulator order)
   std::vector<float> tab;
   tab.reserve((size_t)K * temb_stride(E) + (size_t)PMAX * E + E + D + 4);
@@ -472,6 +510,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   const size_t o_w1t = off; off = align256(off + tw1t.size());
   const size_t o_wht = off; off = align256(off + twht.size());
   const size_t o_tn = off; off = align256(off + tn.size());
+  const size_t o_tnt = off; off = align256(off + tnt.size());
   const size_t o_tab = off; off = align256(off + tab.size() * 4);
   const size_t o_enc = off; off = align256(off + enc.size() * 4);
   void* dev = nullptr;
@@ -488,6 +527,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   if (e == hipSuccess && !tw1t.empty()) e = hipMemcpy(base + o_w1t, tw1t.data(), tw1t.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess && !twht.empty()) e = hipMemcpy(base + o_wht, twht.data(), twht.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess && !tn.empty()) e = hipMemcpy(base + o_tn, tn.data(), tn.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess && !tnt.empty()) e = hipMemcpy(base + o_tnt, tnt.data(), tnt.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_tab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess && !enc.empty()) e = hipMemcpy(base + o_enc, enc.data(), enc.size() * 4, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
@@ -503,6 +543,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.trans_w1t = tw1t.empty() ? nullptr : base + o_w1t;
   m.trans_wht = twht.empty() ? nullptr : base + o_wht;
   m.trans_n = tn.empty() ? nullptr : base + o_tn;
+  m.trans_nt = tnt.empty() ? nullptr : base + o_tnt;
   m.roll_tab = reinterpret_cast<const float*>(base + o_tab);
   m.emb_nat = m.roll_tab;
   const float* encp = reinterpret_cast<const float*>(base + o_enc);

@@ -189,6 +189,17 @@ struct Narrow {
     return (w1_groups(D, E, H, gpk) + w2_groups(D, H, gpk)) * 1024 + (size_t)(H + D) * 4;
   }
   static constexpr size_t wh_bytes(int D, int E, int gpk) { return (size_t)(D / 16) * (E / 32) * gpk * 1024; }
+  // Transposed blob (rollout-loss backward), same operand orders:
+  //   W2^T: chunk c, latent k-fragment kf (z-operand order), row block rb (16
+  //         hidden units 32c + 16rb..): group ((c * D/32 + kf) * 2 + rb) * gpk + hh;
+  //   W1^T: chunk c, output block ob of the D + E inputs (rows 16ob..), over
+  //         the chunk's 32 hidden units in GELU-operand order:
+  //         group W2T + (c * (D+E)/16 + ob) * gpk + hh.
+  static constexpr size_t w2t_groups(int D, int H, int gpk) { return (size_t)(H / 32) * (D / 32) * 2 * gpk; }
+  static constexpr size_t w1t_groups(int D, int E, int H, int gpk) { return (size_t)(H / 32) * ((D + E) / 16) * gpk; }
+  static constexpr size_t t_bytes(int D, int E, int H, int gpk) {
+    return (w2t_groups(D, H, gpk) + w1t_groups(D, E, H, gpk)) * 1024;
+  }
 };
 
 // Action parameters per step are padded to PMAX in the embedding table
@@ -236,6 +247,7 @@ struct DevModel {
   const uint8_t* trans_w1t; // H/32 chunks of W1^T (rollout-loss backward)
   const uint8_t* trans_wht; // Wh^T fragments (paper-form rollout-loss backward)
   const uint8_t* trans_n;   // narrow-tile transition blob (d and e multiples of 32), or null
+  const uint8_t* trans_nt;  // its transposed blob (rollout-loss backward), or null
   const float* roll_tab;    // type_emb [K][E + 4] (padded rows), param_w^T [PMAX][E] (zero rows past P), param_b [E], b2 (acc order) [D]
   const float* emb_nat;     // the first three parts of roll_tab
   const float* enc_w1t;     // We1^T [F][Fh] (bf16-rounded values in bf16 mode)

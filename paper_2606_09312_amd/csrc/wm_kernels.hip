@@ -3253,6 +3253,194 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_rows_kernel(const TrainAr
   }
 }
 
+// Narrow-tile backward of the rollout loss (residual form; one workgroup of
+// W wavefronts per tile of 16 candidates), the mirror of the narrow forward
+// with the products of the 32-candidate row-owned backward.  Per step, from
+// the last to the first:
+//  * wavefront w owns latent blocks 2w, 2w+1 of delta: it adds the step's
+//    seed, stores delta_{t+1}, and publishes the blocks as operand fragment w
+//    in LDS; after a barrier every wavefront reads all of delta;
+//  * for its chunks c = w, w + W, ...: dG^T = W2^T[c] . delta^T (two 16-row
+//    blocks), dA = dG * GELU'(A) (stored), dA as an operand fragment into
+//    LDS, and its partial dE^T += W1^T[c][e blocks] . dA^T (summed across
+//    wavefronts through LDS in a fixed order);
+//  * after a barrier, for its own latent blocks over every chunk:
+//    delta += W1^T[c][block] . dA^T[c].
+// Weight groups stream from L2 through a register ring that wraps from step
+// to step (transposed blob at Narrow::t_bytes).
+template <class NP, int D, int E, int NC, int W>
+struct NarrowBwdGeom {
+  static constexpr int GPK = NP::GPK;
+  static constexpr int NB = D / 16, NBW = NB / W, NZ = D / 32, NBE = E / 16, IB = (D + E) / 16;
+  static constexpr int NCW = NC / W;
+  static constexpr int N2T = NZ * 2 * GPK;                 // W2^T groups per chunk
+  static constexpr int NP1 = N2T + NBE * GPK;              // first-phase groups per chunk
+  static constexpr int NA = NCW * NP1;
+  static constexpr int NI = NA + NC * NBW * GPK;
+  static constexpr int W2TG = NC * NZ * 2 * GPK;           // W2^T groups in the blob
+  static constexpr int ring_depth() {
+    for (int r = 12; r > 1; --r)
+      if (NI % r == 0) return r;
+    return 1;
+  }
+  static constexpr int RD = ring_depth();
+  static_assert(NBW == 2 && NZ == W && NC % W == 0 && NBE <= W, "narrow split");
+  // LDS: [dA fragments: NC][delta fragments: NZ][dE partials: W x NBE x 64 lanes x 4]
+  static constexpr int DA_BYTES = NC * GPK * 1024, DL_BYTES = NZ * GPK * 1024;
+  static constexpr int DE_BYTES = W * NBE * 64 * 16;
+  static constexpr int LDS = DA_BYTES + DL_BYTES + DE_BYTES;
+};
+
+template <class NP, int D, int E, int NC, int W>
+__global__ __launch_bounds__(64 * W, 1) void train_bwd_narrow_kernel(const TrainArgs a) {
+  using BG = NarrowBwdGeom<NP, D, E, NC, W>;
+  using XF = typename NP::XF;
+  constexpr int GPK = BG::GPK, NZ = BG::NZ, NBE = BG::NBE, IB = BG::IB, NBW = BG::NBW, NB = BG::NB;
+  constexpr int NCW = BG::NCW, N2T = BG::N2T, NP1 = BG::NP1, NA = BG::NA, NI = BG::NI, RD = BG::RD;
+  (void)NB;
+
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  uint8_t* dabuf = lds;                                             // dA fragments [NC]
+  uint8_t* dlbuf = lds + BG::DA_BYTES;                              // delta fragments [NZ]
+  float* debuf = reinterpret_cast<float*>(lds + BG::DA_BYTES + BG::DL_BYTES);  // [W][NBE][64][4]
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int n = lane & 15, g = lane >> 4;
+  const int pos = blockIdx.x * 16 + n;
+  const bool valid = pos < a.B;
+  const int cand = valid ? a.perm[pos].x : 0;
+  const int len = valid ? clampi(a.lens[cand], 0, a.T_max) : 0;
+  const int T_wg = __builtin_amdgcn_readfirstlane(
+      clampi(a.lens[a.perm[blockIdx.x * 16].x], 0, a.T_max));
+  const size_t row0 = valid ? (size_t)a.off[cand] : 0;
+
+  // item i -> weight group (compile-time offsets from three bases)
+  gu8* baseA2 = ((gu8*)(a.w2t)) + (size_t)(w * N2T) * 1024 + lane * 16;
+  gu8* baseA1 = ((gu8*)(a.w2t)) + (size_t)(BG::W2TG + (w * IB + NZ * 2) * GPK) * 1024 + lane * 16;
+  gu8* baseB = ((gu8*)(a.w2t)) + (size_t)(BG::W2TG + w * NBW * GPK) * 1024 + lane * 16;
+  auto item_ptr = [&](gu8* p2, gu8* p1, gu8* pb, int i) -> gu32x4* {
+    if (i < NA) {
+      const int cw = i / NP1, k = i % NP1;
+      if (k < N2T) return reinterpret_cast<gu32x4*>(p2 + ((size_t)cw * W * N2T + k) * 1024);
+      return reinterpret_cast<gu32x4*>(p1 + ((size_t)cw * W * IB * GPK + (k - N2T)) * 1024);
+    }
+    const int j = i - NA, c = j / (NBW * GPK), r = j % (NBW * GPK);
+    return reinterpret_cast<gu32x4*>(pb + ((size_t)c * IB * GPK + r) * 1024);
+  };
+  u32x4 ring[RD];
+#pragma unroll
+  for (int i = 0; i < RD; ++i) ring[i] = *item_ptr(baseA2, baseA1, baseB, i);
+
+  f32x4n dq[NBW];
+#pragma unroll
+  for (int bq = 0; bq < NBW; ++bq) dq[bq] = f32x4n{};
+
+  for (int t = T_wg - 1; t >= 0; --t) {
+    const bool active = t < len;
+    const float actf = active ? 1.0f : 0.0f;
+    const uint32_t amask = active ? 0xFFFFFFFFu : 0u;
+    const size_t row = row0 + t;
+    gu8* p2 = baseA2;
+    gu8* p1 = baseA1;
+    gu8* pb = baseB;
+    asm volatile("" : "+v"(p2), "+v"(p1), "+v"(pb));
+    // ---- owned delta blocks: seed, delta_{t+1}, operand fragment w in LDS
+    float v8[8];
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq) {
+      float* sd = a.SD + row * D + 16 * (w * NBW + bq) + 4 * g;
+      if (active) {
+        const f32x4n s4 = *reinterpret_cast<const f32x4n*>(sd);
+        dq[bq] += s4;
+        *reinterpret_cast<f32x4n*>(sd) = dq[bq];
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v8[4 * bq + r] = dq[bq][r];
+    }
+    NP::store(dlbuf, w, lane, NP::cvt(v8));
+    // pre-activations of the own chunks (read early, used after W2^T)
+    f32x4n av[NCW][2];
+#pragma unroll
+    for (int cw = 0; cw < NCW; ++cw)
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+        av[cw][rb] = active ? *reinterpret_cast<const f32x4n*>(a.A + row * a.H + 32 * (w + cw * W) + 16 * rb + 4 * g)
+                            : f32x4n{};
+    __syncthreads();
+    XF dop[NZ];
+#pragma unroll
+    for (int kf = 0; kf < NZ; ++kf) dop[kf] = NP::load(dlbuf, kf, lane);
+
+    f32x4n acc[2], deacc[NBE];
+    acc[0] = f32x4n{}; acc[1] = f32x4n{};
+#pragma unroll
+    for (int q = 0; q < NBE; ++q) deacc[q] = f32x4n{};
+    XF dfr = {}, dcur = {}, dnext = {};
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const u32x4 grp = ring[i % RD];
+      ring[i % RD] = *item_ptr(p2, p1, pb, (i + RD) % NI);   // wraps into the next step
+      if (i < NA) {
+        const int cw = i / NP1, k = i % NP1;
+        if (k < N2T) {
+          const int kf = k / (2 * GPK), rb = (k / GPK) % 2, hh = k % GPK;
+          acc[rb] = NP::mma(grp, hh, dop[kf], acc[rb]);
+          if (k == N2T - 1) {
+            const int c = w + cw * W;
+            float da[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) da[j] = acc[j >> 2][j & 3] * gelu_grad(av[cw][j >> 2][j & 3]) * actf;
+            if (active) {
+#pragma unroll
+              for (int rb2 = 0; rb2 < 2; ++rb2) {
+                const f32x4n d4 = {da[4 * rb2], da[4 * rb2 + 1], da[4 * rb2 + 2], da[4 * rb2 + 3]};
+                *reinterpret_cast<f32x4n*>(a.A + row * a.H + 32 * c + 16 * rb2 + 4 * g) = d4;   // dA
+              }
+            }
+            dfr = NP::gfrag(da, amask);
+            NP::store(dabuf, c, lane, dfr);
+            acc[0] = f32x4n{};
+            acc[1] = f32x4n{};
+          }
+        } else {
+          const int q = (k - N2T) / GPK, hh = (k - N2T) % GPK;
+          deacc[q] = NP::mma(grp, hh, dfr, deacc[q]);
+        }
+        if (i == NA - 1) {
+          // embedding partials into LDS, then every chunk's dA is published
+#pragma unroll
+          for (int q = 0; q < NBE; ++q)
+            *reinterpret_cast<f32x4n*>(debuf + ((w * NBE + q) * 64 + lane) * 4) = deacc[q];
+          __syncthreads();
+          if (w < NBE) {            // dE block w: the partials in wavefront order
+            f32x4n e4 = {};
+#pragma unroll
+            for (int ww = 0; ww < W; ++ww) e4 += *reinterpret_cast<const f32x4n*>(debuf + ((ww * NBE + w) * 64 + lane) * 4);
+            if (active) *reinterpret_cast<f32x4n*>(a.DE + row * E + 16 * w + 4 * g) = e4;
+          }
+          dcur = NP::load(dabuf, 0, lane);
+          dnext = NP::load(dabuf, NC > 1 ? 1 : 0, lane);
+        }
+      } else {
+        const int j = i - NA, c = j / (NBW * GPK), bq = (j / GPK) % NBW, hh = j % GPK;
+        dq[bq] = NP::mma(grp, hh, dcur, dq[bq]);
+        if (bq == NBW - 1 && hh == GPK - 1) {
+          dcur = dnext;
+          if (c + 2 < NC) dnext = NP::load(dabuf, c + 2, lane);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();                // dA / dE / delta buffers are read before the next step writes them
+  }
+  if (valid && a.dz0) {
+#pragma unroll
+    for (int bq = 0; bq < NBW; ++bq)
+      *reinterpret_cast<f32x4n*>(a.dz0 + (size_t)cand * D + 16 * (w * NBW + bq) + 4 * g) = dq[bq];
+  }
+}
+
 // Weight gradients as split-K products over the compact rows, two problems
 // per launch (dW2 = sum R(delta) (x) g, dW1 = sum R(dA) (x) x):
 //   part[split][m][n] = sum over the split's rows r of op(A[r][m]) * op(B[r][n])
@@ -4368,11 +4556,34 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
   return hipErrorInvalidValue;
 }
 
+template <class NP, int NC>
+hipError_t launch_train_bwd_narrow(const DevModel& m, TrainArgs a, int tiles, hipStream_t st) {
+  using BG = NarrowBwdGeom<NP, 256, 64, NC, 8>;
+  static_assert(BG::LDS <= 160 * 1024, "LDS");
+  a.w2t = m.trans_nt;
+  auto kern = train_bwd_narrow_kernel<NP, 256, 64, NC, 8>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, BG::LDS);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
+  }
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(512), BG::LDS, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st) {
   if (io.B == 0) return hipSuccess;
   const TrainArgs a = train_args(m, io);
   const int tiles = (io.B + 31) / 32;
   const bool norm = m.dims.norm == WM_NORM_L2;
+  // residual form, at most one 16-candidate tile per compute unit: narrow tiles
+  const int ntiles = (io.B + 15) / 16;
+  if (m.dims.d == 256 && m.dims.embed_dim == 64 && !norm && m.trans_nt && ntiles <= NARROW_MAX_TILES) {
+    const int NC = m.dims.trans_hidden / 32;
+    if (m.prec == WM_BF16 && NC == 16) return launch_train_bwd_narrow<NarrowBF16, 16>(m, a, ntiles, st);
+    if (m.prec == WM_BF16 && NC == 32) return launch_train_bwd_narrow<NarrowBF16, 32>(m, a, ntiles, st);
+    if (m.prec == WM_FP32 && NC == 16) return launch_train_bwd_narrow<NarrowF32, 16>(m, a, ntiles, st);
+  }
   if (m.dims.d == 256 && m.dims.embed_dim == 64) {
     const int NC = m.dims.trans_hidden / 32;
 #define WM_TBWD_ROWS(N)                                                                         \
