@@ -493,12 +493,19 @@ def main():
 
     lens = I["lens"].astype(np.int64)
     flops_roll = int(lens.sum()) * step_flops(w, args.norm)
+    bytes_roll = rollout_bytes(w, lens, args.norm)
+    # small batches: the rollout launch also scores the candidates (no
+    # separate score launch), so its algorithmic work includes the cost model
+    fused = forest is None and "score" not in kern
+    if fused:
+        flops_roll += w.B * score_flops(w)
+        bytes_roll += (2 if prec == "bf16" else 4) * w.C * (w.d + w.e + w.hw_dim) + 4 * w.B * w.n_hw
     roll_s = kern["rollout"]["avg_ms"] / 1e3
     achieved = flops_roll / roll_s / 1e12
     peak = PEAK_TFLOPS[prec]
     ms_per_step = elapsed / args.steps * 1e3
     value = w.B * args.steps / elapsed
-    total_flops = flops_roll + (w.B * score_flops(w) if forest is None else 0)
+    total_flops = flops_roll + (w.B * score_flops(w) if forest is None and not fused else 0)
     out = {
         "metric": "candidate schedules evaluated/sec (rollout+score+top-k)",
         "value": value,
@@ -521,11 +528,12 @@ def main():
                              f"{w.n_trees} trees of depth {w.tree_depth} on structured action "
                              f"features",
                    "global_batch": w.B, "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "kernel": "rollout", "achieved": achieved, "peak": peak,
+        "roofline": {"bound": "mfma", "kernel": "rollout + score" if fused else "rollout",
+                     "achieved": achieved, "peak": peak,
                      "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": measured_traffic(w.name, prec, args.norm),
                      "flop_per_launch": flops_roll,
-                     "algorithmic_bytes_per_launch": rollout_bytes(w, lens, args.norm)},
+                     "algorithmic_bytes_per_launch": bytes_roll},
         "kernels_avg_ms": {k: v["avg_ms"] for k, v in kern.items()},
         "step_ms": step_ms,
         "whole_path_tflops": total_flops * args.steps / elapsed / 1e12,

@@ -156,6 +156,38 @@ std::vector<uint8_t> pack_transition_narrow(const wm_dims& dm, const wm_weights&
   return blk;
 }
 
+// Narrow cost-model blob (Narrow::c_bytes): Wc1 with the operand orders of
+// the narrow rollout ([z_T] as z fragments, [phi; h] natural), bc1, wc2.
+std::vector<uint8_t> pack_cost_narrow(const wm_dims& dm, const wm_weights& w) {
+  const int D = dm.d, E = dm.embed_dim, HW = dm.hw_dim, C = dm.cost_hidden, IN = D + E + HW;
+  const int NKC = IN / 32;
+  const bool bf = dm.precision == WM_BF16;
+  const int gpk = bf ? 1 : 2, per = 8 / gpk;
+  std::vector<uint8_t> blk(Narrow::c_bytes(D, E, HW, C, gpk), 0);
+  auto put = [&](size_t frag_group0, int lane, int j, float v) {
+    const size_t off = (frag_group0 + (size_t)(j / per)) * 1024 + (size_t)lane * 16;
+    if (bf) {
+      const uint16_t b = f32_to_bf16(v);
+      std::memcpy(&blk[off + (size_t)(j % per) * 2], &b, 2);
+    } else {
+      std::memcpy(&blk[off + (size_t)(j % per) * 4], &v, 4);
+    }
+  };
+  for (int cc = 0; cc < C / 32; ++cc)
+    for (int kf = 0; kf < NKC; ++kf)
+      for (int rb = 0; rb < 2; ++rb)
+        for (int L = 0; L < 64; ++L)
+          for (int j = 0; j < 8; ++j) {
+            const int row = 32 * cc + 16 * rb + (L & 15);
+            put((((size_t)cc * NKC + kf) * 2 + rb) * gpk, L, j,
+                w.wc1[(size_t)row * IN + narrow_x_feature(D, kf, L >> 4, j)]);
+          }
+  const size_t tail = (size_t)(C / 32) * NKC * 2 * gpk * 1024;
+  std::memcpy(&blk[tail], w.bc1, (size_t)C * 4);
+  std::memcpy(&blk[tail + (size_t)C * 4], w.wc2, (size_t)C * 4);
+  return blk;
+}
+
 // Transposed narrow-tile blob for the rollout-loss backward (Narrow::t_bytes).
 std::vector<uint8_t> pack_transposed_narrow(const wm_dims& dm, const wm_weights& w) {
   const int D = dm.d, E = dm.embed_dim, H = dm.trans_hidden, IN = D + E;
@@ -440,7 +472,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.dims = dm;
   m.prec = dm.precision;
   const int D = dm.d, E = dm.embed_dim, K = dm.n_kinds, P = dm.n_params, HW = dm.hw_dim;
-  std::vector<uint8_t> tw1, tw2, cost, twh, tw2t, tw1t, twht, tn, tnt;
+  std::vector<uint8_t> tw1, tw2, cost, twh, tw2t, tw1t, twht, tn, tnt, cn;
   const bool l2 = dm.norm == WM_NORM_L2;
   if (m.prec == WM_BF16) {
     pack_transition<GeomBF16>(dm, *w, tw1, tw2);
@@ -465,6 +497,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   if (D % 32 == 0 && E % 32 == 0) {
     tn = pack_transition_narrow(dm, *w);
     tnt = pack_transposed_narrow(dm, *w);
+    if (HW % 32 == 0 && dm.cost_hidden % 32 == 0) cn = pack_cost_narrow(dm, *w);
   }
   // rollout table: type_emb [K][E + 4], param_w^T [PMAX][E], param_b [E], b2 (accumulator order)
   std::vector<float> tab;
@@ -511,6 +544,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   const size_t o_wht = off; off = align256(off + twht.size());
   const size_t o_tn = off; off = align256(off + tn.size());
   const size_t o_tnt = off; off = align256(off + tnt.size());
+  const size_t o_cn = off; off = align256(off + cn.size());
   const size_t o_tab = off; off = align256(off + tab.size() * 4);
   const size_t o_enc = off; off = align256(off + enc.size() * 4);
   void* dev = nullptr;
@@ -528,6 +562,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   if (e == hipSuccess && !twht.empty()) e = hipMemcpy(base + o_wht, twht.data(), twht.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess && !tn.empty()) e = hipMemcpy(base + o_tn, tn.data(), tn.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess && !tnt.empty()) e = hipMemcpy(base + o_tnt, tnt.data(), tnt.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess && !cn.empty()) e = hipMemcpy(base + o_cn, cn.data(), cn.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(base + o_tab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess && !enc.empty()) e = hipMemcpy(base + o_enc, enc.data(), enc.size() * 4, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
@@ -544,6 +579,7 @@ wm_status wm_model_create(const wm_dims* dims, const wm_weights* w, wm_model** o
   m.trans_wht = twht.empty() ? nullptr : base + o_wht;
   m.trans_n = tn.empty() ? nullptr : base + o_tn;
   m.trans_nt = tnt.empty() ? nullptr : base + o_tnt;
+  m.cost_n = cn.empty() ? nullptr : base + o_cn;
   m.roll_tab = reinterpret_cast<const float*>(base + o_tab);
   m.emb_nat = m.roll_tab;
   const float* encp = reinterpret_cast<const float*>(base + o_enc);
@@ -690,10 +726,11 @@ wm_status wm_evaluate(const wm_model* model, const float* init, int32_t init_is_
   float* sc = scores ? scores : reinterpret_cast<float*>(w8 + L.scores);
   WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, reinterpret_cast<int32_t*>(w8 + L.hist), err, st));
   bool phi_done = false;
+  ScoreFuse sf{hw, n_hw, sc, false};
   WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zTo, phi,
-                                          &phi_done, err, st));
+                                          &phi_done, err, st, &sf));
   if (!phi_done) WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
-  WM_TIMED(TK_SCORE, st, launch_score(model->dm, zTo, phi, B, hw, n_hw, sc, st));
+  if (!sf.done) WM_TIMED(TK_SCORE, st, launch_score(model->dm, zTo, phi, B, hw, n_hw, sc, st));
   WM_TIMED(TK_TOPK, st, launch_topk(sc, n_hw, B, seg, k, idx, val, st));
   return ok();
 }

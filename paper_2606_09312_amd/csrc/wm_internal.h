@@ -200,6 +200,13 @@ struct Narrow {
   static constexpr size_t t_bytes(int D, int E, int H, int gpk) {
     return (w2t_groups(D, H, gpk) + w1t_groups(D, E, H, gpk)) * 1024;
   }
+  // Cost-model blob (scores fused into the narrow rollout): Wc1 chunk cc
+  // (32 cost-hidden units), k-fragment kf over [z_T; phi; h] (z-operand
+  // order, then natural), row block rb: group ((cc * NKC + kf) * 2 + rb) *
+  // gpk + hh, NKC = (D + E + HW) / 32; then bc1 and wc2 (C floats each).
+  static constexpr size_t c_bytes(int D, int E, int HW, int C, int gpk) {
+    return (size_t)(C / 32) * ((D + E + HW) / 32) * 2 * gpk * 1024 + (size_t)C * 8;
+  }
 };
 
 // Action parameters per step are padded to PMAX in the embedding table
@@ -248,6 +255,7 @@ struct DevModel {
   const uint8_t* trans_wht; // Wh^T fragments (paper-form rollout-loss backward)
   const uint8_t* trans_n;   // narrow-tile transition blob (d and e multiples of 32), or null
   const uint8_t* trans_nt;  // its transposed blob (rollout-loss backward), or null
+  const uint8_t* cost_n;    // narrow cost-model blob (hw_dim a multiple of 32), or null
   const float* roll_tab;    // type_emb [K][E + 4] (padded rows), param_w^T [PMAX][E] (zero rows past P), param_b [E], b2 (acc order) [D]
   const float* emb_nat;     // the first three parts of roll_tab
   const float* enc_w1t;     // We1^T [F][Fh] (bf16-rounded values in bf16 mode)
@@ -280,12 +288,20 @@ __host__ __device__ constexpr inline int phi_struct_dim(int K, int P) { return K
 // hist: bucket_groups(B) * (T_max + 1) ints of workspace (unused when 0)
 hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
                          int2* perm, int32_t* hist, int32_t* err, hipStream_t st);
+// Scores requested with a rollout (wm_evaluate): the narrow kernel computes
+// them itself when it runs and sets `done`; otherwise launch_score does.
+struct ScoreFuse {
+  const float* hw;
+  int32_t n_hw;
+  float* scores;
+  bool done;
+};
 // phi (may be null): the kernel families that can also sum the action
 // features write them and set *phi_done; otherwise launch_phi computes them.
 hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
                           int32_t B, int32_t T_max, float* zT, float* phi, bool* phi_done,
-                          int32_t* err, hipStream_t st);
+                          int32_t* err, hipStream_t st, ScoreFuse* sf = nullptr);
 hipError_t launch_phi(const DevModel& m, const int32_t* types, const int32_t* params,
                       const int32_t* lens, int32_t B, int32_t T_max, float* phi, hipStream_t st);
 hipError_t launch_score(const DevModel& m, const float* zT, const float* phi, int32_t B,

@@ -361,6 +361,12 @@ struct RollArgs {
   float *V, *SC;            // paper form: [R][D] Wh e, [R][4] v.z, v.v, |u|, 0
   const int32_t* off;
   int32_t* row_src;
+  // scores fused into the narrow rollout: cost blob, hw [n_hw][HW], scores [n_hw][B]
+  const uint8_t* costn;
+  const float* hw;
+  float* scores;
+  float bc2;
+  int n_hw, HW, C;
 };
 
 // Copies of the next weight chunk (its W1 and/or W2 part) into LDS, issued
@@ -1726,6 +1732,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_rows_kernel(const RollArgs 
 // halves.
 typedef float f32x4n __attribute__((ext_vector_type(4)));
 typedef float f32x8n __attribute__((ext_vector_type(8)));
+constexpr int SCORE_MAX_HW = 32;        // hardware-vector width limit
 
 struct NarrowBF16 {
   using XF = bf16x8;
@@ -1816,9 +1823,16 @@ struct NarrowGeom {
 // per valid step in compact row off[i] + t, the operands X = [z; e], the
 // pre-activations A, the GELU outputs G and the prediction, as the 32-wide
 // row-owned kernel does.
-template <class NP, int D, int E, int NC, int W, bool NORM, bool TRAIN = false>
+// SCORE: after the last step the workgroup also scores its candidates with
+// the cost model (Eq. 3) for every hardware vector: wavefront w takes the
+// cost-hidden chunks w, w + W, ...; the [z_T; phi] part of the first product
+// is shared by the hardware vectors; partial scores are summed over the
+// candidate's lane groups and then over the wavefronts in a fixed order.
+constexpr int NARROW_SCORE_HW = 2;      // hardware vectors per fused launch
+template <class NP, int D, int E, int NC, int W, bool NORM, bool TRAIN = false, bool SCORE = false>
 __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArgs a) {
   static_assert(!(TRAIN && NORM), "narrow training forward: residual form");
+  static_assert(!(TRAIN && SCORE), "scores belong to the evaluator");
   using NG = NarrowGeom<NP, D, E, NC, W>;
   using XF = typename NP::XF;
   constexpr int GPK = NG::GPK, NK = NG::NK, NZ = NG::NZ, NE = NG::NE, NB = NG::NB, NBW = NG::NBW;
@@ -2141,6 +2155,95 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     const float* ph = phib + n * (E + 1) + f0;
 #pragma unroll
     for (int j = 0; j < 8; ++j) a.phi[(size_t)cand * E + f0 + j] = ph[j] * inv;
+  }
+  if constexpr (SCORE) {
+    // x = [z_T; phi; h]: z_T fragments from the last exchange, phi from the
+    // sums (complete after that exchange's barrier), h per hardware vector
+    constexpr int NHF = 1;                           // hw fragments (hw_dim <= 32)
+    const int NH = a.HW / 32, NCC = a.C / 32, NKC = NZ + NE + NH;
+    const float inv = len > 0 ? 1.0f / (float)len : 0.0f;
+    XF pf[NE];
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = phib[n * (E + 1) + 32 * q + 8 * g + j] * inv;
+      pf[q] = NP::cvt(v);
+    }
+    XF hf[NARROW_SCORE_HW][NHF > 0 ? NHF : 1];
+#pragma unroll
+    for (int jj = 0; jj < NARROW_SCORE_HW; ++jj)
+#pragma unroll
+      for (int q = 0; q < (NHF > 0 ? NHF : 1); ++q) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          v[j] = (jj < a.n_hw && q < NH) ? a.hw[(size_t)jj * a.HW + 32 * q + 8 * g + j] : 0.0f;
+        hf[jj][q] = NP::cvt(v);
+      }
+    const float* bc1n = reinterpret_cast<const float*>(a.costn + (size_t)NCC * NKC * 2 * GPK * 1024);
+    const float* wc2n = bc1n + a.C;
+    float part[NARROW_SCORE_HW] = {};
+    for (int cc = w; cc < NCC; cc += W) {
+      const uint8_t* cb = a.costn + (size_t)cc * NKC * 2 * GPK * 1024 + lane * 16;
+      auto grp_at = [&](int kf, int rb, int hh) -> u32x4 {
+        return *reinterpret_cast<const gu32x4*>((gu8*)cb + ((size_t)(kf * 2 + rb) * GPK + hh) * 1024);
+      };
+      f32x4n acc2[2] = {f32x4n{}, f32x4n{}};
+#pragma unroll
+      for (int kf = 0; kf < NZ + NE; ++kf)
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int hh = 0; hh < GPK; ++hh)
+            acc2[rb] = NP::mma(grp_at(kf, rb, hh), hh, kf < NZ ? xf[kf < NZ ? kf : 0] : pf[kf < NZ ? 0 : kf - NZ], acc2[rb]);
+      f32x4n b4[2], w4[2];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        b4[rb] = *reinterpret_cast<const f32x4n*>(bc1n + 32 * cc + 16 * rb + 4 * g);
+        w4[rb] = *reinterpret_cast<const f32x4n*>(wc2n + 32 * cc + 16 * rb + 4 * g);
+      }
+#pragma unroll
+      for (int jj = 0; jj < NARROW_SCORE_HW; ++jj) {
+        if (jj < a.n_hw) {
+          f32x4n aj[2] = {acc2[0], acc2[1]};
+#pragma unroll
+          for (int q = 0; q < (NHF > 0 ? NHF : 1); ++q)
+            if (q < NH)
+#pragma unroll
+              for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+                for (int hh = 0; hh < GPK; ++hh) aj[rb] = NP::mma(grp_at(NZ + NE + q, rb, hh), hh, hf[jj][q], aj[rb]);
+          float sum = 0.0f;
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sum = fmaf(w4[rb][r], gelu(aj[rb][r] + b4[rb][r]), sum);
+          part[jj] += sum;
+        }
+      }
+    }
+    // the candidate's four lane groups, then the wavefronts in order
+    float* red = dots + (NORM ? W * 3 * 16 : 0) + 16 * (E + 1);          // [W][NARROW_SCORE_HW][16]
+#pragma unroll
+    for (int jj = 0; jj < NARROW_SCORE_HW; ++jj) {
+      float v = part[jj];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (g == 0) red[(w * NARROW_SCORE_HW + jj) * 16 + n] = v;
+    }
+    __syncthreads();
+    if (w == 0 && g == 0 && valid) {
+#pragma unroll
+      for (int jj = 0; jj < NARROW_SCORE_HW; ++jj) {
+        if (jj < a.n_hw) {
+          float y = 0.0f;
+#pragma unroll
+          for (int ww = 0; ww < W; ++ww) y += red[(ww * NARROW_SCORE_HW + jj) * 16 + n];
+          a.scores[(size_t)jj * a.B + cand] = y + a.bc2;
+        }
+      }
+    }
   }
   if (valid && !TRAIN) {
 #pragma unroll
@@ -3670,7 +3773,6 @@ __global__ __launch_bounds__(EMB_THREADS) void emb_grad_kernel(const float* __re
 // LDS.  The [z_T; phi] product is shared by all hardware vectors; each vector
 // adds its own small product.  Up to 4 hardware vectors per launch.
 
-constexpr int SCORE_MAX_HW = 32;        // hardware-vector width limit
 constexpr int SCORE_HW_PER_LAUNCH = 2;  // hardware vectors per score launch
 
 struct ScoreArgs {
@@ -4269,13 +4371,13 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
 // compute unit at d = 256, e = 64: bf16 with hidden widths 512 and 1024 (both
 // transition forms), fp32 with hidden width 512 (residual form).
 constexpr int NARROW_MAX_TILES = 256;
-template <class NP, int NC, bool NORM, bool TRAIN = false>
+template <class NP, int NC, bool NORM, bool TRAIN = false, bool SCORE = false>
 hipError_t launch_rollout_narrow(const DevModel& m, RollArgs a, int tiles, hipStream_t st) {
   using NG = NarrowGeom<NP, 256, 64, NC, 8>;
   a.w1 = m.trans_n;
   const int lds = m.roll_tab_bytes + NG::G_BYTES + NG::X_BYTES + (NORM ? 8 * 3 * 16 * 4 : 0) +
-                  (a.phi && !TRAIN ? 16 * (64 + 1) * 4 : 0);
-  auto kern = rollout_narrow_kernel<NP, 256, 64, NC, 8, NORM, TRAIN>;
+                  (a.phi && !TRAIN ? 16 * (64 + 1) * 4 : 0) + (SCORE ? 8 * NARROW_SCORE_HW * 16 * 4 : 0);
+  auto kern = rollout_narrow_kernel<NP, 256, 64, NC, 8, NORM, TRAIN, SCORE>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -4288,7 +4390,7 @@ hipError_t launch_rollout_narrow(const DevModel& m, RollArgs a, int tiles, hipSt
 hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
                           const int32_t* types, const int32_t* params, const int32_t* lens,
                           int32_t B, int32_t T_max, float* zT, float* phi, bool* phi_done,
-                          int32_t* err, hipStream_t st) {
+                          int32_t* err, hipStream_t st, ScoreFuse* sf) {
   RollArgs a{};
   a.w1 = m.trans_w1; a.w2 = m.trans_w2; a.wh = m.trans_wh; a.tab = m.roll_tab; a.z0 = z0; a.perm = perm; a.types = types;
   a.params = params; a.lens = lens; a.zT = zT; a.phi = phi; a.err = err; a.B = B; a.T_max = T_max;
@@ -4306,18 +4408,32 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
   const int ntiles = (B + 15) / 16;
   if (d == 256 && e == 64 && m.trans_n && B > 0 && ntiles <= NARROW_MAX_TILES) {
     const int NC = m.dims.trans_hidden / 32;
-    if (prec == WM_BF16 && (NC == 16 || NC == 32)) {
-      *phi_done = phi != nullptr;
-      if (norm)
-        return NC == 16 ? launch_rollout_narrow<NarrowBF16, 16, true>(m, a, ntiles, st)
-                        : launch_rollout_narrow<NarrowBF16, 32, true>(m, a, ntiles, st);
-      return NC == 16 ? launch_rollout_narrow<NarrowBF16, 16, false>(m, a, ntiles, st)
-                      : launch_rollout_narrow<NarrowBF16, 32, false>(m, a, ntiles, st);
+    // scores fused: phi sums present, the narrow cost blob, at most two
+    // hardware vectors of at most 32 features
+    const bool fuse = sf && phi && m.cost_n && sf->n_hw >= 1 && sf->n_hw <= NARROW_SCORE_HW &&
+                      m.dims.hw_dim <= SCORE_MAX_HW;
+    if (fuse) {
+      a.costn = m.cost_n; a.hw = sf->hw; a.scores = sf->scores; a.bc2 = m.bc2;
+      a.n_hw = sf->n_hw; a.HW = m.dims.hw_dim; a.C = m.dims.cost_hidden;
     }
-    if (prec == WM_FP32 && NC == 16 && !norm) {
+    auto narrow = [&](auto np, auto nc_tag, auto norm_tag) -> hipError_t {
+      using NPT = decltype(np);
+      constexpr int NCT = decltype(nc_tag)::value;
+      constexpr bool NT = decltype(norm_tag)::value;
       *phi_done = phi != nullptr;
-      return launch_rollout_narrow<NarrowF32, 16, false>(m, a, ntiles, st);
-    }
+      if (fuse) {
+        sf->done = true;
+        return launch_rollout_narrow<NPT, NCT, NT, false, true>(m, a, ntiles, st);
+      }
+      return launch_rollout_narrow<NPT, NCT, NT, false, false>(m, a, ntiles, st);
+    };
+    using I16 = std::integral_constant<int, 16>;
+    using I32 = std::integral_constant<int, 32>;
+    using BT = std::true_type;
+    using BF = std::false_type;
+    if (prec == WM_BF16 && NC == 16) return norm ? narrow(NarrowBF16{}, I16{}, BT{}) : narrow(NarrowBF16{}, I16{}, BF{});
+    if (prec == WM_BF16 && NC == 32) return norm ? narrow(NarrowBF16{}, I32{}, BT{}) : narrow(NarrowBF16{}, I32{}, BF{});
+    if (prec == WM_FP32 && NC == 16 && !norm) return narrow(NarrowF32{}, I16{}, BF{});
   }
 #define WM_ROLL(PR, D, E)                                                                          \
   return norm ? launch_rollout_de<PR, D, E, true>(m, a, tiles, blocks, waves, split, phi_done, st)  \

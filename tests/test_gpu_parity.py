@@ -260,8 +260,13 @@ def test_separate_entry_points_match_fused(wm):
     wm.topk(sc, I["seg_off"], k, idx, val)
     wm.device_status(ws)
     np.testing.assert_array_equal(zT.cpu().numpy(), fused["zT"].astype(np.float32))
-    np.testing.assert_array_equal(sc.cpu().numpy(), fused["scores"].astype(np.float32))
-    np.testing.assert_array_equal(idx.cpu().numpy(), fused["idx"])
+    # small batches score inside the rollout launch: the same rounded
+    # operands, another fp32 summation order than the separate score kernel
+    s_sep = sc.cpu().numpy().astype(np.float64)
+    assert np.abs(s_sep - fused["scores"]).max() <= 1e-5 * np.abs(fused["scores"]).max()
+    check_topk_self_consistent(idx.cpu().numpy(), val.cpu().numpy().astype(np.float64), s_sep,
+                               I["seg_off"], k)
+    check_topk_vs_oracle(idx.cpu().numpy(), fused["scores"], I["seg_off"], k, 1e-4)
     ref = O.evaluate(W, I, k, "bf16")
     assert np.abs(phi.cpu().numpy() - ref["phi"]).max() <= 1e-4 * max(1.0, np.abs(ref["phi"]).max())
 
