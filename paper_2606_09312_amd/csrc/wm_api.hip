@@ -191,9 +191,9 @@ std::vector<uint8_t> pack_cost_narrow(const wm_dims& dm, const wm_weights& w) {
 // Transposed narrow-tile blob for the rollout-loss backward (Narrow::t_bytes).
 std::vector<uint8_t> pack_transposed_narrow(const wm_dims& dm, const wm_weights& w) {
   const int D = dm.d, E = dm.embed_dim, H = dm.trans_hidden, IN = D + E;
-  const bool bf = dm.precision == WM_BF16;
+  const bool bf = dm.precision == WM_BF16, l2 = dm.norm == WM_NORM_L2;
   const int gpk = bf ? 1 : 2, per = 8 / gpk;
-  std::vector<uint8_t> blk(Narrow::t_bytes(D, E, H, gpk), 0);
+  std::vector<uint8_t> blk(Narrow::t_bytes(D, E, H, gpk) + (l2 ? Narrow::wht_bytes(D, E, gpk) : 0), 0);
   auto put = [&](size_t frag_group0, int lane, int j, float v) {
     const size_t off = (frag_group0 + (size_t)(j / per)) * 1024 + (size_t)lane * 16;
     if (bf) {
@@ -220,6 +220,16 @@ std::vector<uint8_t> pack_transposed_narrow(const wm_dims& dm, const wm_weights&
           const int feat = 16 * ob + (L & 15), hid = 32 * c + narrow_g_feature(L >> 4, j);
           put(g1 + ((size_t)c * (IN / 16) + ob) * gpk, L, j, w.w1[(size_t)hid * IN + feat]);
         }
+  if (l2) {
+    const size_t gh = g1 + Narrow::w1t_groups(D, E, H, gpk);
+    for (int eb = 0; eb < E / 16; ++eb)
+      for (int kf = 0; kf < D / 32; ++kf)
+        for (int L = 0; L < 64; ++L)
+          for (int j = 0; j < 8; ++j) {
+            const int emb = 16 * eb + (L & 15), lat = narrow_x_feature(D, kf, L >> 4, j);
+            put(gh + ((size_t)eb * (D / 32) + kf) * gpk, L, j, w.wh[(size_t)lat * E + emb]);
+          }
+  }
   return blk;
 }
 

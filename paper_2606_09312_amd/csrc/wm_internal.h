@@ -200,6 +200,9 @@ struct Narrow {
   static constexpr size_t t_bytes(int D, int E, int H, int gpk) {
     return (w2t_groups(D, H, gpk) + w1t_groups(D, E, H, gpk)) * 1024;
   }
+  // paper form: then Wh^T, embedding block eb (16 rows), latent fragment kf
+  // (z-operand order): group (eb * D/32 + kf) * gpk + hh after W1^T.
+  static constexpr size_t wht_bytes(int D, int E, int gpk) { return (size_t)(E / 16) * (D / 32) * gpk * 1024; }
   // Cost-model blob (scores fused into the narrow rollout): Wc1 chunk cc
   // (32 cost-hidden units), k-fragment kf over [z_T; phi; h] (z-operand
   // order, then natural), row block rb: group ((cc * NKC + kf) * 2 + rb) *

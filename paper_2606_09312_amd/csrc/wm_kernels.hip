@@ -1819,10 +1819,10 @@ struct NarrowGeom {
   static constexpr int G_BYTES = NC * GPK * 1024, X_BYTES = NK * GPK * 1024;
 };
 
-// TRAIN (residual form): the training forward of the rollout loss; stores,
-// per valid step in compact row off[i] + t, the operands X = [z; e], the
-// pre-activations A, the GELU outputs G and the prediction, as the 32-wide
-// row-owned kernel does.
+// TRAIN: the training forward of the rollout loss; stores, per valid step in
+// compact row off[i] + t, the operands X = [z; e], the pre-activations A,
+// the GELU outputs G and the prediction, as the 32-wide row-owned kernel
+// does (paper form: the unit prediction, |u|, v and the dots v.z, v.v).
 // SCORE: after the last step the workgroup also scores its candidates with
 // the cost model (Eq. 3) for every hardware vector: wavefront w takes the
 // cost-hidden chunks w, w + W, ...; the [z_T; phi] part of the first product
@@ -1831,7 +1831,6 @@ struct NarrowGeom {
 constexpr int NARROW_SCORE_HW = 2;      // hardware vectors per fused launch
 template <class NP, int D, int E, int NC, int W, bool NORM, bool TRAIN = false, bool SCORE = false>
 __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArgs a) {
-  static_assert(!(TRAIN && NORM), "narrow training forward: residual form");
   static_assert(!(TRAIN && SCORE), "scores belong to the evaluator");
   using NG = NarrowGeom<NP, D, E, NC, W>;
   using XF = typename NP::XF;
@@ -1985,13 +1984,16 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
       whq[i] = *reinterpret_cast<const u32x4*>(whb + ((size_t)w * NBW * NE * GPK + i) * 1024 + lane * 16);
   }
   auto embed_all = [&](int s) {
+    s_cur = s;
     int ty;
     float u[PMAX], af;
     decode(s, ty, u, af);
 #pragma unroll
     for (int q = 0; q < NE; ++q) xe[NORM ? q : 0] = embed_frag(q, ty, u, af);
   };
-  auto boundary = [&](bool renorm, bool project) {
+  // training: the unit prediction of the finished step t and |u| go to row
+  // t, the next step's v, v.z and v.v to row t + 1
+  auto boundary = [&](bool renorm, bool project, int t) {
     f32x4n vq[NBW];
     float vz = 0.0f, vv = 0.0f, zz = 0.0f;
 #pragma unroll
@@ -2028,6 +2030,28 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     }
     const float sc = (renorm && zz > 0.0f) ? rsqrtf(zz) : 1.0f;
     const float al = (project && vv > 0.0f) ? vz / vv : 0.0f;
+    if constexpr (TRAIN) {
+      if (renorm) {                  // step t was active
+        const size_t rt = row0 + t;
+#pragma unroll
+        for (int bq = 0; bq < NBW; ++bq) {
+          const f32x4n pv = zq[bq] * sc;
+          *reinterpret_cast<f32x4n*>(a.Pz + rt * D + 16 * (w * NBW + bq) + 4 * g) = pv;
+        }
+        if (w == 0 && g == 0) a.SC[rt * 4 + 2] = sqrtf(zz);
+      }
+      if (project) {                 // step t + 1 is active
+        const size_t rs = row0 + (t + 1);
+#pragma unroll
+        for (int bq = 0; bq < NBW; ++bq)
+          *reinterpret_cast<f32x4n*>(a.V + rs * D + 16 * (w * NBW + bq) + 4 * g) = vq[bq];
+        if (w == 0 && g == 0) {
+          a.SC[rs * 4 + 0] = vz * sc;
+          a.SC[rs * 4 + 1] = vv;
+          a.SC[rs * 4 + 3] = 0.0f;
+        }
+      }
+    }
 #pragma unroll
     for (int bq = 0; bq < NBW; ++bq)
 #pragma unroll
@@ -2056,7 +2080,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
   wait_vm_then_barrier();
   if constexpr (NORM) {
     embed_all(0);
-    boundary(false, 0 < len);
+    boundary(false, 0 < len, -1);
   } else {
     embed_share(0);
   }
@@ -2136,13 +2160,13 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     for (int bq = 0; bq < NBW; ++bq) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) zq[bq][r] += dz[bq][r] + b2v[bq][r] * actf;
-      if constexpr (TRAIN) {
+      if constexpr (TRAIN && !NORM) {
         if (active) *reinterpret_cast<f32x4n*>(a.Pz + row * D + 16 * (w * NBW + bq) + 4 * g) = zq[bq];
       }
     }
     if constexpr (NORM) {
       embed_all(t + 1);
-      boundary(active, t + 1 < len);
+      boundary(active, t + 1 < len, t);
     } else {
       embed_share(t + 1);
     }
@@ -3392,9 +3416,15 @@ struct NarrowBwdGeom {
   static constexpr int DA_BYTES = NC * GPK * 1024, DL_BYTES = NZ * GPK * 1024;
   static constexpr int DE_BYTES = W * NBE * 64 * 16;
   static constexpr int LDS = DA_BYTES + DL_BYTES + DE_BYTES;
+  static constexpr int DOTS_BYTES = 2 * W * 16 * 4;        // paper form: two dot products
 };
 
-template <class NP, int D, int E, int NC, int W>
+// NORM (paper form, as the one-wavefront kernel): du through the
+// normalisation at the start of a step, and dz, dv through the projection
+// after the MLP part, with the dots summed over the lane groups and then the
+// wavefronts through LDS; the normal map's dE partials (Wh^T . dv over the
+// owned fragment) join the MLP ones.
+template <class NP, int D, int E, int NC, int W, bool NORM>
 __global__ __launch_bounds__(64 * W, 1) void train_bwd_narrow_kernel(const TrainArgs a) {
   using BG = NarrowBwdGeom<NP, D, E, NC, W>;
   using XF = typename NP::XF;
@@ -3406,12 +3436,14 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_narrow_kernel(const Train
   uint8_t* dabuf = lds;                                             // dA fragments [NC]
   uint8_t* dlbuf = lds + BG::DA_BYTES;                              // delta fragments [NZ]
   float* debuf = reinterpret_cast<float*>(lds + BG::DA_BYTES + BG::DL_BYTES);  // [W][NBE][64][4]
+  float* dots = reinterpret_cast<float*>(lds + BG::LDS);            // paper form: [2][W][16]
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n = lane & 15, g = lane >> 4;
   const int pos = blockIdx.x * 16 + n;
   const bool valid = pos < a.B;
-  const int cand = valid ? a.perm[pos].x : 0;
+  const int2 pc = valid ? a.perm[pos] : make_int2(0, 0);
+  const int cand = pc.x;
   const int len = valid ? clampi(a.lens[cand], 0, a.T_max) : 0;
   const int T_wg = __builtin_amdgcn_readfirstlane(
       clampi(a.lens[a.perm[blockIdx.x * 16].x], 0, a.T_max));
@@ -3447,16 +3479,42 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_narrow_kernel(const Train
     gu8* p1 = baseA1;
     gu8* pb = baseB;
     asm volatile("" : "+v"(p2), "+v"(p1), "+v"(pb));
-    // ---- owned delta blocks: seed, delta_{t+1}, operand fragment w in LDS
+    // ---- owned delta blocks: seed, delta_{t+1} (paper form: du through the
+    // normalisation, du = (delta - (delta . z) z) / |u| with z the unit
+    // prediction), operand fragment w in LDS
+    f32x4n sc = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (active) {
+#pragma unroll
+      for (int bq = 0; bq < NBW; ++bq)
+        dq[bq] += *reinterpret_cast<const f32x4n*>(a.SD + row * D + 16 * (w * NBW + bq) + 4 * g);
+    }
+    if constexpr (NORM) {
+      if (active) sc = *reinterpret_cast<const f32x4n*>(a.SC + row * 4);
+      f32x4n pb[NBW];
+      float dz = 0.0f;
+#pragma unroll
+      for (int bq = 0; bq < NBW; ++bq) {
+        pb[bq] = active ? *reinterpret_cast<const f32x4n*>(a.P + row * D + 16 * (w * NBW + bq) + 4 * g) : f32x4n{};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dz = fmaf(dq[bq][r], pb[bq][r], dz);
+      }
+      dz += __shfl_xor(dz, 16);
+      dz += __shfl_xor(dz, 32);
+      if (g == 0) dots[w * 16 + n] = dz;
+      __syncthreads();
+      dz = 0.0f;
+#pragma unroll
+      for (int ww = 0; ww < W; ++ww) dz += dots[ww * 16 + n];
+      const bool nrm = active && sc[2] > 0.0f;
+      const float inu = nrm ? 1.0f / sc[2] : 1.0f;
+      const float cz = nrm ? dz : 0.0f;
+#pragma unroll
+      for (int bq = 0; bq < NBW; ++bq) dq[bq] = (dq[bq] - cz * pb[bq]) * inu;
+    }
     float v8[8];
 #pragma unroll
     for (int bq = 0; bq < NBW; ++bq) {
-      float* sd = a.SD + row * D + 16 * (w * NBW + bq) + 4 * g;
-      if (active) {
-        const f32x4n s4 = *reinterpret_cast<const f32x4n*>(sd);
-        dq[bq] += s4;
-        *reinterpret_cast<f32x4n*>(sd) = dq[bq];
-      }
+      if (active) *reinterpret_cast<f32x4n*>(a.SD + row * D + 16 * (w * NBW + bq) + 4 * g) = dq[bq];
 #pragma unroll
       for (int r = 0; r < 4; ++r) v8[4 * bq + r] = dq[bq][r];
     }
@@ -3479,6 +3537,7 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_narrow_kernel(const Train
 #pragma unroll
     for (int q = 0; q < NBE; ++q) deacc[q] = f32x4n{};
     XF dfr = {}, dcur = {}, dnext = {};
+    f32x4n emlp = {};              // paper form: this wavefront's dE block, MLP part
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
@@ -3520,7 +3579,8 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_narrow_kernel(const Train
             f32x4n e4 = {};
 #pragma unroll
             for (int ww = 0; ww < W; ++ww) e4 += *reinterpret_cast<const f32x4n*>(debuf + ((ww * NBE + w) * 64 + lane) * 4);
-            if (active) *reinterpret_cast<f32x4n*>(a.DE + row * E + 16 * w + 4 * g) = e4;
+            if constexpr (NORM) emlp = e4;
+            else if (active) *reinterpret_cast<f32x4n*>(a.DE + row * E + 16 * w + 4 * g) = e4;
           }
           dcur = NP::load(dabuf, 0, lane);
           dnext = NP::load(dabuf, NC > 1 ? 1 : 0, lane);
@@ -3534,6 +3594,69 @@ __global__ __launch_bounds__(64 * W, 1) void train_bwd_narrow_kernel(const Train
         }
       }
       __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (NORM) {
+      // through z' = z - (w . z) w, w = v / |v|: dz = dz' - (w . dz') w,
+      // dv = (dw - (w . dw) w) / |v| with w . dw = -2 (w . z)(w . dz'),
+      // de += R(Wh)^T R(dv)
+      const bool prj = active && sc[1] > 0.0f;
+      const float inv = prj ? rsqrtf(sc[1]) : 0.0f;
+      const float wz = sc[0] * inv;
+      f32x4n vb[NBW];
+      float wdz = 0.0f;
+#pragma unroll
+      for (int bq = 0; bq < NBW; ++bq) {
+        vb[bq] = prj ? *reinterpret_cast<const f32x4n*>(a.V + row * D + 16 * (w * NBW + bq) + 4 * g) : f32x4n{};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) wdz = fmaf(vb[bq][r], dq[bq][r], wdz);
+      }
+      wdz += __shfl_xor(wdz, 16);
+      wdz += __shfl_xor(wdz, 32);
+      if (g == 0) dots[(W + w) * 16 + n] = wdz;
+      __syncthreads();
+      wdz = 0.0f;
+#pragma unroll
+      for (int ww = 0; ww < W; ++ww) wdz += dots[(W + ww) * 16 + n];
+      wdz *= inv;
+      const float* zin = t > 0 ? a.P + (row - 1) * D : a.z0 + (size_t)pc.y * D;
+      float dv8[8];
+#pragma unroll
+      for (int bq = 0; bq < NBW; ++bq) {
+        const f32x4n zb = prj ? *reinterpret_cast<const f32x4n*>(zin + 16 * (w * NBW + bq) + 4 * g) : f32x4n{};
+        f32x4n dv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float wr = vb[bq][r] * inv;
+          dv[r] = (-(wz * dq[bq][r] + wdz * zb[r]) + 2.0f * wz * wdz * wr) * inv;
+          dq[bq][r] -= wdz * wr;
+          dv8[4 * bq + r] = dv[r];
+        }
+        if (active) *reinterpret_cast<f32x4n*>(a.DV + row * D + 16 * (w * NBW + bq) + 4 * g) = dv;
+      }
+      // normal-map part of dE over the owned latent fragment w
+      const XF dvf = NP::cvt(dv8);
+      gu8* whtb = ((gu8*)(a.wht)) + lane * 16;
+      f32x4n den[NBE];
+#pragma unroll
+      for (int q = 0; q < NBE; ++q) {
+        den[q] = f32x4n{};
+#pragma unroll
+        for (int hh = 0; hh < GPK; ++hh) {
+          const u32x4 grp = *reinterpret_cast<gu32x4*>(whtb + ((size_t)(q * NZ + w) * GPK + hh) * 1024);
+          den[q] = NP::mma(grp, hh, dvf, den[q]);
+        }
+      }
+      // the MLP partials were read before this step's dot barrier
+#pragma unroll
+      for (int q = 0; q < NBE; ++q)
+        *reinterpret_cast<f32x4n*>(debuf + ((w * NBE + q) * 64 + lane) * 4) = den[q];
+      __syncthreads();
+      if (w < NBE) {
+        f32x4n e4 = emlp;
+#pragma unroll
+        for (int ww = 0; ww < W; ++ww) e4 += *reinterpret_cast<const f32x4n*>(debuf + ((ww * NBE + w) * 64 + lane) * 4);
+        if (active) *reinterpret_cast<f32x4n*>(a.DE + row * E + 16 * w + 4 * g) = e4;
+      }
     }
     __syncthreads();                // dA / dE / delta buffers are read before the next step writes them
   }
@@ -4641,12 +4764,17 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
   const bool norm = m.dims.norm == WM_NORM_L2;
   // residual form, at most one 16-candidate tile per compute unit: narrow tiles
   const int ntiles = (io.B + 15) / 16;
-  if (m.dims.d == 256 && m.dims.embed_dim == 64 && !norm && m.trans_n && ntiles <= NARROW_MAX_TILES) {
+  if (m.dims.d == 256 && m.dims.embed_dim == 64 && m.trans_n && m.trans_nt && ntiles <= NARROW_MAX_TILES) {
     const int NC = m.dims.trans_hidden / 32;
-    const RollArgs r = train_roll_args(m, io, false);
-    if (m.prec == WM_BF16 && NC == 16) return launch_rollout_narrow<NarrowBF16, 16, false, true>(m, r, ntiles, st);
-    if (m.prec == WM_BF16 && NC == 32) return launch_rollout_narrow<NarrowBF16, 32, false, true>(m, r, ntiles, st);
-    if (m.prec == WM_FP32 && NC == 16) return launch_rollout_narrow<NarrowF32, 16, false, true>(m, r, ntiles, st);
+    const RollArgs r = train_roll_args(m, io, norm);
+    if (norm) {
+      if (m.prec == WM_BF16 && NC == 16) return launch_rollout_narrow<NarrowBF16, 16, true, true>(m, r, ntiles, st);
+      if (m.prec == WM_BF16 && NC == 32) return launch_rollout_narrow<NarrowBF16, 32, true, true>(m, r, ntiles, st);
+    } else {
+      if (m.prec == WM_BF16 && NC == 16) return launch_rollout_narrow<NarrowBF16, 16, false, true>(m, r, ntiles, st);
+      if (m.prec == WM_BF16 && NC == 32) return launch_rollout_narrow<NarrowBF16, 32, false, true>(m, r, ntiles, st);
+      if (m.prec == WM_FP32 && NC == 16) return launch_rollout_narrow<NarrowF32, 16, false, true>(m, r, ntiles, st);
+    }
   }
   if (m.dims.d == 256 && m.dims.embed_dim == 64) {
     const int NC = m.dims.trans_hidden / 32;
@@ -4672,18 +4800,21 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
   return hipErrorInvalidValue;
 }
 
-template <class NP, int NC>
+template <class NP, int NC, bool NORM>
 hipError_t launch_train_bwd_narrow(const DevModel& m, TrainArgs a, int tiles, hipStream_t st) {
   using BG = NarrowBwdGeom<NP, 256, 64, NC, 8>;
-  static_assert(BG::LDS <= 160 * 1024, "LDS");
+  constexpr int lds = BG::LDS + (NORM ? BG::DOTS_BYTES : 0);
+  static_assert(lds <= 160 * 1024, "LDS");
   a.w2t = m.trans_nt;
-  auto kern = train_bwd_narrow_kernel<NP, 256, 64, NC, 8>;
-  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, BG::LDS);
+  // paper form: the transposed normal map follows W1^T in the blob
+  a.wht = NORM ? m.trans_nt + Narrow::t_bytes(256, 64, NC * 32, NP::GPK) : nullptr;
+  auto kern = train_bwd_narrow_kernel<NP, 256, 64, NC, 8, NORM>;
+  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return e;
   }
-  hipLaunchKernelGGL(kern, dim3(tiles), dim3(512), BG::LDS, st, a);
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(512), lds, st, a);
   return hipGetLastError();
 }
 
@@ -4694,11 +4825,17 @@ hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st
   const bool norm = m.dims.norm == WM_NORM_L2;
   // residual form, at most one 16-candidate tile per compute unit: narrow tiles
   const int ntiles = (io.B + 15) / 16;
-  if (m.dims.d == 256 && m.dims.embed_dim == 64 && !norm && m.trans_nt && ntiles <= NARROW_MAX_TILES) {
+  if (m.dims.d == 256 && m.dims.embed_dim == 64 && m.trans_nt && ntiles <= NARROW_MAX_TILES) {
     const int NC = m.dims.trans_hidden / 32;
-    if (m.prec == WM_BF16 && NC == 16) return launch_train_bwd_narrow<NarrowBF16, 16>(m, a, ntiles, st);
-    if (m.prec == WM_BF16 && NC == 32) return launch_train_bwd_narrow<NarrowBF16, 32>(m, a, ntiles, st);
-    if (m.prec == WM_FP32 && NC == 16) return launch_train_bwd_narrow<NarrowF32, 16>(m, a, ntiles, st);
+    if (norm) {
+      if (m.prec == WM_BF16 && NC == 16) return launch_train_bwd_narrow<NarrowBF16, 16, true>(m, a, ntiles, st);
+      if (m.prec == WM_BF16 && NC == 32) return launch_train_bwd_narrow<NarrowBF16, 32, true>(m, a, ntiles, st);
+      if (m.prec == WM_FP32 && NC == 16) return launch_train_bwd_narrow<NarrowF32, 16, true>(m, a, ntiles, st);
+    } else {
+      if (m.prec == WM_BF16 && NC == 16) return launch_train_bwd_narrow<NarrowBF16, 16, false>(m, a, ntiles, st);
+      if (m.prec == WM_BF16 && NC == 32) return launch_train_bwd_narrow<NarrowBF16, 32, false>(m, a, ntiles, st);
+      if (m.prec == WM_FP32 && NC == 16) return launch_train_bwd_narrow<NarrowF32, 16, false>(m, a, ntiles, st);
+    }
   }
   if (m.dims.d == 256 && m.dims.embed_dim == 64) {
     const int NC = m.dims.trans_hidden / 32;

@@ -313,8 +313,12 @@ def test_l2_loss_parity_scaled(wm, name, prec, B, S):
 
 
 @pytest.mark.parametrize("name,prec,B", [("ansor_round", "bf16", 250), ("ansor_round", "fp32", 130),
-                                         ("tiny", "bf16", 200)])
+                                         ("tiny", "bf16", 200), ("ansor_round", "bf16", 5000),
+                                         ("ansor_round", "fp32", 5000)])
 def test_l2_loss_short_sequences_rowwise(wm, name, prec, B):
+    """Paper form, at most two steps; 5000 candidates take the 32-candidate
+    row-owned kernels (per-element rule for the small batches only, as in
+    the residual form)."""
     w = synth.scaled(synth.workload(name), B=B, lengths="uniform", len_lo=0, len_hi=2)
     print(f"[l2 loss short] {name} {prec} B={B}", flush=True)
     model, W = model_for(wm, name, prec, norm="l2")
@@ -322,7 +326,7 @@ def test_l2_loss_short_sequences_rowwise(wm, name, prec, B):
     tgt, neg = margin_targets(W, I, prec, 3, 83, 0.3, norm="l2")
     g = run_loss(wm, model, I, tgt, neg, 0.5, 0.3)
     rep = check_against_oracle(g, W, I, tgt, neg, 0.5, 0.3, prec, rows=True,
-                               elems=prec == "fp32", norm="l2")
+                               elems=prec == "fp32" and B <= 300, norm="l2")
     print("  " + ", ".join(f"{k} {v:.1e}" for k, v in rep.items()), flush=True)
 
 
