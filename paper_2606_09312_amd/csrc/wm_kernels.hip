@@ -1976,13 +1976,19 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
   // blocks' v come from the matrix cores (Wh groups in registers); the dots
   // are summed over the candidate's four lane groups, then over the
   // wavefronts through LDS.
-  u32x4 whq[NORM ? NBW * NE * GPK : 1];
-  if constexpr (NORM) {
-    const uint8_t* whb = a.w1 + Narrow::bytes(D, E, NC * 32, GPK);
+  // bf16 holds the wavefront's Wh groups in registers; fp32 (twice the
+  // groups, fewer free registers) reads them from L2 at each boundary
+  constexpr bool WH_REG = GPK == 1;
+  const uint8_t* whb = a.w1 + Narrow::bytes(D, E, NC * 32, GPK) + (size_t)w * NBW * NE * GPK * 1024 + lane * 16;
+  u32x4 whq[NORM && WH_REG ? NBW * NE * GPK : 1];
+  if constexpr (NORM && WH_REG) {
 #pragma unroll
-    for (int i = 0; i < NBW * NE * GPK; ++i)
-      whq[i] = *reinterpret_cast<const u32x4*>(whb + ((size_t)w * NBW * NE * GPK + i) * 1024 + lane * 16);
+    for (int i = 0; i < NBW * NE * GPK; ++i) whq[i] = *reinterpret_cast<const u32x4*>(whb + (size_t)i * 1024);
   }
+  auto wh_group = [&](int i) -> u32x4 {
+    if constexpr (NORM && WH_REG) return whq[i];
+    else return *reinterpret_cast<const gu32x4*>((gu8*)whb + (size_t)i * 1024);
+  };
   auto embed_all = [&](int s) {
     s_cur = s;
     int ty;
@@ -2003,7 +2009,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
       for (int q = 0; q < NE; ++q)
 #pragma unroll
         for (int hh = 0; hh < GPK; ++hh)
-          v = NP::mma(whq[NORM ? (bq * NE + q) * GPK + hh : 0], hh, xe[NORM ? q : 0], v);
+          v = NP::mma(wh_group((bq * NE + q) * GPK + hh), hh, xe[NORM ? q : 0], v);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         vz = fmaf(v[r], zq[bq][r], vz);
@@ -4491,8 +4497,8 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
 }
 
 // Narrow tiles (16 candidates) for batches of at most one such tile per
-// compute unit at d = 256, e = 64: bf16 with hidden widths 512 and 1024 (both
-// transition forms), fp32 with hidden width 512 (residual form).
+// compute unit at d = 256, e = 64: bf16 with hidden widths 512 and 1024, fp32
+// with hidden width 512, both transition forms.
 constexpr int NARROW_MAX_TILES = 256;
 template <class NP, int NC, bool NORM, bool TRAIN = false, bool SCORE = false>
 hipError_t launch_rollout_narrow(const DevModel& m, RollArgs a, int tiles, hipStream_t st) {
@@ -4556,7 +4562,7 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
     using BF = std::false_type;
     if (prec == WM_BF16 && NC == 16) return norm ? narrow(NarrowBF16{}, I16{}, BT{}) : narrow(NarrowBF16{}, I16{}, BF{});
     if (prec == WM_BF16 && NC == 32) return norm ? narrow(NarrowBF16{}, I32{}, BT{}) : narrow(NarrowBF16{}, I32{}, BF{});
-    if (prec == WM_FP32 && NC == 16 && !norm) return narrow(NarrowF32{}, I16{}, BF{});
+    if (prec == WM_FP32 && NC == 16) return norm ? narrow(NarrowF32{}, I16{}, BT{}) : narrow(NarrowF32{}, I16{}, BF{});
   }
 #define WM_ROLL(PR, D, E)                                                                          \
   return norm ? launch_rollout_de<PR, D, E, true>(m, a, tiles, blocks, waves, split, phi_done, st)  \
@@ -4770,6 +4776,7 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
     if (norm) {
       if (m.prec == WM_BF16 && NC == 16) return launch_rollout_narrow<NarrowBF16, 16, true, true>(m, r, ntiles, st);
       if (m.prec == WM_BF16 && NC == 32) return launch_rollout_narrow<NarrowBF16, 32, true, true>(m, r, ntiles, st);
+      if (m.prec == WM_FP32 && NC == 16) return launch_rollout_narrow<NarrowF32, 16, true, true>(m, r, ntiles, st);
     } else {
       if (m.prec == WM_BF16 && NC == 16) return launch_rollout_narrow<NarrowBF16, 16, false, true>(m, r, ntiles, st);
       if (m.prec == WM_BF16 && NC == 32) return launch_rollout_narrow<NarrowBF16, 32, false, true>(m, r, ntiles, st);

@@ -56,6 +56,7 @@ CASES = [
     ("ansor_round", "fp32", 300, 1),
     ("ansor_round", "bf16", 300, 1),
     ("ansor_round", "bf16", 5000, 1),
+    ("ansor_round", "fp32", 5000, 1),
     ("long_schedule", "bf16", 270, 1),
     ("large_latent", "bf16", 150, 1),
     ("multi_subgraph", "bf16", 4 * 70, 4),
