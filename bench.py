@@ -127,7 +127,8 @@ def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none", forest=None
         n = min(2 * n, w.B)
     return {"value": total_c / total_t, "unit": "candidates/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{total_c} randomly drawn candidates of the {w.B}-candidate batch "
+            "sample": f"{total_c} candidates in sub-batches of doubling size drawn at random (without "
+                      f"repeats within a sub-batch) from the {w.B}-candidate batch "
                       f"(float64 NumPy oracle, rollout+{'score' if forest is None else 'trees'}"
                       f"+top-k, {total_t:.1f} s)"}
 
@@ -210,7 +211,8 @@ def cpu_baseline_loss(w, W, I, tgt, neg, prec, lam, gamma, budget_s: float, norm
         n = min(2 * n, w.B)
     return {"value": total_c / total_t, "unit": "candidates/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{total_c} randomly drawn candidates of the {w.B}-candidate batch "
+            "sample": f"{total_c} candidates in sub-batches of doubling size drawn at random (without "
+                      f"repeats within a sub-batch) from the {w.B}-candidate batch "
                       f"(float64 NumPy oracle, rollout loss + gradients, {total_t:.1f} s)"}
 
 
