@@ -4123,37 +4123,71 @@ __global__ __launch_bounds__(64 * SPLIT, 1) void score_split_kernel(const ScoreA
 }
 
 // ==========================================================================
-// Encoder: one workgroup per subgraph.  In bf16 mode the input and the hidden
-// layer are rounded to bf16 (the weights already are).
+// Encoder: one workgroup of ENC_THREADS per subgraph.  In bf16 mode the input
+// and the hidden layer are rounded to bf16 (the weights already are).  Each
+// layer splits its contraction over G = ENC_THREADS / outputs thread groups
+// (coalesced weight reads across the outputs), and the G partial sums are
+// added in group order.
+constexpr int ENC_THREADS = 1024;
 
-__global__ __launch_bounds__(256) void encode_kernel(const float* __restrict__ feats,
-                                                      const float* __restrict__ w1t,
-                                                      const float* __restrict__ b1,
-                                                      const float* __restrict__ w2t,
-                                                      const float* __restrict__ b2, int F,
-                                                      int Fh, int D, int bf16,
-                                                      float* __restrict__ z0) {
+// out[o] = sum_k wt[k * N + o] x[k], o < N, through the partial-sum buffer
+__device__ __forceinline__ void enc_layer(const float* __restrict__ wt, const float* x, int K, int N,
+                                          float* part, float* out) {
+  const int tid = threadIdx.x;
+  for (int o0 = 0; o0 < N; o0 += ENC_THREADS) {
+    const int n = min(N - o0, ENC_THREADS);
+    const int G = ENC_THREADS / n, o = o0 + tid % n, grp = tid / n;
+    const int kc = (K + G - 1) / G, k0 = grp * kc, k1 = min(K, k0 + kc);
+    // eight independent loads in flight per thread (the loop is latency-bound)
+    float acc = 0.0f;
+    if (grp < G) {
+      int k = k0;
+      for (; k + 8 <= k1; k += 8) {
+        float wv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) wv[u] = wt[(size_t)(k + u) * N + o];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc = fmaf(wv[u], x[k + u], acc);
+      }
+      for (; k < k1; ++k) acc = fmaf(wt[(size_t)k * N + o], x[k], acc);
+    }
+    part[tid] = acc;
+    __syncthreads();
+    if (tid < n) {
+      float t = part[tid];
+      for (int g2 = 1; g2 < G; ++g2) t += part[g2 * n + tid];
+      out[o0 + tid] = t;
+    }
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(ENC_THREADS) void encode_kernel(const float* __restrict__ feats,
+                                                             const float* __restrict__ w1t,
+                                                             const float* __restrict__ b1,
+                                                             const float* __restrict__ w2t,
+                                                             const float* __restrict__ b2, int F,
+                                                             int Fh, int D, int bf16,
+                                                             float* __restrict__ z0) {
   extern __shared__ float esm[];
-  float* xs = esm;        // [F]
-  float* hs = esm + F;    // [Fh]
+  float* xs = esm;             // [F]
+  float* hs = esm + F;         // [Fh]
+  float* os = hs + Fh;         // [D]
+  float* part = os + D;        // [ENC_THREADS]
   const int s = blockIdx.x;
   for (int f = threadIdx.x; f < F; f += blockDim.x) {
     const float v = feats[(size_t)s * F + f];
     xs[f] = bf16 ? (float)(__bf16)v : v;
   }
   __syncthreads();
+  enc_layer(w1t, xs, F, Fh, part, hs);
   for (int o = threadIdx.x; o < Fh; o += blockDim.x) {
-    float acc = 0.0f;
-    for (int f = 0; f < F; ++f) acc = fmaf(w1t[(size_t)f * Fh + o], xs[f], acc);
-    const float g = gelu(acc + b1[o]);
+    const float g = gelu(hs[o] + b1[o]);
     hs[o] = bf16 ? (float)(__bf16)g : g;
   }
   __syncthreads();
-  for (int o = threadIdx.x; o < D; o += blockDim.x) {
-    float acc = 0.0f;
-    for (int k = 0; k < Fh; ++k) acc = fmaf(w2t[(size_t)k * D + o], hs[k], acc);
-    z0[(size_t)s * D + o] = acc + b2[o];
-  }
+  enc_layer(w2t, hs, Fh, D, part, os);
+  for (int o = threadIdx.x; o < D; o += blockDim.x) z0[(size_t)s * D + o] = os[o] + b2[o];
 }
 
 // ==========================================================================
@@ -4657,8 +4691,8 @@ hipError_t launch_topk(const float* scores, int32_t n_hw, int32_t B, const SegTa
 hipError_t launch_encode(const DevModel& m, const float* feats, int32_t S, float* z0,
                          hipStream_t st) {
   const int F = m.dims.feat_dim, Fh = m.dims.enc_hidden, D = m.dims.d;
-  const int lds = (F + Fh) * (int)sizeof(float);
-  hipLaunchKernelGGL(encode_kernel, dim3(S), dim3(256), lds, st, feats, m.enc_w1t, m.enc_b1,
+  const int lds = (F + Fh + D + ENC_THREADS) * (int)sizeof(float);
+  hipLaunchKernelGGL(encode_kernel, dim3(S), dim3(ENC_THREADS), lds, st, feats, m.enc_w1t, m.enc_b1,
                      m.enc_w2t, m.enc_b2, F, Fh, D, m.prec == WM_BF16 ? 1 : 0, z0);
   return hipGetLastError();
 }

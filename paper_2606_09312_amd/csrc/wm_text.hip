@@ -597,17 +597,32 @@ __global__ __launch_bounds__(1024) void attention_kernel(const __bf16* __restric
 }
 
 // Mean of each chunk's rows over its tokens.  One workgroup per chunk.
-__global__ __launch_bounds__(256) void pool_kernel(const float* __restrict__ h, const TTable tt,
-                                                   int window, int stride, int H,
-                                                   float* __restrict__ pooled) {
-  const int c = blockIdx.x;
+// Masked mean over a chunk's tokens: one workgroup per chunk; thread t sums
+// the feature quad t % (H/4) over the tokens p = t / (H/4) + k G (G token
+// groups, 16-byte loads), then the G partial sums are added in group order.
+constexpr int POOL_THREADS = 1024;
+__global__ __launch_bounds__(POOL_THREADS) void pool_kernel(const float* __restrict__ h, const TTable tt,
+                                                            int window, int stride, int H,
+                                                            float* __restrict__ pooled) {
+  typedef float f4 __attribute__((ext_vector_type(4)));
+  __shared__ f4 part[POOL_THREADS];
+  const int c = blockIdx.x, tid = threadIdx.x;
   int first, len;
   chunk_span(tt, c, window, stride, first, len);
   const float inv = 1.0f / (float)len;
-  for (int f = threadIdx.x; f < H; f += blockDim.x) {
-    float s = 0.0f;
-    for (int p = 0; p < len; ++p) s += h[((size_t)c * window + p) * H + f];
-    pooled[(size_t)c * H + f] = s * inv;
+  const int nq = H / 4, groups = POOL_THREADS / nq;        // H <= 1024: at least 4 groups
+  const int q = tid % nq, grp = tid / nq;
+  f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (grp < groups) {
+    const f4* base = reinterpret_cast<const f4*>(h + (size_t)c * window * H) + q;
+    for (int p = grp; p < len; p += groups) acc += base[(size_t)p * nq];
+  }
+  part[tid] = acc;
+  __syncthreads();
+  if (tid < nq) {
+    f4 t = part[tid];
+    for (int g2 = 1; g2 < groups; ++g2) t += part[g2 * nq + tid];
+    *reinterpret_cast<f4*>(pooled + (size_t)c * H + 4 * tid) = t * inv;
   }
 }
 
@@ -944,7 +959,7 @@ wm_status wm_encode_text(const wm_text_model* m, const int32_t* tokens, const in
       WM_TT(TK_TEXT_GEMM, gemm(dense(f, rows, F, m->w2 + (size_t)l * H * F, H, y, m->b2 + lH, h, 0), 1, false));
       WM_TT(TK_TEXT_OTHER, ln(y, m->ln2_g + lH, m->ln2_b + lH, nullptr));
     }
-    WM_TT(TK_TEXT_OTHER, [&]() { hipLaunchKernelGGL(pool_kernel, dim3(n_chunks), dim3(256), 0, st, h, tt, W,
+    WM_TT(TK_TEXT_OTHER, [&]() { hipLaunchKernelGGL(pool_kernel, dim3(n_chunks), dim3(POOL_THREADS), 0, st, h, tt, W,
                                              d.stride, H, pooled); return hipGetLastError(); }());
   }
   WM_TT(TK_TEXT_OTHER, [&]() { hipLaunchKernelGGL(project_kernel, dim3(S), dim3(256), H * (int)sizeof(float), st,
