@@ -2115,6 +2115,27 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
 #pragma unroll
     for (int bq = 0; bq < NBW; ++bq) dz[bq] = f32x4n{};
     XF gcur = {}, gnext = {};
+    // A chunk's bias-added pre-activations wait in pend while the next
+    // chunk's products run; their GELUs are spread over that chunk's first
+    // eight items (one per item), so the vector work of one chunk overlaps
+    // the matrix work of the next.  The last chunk's GELUs run at once.
+    constexpr int NPC = NK * 2 * GPK;                  // items per chunk
+    static_assert(NPC >= 8, "eight items to spread the GELUs over");
+    float pend[8], gvp[8];
+    auto finish_chunk = [&](int cwf, const float (&gv)[8]) {
+      const int c = w + cwf * W;
+      if constexpr (TRAIN) {
+        if (active) {
+#pragma unroll
+          for (int rb2 = 0; rb2 < 2; ++rb2) {
+            const f32x4n gq = {NP::op(gv[4 * rb2]), NP::op(gv[4 * rb2 + 1]), NP::op(gv[4 * rb2 + 2]),
+                               NP::op(gv[4 * rb2 + 3])};
+            *reinterpret_cast<f32x4n*>(a.G + row * a.H + 32 * c + 16 * rb2 + 4 * g) = gq;
+          }
+        }
+      }
+      NP::store(gbuf, c, lane, NP::gfrag(gv, amask));
+    };
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
@@ -2123,27 +2144,36 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
       if (i < NA) {
         const int cw = i / (NK * 2 * GPK), kf = (i / (2 * GPK)) % NK;
         const int rb = (i / GPK) % 2, hh = i % GPK;
+        const int r_in = i % NPC;
+        // the previous chunk's GELU number r_in
+        if (cw > 0 && r_in < 8) {
+          gvp[r_in] = gelu(pend[r_in]);
+          if (r_in == 7) finish_chunk(cw - 1, gvp);
+        }
         acc[rb] = NP::mma(grp, hh, xf[kf], acc[rb]);
         if (kf == NK - 1 && rb == 1 && hh == GPK - 1) {
-          // bias, GELU, rounding, mask -> the chunk's operand fragment in LDS
-          float gv[8];
+          float av8[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) gv[j] = gelu(acc[j >> 2][j & 3] + b1v[cw][j >> 2][j & 3]);
+          for (int j = 0; j < 8; ++j) av8[j] = acc[j >> 2][j & 3] + b1v[cw][j >> 2][j & 3];
           if constexpr (TRAIN) {
             if (active) {
               const int c = w + cw * W;
 #pragma unroll
-              for (int rb = 0; rb < 2; ++rb) {
-                const f32x4n av = {acc[rb][0] + b1v[cw][rb][0], acc[rb][1] + b1v[cw][rb][1],
-                                   acc[rb][2] + b1v[cw][rb][2], acc[rb][3] + b1v[cw][rb][3]};
-                const f32x4n gq = {NP::op(gv[4 * rb]), NP::op(gv[4 * rb + 1]), NP::op(gv[4 * rb + 2]),
-                                   NP::op(gv[4 * rb + 3])};
-                *reinterpret_cast<f32x4n*>(a.A + row * a.H + 32 * c + 16 * rb + 4 * g) = av;
-                *reinterpret_cast<f32x4n*>(a.G + row * a.H + 32 * c + 16 * rb + 4 * g) = gq;
+              for (int rb2 = 0; rb2 < 2; ++rb2) {
+                const f32x4n av = {av8[4 * rb2], av8[4 * rb2 + 1], av8[4 * rb2 + 2], av8[4 * rb2 + 3]};
+                *reinterpret_cast<f32x4n*>(a.A + row * a.H + 32 * c + 16 * rb2 + 4 * g) = av;
               }
             }
           }
-          NP::store(gbuf, w + cw * W, lane, NP::gfrag(gv, amask));
+          if (cw == NCW - 1) {             // last chunk: GELU, rounding, mask now
+            float gv[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) gv[j] = gelu(av8[j]);
+            finish_chunk(cw, gv);
+          } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) pend[j] = av8[j];
+          }
           acc[0] = f32x4n{};
           acc[1] = f32x4n{};
         }
