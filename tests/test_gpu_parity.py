@@ -186,6 +186,25 @@ def test_multi_segment_multi_hw_ragged_segments(wm):
     check_topk_vs_oracle(g["idx"], ref["scores"], I["seg_off"], k, 2e-2)
 
 
+@pytest.mark.parametrize("prec,n_hw", [("bf16", 1), ("bf16", 2), ("bf16", 3), ("fp32", 2), ("fp32", 3)])
+def test_hardware_vector_counts(wm, prec, n_hw):
+    """Small batches score inside the rollout launch for one or two hardware
+    vectors and with the separate score kernel for more; both against the
+    oracle (ansor_round shapes, 300 candidates in 16-candidate tiles)."""
+    w = synth.scaled(synth.workload("ansor_round"), B=300, n_hw=n_hw)
+    print(f"[hw] ansor_round {prec} n_hw={n_hw}", flush=True)
+    model, W = model_for(wm, "ansor_round", prec)
+    I = synth.make_inputs(w, 3100 + n_hw)
+    k = 16
+    g = run_evaluate(model, w, I, k)
+    ref = O.evaluate(W, I, k, prec)
+    tol = TOL[prec]
+    assert latent_rel(g["zT"], ref["zT"]).max() <= tol
+    assert score_rel(g["scores"], ref["scores"], I["seg_off"]).max() <= tol
+    check_topk_self_consistent(g["idx"], g["val"], g["scores"], I["seg_off"], k)
+    check_topk_vs_oracle(g["idx"], ref["scores"], I["seg_off"], k, tol)
+
+
 @pytest.mark.parametrize("what", ["len_high", "len_negative", "type", "param"])
 def test_device_error_word(wm, what):
     w = synth.scaled(synth.workload("tiny"), B=64)
