@@ -2120,7 +2120,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
     // eight items (one per item), so the vector work of one chunk overlaps
     // the matrix work of the next.  The last chunk's GELUs run at once.
     constexpr int NPC = NK * 2 * GPK;                  // items per chunk
-    static_assert(NPC >= 8, "eight items to spread the GELUs over");
+    constexpr bool DEFER = NPC >= 8;                   // eight items to spread them over
     float pend[8], gvp[8];
     auto finish_chunk = [&](int cwf, const float (&gv)[8]) {
       const int c = w + cwf * W;
@@ -2146,7 +2146,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
         const int rb = (i / GPK) % 2, hh = i % GPK;
         const int r_in = i % NPC;
         // the previous chunk's GELU number r_in
-        if (cw > 0 && r_in < 8) {
+        if (DEFER && cw > 0 && r_in < 8) {
           gvp[r_in] = gelu(pend[r_in]);
           if (r_in == 7) finish_chunk(cw - 1, gvp);
         }
@@ -2165,7 +2165,7 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
               }
             }
           }
-          if (cw == NCW - 1) {             // last chunk: GELU, rounding, mask now
+          if (!DEFER || cw == NCW - 1) {   // last chunk: GELU, rounding, mask now
             float gv[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) gv[j] = gelu(av8[j]);
@@ -4561,22 +4561,24 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
 }
 
 // Narrow tiles (16 candidates) for batches of at most one such tile per
-// compute unit at d = 256, e = 64: bf16 with hidden widths 512 and 1024, fp32
-// with hidden width 512, both transition forms.
+// compute unit: d = 256, e = 64 (8 wavefronts; bf16 with hidden widths 512
+// and 1024, fp32 with 512) and d = 64, e = 32 (2 wavefronts, hidden width
+// 128), both transition forms.
 constexpr int NARROW_MAX_TILES = 256;
-template <class NP, int NC, bool NORM, bool TRAIN = false, bool SCORE = false>
+template <class NP, int NC, bool NORM, bool TRAIN = false, bool SCORE = false, int D = 256, int E = 64,
+          int W = 8>
 hipError_t launch_rollout_narrow(const DevModel& m, RollArgs a, int tiles, hipStream_t st) {
-  using NG = NarrowGeom<NP, 256, 64, NC, 8>;
+  using NG = NarrowGeom<NP, D, E, NC, W>;
   a.w1 = m.trans_n;
-  const int lds = m.roll_tab_bytes + NG::G_BYTES + NG::X_BYTES + (NORM ? 8 * 3 * 16 * 4 : 0) +
-                  (a.phi && !TRAIN ? 16 * (64 + 1) * 4 : 0) + (SCORE ? 8 * NARROW_SCORE_HW * 16 * 4 : 0);
-  auto kern = rollout_narrow_kernel<NP, 256, 64, NC, 8, NORM, TRAIN, SCORE>;
+  const int lds = m.roll_tab_bytes + NG::G_BYTES + NG::X_BYTES + (NORM ? W * 3 * 16 * 4 : 0) +
+                  (a.phi && !TRAIN ? 16 * (E + 1) * 4 : 0) + (SCORE ? W * NARROW_SCORE_HW * 16 * 4 : 0);
+  auto kern = rollout_narrow_kernel<NP, D, E, NC, W, NORM, TRAIN, SCORE>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return e;
   }
-  hipLaunchKernelGGL(kern, dim3(tiles), dim3(512), lds, st, a);
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * W), lds, st, a);
   return hipGetLastError();
 }
 
@@ -4627,6 +4629,14 @@ hipError_t launch_rollout(const DevModel& m, const float* z0, const int2* perm,
     if (prec == WM_BF16 && NC == 16) return norm ? narrow(NarrowBF16{}, I16{}, BT{}) : narrow(NarrowBF16{}, I16{}, BF{});
     if (prec == WM_BF16 && NC == 32) return norm ? narrow(NarrowBF16{}, I32{}, BT{}) : narrow(NarrowBF16{}, I32{}, BF{});
     if (prec == WM_FP32 && NC == 16) return norm ? narrow(NarrowF32{}, I16{}, BT{}) : narrow(NarrowF32{}, I16{}, BF{});
+  }
+  if (d == 64 && e == 32 && m.trans_n && B > 0 && ntiles <= NARROW_MAX_TILES && m.dims.trans_hidden == 128) {
+    *phi_done = phi != nullptr;
+    if (prec == WM_BF16)
+      return norm ? launch_rollout_narrow<NarrowBF16, 4, true, false, false, 64, 32, 2>(m, a, ntiles, st)
+                  : launch_rollout_narrow<NarrowBF16, 4, false, false, false, 64, 32, 2>(m, a, ntiles, st);
+    return norm ? launch_rollout_narrow<NarrowF32, 4, true, false, false, 64, 32, 2>(m, a, ntiles, st)
+                : launch_rollout_narrow<NarrowF32, 4, false, false, false, 64, 32, 2>(m, a, ntiles, st);
   }
 #define WM_ROLL(PR, D, E)                                                                          \
   return norm ? launch_rollout_de<PR, D, E, true>(m, a, tiles, blocks, waves, split, phi_done, st)  \

@@ -40,6 +40,7 @@ def model_for(wm, name, prec, w=None, seed=1000):
 # small enough for the float64 oracle to finish in seconds.
 CASES = [
     ("tiny", "fp32", 300, 1),
+    ("tiny", "fp32", 5000, 1),               # split kernel (over 256 16-candidate tiles)
     ("tiny", "bf16", 300, 1),
     ("ansor_round", "fp32", 300, 1),
     ("ansor_round", "fp32", 5000, 1),        # 32-candidate tiles (over 256 16-candidate tiles)
@@ -356,7 +357,8 @@ def test_large_batch_bucketing(wm, lens_kind):
 # and the persistent kernel where its LDS has room) or from the phi kernel
 # (split kernel, d = 512, fp32 at d = 256): every family against the oracle.
 PHI_CASES = [
-    ("tiny", "fp32", 200, "none"),            # split kernel + phi kernel
+    ("tiny", "fp32", 200, "none"),            # narrow tiles, d = 64
+    ("tiny", "fp32", 5000, "none"),           # split kernel + phi kernel
     ("tiny", "fp32", 8224, "none"),           # persistent, sums in the kernel
     ("ansor_round", "bf16", 300, "none"),     # narrow tiles (16 candidates)
     ("ansor_round", "fp32", 300, "none"),     # narrow tiles, fp32
