@@ -4857,6 +4857,15 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
       if (m.prec == WM_FP32 && NC == 16) return launch_rollout_narrow<NarrowF32, 16, false, true>(m, r, ntiles, st);
     }
   }
+  if (m.dims.d == 64 && m.dims.embed_dim == 32 && m.dims.trans_hidden == 128 && m.trans_n && m.trans_nt &&
+      ntiles <= NARROW_MAX_TILES) {
+    const RollArgs r = train_roll_args(m, io, norm);
+    if (m.prec == WM_BF16)
+      return norm ? launch_rollout_narrow<NarrowBF16, 4, true, true, false, 64, 32, 2>(m, r, ntiles, st)
+                  : launch_rollout_narrow<NarrowBF16, 4, false, true, false, 64, 32, 2>(m, r, ntiles, st);
+    return norm ? launch_rollout_narrow<NarrowF32, 4, true, true, false, 64, 32, 2>(m, r, ntiles, st)
+                : launch_rollout_narrow<NarrowF32, 4, false, true, false, 64, 32, 2>(m, r, ntiles, st);
+  }
   if (m.dims.d == 256 && m.dims.embed_dim == 64) {
     const int NC = m.dims.trans_hidden / 32;
 #define WM_TFWD_ROWS(N)                                                                              \
@@ -4881,21 +4890,21 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
   return hipErrorInvalidValue;
 }
 
-template <class NP, int NC, bool NORM>
+template <class NP, int NC, bool NORM, int D = 256, int E = 64, int W = 8>
 hipError_t launch_train_bwd_narrow(const DevModel& m, TrainArgs a, int tiles, hipStream_t st) {
-  using BG = NarrowBwdGeom<NP, 256, 64, NC, 8>;
+  using BG = NarrowBwdGeom<NP, D, E, NC, W>;
   constexpr int lds = BG::LDS + (NORM ? BG::DOTS_BYTES : 0);
   static_assert(lds <= 160 * 1024, "LDS");
   a.w2t = m.trans_nt;
   // paper form: the transposed normal map follows W1^T in the blob
-  a.wht = NORM ? m.trans_nt + Narrow::t_bytes(256, 64, NC * 32, NP::GPK) : nullptr;
-  auto kern = train_bwd_narrow_kernel<NP, 256, 64, NC, 8, NORM>;
+  a.wht = NORM ? m.trans_nt + Narrow::t_bytes(D, E, NC * 32, NP::GPK) : nullptr;
+  auto kern = train_bwd_narrow_kernel<NP, D, E, NC, W, NORM>;
   hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return e;
   }
-  hipLaunchKernelGGL(kern, dim3(tiles), dim3(512), lds, st, a);
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * W), lds, st, a);
   return hipGetLastError();
 }
 
@@ -4917,6 +4926,14 @@ hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st
       if (m.prec == WM_BF16 && NC == 32) return launch_train_bwd_narrow<NarrowBF16, 32, false>(m, a, ntiles, st);
       if (m.prec == WM_FP32 && NC == 16) return launch_train_bwd_narrow<NarrowF32, 16, false>(m, a, ntiles, st);
     }
+  }
+  if (m.dims.d == 64 && m.dims.embed_dim == 32 && m.dims.trans_hidden == 128 && m.trans_nt &&
+      ntiles <= NARROW_MAX_TILES) {
+    if (m.prec == WM_BF16)
+      return norm ? launch_train_bwd_narrow<NarrowBF16, 4, true, 64, 32, 2>(m, a, ntiles, st)
+                  : launch_train_bwd_narrow<NarrowBF16, 4, false, 64, 32, 2>(m, a, ntiles, st);
+    return norm ? launch_train_bwd_narrow<NarrowF32, 4, true, 64, 32, 2>(m, a, ntiles, st)
+                : launch_train_bwd_narrow<NarrowF32, 4, false, 64, 32, 2>(m, a, ntiles, st);
   }
   if (m.dims.d == 256 && m.dims.embed_dim == 64) {
     const int NC = m.dims.trans_hidden / 32;

@@ -223,12 +223,13 @@ def test_loss_terms(wm, prec, lam, gamma, mode):
 
 @pytest.mark.parametrize("name,prec,B", [("tiny", "bf16", 300), ("ansor_round", "bf16", 250),
                                          ("long_schedule", "bf16", 130), ("ansor_round", "fp32", 130),
-                                         ("ansor_round", "bf16", 5000), ("ansor_round", "fp32", 5000)])
+                                         ("ansor_round", "bf16", 5000), ("ansor_round", "fp32", 5000),
+                                         ("tiny", "fp32", 5000)])
 def test_loss_short_sequences_rowwise(wm, name, prec, B):
     """At most two steps: every gradient row (and, in fp32, element)
-    against the oracle's.  Up to 4096 candidates the forward runs in
-    16-candidate tiles; 5000 candidates take the 32-candidate row-owned
-    tiles.  The per-element rule is for the small batches: an element of
+    against the oracle's.  Up to 4096 candidates the forward and backward
+    run in 16-candidate tiles; 5000 candidates take the 32-candidate
+    row-owned kernels (d = 256) or one wavefront per tile (d = 64).  The per-element rule is for the small batches: an element of
     a weight gradient over 5000 rows is an fp32 sum of 5000 terms of mixed
     sign, whose rounding (about sqrt(rows) ulp of the terms) exceeds 1e-4 of
     the element scale where the terms cancel; rows and the whole tensor
@@ -314,7 +315,7 @@ def test_l2_loss_parity_scaled(wm, name, prec, B, S):
 
 @pytest.mark.parametrize("name,prec,B", [("ansor_round", "bf16", 250), ("ansor_round", "fp32", 130),
                                          ("tiny", "bf16", 200), ("ansor_round", "bf16", 5000),
-                                         ("ansor_round", "fp32", 5000)])
+                                         ("ansor_round", "fp32", 5000), ("tiny", "fp32", 5000)])
 def test_l2_loss_short_sequences_rowwise(wm, name, prec, B):
     """Paper form, at most two steps; 5000 candidates take the 32-candidate
     row-owned kernels (per-element rule for the small batches only, as in
