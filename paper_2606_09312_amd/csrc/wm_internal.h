@@ -345,7 +345,7 @@ struct GradParts {
   int splits, emb_blocks;
 };
 inline int train_splits(long long rows_bound) {
-  const long long s = (rows_bound + 2047) / 2048;
+  const long long s = (rows_bound + 511) / 512;     // small batches: more splits, shorter row loops
   return (int)(s < 1 ? 1 : (s > 32 ? 32 : s));
 }
 // Row blocks of the embedding-gradient kernel (about 256 rows each).

@@ -3856,21 +3856,36 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   }
 }
 
-// out[q] = sum over k of part[k * stride + q] in a fixed order: eight
-// running sums (k mod 8, so the loads are independent), then a fixed tree.
-__global__ __launch_bounds__(256) void sum_splits_kernel(const float* __restrict__ part, int splits,
-                                                         long long stride, long long n,
-                                                         float* __restrict__ out) {
+// All the split sums of one gradient call in one launch: job j adds the
+// splits of `part` (stride apart) for its n outputs in a fixed order (eight
+// running sums, k mod 8, so the loads are independent, then a fixed tree);
+// the threads cover the jobs' outputs back to back.
+constexpr int SUM_JOBS = 8;
+struct SumJobs {
+  const float* part[SUM_JOBS];
+  float* out[SUM_JOBS];
+  long long stride[SUM_JOBS];
+  long long start[SUM_JOBS + 1];    // prefix of the output counts
+  int splits[SUM_JOBS];
+  int count;
+};
+__global__ __launch_bounds__(256) void sum_jobs_kernel(const SumJobs jb) {
   const long long q = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= n) return;
+  if (q >= jb.start[jb.count]) return;
+  int j = 0;
+  while (j + 1 < jb.count && q >= jb.start[j + 1]) ++j;
+  const long long i = q - jb.start[j];
+  const float* part = jb.part[j];
+  const long long stride = jb.stride[j];
+  const int splits = jb.splits[j];
   float s[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
   int k = 0;
   for (; k + 8 <= splits; k += 8) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s[j] += part[(size_t)(k + j) * stride + q];
+    for (int u = 0; u < 8; ++u) s[u] += part[(size_t)(k + u) * stride + i];
   }
-  for (int j = 0; k + j < splits; ++j) s[j] += part[(size_t)(k + j) * stride + q];
-  out[q] = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
+  for (int u = 0; k + u < splits; ++u) s[u] += part[(size_t)(k + u) * stride + i];
+  jb.out[j][i] = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
 }
 
 // Embedding gradients over one block of the compact rows:
@@ -4977,10 +4992,6 @@ hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradP
   const int D = m.dims.d, E = m.dims.embed_dim, H = m.dims.trans_hidden, IN = D + E;
   const int K = m.dims.n_kinds, P = m.dims.n_params, W = K * E + E * P + E;
   const int S = g.splits;
-  auto sums = [&](const float* part, long long stride, long long n, float* out) {
-    hipLaunchKernelGGL(sum_splits_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, S,
-                       stride, n, out);
-  };
   WgradArgs a;
   auto prob = [](const float* A, int M, int lda, const float* Bm, int N, int ldb, float* part,
                  float* colsum) {
@@ -5007,18 +5018,22 @@ hipError_t launch_weight_grads(const DevModel& m, const TrainIO& io, const GradP
   }
   hipLaunchKernelGGL(emb_grad_kernel, dim3(g.emb_blocks), dim3(EMB_THREADS), lds, st, io.DE, E,
                      io.row_src, io.types, io.params, K, P, io.off, io.B, g.emb_blocks, g.emb);
-  sums(g.w1, (long long)H * IN, (long long)H * IN, gw1);
-  sums(g.w2, (long long)D * H, (long long)D * H, gw2);
-  if (gwh) sums(g.wh, (long long)D * E, (long long)D * E, gwh);
-  sums(g.b1, H, H, gb1);
-  sums(g.b2, D, D, gb2);
-  auto sums_emb = [&](const float* part, long long n, float* out) {
-    hipLaunchKernelGGL(sum_splits_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part,
-                       g.emb_blocks, (long long)W, n, out);
+  SumJobs jb{};
+  auto job = [&](const float* part, int splits, long long stride, long long n, float* out) {
+    const int j = jb.count++;
+    jb.part[j] = part; jb.out[j] = out; jb.stride[j] = stride; jb.splits[j] = splits;
+    jb.start[j + 1] = jb.start[j] + n;
   };
-  sums_emb(g.emb, (long long)K * E, gtemb);
-  sums_emb(g.emb + (size_t)K * E, (long long)E * P, gpw);
-  sums_emb(g.emb + (size_t)K * E + (size_t)E * P, E, gpb);
+  job(g.w1, S, (long long)H * IN, (long long)H * IN, gw1);
+  job(g.w2, S, (long long)D * H, (long long)D * H, gw2);
+  if (gwh) job(g.wh, S, (long long)D * E, (long long)D * E, gwh);
+  job(g.b1, S, H, H, gb1);
+  job(g.b2, S, D, D, gb2);
+  job(g.emb, g.emb_blocks, (long long)W, (long long)K * E, gtemb);
+  job(g.emb + (size_t)K * E, g.emb_blocks, (long long)W, (long long)E * P, gpw);
+  job(g.emb + (size_t)K * E + (size_t)E * P, g.emb_blocks, (long long)W, E, gpb);
+  const long long total = jb.start[jb.count];
+  hipLaunchKernelGGL(sum_jobs_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, jb);
   return hipGetLastError();
 }
 
