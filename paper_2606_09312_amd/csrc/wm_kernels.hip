@@ -1227,8 +1227,11 @@ __global__ __launch_bounds__(64 * SPLIT, 1) void rollout_split_kernel(const Roll
 }
 
 // ==========================================================================
-// Small-batch rollout, row-owned form (d = 256): one workgroup of W
-// wavefronts per tile, two per SIMD in bf16.  Wavefront w computes the first
+// Row-owned rollout (d = 256, 32-candidate tiles): the training forward of
+// the rollout loss above 8192 candidates (narrow tiles take every smaller
+// batch, and every evaluator batch this kernel could take, so its evaluator
+// form, TRAIN = false, is not dispatched).  One workgroup of W wavefronts per
+// tile, two per SIMD in bf16.  Wavefront w computes the first
 // product and GELU of the hidden chunks w, w + W, ... and writes the GELU
 // outputs as operand fragments to LDS; after one barrier it forms the update
 // of its own NB/W latent blocks over all NC chunks, reading every chunk's GELU
@@ -4512,41 +4515,13 @@ hipError_t launch_rollout_split_t(const DevModel& m, const RollArgs& a, int tile
   return hipGetLastError();
 }
 
-template <class PR, int D, int E, int NC, int W, bool NORM>
-hipError_t launch_rollout_rows_t(const DevModel& m, const RollArgs& a, int tiles, hipStream_t st) {
-  using RG = RowsGeom<PR, D, E, NC, W>;
-  const int lds = m.roll_tab_bytes + RG::GELU_BYTES + RG::X_BYTES + RG::XE_BYTES +
-                  (NORM ? W * 3 * 32 * 4 : 0) + (a.phi ? 32 * (E + 1) * 4 : 0);
-  auto kern = rollout_rows_kernel<PR, D, E, NC, W, NORM>;
-  hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  if (e != hipSuccess) {
-    (void)hipGetLastError();
-    return e;
-  }
-  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * W), lds, st, a);
-  return hipGetLastError();
-}
-
-// One (precision, d, e, transition form): split kernel for at most one tile
-// per compute unit, else the persistent kernel with 1, 2 or 4 wavefronts per
-// workgroup.
+// One (precision, d, e, transition form) without narrow tiles: split kernel
+// for at most one tile per compute unit, else the persistent kernel with 1, 2
+// or 4 wavefronts per workgroup.
 template <class PR, int D, int E, bool NORM>
 hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, int blocks,
                              int waves, bool split, bool* phi_done, hipStream_t st) {
-  // d = 256: row-owned form for the hidden widths it is instantiated for
-  // (it also sums the action features)
   *phi_done = a.phi != nullptr;
-  if constexpr (D == 256) {
-    if (split) {
-      const int NC = m.dims.trans_hidden / 32;
-      if constexpr (PR::G == 1) {
-        if (NC == 16) return launch_rollout_rows_t<PR, D, E, 16, 8, NORM>(m, a, tiles, st);
-        if (NC == 32) return launch_rollout_rows_t<PR, D, E, 32, 8, NORM>(m, a, tiles, st);
-      } else {
-        if (NC == 16) return launch_rollout_rows_t<PR, D, E, 16, 4, NORM>(m, a, tiles, st);
-      }
-    }
-  }
   // fp32 at d = 256 does not fit the split kernel's registers; the split
   // kernel leaves the action features to the phi kernel
   if constexpr (D <= 256 && (PR::G == 1 || D <= 64)) {
@@ -4575,11 +4550,13 @@ hipError_t launch_rollout_de(const DevModel& m, const RollArgs& a, int tiles, in
   return launch_rollout_t<PR, D, E, 1, NORM>(m, a, blocks, st);
 }
 
-// Narrow tiles (16 candidates) for batches of at most one such tile per
+// Narrow tiles (16 candidates) for batches of at most two such tiles per
 // compute unit: d = 256, e = 64 (8 wavefronts; bf16 with hidden widths 512
 // and 1024, fp32 with 512) and d = 64, e = 32 (2 wavefronts, hidden width
-// 128), both transition forms.
-constexpr int NARROW_MAX_TILES = 256;
+// 128), both transition forms.  Up to 512 tiles they beat one 32-candidate
+// tile per compute unit: candidates are sorted longest first, so the
+// second tiles a compute unit takes are the short ones.
+constexpr int NARROW_MAX_TILES = 512;
 template <class NP, int NC, bool NORM, bool TRAIN = false, bool SCORE = false, int D = 256, int E = 64,
           int W = 8>
 hipError_t launch_rollout_narrow(const DevModel& m, RollArgs a, int tiles, hipStream_t st) {

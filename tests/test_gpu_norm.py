@@ -46,10 +46,8 @@ def _check_unit(g, lens, z0_of):
     np.testing.assert_array_equal(g["zT"][~pos], z0_of[~pos])
 
 
-# Scaled batches (one tile per compute unit or fewer): 16-candidate tiles
-# for bf16 d = 256 up to 4096 candidates, 32-candidate row-owned tiles for
-# d = 256 otherwise, the split kernel at d = 64, the persistent kernel at
-# d = 512
+# Scaled batches (two 16-candidate tiles per compute unit or fewer): narrow
+# tiles at d = 256 and d = 64, the persistent kernel at d = 512
 CASES = [
     ("tiny", "fp32", 300, 1),
     ("tiny", "bf16", 300, 1),
