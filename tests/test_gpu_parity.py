@@ -193,13 +193,14 @@ def test_multi_segment_multi_hw_ragged_segments(wm):
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
 def test_split_kernel_other_hidden_width(wm, prec, norm):
     """A hidden width without narrow-tile kernels (d = 64, H = 256): the
-    split kernel and the phi kernel, both transition forms, against the
-    oracle."""
-    if prec == "bf16":
-        pytest.skip("bf16 at d = 64, H = 256 (residual form): one of 300 scores measured 2.9e-2 "
-                    "from the oracle's, every latent within 2e-2, and not among the 6 scores the "
-                    "oracle itself moves by over 1e-2 under 1e-6 relative noise on z0; cause not "
-                    "yet shown, so both forms stay off until it is")
+    split kernel, the phi kernel and the score kernel, both transition
+    forms, against the oracle.  fp32 end to end.  bf16 stage by stage: the
+    latents against the oracle's, then the scores against the oracle's cost
+    model applied to the kernel's own latents.  With these weights the bf16
+    score is ill-conditioned in the latent (one candidate whose latent is
+    within 1e-3 of the oracle's, 20 of its 64 features rounding to another
+    bf16 value, scores 2.9e-2 away), so the composed score is not held to
+    the bound that each stage meets."""
     base = dataclasses.replace(synth.workload("tiny"), H=256)
     w = synth.scaled(base, B=300)
     print(f"[split] tiny H=256 {prec} {norm}", flush=True)
@@ -213,8 +214,20 @@ def test_split_kernel_other_hidden_width(wm, prec, norm):
     ref = O.evaluate(W, I, k, prec, norm=norm)
     tol = TOL[prec]
     assert latent_rel(g["zT"], ref["zT"]).max() <= tol
-    assert score_rel(g["scores"], ref["scores"], I["seg_off"]).max() <= tol
     check_topk_self_consistent(g["idx"], g["val"], g["scores"], I["seg_off"], k)
+    if prec == "bf16":
+        Wd = O.prepare(W, prec)
+        _, phi = O.rollout(Wd, I["z0"], I["seg_off"], I["types"], I["params"], I["lens"], prec,
+                           norm=norm)
+        own = O.score(Wd, g["zT"], phi, I["hw"], prec)
+        srel = score_rel(g["scores"], own, I["seg_off"])
+        print(f"  score vs oracle cost model on the kernel's latents {srel.max():.2e}, "
+              f"end to end {score_rel(g['scores'], ref['scores'], I['seg_off']).max():.2e}",
+              flush=True)
+        assert srel.max() <= tol
+        check_topk_vs_oracle(g["idx"], own, I["seg_off"], k, tol)
+        return
+    assert score_rel(g["scores"], ref["scores"], I["seg_off"]).max() <= tol
     check_topk_vs_oracle(g["idx"], ref["scores"], I["seg_off"], k, tol)
 
 
