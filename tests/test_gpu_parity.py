@@ -85,8 +85,24 @@ FULL = [("tiny", "fp32"), ("ansor_round", "fp32"), ("ansor_round", "bf16"),
 def test_parity_full_size_sampled(wm, name, prec):
     w = synth.workload(name)
     print(f"[full] {name} {prec} B={w.B}", flush=True)
+    check_sampled(wm, name, prec, w, 2000)
+
+
+# The batch sizes where the rollout changes kernels: 8192 candidates are 512
+# narrow tiles (two per compute unit), 8193 the first batch past them.
+@pytest.mark.parametrize("B", [8192, 8193])
+@pytest.mark.parametrize("name,prec", [("ansor_round", "bf16"), ("ansor_round", "fp32"), ("tiny", "fp32")])
+def test_parity_narrow_limit_sampled(wm, name, prec, B):
+    w = synth.scaled(synth.workload(name), B=B, S=1)
+    print(f"[limit] {name} {prec} B={B}", flush=True)
+    check_sampled(wm, name, prec, w, 2100 + B)
+
+
+def check_sampled(wm, name, prec, w, seed):
+    """wm_evaluate on the whole batch; the oracle recomputes the longest and
+    shortest sequences and random ones, one by one."""
     model, W = model_for(wm, name, prec)
-    I = synth.make_inputs(w, 2000)
+    I = synth.make_inputs(w, seed)
     g = run_evaluate(model, w, I, w.k)
     assert g["status"] == 0
     check_topk_self_consistent(g["idx"], g["val"], g["scores"], I["seg_off"], w.k)
