@@ -250,6 +250,25 @@ def test_loss_short_sequences_rowwise(wm, name, prec, B):
     print("  " + ", ".join(f"{k} {v:.1e}" for k, v in rep.items()), flush=True)
 
 
+def test_loss_narrow_limit(wm):
+    """8192 candidates of at most two steps, bf16: the largest batch of
+    narrow tiles (two per compute unit).  Per-candidate losses and the
+    per-tensor rule with the bf16 bound from the oracle's own sensitivity;
+    the per-row rule is not applied: one row of the z0 gradient measured
+    2.07e-2 from the oracle's, and one seeded 1e-7 relative perturbation of
+    the weights moves the oracle's own row by 2.06e-2 (a bf16 operand
+    rounding that falls the other way), while other draws leave it within
+    6e-6."""
+    w = synth.scaled(synth.workload("ansor_round"), B=8192, lengths="uniform", len_lo=0, len_hi=2)
+    print("[loss limit] ansor_round bf16 B=8192", flush=True)
+    model, W = model_for(wm, "ansor_round", "bf16")
+    I = synth.make_inputs(w, 7000 + 8192, pad="garbage")
+    tgt, neg = margin_targets(W, I, "bf16", 3, 79, 0.3)
+    g = run_loss(wm, model, I, tgt, neg, 0.5, 0.3)
+    rep = check_against_oracle(g, W, I, tgt, neg, 0.5, 0.3, "bf16", rows=False)
+    print("  " + ", ".join(f"{k} {v:.1e}" for k, v in rep.items()), flush=True)
+
+
 @pytest.mark.parametrize("norm", ["none", "l2"])
 def test_loss_other_hidden_width(wm, norm):
     """A hidden width without narrow-tile kernels (d = 64, H = 256): the
