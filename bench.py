@@ -6,7 +6,7 @@ candidates evaluated per second, the roofline of the dominant kernel (the
 persistent rollout) from HIP events recorded on its launch stream, and the
 CPU oracle's throughput on a bounded sample of the same workload.
 
-  python bench.py [--workload ansor_round] [--precision bf16] [--steps K] [--warmup W]
+  python bench.py [--workload large_latent] [--precision bf16] [--steps K] [--warmup W]
   python bench.py --loss [...]     (rollout loss + gradients instead)
   python bench.py --encoder [...]  (chunked transformer state encoder instead)
 """
@@ -90,20 +90,35 @@ def rollout_bytes(w, lens, norm: str = "none") -> int:
     return steps * 4 * (1 + w.n_params) + 4 * w.B + 4 * w.S * w.d + wbytes + 4 * w.B * w.d
 
 
-def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none", forest=None):
-    """Oracle throughput on a bounded random sample of the batch (candidates
-    are independent, so throughput scales with the sample)."""
-    from oracle import wm_oracle as O
+def host_info() -> dict:
+    """The host the oracle runs on: usable cores, CPU model, BLAS library."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        libs = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        if libs:
+            p = libs[0]
+            blas = f"{p.get('internal_api')} {p.get('version')} ({os.path.basename(p.get('filepath', ''))})"
     except Exception:
-        threads = len(os.sched_getaffinity(0))
-    rng = np.random.default_rng(0)
+        pass
+    return {"cores": len(os.sched_getaffinity(0)), "cpu_model": model, "blas": blas}
+
+
+def _oracle_rate(w, Wd, z0, I, prec, budget_s, norm, forest, rng):
+    """Oracle candidates/s on random sub-batches of doubling size until the
+    budget is spent; returns (rate, candidates, seconds)."""
+    from oracle import wm_oracle as O
     n = min(w.B, 64)
     total_c, total_t = 0, 0.0
-    Wd = O.prepare(W, prec)
-    z0 = O.encode(Wd, I["feats"], prec) if "feats" in I else I["z0"].astype(np.float64)
     seg_of = O.segment_of(I["seg_off"], w.B)
     while True:
         pick = rng.choice(w.B, n, replace=False)
@@ -125,12 +140,34 @@ def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none", forest=None
         if total_t >= budget_s:
             break
         n = min(2 * n, w.B)
-    return {"value": total_c / total_t, "unit": "candidates/s", "cores": int(threads),
+    return total_c / total_t, total_c, total_t
+
+
+def cpu_baseline(w, W, I, prec, budget_s: float, norm: str = "none", forest=None):
+    """Oracle throughput on bounded random samples of the batch (candidates
+    are independent, so throughput scales with the sample), once with BLAS
+    on every usable core and once on a single thread."""
+    from oracle import wm_oracle as O
+    from threadpoolctl import threadpool_limits
+    info = host_info()
+    Wd = O.prepare(W, prec)
+    z0 = O.encode(Wd, I["feats"], prec) if "feats" in I else I["z0"].astype(np.float64)
+    with threadpool_limits(limits=info["cores"], user_api="blas"):
+        rate, nc, secs = _oracle_rate(w, Wd, z0, I, prec, budget_s, norm, forest,
+                                      np.random.default_rng(0))
+    with threadpool_limits(limits=1, user_api="blas"):
+        rate1, nc1, secs1 = _oracle_rate(w, Wd, z0, I, prec, budget_s, norm, forest,
+                                         np.random.default_rng(1))
+    what = f"rollout+{'score' if forest is None else 'trees'}+top-k"
+    return {"value": rate, "unit": "candidates/s", "cores": info["cores"],
             "kind": "oracle",
-            "sample": f"{total_c} candidates in sub-batches of doubling size drawn at random (without "
-                      f"repeats within a sub-batch) from the {w.B}-candidate batch "
-                      f"(float64 NumPy oracle, rollout+{'score' if forest is None else 'trees'}"
-                      f"+top-k, {total_t:.1f} s)"}
+            "sample": f"{nc} candidates in sub-batches of doubling size (64, 128, ...) drawn at random "
+                      f"(without repeats within a sub-batch) from the {w.B}-candidate batch "
+                      f"(float64 NumPy oracle, {what}, BLAS on {info['cores']} threads, {secs:.1f} s)",
+            "single_thread": {"value": rate1, "unit": "candidates/s", "cores": 1,
+                              "sample": f"{nc1} candidates drawn the same way, BLAS on 1 thread "
+                                        f"({secs1:.1f} s)"},
+            "cpu_model": info["cpu_model"], "blas": info["blas"]}
 
 
 def measure_peaks(torch) -> dict:
@@ -397,7 +434,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="ansor_round", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--workload", default="large_latent", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--precision", default=None, choices=["fp32", "bf16"])
     ap.add_argument("--norm", default="none", choices=["none", "l2"],
                     help="transition form: residual MLP (none) or the paper's projected, "
@@ -412,7 +449,8 @@ def main():
     ap.add_argument("--encoder", action="store_true",
                     help="time the chunked transformer state encoder instead of the evaluator")
     ap.add_argument("--text-workload", default="codebert", choices=sorted(synth.TEXT_WORKLOADS))
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of oracle work per CPU run (all cores, then one thread)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the achievable-peak measurements (library matrix products, copy)")
@@ -505,6 +543,7 @@ def main():
     roll_s = kern["rollout"]["avg_ms"] / 1e3
     achieved = flops_roll / roll_s / 1e12
     peak = PEAK_TFLOPS[prec]
+    ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
     ms_per_step = elapsed / args.steps * 1e3
     value = w.B * args.steps / elapsed
     total_flops = flops_roll + (w.B * score_flops(w) if forest is None and not fused else 0)
@@ -530,12 +569,18 @@ def main():
                              f"{w.n_trees} trees of depth {w.tree_depth} on structured action "
                              f"features",
                    "global_batch": w.B, "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "kernel": "rollout + score" if fused else "rollout",
+        # the binding roof follows from the launch's arithmetic intensity
+        # against the ridge point of the published peaks
+        "roofline": {"bound": "mfma" if flops_roll / bytes_roll > ridge else "hbm",
+                     "kernel": "rollout + score" if fused else "rollout",
                      "achieved": achieved, "peak": peak,
                      "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": measured_traffic(w.name, prec, args.norm),
                      "flop_per_launch": flops_roll,
-                     "algorithmic_bytes_per_launch": bytes_roll},
+                     "algorithmic_bytes_per_launch": bytes_roll,
+                     "flop_per_byte": flops_roll / bytes_roll, "ridge_flop_per_byte": ridge,
+                     "hbm_achieved_gbs": bytes_roll / roll_s / 1e9,
+                     "hbm_frac": bytes_roll / roll_s / 1e9 / PEAK_HBM_GBS},
         "kernels_avg_ms": {k: v["avg_ms"] for k, v in kern.items()},
         "step_ms": step_ms,
         "whole_path_tflops": total_flops * args.steps / elapsed / 1e12,

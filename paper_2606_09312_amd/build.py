@@ -7,6 +7,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SOURCES = ["csrc/wm_api.hip", "csrc/wm_kernels.hip", "csrc/wm_text.hip"]
+HOST_SOURCES = ["csrc/wm_pack.cpp"]      # plain C++ (the tests also build it alone)
 LIB = os.path.join(HERE, "libwm.so")
 
 FLAGS = [
@@ -31,14 +32,18 @@ def build(verbose: bool = False) -> str:
 
     def compile_one(src):
         obj = os.path.join(objdir, os.path.basename(src) + ".o")
-        res = subprocess.run([hipcc, *cflags, "-c", os.path.join(HERE, src), "-o", obj],
-                             capture_output=True, text=True)
+        if src in HOST_SOURCES:
+            cmd = ["g++", "-std=c++17", "-O2", "-fPIC", "-c", os.path.join(HERE, src), "-o", obj]
+        else:
+            cmd = [hipcc, *cflags, "-c", os.path.join(HERE, src), "-o", obj]
+        res = subprocess.run(cmd, capture_output=True, text=True)
         return obj, res
 
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        results = list(ex.map(compile_one, SOURCES))
+    srcs = SOURCES + HOST_SOURCES
+    with ThreadPoolExecutor(max_workers=len(srcs)) as ex:
+        results = list(ex.map(compile_one, srcs))
     objs = []
-    for (obj, res), src in zip(results, SOURCES):
+    for (obj, res), src in zip(results, srcs):
         err = "\n".join(l for l in res.stderr.splitlines() if noise not in l)
         if res.returncode != 0:
             raise RuntimeError(f"hipcc failed on {src} ({res.returncode}):\n{err}")

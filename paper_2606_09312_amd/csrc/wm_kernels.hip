@@ -16,185 +16,9 @@
 
 #include <type_traits>
 
-#include "wm_internal.h"
+#include "wm_device.h"
 
 namespace wm {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-// Global-memory (address space 1) views.  A pointer that passes through an
-// asm statement keeps its address space only if its type says so; a generic
-// pointer would turn the loads into flat loads, which also count against the
-// LDS counter, so every LDS wait would drain them.
-typedef __attribute__((address_space(1))) const uint8_t gu8;
-typedef __attribute__((address_space(1))) const u32x4 gu32x4;
-
-// --------------------------------------------------------------------------
-// Precision traits: operand fragment type, conversion, matrix-core product.
-
-struct PBF16 : GeomBF16 {
-  using Frag = bf16x8;
-  static __device__ __forceinline__ f32x16 mfma(Frag a, Frag b, f32x16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-  }
-  // 8 floats -> 8 bf16 (round to nearest even)
-  static __device__ __forceinline__ Frag cvt(const float* v) {
-    Frag f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) f[j] = (__bf16)v[j];
-    return f;
-  }
-  // fragment `w` (0 <= w < G) of a 16-byte lane group
-  static __device__ __forceinline__ Frag pick(u32x4 g, int) { return __builtin_bit_cast(Frag, g); }
-  // all elements kept (mask = ~0) or zeroed (mask = 0)
-  static __device__ __forceinline__ Frag mask(Frag f, uint32_t m) {
-    u32x4 u = __builtin_bit_cast(u32x4, f);
-    u &= m;
-    return __builtin_bit_cast(Frag, u);
-  }
-  // two GELU outputs -> one packed register (bf16 pair), masked
-  using Packed = uint32_t;
-  static __device__ __forceinline__ Packed pack2(float a, float b, uint32_t m) {
-    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    const bf16x2 v = {(__bf16)a, (__bf16)b};
-    return __builtin_bit_cast(uint32_t, v) & m;
-  }
-  // operand fragment f (8 values = 4 packed pairs) of the second product
-  static __device__ __forceinline__ Frag gfrag(const Packed (&gp)[8], int f) {
-    const u32x4 u = {gp[4 * f], gp[4 * f + 1], gp[4 * f + 2], gp[4 * f + 3]};
-    return __builtin_bit_cast(Frag, u);
-  }
-};
-
-struct PF32 : GeomF32 {
-  using Frag = float;
-  static __device__ __forceinline__ f32x16 mfma(Frag a, Frag b, f32x16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-  }
-  static __device__ __forceinline__ Frag cvt(const float* v) { return v[0]; }
-  // Copy the element out first: a bit_cast applied directly to a vector
-  // element expression lowers to element 0 whatever the index.
-  static __device__ __forceinline__ Frag pick(u32x4 g, int w) {
-    const uint32_t u = g[w];
-    return __uint_as_float(u);
-  }
-  static __device__ __forceinline__ Frag mask(Frag f, uint32_t m) {
-    return __uint_as_float(__float_as_uint(f) & m);
-  }
-  // fp32 keeps both values of a pair unpacked
-  struct Packed { float a, b; };
-  static __device__ __forceinline__ Packed pack2(float a, float b, uint32_t m) {
-    return {__uint_as_float(__float_as_uint(a) & m), __uint_as_float(__float_as_uint(b) & m)};
-  }
-  // operand fragment f (one value) of the second product
-  static __device__ __forceinline__ Frag gfrag(const Packed (&gp)[8], int f) {
-    return (f & 1) ? gp[f >> 1].b : gp[f >> 1].a;
-  }
-};
-
-// GELU(x) = x * Phi(x) = (x + |x| * erf(|x| / sqrt 2)) / 2, with erf from
-// Abramowitz & Stegun, Handbook of Mathematical Functions, formula 7.1.26:
-//   erf(a) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-a^2),
-//   t = 1 / (1 + p a), a >= 0, |error| <= 1.5e-7.
-// The 1/sqrt 2 scaling is folded into the constants: one reciprocal, one
-// exp2, ten multiply-adds, no branches; -> 0 and -> x in the tails, 0 at 0.
-__device__ __forceinline__ float gelu(float x) {
-  const float ax = fabsf(x);
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.70710678118654752f, ax, 1.0f));
-  float p = fmaf(1.061405429f, t, -1.453152027f);
-  p = fmaf(p, t, 1.421413741f);
-  p = fmaf(p, t, -0.284496736f);
-  p = fmaf(p, t, 0.254829592f);
-  const float ex = __builtin_amdgcn_exp2f((x * x) * (-0.5f * 1.4426950408889634f));
-  const float erf_a = fmaf(-(p * t), ex, 1.0f);
-  return 0.5f * fmaf(ax, erf_a, x);
-}
-
-template <class PR>
-__device__ __forceinline__ float op_value(float v) {   // the value a product operand takes
-  if constexpr (PR::G == 1) return (float)(__bf16)v;
-  else return v;
-}
-
-// 16 accumulator values of one 32-row block <-> a row in natural order
-// (rows acc_row(h, 4q .. 4q+3) are consecutive: four 16-byte accesses).
-__device__ __forceinline__ void store_acc(float* row, const f32x16& v, int h) {
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const f32x4 x = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-    *reinterpret_cast<f32x4*>(row + acc_row(h, 4 * q)) = x;
-  }
-}
-__device__ __forceinline__ f32x16 load_acc(const float* row, int h) {
-  f32x16 v;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const f32x4 x = *reinterpret_cast<const f32x4*>(row + acc_row(h, 4 * q));
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[4 * q + i] = x[i];
-  }
-  return v;
-}
-
-__device__ __forceinline__ u32x4 lds_group(const uint8_t* base, int group, int lane) {
-  return *reinterpret_cast<const u32x4*>(base + group * 1024 + lane * 16);
-}
-
-// Copy `bytes` (multiple of 16) from global memory into LDS with the
-// direct global->LDS path: every lane moves 16 bytes, a wavefront fills 1 KiB
-// at LDS address base + lane*16.  Completion is tracked by vmcnt.
-__device__ __forceinline__ void stage_to_lds(const uint8_t* __restrict__ src, uint8_t* dst,
-                                             int bytes, int tid, int nthreads) {
-  const int units = bytes >> 4;
-  const int wave_base = tid & ~63;
-  for (int u0 = 0; u0 < units; u0 += nthreads) {
-    const int u = u0 + tid;
-    if (u < units) {
-      __builtin_amdgcn_global_load_lds(
-          (const void*)(src + (size_t)u * 16),
-          (__attribute__((address_space(3))) void*)(dst + (size_t)(u0 + wave_base) * 16), 16, 0, 0);
-    }
-  }
-}
-
-// Same copy with a compile-time size: straight-line code, one guarded tail.
-template <int BYTES, int NT>
-__device__ __forceinline__ void stage_fixed(const uint8_t* __restrict__ src, uint8_t* dst, int tid) {
-  static_assert(BYTES % 16 == 0, "16-byte units");
-  constexpr int UNITS = BYTES / 16, FULL = UNITS / NT;
-  const int wave_base = tid & ~63;
-#pragma unroll
-  for (int i = 0; i < FULL; ++i) {
-    __builtin_amdgcn_global_load_lds(
-        (const void*)(src + (size_t)(i * NT + tid) * 16),
-        (__attribute__((address_space(3))) void*)(dst + (size_t)(i * NT + wave_base) * 16), 16, 0, 0);
-  }
-  if constexpr (UNITS % NT != 0) {
-    if (FULL * NT + tid < UNITS)
-      __builtin_amdgcn_global_load_lds(
-          (const void*)(src + (size_t)(FULL * NT + tid) * 16),
-          (__attribute__((address_space(3))) void*)(dst + (size_t)(FULL * NT + wave_base) * 16), 16, 0, 0);
-  }
-}
-
-__device__ __forceinline__ void wait_vm_then_barrier() {
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's global->LDS copies landed
-  __syncthreads();
-}
-
-__device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
-
-// Subgraph of candidate i: the largest s with off[s] <= i.
-__device__ __forceinline__ int segment_of(const SegTable& seg, int i) {
-  int lo = 0, hi = seg.n - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (seg.off[mid] <= i) lo = mid; else hi = mid - 1;
-  }
-  return lo;
-}
 
 // ==========================================================================
 // Bucketing: one workgroup sorts all candidates by length, longest first.
@@ -341,49 +165,49 @@ __global__ __launch_bounds__(1024) void bucket_scatter_kernel(const int32_t* __r
 // length keeps z unchanged: its GELU outputs and b2 are zeroed, so the second
 // product adds exact zeros.
 
-struct RollArgs {
-  const uint8_t* w1;        // packed transition chunks, W1 part
-  const uint8_t* w2;        // packed transition chunks, W2 part
-  const uint8_t* wh;        // packed hyperplane-normal map (paper-form transition)
-  const float* tab;         // rollout table (see DevModel::roll_tab)
-  const float* z0;          // [S][D]
-  const int2* perm;         // sorted (candidate, subgraph)
-  const int32_t* types;     // [B][T_max]
-  const int32_t* params;    // [B][T_max][P]
-  const int32_t* lens;      // [B]
-  float* zT;                // [B][D]
-  float* phi;               // [B][E] mean step embedding, or null (the phi kernel computes it)
-  int32_t* err;
-  int B, T_max, P, K, H, tab_bytes;
-  // training forward of the rollout loss (row-owned kernel only): the
-  // activations of every valid step in compact rows off[i] + t
-  float *X, *A, *G, *Pz;    // [R][D+E], [R][H], [R][H], [R][D]
-  float *V, *SC;            // paper form: [R][D] Wh e, [R][4] v.z, v.v, |u|, 0
-  const int32_t* off;
-  int32_t* row_src;
-  // scores fused into the narrow rollout: cost blob, hw [n_hw][HW], scores [n_hw][B]
-  const uint8_t* costn;
-  const float* hw;
-  float* scores;
-  float bc2;
-  int n_hw, HW, C;
-};
 
 // Copies of the next weight chunk (its W1 and/or W2 part) into LDS, issued
 // a few at a time between the matrix-fragment groups of an iteration so the
 // L2 -> LDS traffic runs continuously underneath the computation.
-typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
 struct CopyPlan {
-  const uint8_t* s1;
+  uint32_t o1;        // byte offset of the W1 part in the W1 chunk array
   lds_u8* d1;
   bool e1;            // copy the W1 part
-  const uint8_t* s2;
+  uint32_t o2;        // byte offset of the W2 part in the W2 chunk array
   lds_u8* d2;
-  bool e2;            // copy the W2 part
+  bool e2;
 };
 
-__device__ __forceinline__ lds_u8* to_lds(uint8_t* p) { return (lds_u8*)p; }
+// Copy sources as raw buffer resources over the packed chunk arrays: a copy
+// is a buffer load straight to LDS with the chunk's byte offset in a scalar
+// register and one lane offset (tid * 16) shared by all copies, so no 64-bit
+// address is kept per copy.  The hardware bounds-checks every copy against
+// the array size.
+struct CopySrc {
+  __amdgpu_buffer_rsrc_t r1, r2;
+  uint32_t voff;      // tid * 16
+  int wave_base;      // first thread of the wavefront (uniform)
+};
+typedef __attribute__((address_space(3))) void lds_void;
+
+// `BYTES` (multiple of 16) from byte offset `off` of a buffer into LDS.
+template <int BYTES, int NT>
+__device__ __forceinline__ void stage_buf(__amdgpu_buffer_rsrc_t r, uint32_t off, uint8_t* dst,
+                                          const CopySrc& cs, int tid) {
+  static_assert(BYTES % 16 == 0, "16-byte units");
+  constexpr int UNITS = BYTES / 16, FULL = UNITS / NT;
+#pragma unroll
+  for (int i = 0; i < FULL; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(dst + (size_t)(i * NT + cs.wave_base) * 16), 16,
+                                             cs.voff, off + i * NT * 16, 0, 0);
+  if constexpr (UNITS % NT != 0) {
+    if (FULL * NT + tid < UNITS)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(dst + (size_t)(FULL * NT + cs.wave_base) * 16), 16,
+                                               cs.voff, off + FULL * NT * 16, 0, 0);
+  }
+}
+
 
 // Per-wavefront pieces of one transition step.  Chunk c covers hidden units
 // [32c, 32c+32): the first product forms G^T[chunk] = b1 + W1[chunk] . X^T in
@@ -417,20 +241,17 @@ struct Roll {
   template <int NT>
   static constexpr int U2 = (W2B / 16 + NT - 1) / NT;
   template <int NT>
-  static __device__ __forceinline__ void copy_unit(const CopyPlan& cp, int u, int tid) {
-    const int wave_base = tid & ~63;
+  static __device__ __forceinline__ void copy_unit(const CopyPlan& cp, const CopySrc& cs, int u, int tid) {
     if (u < U1<NT>) {
       const int k = u * NT;
       if (cp.e1 && k + tid < W1B / 16)
-        __builtin_amdgcn_global_load_lds(
-            (const void*)(cp.s1 + (size_t)(k + tid) * 16),
-            (__attribute__((address_space(3))) void*)(cp.d1 + (k + wave_base) * 16), 16, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(cs.r1, (lds_void*)(cp.d1 + (k + cs.wave_base) * 16), 16,
+                                                 cs.voff, cp.o1 + k * 16, 0, 0);
     } else {
       const int k = (u - U1<NT>) * NT;
       if (cp.e2 && k + tid < W2B / 16)
-        __builtin_amdgcn_global_load_lds(
-            (const void*)(cp.s2 + (size_t)(k + tid) * 16),
-            (__attribute__((address_space(3))) void*)(cp.d2 + (k + wave_base) * 16), 16, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(cs.r2, (lds_void*)(cp.d2 + (k + cs.wave_base) * 16), 16,
+                                                 cs.voff, cp.o2 + k * 16, 0, 0);
     }
   }
 
@@ -439,7 +260,8 @@ struct Roll {
                                                    const Frag (&xz)[NZ], const Frag (&xe)[NE],
                                                    const f32x16& acc1, uint32_t mask,
                                                    f32x16& acc1n, f32x16 (&zacc)[NB],
-                                                   int lane, int h, const CopyPlan& cp, int tid) {
+                                                   int lane, int h, const CopyPlan& cp,
+                                                   const CopySrc& cs, int tid) {
     constexpr int N1 = DO_G1 ? NK1 / G : 0;
     constexpr int N2 = DO_G2 ? NK2 / G : 0;
     constexpr int NI = N1 + N2;
@@ -473,7 +295,7 @@ struct Roll {
       if constexpr (NU > 0) {
 #pragma unroll
         for (int u = 0; u < NU; ++u)
-          if ((u * NI) / NU == i) copy_unit<NT>(cp, u, tid);
+          if ((u * NI) / NU == i) copy_unit<NT>(cp, cs, u, tid);
       }
       if (i < N1) {
 #pragma unroll
@@ -698,9 +520,14 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
   // Tables and the first chunks.
   stage_to_lds(reinterpret_cast<const uint8_t*>(a.tab), reinterpret_cast<uint8_t*>(tab),
                a.tab_bytes, tid, NT);
-  stage_fixed<W1B, NT>(a.w1, w1a, tid);
-  stage_fixed<W2B, NT>(a.w2, w2a, tid);
-  if constexpr (PIPE) stage_fixed<W1B, NT>(a.w1 + W1B, w1b, tid);
+  CopySrc cs;
+  cs.r1 = __builtin_amdgcn_make_buffer_rsrc((void*)a.w1, (short)0, NC * W1B, 0x00020000);
+  cs.r2 = __builtin_amdgcn_make_buffer_rsrc((void*)a.w2, (short)0, NC * W2B, 0x00020000);
+  cs.voff = (uint32_t)tid * 16u;
+  cs.wave_base = __builtin_amdgcn_readfirstlane(tid & ~63);
+  stage_buf<W1B, NT>(cs.r1, 0u, w1a, cs, tid);
+  stage_buf<W2B, NT>(cs.r2, 0u, w2a, cs, tid);
+  if constexpr (PIPE) stage_buf<W1B, NT>(cs.r1, (uint32_t)W1B, w1b, cs, tid);
   if constexpr (WH_LDS) stage_fixed<HY::BYTES, NT>(a.wh, whs, tid);
   if (do_phi)
     for (int i = tid; i < WAVES * 32 * (E + 1); i += NT) phib[i] = 0.0f;
@@ -804,13 +631,13 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
     }
 
     const int g0 = t * NC;
-    const CopyPlan none = {nullptr, nullptr, false, nullptr, nullptr, false};
+    const CopyPlan none = {0u, nullptr, false, 0u, nullptr, false};
     if constexpr (PIPE) {
       // first product of chunk 0 (its W1 part is in w1a); accumulators accA
       // and accB alternate between "GELU input" and "next first product"
       f32x16 accA, accB;
       R::template iteration<true, false, NT, false>(w1a, w2a, xz, xe, accB, amask, accA, zacc,
-                                                    lane, h, none, tid);
+                                                    lane, h, none, cs, tid);
       __syncthreads();                 // all wavefronts are done with w1a
       for (int c = 0; c < NC; c += 2) {
         const int g = g0 + c;
@@ -818,21 +645,21 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
         // part of chunk c+1 is copied into w2b and the W1 part of chunk c+2
         // into w1a (issued together up front: spreading them measured slower
         // for this schedule)
-        if (g + 1 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 1) % NC) * W2B, w2b, tid);
-        if (g + 2 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 2) % NC) * W1B, w1a, tid);
+        if (g + 1 < total) stage_buf<W2B, NT>(cs.r2, (uint32_t)(((c + 1) % NC) * W2B), w2b, cs, tid);
+        if (g + 2 < total) stage_buf<W1B, NT>(cs.r1, (uint32_t)(((c + 2) % NC) * W1B), w1a, cs, tid);
         __builtin_amdgcn_sched_barrier(0);
         R::template iteration<true, true, NT, false>(w1b, w2a, xz, xe, accA, amask, accB, zacc,
-                                                     lane, h, none, tid);
+                                                     lane, h, none, cs, tid);
         wait_vm_then_barrier();
         // -- chunk c+1: W2 part in w2b, next W1 part (chunk c+2) in w1a.  At
         // c + 2 == NC this first product is discarded (w1a then holds the
         // next step's chunk 0 or stale data; the step prologue recomputes it
         // with the new X): one branch-free body keeps register use down.
-        if (g + 2 < total) stage_fixed<W2B, NT>(a.w2 + (size_t)((c + 2) % NC) * W2B, w2a, tid);
-        if (g + 3 < total) stage_fixed<W1B, NT>(a.w1 + (size_t)((c + 3) % NC) * W1B, w1b, tid);
+        if (g + 2 < total) stage_buf<W2B, NT>(cs.r2, (uint32_t)(((c + 2) % NC) * W2B), w2a, cs, tid);
+        if (g + 3 < total) stage_buf<W1B, NT>(cs.r1, (uint32_t)(((c + 3) % NC) * W1B), w1b, cs, tid);
         __builtin_amdgcn_sched_barrier(0);
         R::template iteration<true, true, NT, false>(w1a, w2b, xz, xe, accB, amask, accA, zacc,
-                                                     lane, h, none, tid);
+                                                     lane, h, none, cs, tid);
         wait_vm_then_barrier();
       }
     } else {
@@ -842,19 +669,19 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
       f32x16 acc;
       for (int c = 0; c < NC; c += 2) {
         const int g = g0 + c;
-        const CopyPlan cp0 = {a.w1 + (size_t)((c + 1) % NC) * W1B, to_lds(w1b), g + 1 < total,
-                              a.w2 + (size_t)((c + 1) % NC) * W2B, to_lds(w2b), g + 1 < total};
+        const CopyPlan cp0 = {(uint32_t)(((c + 1) % NC) * W1B), to_lds(w1b), g + 1 < total,
+                              (uint32_t)(((c + 1) % NC) * W2B), to_lds(w2b), g + 1 < total};
         R::template iteration<true, false, NT, true>(w1a, w2a, xz, xe, acc, amask, acc, zacc,
-                                                     lane, h, cp0, tid);
+                                                     lane, h, cp0, cs, tid);
         R::template iteration<false, true, NT, false>(w1a, w2a, xz, xe, acc, amask, acc, zacc,
-                                                      lane, h, none, tid);
+                                                      lane, h, none, cs, tid);
         wait_vm_then_barrier();
-        const CopyPlan cp1 = {a.w1 + (size_t)((c + 2) % NC) * W1B, to_lds(w1a), g + 2 < total,
-                              a.w2 + (size_t)((c + 2) % NC) * W2B, to_lds(w2a), g + 2 < total};
+        const CopyPlan cp1 = {(uint32_t)(((c + 2) % NC) * W1B), to_lds(w1a), g + 2 < total,
+                              (uint32_t)(((c + 2) % NC) * W2B), to_lds(w2a), g + 2 < total};
         R::template iteration<true, false, NT, true>(w1b, w2b, xz, xe, acc, amask, acc, zacc,
-                                                     lane, h, cp1, tid);
+                                                     lane, h, cp1, cs, tid);
         R::template iteration<false, true, NT, false>(w1b, w2b, xz, xe, acc, amask, acc, zacc,
-                                                      lane, h, none, tid);
+                                                      lane, h, none, cs, tid);
         wait_vm_then_barrier();
       }
     }
@@ -4669,7 +4496,7 @@ hipError_t launch_score_trees(const DevForest& f, const float* zT, int32_t d, co
     (void)hipGetLastError();
     return e;
   }
-  hipLaunchKernelGGL(score_trees_kernel, dim3((B + TREE_CPB - 1) / TREE_CPB, n_hw), dim3(TREE_THREADS), lds, st, f.nodes,
+  hipLaunchKernelGGL(score_trees_kernel, dim3((B + TREE_CPB - 1) / TREE_CPB, n_hw), dim3(TREE_THREADS), lds, st, static_cast<const int2*>(f.nodes),
                      f.leaves, f.n_trees, f.depth, f.base, zT, d, phi_s, phi_dim, hw, hw_dim, B,
                      scores);
   return hipGetLastError();

@@ -113,3 +113,58 @@ def sub_batch(I, pick, seg_of, z0_full):
         "types": I["types"][pick], "params": I["params"][pick], "lens": I["lens"][pick],
         "hw": I["hw"], "z0": z0_full[seg_of[pick]], "seg_off": np.arange(n + 1, dtype=np.int32),
     }
+
+
+# --------------------------------------------------------------------------
+# Whole-batch oracle: the candidates are independent (the oracle's
+# batch-splitting pin), so the float64 oracle runs on sub-batches in worker
+# processes with one BLAS thread each and the results are put back in order.
+
+_W = {}
+
+
+def _worker_init(W, prec, norm):
+    from threadpoolctl import threadpool_limits
+    from oracle import wm_oracle as O
+    _W["Wd"] = O.prepare(W, prec)
+    _W["prec"], _W["norm"] = prec, norm
+    _W["limit"] = threadpool_limits(limits=1, user_api="blas")
+
+
+def _oracle_part(z0s, types, params, lens, hw):
+    from oracle import wm_oracle as O
+    n = lens.shape[0]
+    zT, phi = O.rollout(_W["Wd"], z0s, np.arange(n + 1), types, params, lens, _W["prec"],
+                        norm=_W["norm"])
+    return zT, O.score(_W["Wd"], zT, phi, hw, _W["prec"])
+
+
+def oracle_full(W, I, prec, k, norm="none", workers=None, parts_per_worker=4):
+    """O.evaluate over the whole batch, computed in parallel sub-batches:
+    returns z_T [B][d], scores [n_hw][B], idx and val of the top-k."""
+    import multiprocessing as mp
+    import os
+    from concurrent.futures import ProcessPoolExecutor
+    from oracle import wm_oracle as O
+    B = I["lens"].shape[0]
+    Wd = O.prepare(W, prec)
+    z0 = O.encode(Wd, I["feats"], prec) if "feats" in I else I["z0"].astype(np.float64)
+    seg_of = O.segment_of(I["seg_off"], B)
+    workers = workers or min(16, len(os.sched_getaffinity(0)))
+    n_parts = max(1, min(B, workers * parts_per_worker))
+    # balance by total steps: deal the candidates out in length order
+    order = np.argsort(-I["lens"].astype(np.int64), kind="stable")
+    parts = [np.sort(order[p::n_parts]) for p in range(n_parts)]
+    zT = np.empty((B, W["w2"].shape[0]))
+    y = np.empty((I["hw"].shape[0], B))
+    ctx = mp.get_context("spawn")
+    with ProcessPoolExecutor(max_workers=workers, mp_context=ctx, initializer=_worker_init,
+                             initargs=(W, prec, norm)) as ex:
+        futs = [ex.submit(_oracle_part, z0[seg_of[p]], I["types"][p], I["params"][p], I["lens"][p],
+                          I["hw"]) for p in parts]
+        for p, f in zip(parts, futs):
+            zp, yp = f.result()
+            zT[p] = zp
+            y[:, p] = yp
+    idx, val = O.topk(y, I["seg_off"], k)
+    return {"zT": zT, "scores": y, "idx": idx, "val": val}
