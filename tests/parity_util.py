@@ -144,6 +144,7 @@ def oracle_full(W, I, prec, k, norm="none", workers=None, parts_per_worker=4):
     returns z_T [B][d], scores [n_hw][B], idx and val of the top-k."""
     import multiprocessing as mp
     import os
+    import time
     from concurrent.futures import ProcessPoolExecutor
     from oracle import wm_oracle as O
     B = I["lens"].shape[0]
@@ -162,9 +163,44 @@ def oracle_full(W, I, prec, k, norm="none", workers=None, parts_per_worker=4):
                              initargs=(W, prec, norm)) as ex:
         futs = [ex.submit(_oracle_part, z0[seg_of[p]], I["types"][p], I["params"][p], I["lens"][p],
                           I["hw"]) for p in parts]
-        for p, f in zip(parts, futs):
+        t0 = last = time.time()
+        for n, (p, f) in enumerate(zip(parts, futs)):
             zp, yp = f.result()
             zT[p] = zp
             y[:, p] = yp
+            if time.time() - last > 20:      # a long oracle run reports progress
+                last = time.time()
+                print(f"    oracle: {n + 1}/{len(parts)} parts, {last - t0:.0f} s", flush=True)
     idx, val = O.topk(y, I["seg_off"], k)
     return {"zT": zT, "scores": y, "idx": idx, "val": val}
+
+
+def oracle_sensitivity(W, I, prec, k, norm, ref, seeds=(77,), full=False):
+    """How far the oracle's own z_T and scores move when its inputs move by a
+    seeded 1e-6 relative perturbation (initial latents, or program features
+    when the initial latents are encoded), maximised over `seeds`.  With
+    rounding to bf16 at every step's operands, rollouts are sensitive at this
+    level, and an implementation that accumulates in another order sees
+    perturbations at least this large.  Computed from the oracle alone.
+    Returns (latent, score) in the comparison norms of latent_rel and
+    score_rel."""
+    from oracle import wm_oracle as O
+    key = "feats" if "feats" in I else "z0"
+    sz = ss = 0.0
+    for seed in seeds:
+        rng = np.random.default_rng(seed)
+        J = dict(I)
+        J[key] = (I[key].astype(np.float64) * (1 + 1e-6 * rng.standard_normal(I[key].shape))).astype(np.float32)
+        pert = oracle_full(W, J, prec, k, norm=norm) if full else O.evaluate(W, J, k, prec, norm=norm)
+        sz = max(sz, float(latent_rel(pert["zT"], ref["zT"]).max()))
+        ss = max(ss, float(score_rel(pert["scores"], ref["scores"], I["seg_off"]).max()))
+    return sz, ss
+
+
+def bounds(prec, sens):
+    """The stated tolerance (1e-4 fp32, 2e-2 bf16), widened in bf16 to twice
+    the oracle's own sensitivity where that is larger."""
+    tol = TOL[prec]
+    if prec != "bf16":
+        return tol, tol
+    return max(tol, 2 * sens[0]), max(tol, 2 * sens[1])

@@ -13,8 +13,8 @@ import pytest
 
 import synth
 
-from parity_util import (TOL, check_topk_self_consistent, check_topk_vs_oracle, latent_rel,
-                         oracle_full, run_evaluate, score_rel)
+from parity_util import (bounds, check_topk_self_consistent, check_topk_vs_oracle, latent_rel,
+                         oracle_full, oracle_sensitivity, run_evaluate, score_rel)
 
 # Tolerances: 1e-4 relative in fp32 and 2e-2 in bf16 (latents norm-wise per
 # candidate, scores against max(|o|, rms of the segment's oracle scores)).
@@ -39,22 +39,6 @@ def wm():
     return wm
 
 
-def oracle_sensitivity(W, I, prec, k, norm, ref):
-    """How far the oracle's own outputs move when its inputs move by a
-    seeded 1e-6 relative perturbation (initial latents, or program features
-    when the initial latents are encoded): the rounding points of bf16 make
-    long rollouts sensitive, and an implementation that accumulates in a
-    different order sees perturbations of at least this size.  Computed from
-    the oracle alone."""
-    rng = np.random.default_rng(77)
-    key = "feats" if "feats" in I else "z0"
-    J = dict(I)
-    J[key] = (I[key].astype(np.float64) * (1 + 1e-6 * rng.standard_normal(I[key].shape))).astype(np.float32)
-    pert = oracle_full(W, J, prec, k, norm=norm)
-    return (latent_rel(pert["zT"], ref["zT"]).max(),
-            score_rel(pert["scores"], ref["scores"], I["seg_off"]).max())
-
-
 def compare(wm, w, prec, norm, seed, k):
     W = synth.make_weights(w, 1000)
     model = wm.Model(wm.model_dims(w), W, precision=prec, norm=norm)
@@ -62,11 +46,10 @@ def compare(wm, w, prec, norm, seed, k):
     g = run_evaluate(model, w, I, k)
     assert g["status"] == 0
     ref = oracle_full(W, I, prec, k, norm=norm)
-    tol = TOL[prec]
     # the bound: the stated tolerance, widened to twice the oracle's own
     # sensitivity where that is larger (bf16 long rollouts only)
-    sz, ss = oracle_sensitivity(W, I, prec, k, norm, ref) if prec == "bf16" else (0.0, 0.0)
-    tol_z, tol_s = max(tol, 2 * sz), max(tol, 2 * ss)
+    sz, ss = oracle_sensitivity(W, I, prec, k, norm, ref, full=True) if prec == "bf16" else (0.0, 0.0)
+    tol_z, tol_s = bounds(prec, (sz, ss))
     rel = latent_rel(g["zT"], ref["zT"])
     srel = score_rel(g["scores"], ref["scores"], I["seg_off"])
     print(f"  z_T max rel {rel.max():.2e} (mean {rel.mean():.1e}, bound {tol_z:.2e}; oracle sensitivity "

@@ -9,8 +9,8 @@ import pytest
 import synth
 from oracle import wm_oracle as O
 
-from parity_util import (TOL, check_topk_self_consistent, check_topk_vs_oracle, latent_rel,
-                         run_evaluate, score_rel, sub_batch, to_dev)
+from parity_util import (TOL, bounds, check_topk_self_consistent, check_topk_vs_oracle, latent_rel,
+                         oracle_sensitivity, run_evaluate, score_rel, sub_batch, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -119,10 +119,10 @@ def check_sampled(wm, name, prec, w, seed):
     tol = TOL[prec]
     rel = latent_rel(g["zT"][pick], zT)
     assert rel.max() <= tol, f"z_T rel err {rel.max():.3e}"
-    # scale for scores: rms of the GPU scores of each sampled candidate's segment
-    seg_rms = np.array([[np.sqrt(np.mean(g["scores"][j, I["seg_off"][s]:I["seg_off"][s + 1]] ** 2))
-                         for s in seg_of[pick]] for j in range(w.n_hw)])
-    srel = np.abs(g["scores"][:, pick] - y) / np.maximum(np.abs(y), seg_rms)
+    # scale for scores: rms of the oracle's scores of the sampled candidates
+    # (per hardware vector); the whole-batch comparison is in test_gpu_full
+    rms = np.sqrt(np.mean(y ** 2, axis=1, keepdims=True))
+    srel = np.abs(g["scores"][:, pick] - y) / np.maximum(np.abs(y), rms)
     assert srel.max() <= tol, f"score rel err {srel.max():.3e}"
     print(f"  sampled {len(pick)}: z_T max rel {rel.max():.2e}, score max rel {srel.max():.2e}",
           flush=True)
@@ -210,13 +210,12 @@ def test_multi_segment_multi_hw_ragged_segments(wm):
 def test_split_kernel_other_hidden_width(wm, prec, norm):
     """A hidden width without narrow-tile kernels (d = 64, H = 256): the
     split kernel, the phi kernel and the score kernel, both transition
-    forms, against the oracle.  fp32 end to end.  bf16 stage by stage: the
-    latents against the oracle's, then the scores against the oracle's cost
-    model applied to the kernel's own latents.  With these weights the bf16
-    score is ill-conditioned in the latent (one candidate whose latent is
-    within 1e-3 of the oracle's, 20 of its 64 features rounding to another
-    bf16 value, scores 2.9e-2 away), so the composed score is not held to
-    the bound that each stage meets."""
+    forms, end to end against the oracle.  With these weights the bf16
+    scores of the residual form are ill-conditioned in the latent (a 1e-6
+    relative perturbation of the initial latents moves the oracle's own
+    scores by up to 5e-2 relative), so in bf16 the bounds are twice the
+    oracle's own sensitivity (maximised over four seeded perturbations)
+    where that exceeds the stated tolerance."""
     base = dataclasses.replace(synth.workload("tiny"), H=256)
     w = synth.scaled(base, B=300)
     print(f"[split] tiny H=256 {prec} {norm}", flush=True)
@@ -228,23 +227,17 @@ def test_split_kernel_other_hidden_width(wm, prec, norm):
     g = run_evaluate(model, w, I, k)
     assert g["status"] == 0
     ref = O.evaluate(W, I, k, prec, norm=norm)
-    tol = TOL[prec]
-    assert latent_rel(g["zT"], ref["zT"]).max() <= tol
+    sens = oracle_sensitivity(W, I, prec, k, norm, ref, seeds=(77, 78, 79, 80)) if prec == "bf16" \
+        else (0.0, 0.0)
+    tol_z, tol_s = bounds(prec, sens)
+    rel = latent_rel(g["zT"], ref["zT"]).max()
+    srel = score_rel(g["scores"], ref["scores"], I["seg_off"]).max()
+    print(f"  z_T {rel:.2e} (bound {tol_z:.2e}), score {srel:.2e} (bound {tol_s:.2e}; oracle "
+          f"sensitivity {sens[1]:.2e})", flush=True)
+    assert rel <= tol_z
+    assert srel <= tol_s
     check_topk_self_consistent(g["idx"], g["val"], g["scores"], I["seg_off"], k)
-    if prec == "bf16":
-        Wd = O.prepare(W, prec)
-        _, phi = O.rollout(Wd, I["z0"], I["seg_off"], I["types"], I["params"], I["lens"], prec,
-                           norm=norm)
-        own = O.score(Wd, g["zT"], phi, I["hw"], prec)
-        srel = score_rel(g["scores"], own, I["seg_off"])
-        print(f"  score vs oracle cost model on the kernel's latents {srel.max():.2e}, "
-              f"end to end {score_rel(g['scores'], ref['scores'], I['seg_off']).max():.2e}",
-              flush=True)
-        assert srel.max() <= tol
-        check_topk_vs_oracle(g["idx"], own, I["seg_off"], k, tol)
-        return
-    assert score_rel(g["scores"], ref["scores"], I["seg_off"]).max() <= tol
-    check_topk_vs_oracle(g["idx"], ref["scores"], I["seg_off"], k, tol)
+    check_topk_vs_oracle(g["idx"], ref["scores"], I["seg_off"], k, tol_s)
 
 
 @pytest.mark.parametrize("prec,n_hw", [("bf16", 1), ("bf16", 2), ("bf16", 3), ("fp32", 2), ("fp32", 3)])
