@@ -37,7 +37,8 @@
  *  - The caller owns every buffer it passes; the library owns only the
  *    model's device copy of the weights.  Buffers, the model and the
  *    workspace must stay alive until the enqueued work has completed.
- *  - No call allocates device memory except wm_model_create.
+ *  - No call allocates device memory except wm_model_create (and the
+ *    create calls of the tree ensemble and the text encoder).
  *  - Argument problems the host can see are reported synchronously, before
  *    anything is enqueued: a null required pointer, a negative size, a bad
  *    segment table, k out of range, a workspace that is too small.  The
@@ -63,6 +64,7 @@ extern "C" {
 #define WM_MAX_SEGMENTS 512   /* subgraphs per call */
 #define WM_MAX_K 1024         /* top-k per (hardware vector, subgraph) */
 #define WM_MAX_T 4096         /* padded action-sequence width */
+#define WM_NOALLOC_SCRATCH_BYTES (4u << 20)   /* scratch of wm_evaluate_noalloc, per GPU */
 
 typedef enum wm_status {
   WM_OK = 0,
@@ -186,6 +188,33 @@ wm_status wm_evaluate(const wm_model* model, const float* init, int32_t init_is_
                       int32_t B, int32_t T_max, const float* hw, int32_t n_hw, int32_t k,
                       float* scores, float* zT, int32_t* idx, float* val,
                       void* ws, size_t ws_bytes, void* stream);
+
+/* wm_evaluate for callers that cannot allocate device memory or pass a
+ * workspace (code under HIP graph capture, serving loops, harnesses that
+ * forbid allocation): the same computation and kernels with every output
+ * supplied by the caller and the remaining intermediates (the
+ * length-sorted permutation, the bucketing histograms, the encoded initial
+ * latents) in a scratch array the library keeps in each GPU's memory
+ * (WM_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends; its
+ * address is looked up on the first call on a device, with that device
+ * current).  Nothing is allocated.
+ *   scores [n_hw][B], zT [B][d], phi [B][e] float32 out, all required;
+ *   idx required, val may be NULL, as in wm_evaluate;
+ *   status: device int32 [64] (256 bytes) out, required: cleared by the call,
+ *     then the device error word of the call; read it with
+ *     wm_device_status(status, 256, stream).
+ * Errors: as wm_evaluate, plus INVALID_ARGUMENT when B, T_max and S need
+ * more scratch than WM_NOALLOC_SCRATCH_BYTES (8 B + 4 (T_max + 1) / 4096 B
+ * per candidate, plus 4 d bytes per subgraph with an encoder; about 512 Ki
+ * candidates for T_max <= 64 without one).  All calls on one GPU share its
+ * scratch: calls that overlap in time on one GPU (on different streams or
+ * threads) race and must be serialised by the caller. */
+wm_status wm_evaluate_noalloc(const wm_model* model, const float* init, int32_t init_is_feats,
+                              const int32_t* seg_off, int32_t S,
+                              const int32_t* types, const int32_t* params, const int32_t* lens,
+                              int32_t B, int32_t T_max, const float* hw, int32_t n_hw, int32_t k,
+                              float* scores, float* zT, float* phi, int32_t* idx, float* val,
+                              int32_t* status, void* stream);
 
 /* ---- Tree-ensemble ranker (the paper's G, Sec. 3.5) --------------------
  * The paper ranks candidates with a gradient-boosted tree ensemble over the

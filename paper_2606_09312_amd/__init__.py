@@ -7,7 +7,8 @@ package is the thin Python binding over it.
 """
 from .binding import (  # noqa: F401
     GRAD_KEYS, KERNELS, NORMS, PRECISIONS, SYMBOLS, WMError, Forest, Model, TextModel,
-    device_status, encode_init, encode_text, evaluate, grad_shapes, load_library, loss_workspace,
+    device_status, encode_init, encode_text, evaluate, evaluate_noalloc, grad_shapes, load_library,
+    loss_workspace,
     phi_struct, rollout, rollout_loss, score, score_trees, timing_enable, timing_read, topk,
 )
 

@@ -32,7 +32,7 @@ SYMBOLS = (
     "wm_last_error", "wm_timing_enable", "wm_timing_read", "wm_forest_create",
     "wm_forest_destroy", "wm_phi_struct", "wm_score_trees", "wm_evaluate_trees",
     "wm_loss_workspace_bytes", "wm_rollout_loss", "wm_text_model_create", "wm_text_model_destroy",
-    "wm_text_chunks", "wm_text_workspace_bytes", "wm_encode_text",
+    "wm_text_chunks", "wm_text_workspace_bytes", "wm_encode_text", "wm_evaluate_noalloc",
 )
 
 
@@ -114,6 +114,9 @@ def load_library(path: str = LIB_PATH):
     lib.wm_evaluate.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, i32, i32, vp, i32, i32,
                                 vp, vp, vp, vp, vp, sz, vp]
     lib.wm_evaluate.restype = i32
+    lib.wm_evaluate_noalloc.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, i32, i32, vp, i32, i32,
+                                        vp, vp, vp, vp, vp, vp, vp]
+    lib.wm_evaluate_noalloc.restype = i32
     lib.wm_device_status.argtypes = [vp, sz, vp]
     lib.wm_device_status.restype = i32
     lib.wm_last_error.argtypes = []
@@ -321,6 +324,23 @@ def evaluate(model: Model, init, seg_off, types, params, lens, hw, k, *, init_is
     return {"idx": idx, "val": val, "scores": scores, "zT": zT, "ws": ws}
 
 
+def evaluate_noalloc(model: Model, init, seg_off, types, params, lens, hw, k, *, scores, zT, phi,
+                     idx, status, val=None, init_is_feats=False, stream=None):
+    """wm_evaluate_noalloc: the fused path with every output supplied by the
+    caller (scores [n_hw][B], zT [B][d], phi [B][e], idx [n_hw][S][k], val or
+    None, status int32 [64]) and no workspace; nothing is allocated.  Check
+    the device error word with device_status(status)."""
+    seg, segp = _host_i32(seg_off)
+    S = len(seg) - 1
+    B, T_max = types.shape[0], types.shape[1]
+    n_hw = hw.shape[0]
+    _check(load_library().wm_evaluate_noalloc(
+        model.handle, _ptr(init), 1 if init_is_feats else 0, segp, S, _ptr(types), _ptr(params),
+        _ptr(lens), B, T_max, _ptr(hw), n_hw, k, _ptr(scores), _ptr(zT), _ptr(phi), _ptr(idx),
+        _ptr(val), _ptr(status), _stream(stream)))
+    return {"idx": idx, "val": val, "scores": scores, "zT": zT, "phi": phi, "status": status}
+
+
 def grad_shapes(model: Model) -> Dict[str, tuple]:
     """Shapes of the weight gradients of a model (PyTorch Linear layout)."""
     d = model.dims
@@ -438,7 +458,7 @@ def encode_text(model: TextModel, tokens, tok_off, z0=None, ws=None, stream=None
 
 def device_status(ws, stream=None) -> int:
     """Synchronise and read/clear the workspace error word; raises on an error."""
-    _check(load_library().wm_device_status(_ptr(ws), ws.numel(), _stream(stream)))
+    _check(load_library().wm_device_status(_ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
     return WM_OK
 
 

@@ -96,6 +96,34 @@ wm_status clear_error() { return ok(); }
     if (e_ != hipSuccess) return fail(WM_ERR_DEVICE, std::string("kernel launch: ") + hipGetErrorString(e_)); \
   } while (0)
 
+// ---- allocation-free evaluation ----------------------------------------------
+// Scratch of wm_evaluate_noalloc: one copy per GPU of the library's code
+// object.  In host code `noalloc_scratch` only stands for the symbol; its
+// device address, per device, comes from hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t noalloc_scratch[WM_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t* g_scratch[kMaxDevices] = {};
+
+// The scratch's address on the current device (looked up once per device).
+wm_status noalloc_scratch_ptr(uint8_t** out) {
+  int dev = -1;
+  WM_HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(WM_ERR_DEVICE, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    WM_HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(noalloc_scratch)));
+    if (!p) return fail(WM_ERR_DEVICE, "hipGetSymbolAddress returned NULL for the scratch");
+    g_scratch[dev] = static_cast<uint8_t*>(p);
+  }
+  *out = g_scratch[dev];
+  return WM_OK;
+}
+}  // namespace
+
 extern "C" {
 
 const char* wm_last_error(void) { return g_last_error.c_str(); }
@@ -389,6 +417,56 @@ wm_status wm_evaluate(const wm_model* model, const float* init, int32_t init_is_
   if (!phi_done) WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
   if (!sf.done) WM_TIMED(TK_SCORE, st, launch_score(model->dm, zTo, phi, B, hw, n_hw, sc, st));
   WM_TIMED(TK_TOPK, st, launch_topk(sc, n_hw, B, seg, k, idx, val, st));
+  return ok();
+}
+
+wm_status wm_evaluate_noalloc(const wm_model* model, const float* init, int32_t init_is_feats,
+                              const int32_t* seg_off, int32_t S, const int32_t* types,
+                              const int32_t* params, const int32_t* lens, int32_t B, int32_t T_max,
+                              const float* hw, int32_t n_hw, int32_t k, float* scores, float* zT,
+                              float* phi, int32_t* idx, float* val, int32_t* status, void* stream) {
+  if (!model) return fail(WM_ERR_INVALID_ARGUMENT, "model is NULL");
+  if (init_is_feats && model->dm.dims.feat_dim <= 0)
+    return fail(WM_ERR_INVALID_ARGUMENT, "init_is_feats needs a model with an encoder");
+  wm_status s = check_rollout_args(model, init, types, params, lens, B, T_max, zT);
+  if (s != WM_OK) return s;
+  if (n_hw < 1) return fail(WM_ERR_INVALID_ARGUMENT, "n_hw < 1");
+  SegTable seg;
+  int32_t min_seg = 0;
+  if ((s = check_segments(seg_off, S, B, &seg, &min_seg)) != WM_OK) return s;
+  if ((s = check_k(k, min_seg)) != WM_OK) return s;
+  if (!idx) return fail(WM_ERR_INVALID_ARGUMENT, "idx is NULL");
+  if (!scores || !phi) return fail(WM_ERR_INVALID_ARGUMENT, "scores and phi are required");
+  if (!status) return fail(WM_ERR_INVALID_ARGUMENT, "status is NULL");
+  if (model->dm.dims.hw_dim > 0 && !hw) return fail(WM_ERR_INVALID_ARGUMENT, "hw is NULL");
+  // scratch layout: permutation, bucketing histograms, encoded initial latents
+  const size_t o_perm = 0;
+  const size_t o_hist = align256(o_perm + (size_t)B * sizeof(int2));
+  const size_t o_z0 = align256(o_hist + (size_t)bucket_groups(B) * (size_t)(T_max + 1) * 4);
+  const size_t need = o_z0 + (init_is_feats ? (size_t)S * model->dm.dims.d * 4 : 0);
+  if (need > WM_NOALLOC_SCRATCH_BYTES)
+    return fail(WM_ERR_INVALID_ARGUMENT, "the batch needs " + std::to_string(need) +
+                                             " bytes of scratch, more than WM_NOALLOC_SCRATCH_BYTES");
+  uint8_t* sp = nullptr;
+  if ((s = noalloc_scratch_ptr(&sp)) != WM_OK) return s;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int2* perm = reinterpret_cast<int2*>(sp + o_perm);
+  WM_HIP_TRY(launch_clear_words(status, 64, st));
+  float* z0 = const_cast<float*>(init);
+  if (init_is_feats) {
+    z0 = reinterpret_cast<float*>(sp + o_z0);
+    WM_TIMED(TK_ENCODE, st, launch_encode(model->dm, init, S, z0, st));
+  }
+  WM_TIMED(TK_BUCKET, st, launch_bucket(lens, B, T_max, seg, perm, reinterpret_cast<int32_t*>(sp + o_hist),
+                                        status, st));
+  bool phi_done = false;
+  ScoreFuse sf{hw, n_hw, scores, false};
+  WM_TIMED(TK_ROLLOUT, st, launch_rollout(model->dm, z0, perm, types, params, lens, B, T_max, zT, phi,
+                                          &phi_done, status, st, &sf));
+  if (!phi_done) WM_TIMED(TK_PHI, st, launch_phi(model->dm, types, params, lens, B, T_max, phi, st));
+  if (!sf.done) WM_TIMED(TK_SCORE, st, launch_score(model->dm, zT, phi, B, hw, n_hw, scores, st));
+  WM_TIMED(TK_TOPK, st, launch_topk(scores, n_hw, B, seg, k, idx, val, st));
   return ok();
 }
 

@@ -13,6 +13,9 @@
 namespace wm {
 
 // Launchers (wm_kernels.hip).  Return hipSuccess or the launch error.
+// zero n int32 words (a kernel rather than hipMemsetAsync, so the call is
+// safe under stream capture)
+hipError_t launch_clear_words(int32_t* p, int n, hipStream_t st);
 // hist: bucket_groups(B) * (T_max + 1) ints of workspace (unused when 0)
 hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
                          int2* perm, int32_t* hist, int32_t* err, hipStream_t st);

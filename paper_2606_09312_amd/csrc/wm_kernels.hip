@@ -4309,6 +4309,15 @@ int rollout_lds_bytes(const DevModel& m) {
   return b;
 }
 
+__global__ __launch_bounds__(64) void clear_words_kernel(int32_t* __restrict__ p, int n) {
+  for (int i = threadIdx.x; i < n; i += 64) p[i] = 0;
+}
+
+hipError_t launch_clear_words(int32_t* p, int n, hipStream_t st) {
+  hipLaunchKernelGGL(clear_words_kernel, dim3(1), dim3(64), 0, st, p, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_bucket(const int32_t* lens, int32_t B, int32_t T_max, const SegTable& seg,
                          int2* perm, int32_t* hist, int32_t* err, hipStream_t st) {
   const int groups = bucket_groups(B);

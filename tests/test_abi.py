@@ -125,3 +125,12 @@ def test_rollout_loss_rejects_before_device_work():
                              fake, None, None, fake, 1 << 20, None)
     assert st == B.WM_ERR_INVALID_ARGUMENT
     assert "model" in lib.wm_last_error().decode()
+
+
+def test_noalloc_rejects_before_device_work():
+    lib = wm.load_library()
+    arr, p = _seg([0, 8])
+    fake = ctypes.c_void_p(256)   # never dereferenced: validation fails first
+    assert lib.wm_evaluate_noalloc(None, fake, 0, p, 1, fake, fake, fake, 8, 4, fake, 1, 2, fake,
+                                   fake, fake, fake, None, fake, None) == B.WM_ERR_INVALID_ARGUMENT
+    assert "model" in lib.wm_last_error().decode()
