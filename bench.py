@@ -30,7 +30,9 @@ PEAK_HBM_GBS = 8000.0
 
 
 KERNEL_SOURCES = ("paper_2606_09312_amd/csrc/wm_kernels.hip", "paper_2606_09312_amd/csrc/wm_internal.h",
-                  "paper_2606_09312_amd/csrc/wm_api.hip", "paper_2606_09312_amd/build.py")
+                  "paper_2606_09312_amd/csrc/wm_device.h", "paper_2606_09312_amd/csrc/wm_layout.h",
+                  "paper_2606_09312_amd/csrc/wm_api.hip", "paper_2606_09312_amd/csrc/wm_pack.cpp",
+                  "paper_2606_09312_amd/build.py")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_rollout.md")
 
 
