@@ -555,18 +555,20 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
       }
   }
 
-  // Action of the current step (prefetched one step ahead).  Parameters past
-  // P read as 1 (log2 = 0) and meet zero weights in the padded table.
-  const int32_t* ty_row = a.types + (size_t)cand * a.T_max;
-  const int32_t* pa_row = a.params + (size_t)cand * a.T_max * a.P;
+  // Action of the current step (prefetched one step ahead; at d = 512, where
+  // the latent fills the accumulator registers, loaded after the previous
+  // step's chunks instead, so the prefetched values do not occupy registers
+  // through the step).  Parameters past P read as 1 (log2 = 0) and meet
+  // zero weights in the padded table.
+  constexpr bool LATE_ACTION = D >= 512;
   int nx_type = 0;
   int nx_par[PMAX];
 #pragma unroll
   for (int p = 0; p < PMAX; ++p) nx_par[p] = 1;
   if (0 < len) {
-    nx_type = ty_row[0];
+    nx_type = a.types[(size_t)cand * a.T_max];
 #pragma unroll
-    for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[p];
+    for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = a.params[(size_t)cand * a.T_max * a.P + p];
   }
   int errbits = 0;
 
@@ -588,10 +590,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
       u[p] = active ? log2f((float)nx_par[p]) : 0.0f;
     }
     errbits |= (bad_type ? ERRBIT_TYPE : 0) | (bad_par ? ERRBIT_PARAM : 0);
-    if (t + 1 < len) {   // prefetch the next action
-      nx_type = ty_row[t + 1];
+    if (!LATE_ACTION && t + 1 < len) {   // prefetch the next action
+      const size_t row = (size_t)cand * a.T_max + t + 1;
+      nx_type = a.types[row];
 #pragma unroll
-      for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = pa_row[(size_t)(t + 1) * a.P + p];
+      for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = a.params[row * a.P + p];
     }
     Frag xe[NE];
 #pragma unroll
@@ -684,6 +687,12 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
                                                       lane, h, none, cs, tid);
         wait_vm_then_barrier();
       }
+    }
+    if (LATE_ACTION && t + 1 < len) {    // the next action
+      const size_t row = (size_t)cand * a.T_max + t + 1;
+      nx_type = a.types[row];
+#pragma unroll
+      for (int p = 0; p < PMAX; ++p) if (p < a.P) nx_par[p] = a.params[row * a.P + p];
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b)
