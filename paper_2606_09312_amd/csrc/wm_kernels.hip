@@ -634,6 +634,16 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
     }
 
     const int g0 = t * NC;
+    // Chunk at position pos (0 <= pos < 2 NC, positions past NC belong to the
+    // next step) of the workgroup's sequence: odd steps walk the chunks in
+    // descending order, so a step starts with the chunks the previous one
+    // used last.  Where the transition weights exceed an XCD's L2 (d = 512),
+    // an ascending sweep every step would find each chunk evicted.
+    auto chunk_of = [NC, t](int pos) -> uint32_t {
+      const bool next = pos >= NC;
+      const int c = next ? pos - NC : pos;
+      return (uint32_t)((((t + (next ? 1 : 0)) & 1) != 0) ? NC - 1 - c : c);
+    };
     const CopyPlan none = {0u, nullptr, false, 0u, nullptr, false};
     if constexpr (PIPE) {
       // first product of chunk 0 (its W1 part is in w1a); accumulators accA
@@ -648,8 +658,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
         // part of chunk c+1 is copied into w2b and the W1 part of chunk c+2
         // into w1a (issued together up front: spreading them measured slower
         // for this schedule)
-        if (g + 1 < total) stage_buf<W2B, NT>(cs.r2, (uint32_t)(((c + 1) % NC) * W2B), w2b, cs, tid);
-        if (g + 2 < total) stage_buf<W1B, NT>(cs.r1, (uint32_t)(((c + 2) % NC) * W1B), w1a, cs, tid);
+        if (g + 1 < total) stage_buf<W2B, NT>(cs.r2, chunk_of(c + 1) * (uint32_t)W2B, w2b, cs, tid);
+        if (g + 2 < total) stage_buf<W1B, NT>(cs.r1, chunk_of(c + 2) * (uint32_t)W1B, w1a, cs, tid);
         __builtin_amdgcn_sched_barrier(0);
         R::template iteration<true, true, NT, false>(w1b, w2a, xz, xe, accA, amask, accB, zacc,
                                                      lane, h, none, cs, tid);
@@ -658,8 +668,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
         // c + 2 == NC this first product is discarded (w1a then holds the
         // next step's chunk 0 or stale data; the step prologue recomputes it
         // with the new X): one branch-free body keeps register use down.
-        if (g + 2 < total) stage_buf<W2B, NT>(cs.r2, (uint32_t)(((c + 2) % NC) * W2B), w2a, cs, tid);
-        if (g + 3 < total) stage_buf<W1B, NT>(cs.r1, (uint32_t)(((c + 3) % NC) * W1B), w1b, cs, tid);
+        if (g + 2 < total) stage_buf<W2B, NT>(cs.r2, chunk_of(c + 2) * (uint32_t)W2B, w2a, cs, tid);
+        if (g + 3 < total) stage_buf<W1B, NT>(cs.r1, chunk_of(c + 3) * (uint32_t)W1B, w1b, cs, tid);
         __builtin_amdgcn_sched_barrier(0);
         R::template iteration<true, true, NT, false>(w1a, w2b, xz, xe, accB, amask, accA, zacc,
                                                      lane, h, none, cs, tid);
@@ -672,15 +682,15 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
       f32x16 acc;
       for (int c = 0; c < NC; c += 2) {
         const int g = g0 + c;
-        const CopyPlan cp0 = {(uint32_t)(((c + 1) % NC) * W1B), to_lds(w1b), g + 1 < total,
-                              (uint32_t)(((c + 1) % NC) * W2B), to_lds(w2b), g + 1 < total};
+        const CopyPlan cp0 = {chunk_of(c + 1) * (uint32_t)W1B, to_lds(w1b), g + 1 < total,
+                              chunk_of(c + 1) * (uint32_t)W2B, to_lds(w2b), g + 1 < total};
         R::template iteration<true, false, NT, true>(w1a, w2a, xz, xe, acc, amask, acc, zacc,
                                                      lane, h, cp0, cs, tid);
         R::template iteration<false, true, NT, false>(w1a, w2a, xz, xe, acc, amask, acc, zacc,
                                                       lane, h, none, cs, tid);
         wait_vm_then_barrier();
-        const CopyPlan cp1 = {(uint32_t)(((c + 2) % NC) * W1B), to_lds(w1a), g + 2 < total,
-                              (uint32_t)(((c + 2) % NC) * W2B), to_lds(w2a), g + 2 < total};
+        const CopyPlan cp1 = {chunk_of(c + 2) * (uint32_t)W1B, to_lds(w1a), g + 2 < total,
+                              chunk_of(c + 2) * (uint32_t)W2B, to_lds(w2a), g + 2 < total};
         R::template iteration<true, false, NT, true>(w1b, w2b, xz, xe, acc, amask, acc, zacc,
                                                      lane, h, cp1, cs, tid);
         R::template iteration<false, true, NT, false>(w1b, w2b, xz, xe, acc, amask, acc, zacc,
