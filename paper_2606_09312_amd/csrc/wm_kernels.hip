@@ -4689,7 +4689,8 @@ hipError_t launch_train_fwd(const DevModel& m, const TrainIO& io, hipStream_t st
   const TrainArgs a = train_args(m, io);
   const int tiles = (io.B + 31) / 32;
   const bool norm = m.dims.norm == WM_NORM_L2;
-  // residual form, at most one 16-candidate tile per compute unit: narrow tiles
+  // both transition forms, up to NARROW_MAX_TILES = 512 tiles of 16 candidates
+  // (two per compute unit): narrow tiles
   const int ntiles = (io.B + 15) / 16;
   if (m.dims.d == 256 && m.dims.embed_dim == 64 && m.trans_n && m.trans_nt && ntiles <= NARROW_MAX_TILES) {
     const int NC = m.dims.trans_hidden / 32;
@@ -4760,7 +4761,8 @@ hipError_t launch_train_bwd(const DevModel& m, const TrainIO& io, hipStream_t st
   const TrainArgs a = train_args(m, io);
   const int tiles = (io.B + 31) / 32;
   const bool norm = m.dims.norm == WM_NORM_L2;
-  // residual form, at most one 16-candidate tile per compute unit: narrow tiles
+  // both transition forms, up to NARROW_MAX_TILES = 512 tiles of 16 candidates
+  // (two per compute unit): narrow tiles
   const int ntiles = (io.B + 15) / 16;
   if (m.dims.d == 256 && m.dims.embed_dim == 64 && m.trans_nt && ntiles <= NARROW_MAX_TILES) {
     const int NC = m.dims.trans_hidden / 32;
