@@ -29,6 +29,19 @@ struct PBF16 : GeomBF16 {
   static __device__ __forceinline__ f32x16 mfma(Frag a, Frag b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
+  // The same product with the accumulator held in VGPRs, for a chain whose
+  // accumulator lives beside a latent that fills the AGPRs.  The compiler's
+  // hazard checks do not see inline assembly: the caller provides NOPS wait
+  // states before the product (its accumulator written by VALU just before)
+  // and waits before the first VALU access to the result.
+  template <int NOPS>
+  static __device__ __forceinline__ void mfma_v(Frag a, Frag b, f32x16& c) {
+    if constexpr (NOPS > 0)
+      asm volatile("s_nop %3\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
+                   : "+v"(c) : "v"(a), "v"(b), "i"(NOPS - 1));
+    else
+      asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
+  }
   // 8 floats -> 8 bf16 (round to nearest even)
   static __device__ __forceinline__ Frag cvt(const float* v) {
     Frag f;

@@ -264,6 +264,8 @@ struct Roll {
                                                    const CopySrc& cs, int tid) {
     constexpr int N1 = DO_G1 ? NK1 / G : 0;
     constexpr int N2 = DO_G2 ? NK2 / G : 0;
+    // d = 512 (first product alone, its GELU after it): the accumulator in VGPRs
+    constexpr bool VACC = DO_G1 && !DO_G2 && G == 1 && D >= 512;
     constexpr int NI = N1 + N2;
     constexpr int NU = COPY ? U1<NT> + U2<NT> : 0;     // copy units, spread over the items
     constexpr int P = 4;                                   // LDS reads in flight
@@ -298,10 +300,19 @@ struct Roll {
           if ((u * NI) / NU == i) copy_unit<NT>(cp, cs, u, tid);
       }
       if (i < N1) {
+        if constexpr (VACC) {
+          // accumulator in VGPRs (the latent fills the AGPRs): 5 wait states
+          // after its VALU initialisation; the first VALU access follows
+          // the iteration's closing wait
+          const Frag b = i < NZ ? xz[i < NZ ? i : 0] : xe[i < NZ ? 0 : i - NZ];
+          if (i == 0) PR::template mfma_v<5>(PR::pick(grp, 0), b, acc1n);
+          else PR::template mfma_v<0>(PR::pick(grp, 0), b, acc1n);
+        } else {
 #pragma unroll
-        for (int w = 0; w < G; ++w) {
-          const int kf = i * G + w;
-          acc1n = PR::mfma(PR::pick(grp, w), kf < NZ ? xz[kf < NZ ? kf : 0] : xe[kf < NZ ? 0 : kf - NZ], acc1n);
+          for (int w = 0; w < G; ++w) {
+            const int kf = i * G + w;
+            acc1n = PR::mfma(PR::pick(grp, w), kf < NZ ? xz[kf < NZ ? kf : 0] : xe[kf < NZ ? 0 : kf - NZ], acc1n);
+          }
         }
         if constexpr (DO_G2) {
           // value pairs spread evenly over the N1 items of the first product
@@ -318,6 +329,10 @@ struct Roll {
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    // wait states between the last product into a VGPR accumulator and the
+    // next VALU access to it (the accumulator is an operand, so no access is
+    // scheduled above them)
+    if constexpr (VACC && N2 == 0) asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(acc1n));
   }
 
   // SL consecutive floats of an LDS table row
