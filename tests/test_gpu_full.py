@@ -103,3 +103,53 @@ def test_persistent_waves(wm, name, prec, B):
     w = synth.scaled(base, B=B, S=1)
     print(f"[waves] {name} {prec} B={B}", flush=True)
     compare(wm, w, prec, "none", 2300 + B, base.k)
+
+
+# One- and two-step sequences through the persistent kernels at every
+# wavefront count, with a bound on the batch mean of the per-candidate errors.
+# Within one or two steps the operands the kernel and the oracle round to
+# bf16 differ only where a different fp32 accumulation order (about 1e-6
+# relative) moves a value across a rounding boundary: a rare, independent
+# event that changes one operand by one bf16 step (2^-8 relative).  One such
+# operand among the H = 2048 GELU outputs moves z by about 2^-8 / sqrt(2048),
+# i.e. 1e-4 relative, and most candidates see none, so the batch mean stays
+# near 1e-4 at most (the largest single differences, a few 1e-3, stay under
+# the standard tolerance checked as well).  A matrix product whose result is
+# read before it completes, or a contraction step left out, shifts every
+# candidate by about a whole term (1e-2 and more) and fails the mean bound
+# even where long rollouts hide it inside their per-candidate bound.
+SHORT_MEAN = 5e-4
+SHORT = [
+    ("large_latent", "none", 300),           # one wavefront per workgroup
+    ("large_latent", "none", 20000),         # two
+    ("large_latent", "none", 32768 + 17),    # four
+    ("large_latent", "l2", 20000),
+    ("multi_subgraph", "none", 20000),
+    ("multi_subgraph", "none", 32768),
+]
+
+
+@pytest.mark.parametrize("name,norm,B", SHORT)
+@pytest.mark.timeout(600)
+def test_short_sequences_tight(wm, name, norm, B):
+    base = synth.workload(name)
+    w = synth.scaled(base, B=B, len_lo=1, len_hi=2, T_max=2)
+    print(f"[short] {name} {norm} B={B}", flush=True)
+    W = synth.make_weights(w, 1000)
+    model = wm.Model(wm.model_dims(w), W, precision="bf16", norm=norm)
+    I = synth.make_inputs(w, 4100 + B)
+    k = base.k
+    g = run_evaluate(model, w, I, k)
+    assert g["status"] == 0
+    ref = oracle_full(W, I, "bf16", k, norm=norm)
+    tol_z, tol_s = bounds("bf16", (0.0, 0.0))
+    rel = latent_rel(g["zT"], ref["zT"])
+    srel = score_rel(g["scores"], ref["scores"], I["seg_off"])
+    print(f"  z_T mean rel {rel.mean():.1e} (bound {SHORT_MEAN:.0e}), max {rel.max():.2e}; score mean "
+          f"rel {srel.mean():.1e} (bound {SHORT_MEAN:.0e}), max {srel.max():.2e}", flush=True)
+    assert rel.mean() <= SHORT_MEAN, f"z_T mean rel err {rel.mean():.3e}"
+    assert srel.mean() <= SHORT_MEAN, f"score mean rel err {srel.mean():.3e}"
+    assert rel.max() <= tol_z, f"z_T rel err {rel.max():.3e}"
+    assert srel.max() <= tol_s, f"score rel err {srel.max():.3e}"
+    check_topk_self_consistent(g["idx"], g["val"], g["scores"], I["seg_off"], k)
+    check_topk_vs_oracle(g["idx"], ref["scores"], I["seg_off"], k, tol_s)
