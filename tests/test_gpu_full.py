@@ -106,15 +106,16 @@ def test_persistent_waves(wm, name, prec, B):
 
 
 # One- and two-step sequences through the persistent kernels at every
-# wavefront count, with a bound on the batch mean of the per-candidate errors.
+# wavefront count and through the narrow-tile kernels, with a bound on the
+# batch mean of the per-candidate errors.
 # Within one or two steps the operands the kernel and the oracle round to
 # bf16 differ only where a different fp32 accumulation order (about 1e-6
 # relative) moves a value across a rounding boundary: a rare, independent
 # event that changes one operand by one bf16 step (2^-8 relative).  One such
-# operand among the H = 2048 GELU outputs moves z by about 2^-8 / sqrt(2048),
-# i.e. 1e-4 relative, and most candidates see none, so the batch mean stays
-# near 1e-4 at most (the largest single differences, a few 1e-3, stay under
-# the standard tolerance checked as well).  A matrix product whose result is
+# operand among the H GELU outputs moves z by about 2^-8 / sqrt(H), i.e.
+# 1e-4 to 2e-4 relative for H = 2048 to 512, and most candidates see none,
+# so the batch mean stays below that (the largest single differences, a few
+# 1e-3, stay under the standard tolerance checked as well).  A matrix product whose result is
 # read before it completes, or a contraction step left out, shifts every
 # candidate by about a whole term (1e-2 and more) and fails the mean bound
 # even where long rollouts hide it inside their per-candidate bound.
@@ -126,12 +127,17 @@ SHORT = [
     ("large_latent", "l2", 20000),
     ("multi_subgraph", "none", 20000),
     ("multi_subgraph", "none", 32768),
+    ("ansor_round", "none", 2048),           # narrow tiles (H = 512)
+    ("ansor_round", "l2", 2048),
+    ("long_schedule", "none", 8192),         # narrow tiles, two per compute unit (H = 1024)
 ]
 
 
 @pytest.mark.parametrize("name,norm,B", SHORT)
 @pytest.mark.timeout(600)
 def test_short_sequences_tight(wm, name, norm, B):
+    """Persistent (and, for the smaller batches, narrow-tile) kernels on one-
+    and two-step sequences in bf16: batch-mean errors against the oracle."""
     base = synth.workload(name)
     w = synth.scaled(base, B=B, len_lo=1, len_hi=2, T_max=2)
     print(f"[short] {name} {norm} B={B}", flush=True)
