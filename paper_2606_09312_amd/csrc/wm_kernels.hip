@@ -382,6 +382,10 @@ struct Hyper {
   static constexpr int BYTES = HyperGeom<PR>::bytes(D, E);
   // keep V in registers between the two passes where the latent leaves room
   static constexpr bool HOLD = D <= 64 || (G == 1 && D <= 256);
+  // d = 512: the latent fills the AGPRs; V's accumulator goes to VGPRs
+  static constexpr bool VACC = G == 1 && D >= 512;
+  // latent operand fragments: NF2 per 32-row block, SL values each per lane
+  static constexpr int SL = PR::SL, NF2 = 32 / PR::KF, NZ = D / PR::KF;
 
   static __device__ __forceinline__ u32x4 group(const uint8_t* src, int g, int lane) {
     return *reinterpret_cast<const u32x4*>(src + g * 1024 + lane * 16);
@@ -407,7 +411,7 @@ struct Hyper {
   static __device__ __forceinline__ void pass(const uint8_t* src, const Frag (&xe)[NE],
                                               f32x16 (&z)[NB], f32x16 (&vh)[HOLD ? NB : 1],
                                               float& vz, float& vv, float& zz, float al, float s,
-                                              int lane) {
+                                              Frag (&xz)[NZ], int lane) {
     // global source: lane offset folded into an opaque base (lane argument 0)
     const uint8_t* base = GLOBAL ? lane_base(src, lane) : src;
     const int ln = GLOBAL ? 0 : lane;
@@ -427,11 +431,21 @@ struct Hyper {
         const int g = b * GPB + k;
         const u32x4 grp = ring[g % RD];
         if (g + RD < NG) ring[g % RD] = ld(g + RD);
+        if constexpr (VACC) {
+          // accumulator in VGPRs (the latent fills the AGPRs): 5 wait
+          // states after its zero initialisation
+          if (k == 0) PR::template mfma_v<5>(PR::pick(grp, 0), xe[k], vb);
+          else PR::template mfma_v<0>(PR::pick(grp, 0), xe[k], vb);
+        } else {
 #pragma unroll
-        for (int w = 0; w < G; ++w) vb = PR::mfma(PR::pick(grp, w), xe[k * G + w], vb);
+          for (int w = 0; w < G; ++w) vb = PR::mfma(PR::pick(grp, w), xe[k * G + w], vb);
+        }
         // keep the reads RD groups ahead, not hoisted all to the top
         __builtin_amdgcn_sched_barrier(0);
       }
+      // wait states before the first VALU access to a VGPR accumulator (an
+      // operand of the wait, so no access is scheduled above it)
+      if constexpr (VACC) asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(vb));
       if constexpr (PASS == 0) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -443,17 +457,35 @@ struct Hyper {
       } else {
 #pragma unroll
         for (int r = 0; r < 16; ++r) z[b][r] = (z[b][r] - al * vb[r]) * s;
+        frags_of(z[b], b, xz);
       }
     }
   }
 
+  // The step's operand fragments of latent block b (the state after the
+  // projection), formed as each block is updated so that the latent is read
+  // once.
+  static __device__ __forceinline__ void frags_of(const f32x16& zb, int b, Frag (&xz)[NZ]) {
+#pragma unroll
+    for (int f = 0; f < NF2; ++f) {
+      float v[SL];
+#pragma unroll
+      for (int j = 0; j < SL; ++j) v[j] = zb[f * SL + j];
+      xz[b * NF2 + f] = PR::cvt(v);
+      // formed here, not sunk to its first use (which would keep every
+      // updated value alive, and spill)
+      asm volatile("" : "+v"(xz[b * NF2 + f]));
+    }
+  }
+
   template <int RD, bool GLOBAL>
+  // Also forms the step's latent operand fragments xz from the projected state.
   static __device__ __forceinline__ void step_in(f32x16 (&z)[NB], const Frag (&xe)[NE],
                                                  const uint8_t* src, bool project, bool renorm,
-                                                 int lane) {
+                                                 Frag (&xz)[NZ], int lane) {
     float vz = 0.0f, vv = 0.0f, zz = 0.0f;
     f32x16 vh[HOLD ? NB : 1];
-    pass<0, RD, GLOBAL>(src, xe, z, vh, vz, vv, zz, 0.0f, 1.0f, lane);
+    pass<0, RD, GLOBAL>(src, xe, z, vh, vz, vv, zz, 0.0f, 1.0f, xz, lane);
     vz = pair_sum(vz);
     vv = pair_sum(vv);
     zz = pair_sum(zz);
@@ -461,11 +493,18 @@ struct Hyper {
     const float al = (project && vv > 0.0f) ? vz / vv : 0.0f;
     if constexpr (HOLD) {
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
+      for (int b = 0; b < NB; ++b) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) z[b][r] = (z[b][r] - al * vh[b][r]) * s;
+        frags_of(z[b], b, xz);
+      }
     } else {
-      pass<1, RD, GLOBAL>(src, xe, z, vh, vz, vv, zz, al, s, lane);
+      // The latent lives in the AGPRs; without this fence the compiler keeps
+      // the VGPR copies pass 0 read for its dots alive into pass 1 (all of
+      // z twice over), and spills.
+#pragma unroll
+      for (int b = 0; b < NB; ++b) asm volatile("" : "+a"(z[b]));
+      pass<1, RD, GLOBAL>(src, xe, z, vh, vz, vv, zz, al, s, xz, lane);
     }
   }
 
@@ -633,19 +672,21 @@ __global__ __launch_bounds__(64 * WAVES, 1) void rollout_kernel(const RollArgs a
         for (int j = 0; j < SL; ++j) ph[j] += ev[j];
       }
     }
-    if constexpr (NORM) {
-      // unit length for the previous step's output, hyperplane projection for this step
-      if constexpr (WH_LDS) HY::template step_in<4, false>(zacc, xe, whs, active, t > 0 && t <= len, lane);
-      else HY::template step_in<8, true>(zacc, xe, a.wh, active, t > 0 && t <= len, lane);
-    }
     // ---- z operand fragments (state at the start of the step)
     Frag xz[NZ];
+    if constexpr (NORM) {
+      // unit length for the previous step's output, hyperplane projection
+      // for this step; the operand fragments come from the projected state
+      if constexpr (WH_LDS) HY::template step_in<4, false>(zacc, xe, whs, active, t > 0 && t <= len, xz, lane);
+      else HY::template step_in<8, true>(zacc, xe, a.wh, active, t > 0 && t <= len, xz, lane);
+    } else {
 #pragma unroll
-    for (int kf = 0; kf < NZ; ++kf) {
-      float v[SL];
+      for (int kf = 0; kf < NZ; ++kf) {
+        float v[SL];
 #pragma unroll
-      for (int j = 0; j < SL; ++j) v[j] = zacc[kf / NF2][(kf % NF2) * SL + j];
-      xz[kf] = PR::cvt(v);
+        for (int j = 0; j < SL; ++j) v[j] = zacc[kf / NF2][(kf % NF2) * SL + j];
+        xz[kf] = PR::cvt(v);
+      }
     }
 
     const int g0 = t * NC;
