@@ -458,6 +458,7 @@ struct Hyper {
 #pragma unroll
         for (int r = 0; r < 16; ++r) z[b][r] = (z[b][r] - al * vb[r]) * s;
         frags_of(z[b], b, xz);
+        asm volatile("" : "+a"(z[b]));    // the updated block back in the AGPRs here
       }
     }
   }
