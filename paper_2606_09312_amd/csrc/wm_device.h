@@ -36,6 +36,7 @@ struct PBF16 : GeomBF16 {
   // and waits before the first VALU access to the result.
   template <int NOPS>
   static __device__ __forceinline__ void mfma_v(Frag a, Frag b, f32x16& c) {
+    static_assert(NOPS >= 0 && NOPS <= 16, "one s_nop covers 1 to 16 wait states");
     if constexpr (NOPS > 0)
       asm volatile("s_nop %3\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
                    : "+v"(c) : "v"(a), "v"(b), "i"(NOPS - 1));
