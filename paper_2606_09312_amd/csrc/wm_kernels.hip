@@ -2222,10 +2222,8 @@ __global__ __launch_bounds__(64 * W, 1) void rollout_narrow_kernel(const RollArg
 // Action features: phi_i = (1/len_i) sum_t e_t.  The sum is regrouped by
 // what varies per step:  sum_t e_t = sum_k n_k type_emb[k] + param_w .
 // sum_t log2(params_t) + len_i param_b, with n_k the number of steps of
-// kind k.  One wavefront per candidate: lanes take the steps (64 at a time),
-// kind counts come from one ballot per kind, the log2-parameter sums from a
-// wavefront reduction; then every lane forms features f = lane, lane+64, ...
-// Kinds are clamped into range here (the rollout kernel reports them).
+// kind k.  Kinds are clamped into range here (the rollout kernel reports
+// them).
 
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
@@ -2233,46 +2231,61 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+__device__ __forceinline__ float group16_sum(float x) {
+  // butterfly over the 16 lanes of a group (xor 1, 2, 4, 8 stays inside it)
+#pragma unroll
+  for (int m = 8; m >= 1; m >>= 1) x += __shfl_xor(x, m);
+  return x;
+}
+
+// a4 where the rollout kernel does not sum phi itself: 16 lanes per candidate
+// (four candidates per wavefront), lane s taking steps s, s + 16, ...; the
+// kind counts and log2-parameter sums are reduced over the candidate's 16
+// lanes, then lane s forms features s, s + 16, ... of the regrouped mean
+// (0 for an empty sequence).
 __global__ __launch_bounds__(256) void phi_kernel(const float* __restrict__ emb,
                                                    const int32_t* __restrict__ types,
                                                    const int32_t* __restrict__ params,
                                                    const int32_t* __restrict__ lens, int B,
                                                    int T_max, int E, int P, int K,
                                                    float* __restrict__ phi) {
-  const int lane = threadIdx.x & 63;
-  const int i = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  if (i >= B) return;                                  // whole wavefront leaves together
+  const int lane = threadIdx.x & 63, s = lane & 15;
+  const int i = (blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * 4 + (lane >> 4);
+  const bool valid = i < B;
   const float* t_emb = emb;
   const float* t_pw = emb + K * temb_stride(E);        // [PMAX][E], zero rows past P
   const float* t_pb = t_pw + PMAX * E;
-  const int len = clampi(lens[i], 0, T_max);
-  int cnt[32];                                         // n_k (wave-uniform), K <= 32
+  const int len = valid ? clampi(lens[i], 0, T_max) : 0;
+  float cnt[32];                                       // n_k, K <= 32 (exact in float)
 #pragma unroll
-  for (int k = 0; k < 32; ++k) cnt[k] = 0;
-  float us[PMAX];                                      // per-lane sums of log2(params)
+  for (int k = 0; k < 32; ++k) cnt[k] = 0.0f;
+  float us[PMAX];                                      // sums of log2(params)
 #pragma unroll
   for (int p = 0; p < PMAX; ++p) us[p] = 0.0f;
-  const int32_t* ty_row = types + (size_t)i * T_max;
-  const int32_t* pa_row = params + (size_t)i * T_max * P;
-  for (int t0 = 0; t0 < len; t0 += 64) {
-    const int t = t0 + lane;
-    const bool v = t < len;
-    const int ty = v ? clampi(ty_row[t], 0, K - 1) : -1;
-#pragma unroll
-    for (int p = 0; p < PMAX; ++p)
-      if (p < P && v) us[p] += log2f((float)pa_row[(size_t)t * P + p]);
+  const int32_t* ty_row = types + (size_t)(valid ? i : 0) * T_max;
+  const int32_t* pa_row = params + (size_t)(valid ? i : 0) * T_max * P;
+  for (int t = s; t < len; t += 16) {
+    const int ty = clampi(ty_row[t], 0, K - 1);
 #pragma unroll
     for (int k = 0; k < 32; ++k)
-      if (k < K) cnt[k] += __popcll(__ballot(ty == k));
-  }
+      if (k < K) cnt[k] += ty == k ? 1.0f : 0.0f;
 #pragma unroll
-  for (int p = 0; p < PMAX; ++p) us[p] = p < P ? wave_sum(us[p]) : 0.0f;
+    for (int p = 0; p < PMAX; ++p)
+      if (p < P) us[p] += log2f((float)pa_row[(size_t)t * P + p]);
+  }
+  // every lane takes part in the reductions (invalid groups sum zeros)
+#pragma unroll
+  for (int k = 0; k < 32; ++k)
+    if (k < K) cnt[k] = group16_sum(cnt[k]);
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p) us[p] = p < P ? group16_sum(us[p]) : 0.0f;
+  if (!valid) return;
   const float inv = len > 0 ? 1.0f / (float)len : 0.0f;
-  for (int f = lane; f < E; f += 64) {
+  for (int f = s; f < E; f += 16) {
     float acc = 0.0f;
 #pragma unroll
     for (int k = 0; k < 32; ++k)
-      if (k < K) acc = fmaf((float)cnt[k], t_emb[k * temb_stride(E) + f], acc);
+      if (k < K) acc = fmaf(cnt[k], t_emb[k * temb_stride(E) + f], acc);
 #pragma unroll
     for (int p = 0; p < PMAX; ++p) acc = fmaf(us[p], t_pw[p * E + f], acc);
     phi[(size_t)i * E + f] = len > 0 ? fmaf(acc, inv, t_pb[f]) : 0.0f;
@@ -4554,7 +4567,7 @@ hipError_t launch_phi(const DevModel& m, const int32_t* types, const int32_t* pa
                       const int32_t* lens, int32_t B, int32_t T_max, float* phi, hipStream_t st) {
   const int E = m.dims.embed_dim;
   if (B == 0) return hipSuccess;
-  const int blocks = (B + 3) / 4;                 // four candidates (wavefronts) per workgroup
+  const int blocks = (B + 15) / 16;               // four wavefronts of four candidates each
   hipLaunchKernelGGL(phi_kernel, dim3(blocks), dim3(256), 0, st, m.emb_nat, types, params, lens,
                      B, T_max, E, m.dims.n_params, m.dims.n_kinds, phi);
   return hipGetLastError();
