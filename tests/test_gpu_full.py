@@ -123,7 +123,9 @@ SHORT_MEAN = 5e-4
 SHORT = [
     ("large_latent", "none", 300),           # one wavefront per workgroup
     ("large_latent", "none", 20000),         # two
-    ("large_latent", "none", 32768 + 17),    # four
+    ("large_latent", "none", 20000 + 13),    # two, ragged last tile
+    ("large_latent", "none", 32768 + 17),    # four, ragged last tile
+    ("ansor_round", "none", 20000 + 13),     # d = 256 persistent, two, ragged
     ("large_latent", "l2", 20000),
     ("multi_subgraph", "none", 20000),
     ("multi_subgraph", "none", 32768),
@@ -139,8 +141,8 @@ def test_short_sequences_tight(wm, name, norm, B):
     """Persistent (and, for the smaller batches, narrow-tile) kernels on one-
     and two-step sequences in bf16: batch-mean errors against the oracle."""
     base = synth.workload(name)
-    w = synth.scaled(base, B=B, len_lo=1, len_hi=2, T_max=2)
-    print(f"[short] {name} {norm} B={B}", flush=True)
+    w = synth.scaled(base, B=B, S=base.S if B % base.S == 0 else 1, len_lo=1, len_hi=2, T_max=2)
+    print(f"[short] {name} {norm} B={B} S={w.S}", flush=True)
     W = synth.make_weights(w, 1000)
     model = wm.Model(wm.model_dims(w), W, precision="bf16", norm=norm)
     I = synth.make_inputs(w, 4100 + B)
